@@ -1,0 +1,268 @@
+/*
+ * GMC oracle: a plain, slow, single-threaded CPU statement of what one
+ * iteration of Global Momentum Compression computes (Algorithm 1, GMC, of
+ * "Global Momentum Compression for Sparse Communication in Distributed
+ * Learning", Shi, Zhao, Xie, Gao, Li).
+ *
+ * TEST INFRASTRUCTURE.  Only the test suite, the smoke check and the bench's
+ * CPU-baseline leg may load or call this library.  It shares no code, header,
+ * table or helper with the device library; the only thing the two sides have
+ * in common is the seeded input generator.
+ *
+ * Arithmetic: IEEE-754 binary32, one rounding per operation, no contraction
+ * into fused multiply-adds (built with -ffp-contract=off, SSE2 scalar float,
+ * no fast-math), denormals kept.  The paper states the update in real
+ * arithmetic; binary32 is the precision of the device path and the selection
+ * of the compressor is an integer decision taken on binary32 values, so both
+ * sides must take it on the same bits.
+ *
+ * Readings of points on which the paper is silent (each one is listed with
+ * its reason in the design notes of the repository):
+ *   - c = fl32(beta/eta) and s = fl32(eta/K), each formed in double and
+ *     rounded once;
+ *   - u = fl(fl(e + g) - fl(c * fl(w_t - w_prev))), evaluated left to right as
+ *     printed in step "e_{t+1/2,k} = e_{t,k} + grad - (beta/eta)(w_t - w_{t-1})";
+ *   - the number kept per segment of n components is
+ *     k = min(n, max(1, ceil(ratio * n))), the product formed in binary64;
+ *   - top-s ranks by the magnitude bits |u| = bits(u) & 0x7FFFFFFF (NaN above
+ *     Inf, -0 equal to +0) and breaks ties by the lower index;
+ *   - the server sum over workers runs in worker order 0..K-1 from +0.0f and
+ *     the scale eta/K is applied once afterwards: delta = -(s * acc);
+ *   - RBGS draws its blocks with Floyd's sampling algorithm fed by a SplitMix64
+ *     stream whose state is seed XOR mix(t+1); the same blocks on every worker.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------- */
+/* Constants and counts                                                       */
+/* ------------------------------------------------------------------------- */
+
+/* Components kept from a segment of n: ceil(ratio * n) with the product
+ * formed in binary64, clamped to [1, n].  The paper sets s = d/1024 for its
+ * experiments (Section 5.1) and states top-s as keeping the s largest
+ * components (Section 1); a ratio that is a power of two gives that s
+ * exactly. */
+int64_t orc_count(int64_t n, double ratio)
+{
+    double x = ratio * (double)n;
+    int64_t k = (int64_t)ceil(x);
+    if (k < 1) k = 1;
+    if (k > n) k = n;
+    return k;
+}
+
+/* beta/eta multiplies the parameter difference in the global momentum term;
+ * eta/K scales the server's sum (Algorithm 1, server update). */
+void orc_constants(double beta, double eta, int K, float* c, float* s)
+{
+    *c = (float)(beta / eta);
+    *s = (float)(eta / (double)K);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Worker side: global momentum plus error feedback (Algorithm 1, workers)    */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * u = e_{t,k} + g_{t,k} - (beta/eta) (w_t - w_{t-1})          (Algorithm 1)
+ *
+ * -(w_t - w_{t-1})/eta is the paper's global momentum (Section 2.3); beta
+ * times it enters every worker's pre-compression vector.
+ */
+void orc_precompress(int64_t d, float c, const float* w_t, const float* w_prev,
+                     const float* g, const float* e, float* u)
+{
+    for (int64_t j = 0; j < d; ++j) {
+        float diff = w_t[j] - w_prev[j];
+        float mom = c * diff;
+        float acc = e[j] + g[j];
+        u[j] = acc - mom;
+    }
+}
+
+/* Magnitude key: the sign bit cleared. */
+static uint32_t key_of(float x)
+{
+    uint32_t b;
+    memcpy(&b, &x, sizeof b);
+    return b & 0x7fffffffu;
+}
+
+typedef struct {
+    uint32_t key;
+    int64_t pos;
+} keyed;
+
+/* Strict total order: larger magnitude first, then lower position. */
+static int cmp_rank(const void* a, const void* b)
+{
+    const keyed* x = (const keyed*)a;
+    const keyed* y = (const keyed*)b;
+    if (x->key != y->key) return x->key > y->key ? -1 : 1;
+    if (x->pos != y->pos) return x->pos < y->pos ? -1 : 1;
+    return 0;
+}
+
+static int cmp_i64(const void* a, const void* b)
+{
+    int64_t x = *(const int64_t*)a, y = *(const int64_t*)b;
+    return (x > y) - (x < y);
+}
+
+/*
+ * top-s: the k positions of u[0..n) with the largest |u|, ties to the lower
+ * position, returned in ascending position order.  A full sort under the
+ * ranking order, then the first k: slow and plain.  Returns 0, or -1 if the
+ * scratch allocation fails.
+ */
+int orc_topk(int64_t n, const float* u, int64_t k, int64_t* out_pos)
+{
+    keyed* r = (keyed*)malloc((size_t)(n > 0 ? n : 1) * sizeof(keyed));
+    if (!r) return -1;
+    for (int64_t j = 0; j < n; ++j) {
+        r[j].key = key_of(u[j]);
+        r[j].pos = j;
+    }
+    qsort(r, (size_t)n, sizeof(keyed), cmp_rank);
+    for (int64_t i = 0; i < k; ++i) out_pos[i] = r[i].pos;
+    free(r);
+    qsort(out_pos, (size_t)k, sizeof(int64_t), cmp_i64);
+    return 0;
+}
+
+/*
+ * C(u) for top-s applied to each segment [seg_off[i], seg_off[i+1]) of u, and
+ * the residual e_{t+1,k} = u - C(u), written over u in place (a kept
+ * component becomes u - u = +0.0f, every other component keeps u).
+ * Messages: idx (int32, ascending) and val = u[idx], segment after segment.
+ * Returns the message length, or -1 on allocation failure.
+ */
+int64_t orc_compress_topk(float* u, int64_t n_seg, const int64_t* seg_off, double ratio,
+                          int32_t* idx, float* val)
+{
+    int64_t m = 0;
+    for (int64_t s = 0; s < n_seg; ++s) {
+        int64_t lo = seg_off[s], n = seg_off[s + 1] - lo;
+        int64_t k = orc_count(n, ratio);
+        int64_t* pos = (int64_t*)malloc((size_t)k * sizeof(int64_t));
+        if (!pos) return -1;
+        if (orc_topk(n, u + lo, k, pos) != 0) {
+            free(pos);
+            return -1;
+        }
+        for (int64_t i = 0; i < k; ++i) {
+            int64_t j = lo + pos[i];
+            idx[m] = (int32_t)j;
+            val[m] = u[j];
+            ++m;
+        }
+        free(pos);
+    }
+    for (int64_t i = 0; i < m; ++i) {
+        float sent = val[i];
+        u[idx[i]] = u[idx[i]] - sent;   /* u - C(u) at a kept component */
+    }
+    return m;
+}
+
+/* ------------------------------------------------------------------------- */
+/* RBGS: random blocks with a seed shared by all workers (Sections 4, 5.2)    */
+/* ------------------------------------------------------------------------- */
+
+/* SplitMix64 output mixing function (Steele, Lea, Flood, OOPSLA 2014). */
+uint64_t orc_splitmix64_mix(uint64_t z)
+{
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+    return z ^ (z >> 31);
+}
+
+/* Draw i (i = 0, 1, ...) of step t: output i of a SplitMix64 generator whose
+ * state starts at seed XOR mix(t + 1) and advances by the golden gamma. */
+uint64_t orc_rbgs_draw(uint64_t seed, uint64_t t, uint64_t i)
+{
+    const uint64_t gamma = 0x9e3779b97f4a7c15ULL;
+    uint64_t state = seed ^ orc_splitmix64_mix(t + 1);
+    return orc_splitmix64_mix(state + (i + 1) * gamma);
+}
+
+static int cmp_i32(const void* a, const void* b)
+{
+    int32_t x = *(const int32_t*)a, y = *(const int32_t*)b;
+    return (x > y) - (x < y);
+}
+
+/*
+ * n_sel distinct block ids out of nb, sorted ascending: Floyd's sampling
+ * algorithm (Bentley and Floyd, "Programming Pearls: A Sample of
+ * Brilliance", CACM 1987).  For J = nb-n_sel .. nb-1 draw r uniform on
+ * [0, J]; keep r, or J when r was already kept.  The draw maps the top 32
+ * random bits onto [0, J] by multiply-shift.
+ */
+void orc_rbgs_blocks(uint64_t seed, uint64_t t, int32_t nb, int32_t n_sel, int32_t* blocks)
+{
+    int32_t have = 0;
+    for (int64_t J = (int64_t)nb - n_sel; J < nb; ++J) {
+        uint64_t x = orc_rbgs_draw(seed, t, (uint64_t)(J - ((int64_t)nb - n_sel)));
+        int32_t r = (int32_t)(((x >> 32) * (uint64_t)(J + 1)) >> 32);
+        int dup = 0;
+        for (int32_t q = 0; q < have; ++q)
+            if (blocks[q] == r) dup = 1;
+        blocks[have++] = dup ? (int32_t)J : r;
+    }
+    qsort(blocks, (size_t)n_sel, sizeof(int32_t), cmp_i32);
+}
+
+/*
+ * C(u) for RBGS: every component of the selected blocks (block b covers
+ * [b*B, min((b+1)*B, d))), in ascending block order; the residual u - C(u)
+ * is written over u.  Returns the message length.
+ */
+int64_t orc_compress_rbgs(float* u, int64_t d, int64_t B, const int32_t* blocks, int32_t n_sel,
+                          float* val)
+{
+    int64_t m = 0;
+    for (int32_t q = 0; q < n_sel; ++q) {
+        int64_t lo = (int64_t)blocks[q] * B, hi = lo + B;
+        if (hi > d) hi = d;
+        for (int64_t j = lo; j < hi; ++j) {
+            float sent = u[j];
+            val[m++] = sent;
+            u[j] = u[j] - sent;
+        }
+    }
+    return m;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Server side (Algorithm 1, server) and the workers' apply                   */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * delta = w_{t+1} - w_t = -(eta/K) sum_k C(u_k):
+ * acc = +0.0f; acc += C(u_k) for k = 0..K-1 in order (only the components
+ * worker k sent are nonzero in C(u_k)); delta = -(s * acc), dense over d.
+ * idx[k], val[k], len[k] are worker k's message.
+ */
+int orc_aggregate(int64_t d, int K, float s, const int32_t* const* idx,
+                  const float* const* val, const int64_t* len, float* delta)
+{
+    float* acc = (float*)malloc((size_t)(d > 0 ? d : 1) * sizeof(float));
+    if (!acc) return -1;
+    for (int64_t j = 0; j < d; ++j) acc[j] = 0.0f;
+    for (int k = 0; k < K; ++k)
+        for (int64_t i = 0; i < len[k]; ++i)
+            acc[idx[k][i]] = acc[idx[k][i]] + val[k][i];
+    for (int64_t j = 0; j < d; ++j) delta[j] = -(s * acc[j]);
+    free(acc);
+    return 0;
+}
+
+/* w_{t+1} = w_t + (w_{t+1} - w_t)   (Algorithm 1, workers' last step) */
+void orc_apply(int64_t d, float* w, const float* delta)
+{
+    for (int64_t j = 0; j < d; ++j) w[j] = w[j] + delta[j];
+}

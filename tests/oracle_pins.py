@@ -1,0 +1,399 @@
+"""Checks that pin the CPU oracle to what the paper and mathematics fix.
+
+Each ``pin_*`` function takes an oracle library handle and raises
+AssertionError when the oracle disagrees with:
+
+* closed forms the paper states: GMC without compression is momentum SGD
+  (Section 2.3, eq. 3); the update-rule rewrite (eq. 8); the auxiliary
+  sequence z_t of Lemma 1; the toy quadratic of Section 3.2, whose
+  uncompressed run has a closed form;
+* properties of the compressors: top-s equals a brute-force sort; the
+  delta-approximation bound of Assumption 1; the error-feedback identity
+  C(u) + e_{t+1} = u; RBGS blocks that are distinct, sorted, reproducible,
+  shared by the workers and uniform; the RBGS communication cost of
+  Section 5.2;
+* published test vectors (SplitMix64).
+
+They are plain functions so that the mutation tests can run them against
+deliberately broken builds of the oracle and check that each planted mistake
+is caught by at least one of them.
+"""
+from __future__ import annotations
+
+import itertools
+import math
+import os
+
+import numpy as np
+
+import oracle
+import synth
+
+EPS32 = 2.0 ** -24
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _bits(a: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+
+
+def _keys(a: np.ndarray) -> np.ndarray:
+    return _bits(a) & np.uint32(0x7FFFFFFF)
+
+
+def brute_topk(u: np.ndarray, k: int) -> np.ndarray:
+    """Independent top-k: Python's sort of (-|u| bits, index) tuples."""
+    keys = _keys(u).tolist()
+    order = sorted(range(len(keys)), key=lambda j: (-keys[j], j))
+    return np.array(sorted(order[:k]), dtype=np.int64)
+
+
+def _run(lib, wl: synth.Workload, ratio: float, steps: int, grad_fn=None, w0=None):
+    """Drive the oracle for `steps` iterations; returns per-step records."""
+    orc = oracle.GmcOracle(wl.d, wl.K, "topk", ratio, wl.beta, wl.eta,
+                           seg_off=[0, wl.d], lib=lib)
+    w = (wl.w0() if w0 is None else np.asarray(w0, np.float32)).copy()
+    w_prev = w.copy()
+    err = np.zeros((wl.K, wl.d), np.float32)
+    recs = []
+    for t in range(steps):
+        g = wl.grads(t) if grad_fn is None else grad_fn(t, w)
+        e_before = err.copy()
+        us = np.stack([orc.precompress(w, w_prev, g[k], err[k]) for k in range(wl.K)])
+        idx, val, ln = orc.step(w, w_prev, g, err)
+        delta = orc.aggregate(idx, val, ln)
+        w_next = w.copy()
+        orc.apply(w_next, delta)
+        recs.append(dict(w_prev=w_prev, w=w, w_next=w_next, g=g, e=e_before, e_next=err.copy(),
+                         u=us, idx=idx, val=val, ln=ln, delta=delta))
+        w_prev, w = w, w_next
+    return recs
+
+
+# ---------------------------------------------------------------------------
+# counts and constants
+# ---------------------------------------------------------------------------
+
+def pin_count_rule(lib):
+    # s = d/1024 (Section 5.1) is exact for a power-of-two ratio
+    for d in (1024, 1 << 20, 25557032):
+        assert oracle.count(d, 1 / 1024, lib) == math.ceil(d / 1024)
+    # the workloads' stated per-worker counts
+    assert oracle.count(1 << 20, 0.01, lib) == 10486
+    assert oracle.count(25557032, 0.001, lib) == 25558
+    assert oracle.count(11173962, 0.01, lib) == 111740
+    assert oracle.count(6240, 0.01, lib) == 63
+    # clamps: at least one, at most all
+    assert oracle.count(768, 0.001, lib) == 1
+    assert oracle.count(5, 1.0, lib) == 5
+    assert oracle.count(1, 1e-9, lib) == 1
+
+
+def pin_constants(lib):
+    c, s = oracle.constants(0.9, 0.1, 16, lib)
+    assert c == np.float32(9.0)
+    assert s == np.float32(0.1 / 16)
+    c, s = oracle.constants(0.9, 0.05, 8, lib)
+    assert c == np.float32(18.0) and s == np.float32(0.05 / 8)
+
+
+# ---------------------------------------------------------------------------
+# top-s against brute force, delta-approximation, error feedback
+# ---------------------------------------------------------------------------
+
+def _adversarial_vectors():
+    rng = np.random.default_rng(1234)
+    vecs = []
+    vecs.append(rng.standard_normal(1000).astype(np.float32))
+    vecs.append(rng.choice(np.array([0, 1, -1, 2, -2], np.float32), 777))          # heavy ties
+    z = rng.choice(np.array([0.0, -0.0, 1e-45, -1e-45, 3e-40, 1.0], np.float32), 300)
+    vecs.append(z)                                                                  # +-0, denormals
+    x = rng.standard_normal(200).astype(np.float32)
+    x[[3, 50, 51]] = [np.inf, -np.inf, np.nan]
+    vecs.append(x)                                                                  # non-finite
+    vecs.append(np.full(129, -3.5, np.float32))                                     # all equal
+    return vecs
+
+
+def pin_topk_bruteforce(lib):
+    for u in _adversarial_vectors():
+        n = u.size
+        for k in sorted({1, 2, 7, n // 3, n - 1, n}):
+            if k < 1:
+                continue
+            got = oracle.topk(u, k, lib)
+            want = brute_topk(u, k)
+            assert np.array_equal(got, want), (n, k)
+
+
+def pin_delta_approximation(lib):
+    """Assumption 1: top-k is a delta-approximate compressor with
+    delta = k/n: ||C(u) - u||^2 <= (1 - k/n) ||u||^2 for every u."""
+    rng = np.random.default_rng(7)
+    for n, k in [(1000, 10), (4096, 41), (333, 333), (500, 1)]:
+        u = (rng.standard_t(3, n) * rng.uniform(0.1, 10)).astype(np.float32)
+        u0 = u.copy()
+        idx, val = oracle.compress_topk(u, [0, n], k / n, lib)
+        assert idx.size == k
+        lhs = float(np.sum(u.astype(np.float64) ** 2))        # ||u - C(u)||^2: the residual
+        rhs = (1 - k / n) * float(np.sum(u0.astype(np.float64) ** 2))
+        assert lhs <= rhs * (1 + 1e-12) + 1e-300
+
+
+def pin_error_feedback_identity(lib):
+    """e_{t+1} = u - C(u): the kept components are sent unchanged and leave
+    u - u = +0 behind; every other component keeps u bit for bit."""
+    rng = np.random.default_rng(11)
+    for u0 in [rng.standard_normal(5000).astype(np.float32)] + _adversarial_vectors()[:3]:
+        n = u0.size
+        seg = [0, n // 3, n // 3 + 1, n] if n > 10 else [0, n]
+        u = u0.copy()
+        idx, val = oracle.compress_topk(u, seg, 0.05, lib)
+        assert np.all(np.diff(idx) > 0)
+        assert np.array_equal(_bits(val), _bits(u0[idx]))
+        assert np.all(_bits(u[idx]) == 0)
+        mask = np.ones(n, bool)
+        mask[idx] = False
+        assert np.array_equal(_bits(u[mask]), _bits(u0[mask]))
+        # per segment the kept set is that segment's own top-k
+        for a, b in zip(seg[:-1], seg[1:]):
+            sel = idx[(idx >= a) & (idx < b)] - a
+            k = oracle.count(b - a, 0.05, lib)
+            assert np.array_equal(sel, brute_topk(u0[a:b], k))
+
+
+# ---------------------------------------------------------------------------
+# multi-step closed forms (Section 2.3, eq. 8, Lemma 1)
+# ---------------------------------------------------------------------------
+
+def pin_msgd_reduction(lib):
+    """Without compression (s = d) GMC is serial momentum SGD on the average
+    gradient: m_{t+1} = beta m_t + eta gbar_t, w_{t+1} = w_t - m_{t+1}
+    (Section 2.3), and the residual stays zero."""
+    for K in (1, 4):
+        wl = synth.Workload("msgd", [3000, 17], K=K, ratio=1.0, beta=0.9, eta=0.1, steps=25,
+                            compressor="topk", dist="normal")
+        recs = _run(lib, wl, 1.0, wl.steps)
+        m = np.zeros(wl.d)
+        w = recs[0]["w"].astype(np.float64)
+        for r in recs:
+            gbar = r["g"].astype(np.float64).mean(axis=0)
+            m = wl.beta * m + wl.eta * gbar
+            w = w - m
+            assert np.all(_bits(r["e_next"]) == 0)
+            got = r["w_next"].astype(np.float64)
+            assert np.max(np.abs(got - w)) <= 2e-5 * (1 + np.max(np.abs(w))), K
+
+
+def _eq8_terms(r, wl):
+    f = lambda a: np.asarray(a, np.float64)
+    gbar = f(r["g"]).mean(0)
+    ebar, ebar1 = f(r["e"]).mean(0), f(r["e_next"]).mean(0)
+    return gbar, ebar, ebar1
+
+
+def pin_update_rule_eq8(lib):
+    """eq. 8: w_{t+1} = w_t - eta gbar_t - eta ebar_t + eta ebar_{t+1}
+    + beta (w_t - w_{t-1}), for any compressor; checked within the
+    binary32 rounding bound of the operations involved."""
+    wl = synth.Workload("eq8", [2500, 1500, 96], K=4, ratio=0.02, beta=0.9, eta=0.1, steps=12,
+                        compressor="topk", dist="normal", scale_lo=1e-2, scale_hi=1.0)
+    for r in _run(lib, wl, wl.ratio, wl.steps):
+        f = lambda a: np.asarray(a, np.float64)
+        gbar, ebar, ebar1 = _eq8_terms(r, wl)
+        w, wp, wn = f(r["w"]), f(r["w_prev"]), f(r["w_next"])
+        rhs = w - wl.eta * gbar - wl.eta * ebar + wl.eta * ebar1 + wl.beta * (w - wp)
+        scale = (np.abs(w) + np.abs(wn) + wl.beta * np.abs(w - wp)
+                 + wl.eta * (np.abs(f(r["g"])).mean(0) + np.abs(f(r["e"])).mean(0)
+                             + wl.K * np.abs(f(r["u"])).mean(0)))
+        assert np.all(np.abs(wn - rhs) <= 16 * EPS32 * scale + 1e-30)
+
+
+def pin_lemma1(lib):
+    """Lemma 1: z_t = w_t + beta/(1-beta)(w_t - w_{t-1}) - eta/(1-beta) ebar_t
+    satisfies z_{t+1} = z_t - eta/(1-beta) gbar_t."""
+    wl = synth.Workload("lemma1", [4000, 95], K=3, ratio=0.05, beta=0.9, eta=0.1, steps=10,
+                        compressor="topk", dist="student_t", nu=3, scale_lo=1e-3, scale_hi=1.0)
+    recs = _run(lib, wl, wl.ratio, wl.steps)
+    b, eta = wl.beta, wl.eta
+    f = lambda a: np.asarray(a, np.float64)
+    for r in recs:
+        gbar, ebar, ebar1 = _eq8_terms(r, wl)
+        w, wp, wn = f(r["w"]), f(r["w_prev"]), f(r["w_next"])
+        z = w + b / (1 - b) * (w - wp) - eta / (1 - b) * ebar
+        z1 = wn + b / (1 - b) * (wn - w) - eta / (1 - b) * ebar1
+        scale = (np.abs(w) + np.abs(wn) + np.abs(wp)
+                 + eta * (np.abs(f(r["g"])).mean(0) + np.abs(f(r["e"])).mean(0)
+                          + wl.K * np.abs(f(r["u"])).mean(0)))
+        assert np.all(np.abs(z1 - (z - eta / (1 - b) * gbar)) <= 64 / (1 - b) * EPS32 * scale + 1e-30)
+
+
+# ---------------------------------------------------------------------------
+# aggregation and apply
+# ---------------------------------------------------------------------------
+
+def pin_aggregate_single_worker(lib):
+    """K = 1: delta = -(eta) C(u): -(s*v) at the sent indices, -0 elsewhere,
+    bit for bit, and w + delta = w - s*C(u)."""
+    rng = np.random.default_rng(5)
+    d = 1000
+    idx = np.sort(rng.choice(d, 37, replace=False)).astype(np.int32)
+    val = rng.standard_normal(37).astype(np.float32)
+    s = np.float32(0.1)
+    delta = oracle.aggregate(d, s, [idx], [val], lib)
+    want = np.full(d, -0.0, np.float32)
+    want[idx] = -(s * val)
+    assert np.array_equal(_bits(delta), _bits(want))
+    w = rng.standard_normal(d).astype(np.float32)
+    w1 = w.copy()
+    oracle.apply(w1, delta, lib)
+    c = np.zeros(d, np.float32)
+    c[idx] = val
+    assert np.array_equal(_bits(w1), _bits(w - s * c))
+
+
+def pin_aggregate_sum(lib):
+    """The server's sum over workers is the plain sum of the sparse vectors:
+    checked against an fp64 sum within K rounding errors, and on integer
+    values (exact in binary32) bit for bit."""
+    rng = np.random.default_rng(6)
+    d, K = 5000, 6
+    idx = [np.sort(rng.choice(d, 400, replace=False)).astype(np.int32) for _ in range(K)]
+    val = [rng.integers(-50, 50, 400).astype(np.float32) for _ in range(K)]
+    s = np.float32(0.25)
+    delta = oracle.aggregate(d, s, idx, val, lib)
+    dense = np.zeros((K, d))
+    for k in range(K):
+        dense[k, idx[k]] = val[k]
+    want = -(0.25 * dense.sum(0))
+    assert np.array_equal(delta.astype(np.float64), want)
+    val = [rng.standard_normal(400).astype(np.float32) for _ in range(K)]
+    delta = oracle.aggregate(d, np.float32(0.1 / K), idx, val, lib)
+    for k in range(K):
+        dense[k] = 0
+        dense[k, idx[k]] = val[k]
+    want = -(np.float32(0.1 / K) * dense.sum(0))
+    bound = (K + 1) * EPS32 * (0.1 / K) * np.abs(dense).sum(0)
+    assert np.all(np.abs(delta - want) <= bound + 1e-30)
+
+
+# ---------------------------------------------------------------------------
+# RBGS
+# ---------------------------------------------------------------------------
+
+def pin_splitmix64_vectors(lib):
+    with open(os.path.join(GOLDEN, "splitmix64_seed0.txt")) as f:
+        want = [int(ln, 16) for ln in f.read().splitlines() if ln.startswith("0x")]
+    gamma = 0x9E3779B97F4A7C15
+    got = [oracle.splitmix64_mix((i * gamma) % (1 << 64), lib) for i in range(1, len(want) + 1)]
+    assert got == want
+
+
+def pin_rbgs_blocks(lib):
+    for nb, n_sel in [(6240, 63), (10, 10), (7, 1), (1000, 999)]:
+        for t in range(6):
+            b = oracle.rbgs_blocks(42, t, nb, n_sel, lib)
+            assert b.size == n_sel
+            assert np.all(np.diff(b) > 0) and b[0] >= 0 and b[-1] < nb
+            assert np.array_equal(b, oracle.rbgs_blocks(42, t, nb, n_sel, lib))
+    a = [tuple(oracle.rbgs_blocks(1, t, 6240, 63, lib)) for t in range(20)]
+    assert len(set(a)) == 20
+    # uniform over subsets: every 3-subset of 8 blocks equally likely
+    from scipy.stats import chisquare
+    T = 28000
+    counts = {c: 0 for c in itertools.combinations(range(8), 3)}
+    for t in range(T):
+        counts[tuple(int(x) for x in oracle.rbgs_blocks(9, t, 8, 3, lib))] += 1
+    obs = np.array(list(counts.values()), dtype=float)
+    assert chisquare(obs).pvalue > 1e-4
+
+
+def pin_rbgs_step_and_cost(lib):
+    """GMC with RBGS: the blocks are the same on every worker, so the
+    aggregated update is nonzero exactly on those m components, and the
+    relative communication cost (values only, Section 5.2) is m/d."""
+    d, K, B = 50000, 3, 4096
+    orc = oracle.GmcOracle(d, K, "rbgs", 0.1, 0.9, 0.1, seed=3, block=B, lib=lib)
+    rng = np.random.default_rng(2)
+    w = rng.standard_normal(d).astype(np.float32)
+    wp = w.copy()
+    err = np.zeros((K, d), np.float32)
+    for t in range(4):
+        g = rng.standard_normal((K, d)).astype(np.float32)
+        us = [orc.precompress(w, wp, g[k], err[k]) for k in range(K)]
+        idx, val, ln = orc.step(w, wp, g, err)
+        blocks = oracle.rbgs_blocks(3, t, orc.nb, orc.n_sel, lib)
+        assert all(np.array_equal(idx[k], blocks) for k in range(K))
+        ei = orc.element_indices(idx[0], int(ln[0]))
+        m = sum(min((b + 1) * B, d) - b * B for b in blocks)
+        assert np.all(ln == m) and ei.size == m
+        for k in range(K):
+            assert np.array_equal(_bits(val[k, :m]), _bits(us[k][ei]))
+            assert np.all(_bits(err[k][ei]) == 0)
+            rest = np.ones(d, bool)
+            rest[ei] = False
+            assert np.array_equal(_bits(err[k][rest]), _bits(us[k][rest]))
+        delta = orc.aggregate(idx, val, ln)
+        nnz = int(np.count_nonzero(delta))
+        assert nnz == m
+        rcc = (K * nnz + int(ln.sum())) / (2 * d * K)
+        assert abs(rcc - m / d) < 1e-15
+        w_next = w.copy()
+        orc.apply(w_next, delta)
+        wp, w = w, w_next
+
+
+# ---------------------------------------------------------------------------
+# the toy quadratic of Section 3.2
+# ---------------------------------------------------------------------------
+
+def _toy_grads(d):
+    i = np.arange(d, dtype=np.float32)
+    coef = np.float32(2.0) * (np.float32(d) - i)
+    shift = i + np.float32(1.0)
+
+    def fn(t, w):
+        return np.stack([coef * (w - shift), coef * (w + shift)]).astype(np.float32)
+    return fn
+
+
+def pin_toy_quadratic_closed_form(lib):
+    """F(w) = sum_i (d-i)(w_i^2 + (i+1)^2) with K = 2 workers holding
+    F_0, F_1.  With s = d GMC is momentum SGD on F, whose iterates solve
+    w_{t+1} = (1 + beta - 2 eta (d-i)) w_t - beta w_{t-1}, w_{-1} = w_0."""
+    beta, eta = 0.9, 0.005
+    for d, w0 in [(2, [-1.0, 2.0]), (20, list(np.linspace(-3, 3, 20)))]:
+        wl = synth.Workload("toy", [d], K=2, ratio=1.0, beta=beta, eta=eta, steps=300,
+                            compressor="topk", dist="normal")
+        recs = _run(lib, wl, 1.0, wl.steps, grad_fn=_toy_grads(d), w0=w0)
+        w0 = np.asarray(w0, np.float64)
+        a = 2 * eta * (d - np.arange(d))
+        tr = 1 + beta - a
+        disc = np.sqrt((tr ** 2 - 4 * beta).astype(complex))
+        l1, l2 = (tr + disc) / 2, (tr - disc) / 2
+        w1 = (1 - a) * w0
+        B_ = (w1 - l1 * w0) / (l2 - l1)
+        A_ = w0 - B_
+        for t, r in enumerate(recs, start=1):
+            want = np.real(A_ * l1 ** t + B_ * l2 ** t)
+            got = r["w_next"].astype(np.float64)
+            assert np.max(np.abs(got - want)) <= 1e-4 * (1 + np.max(np.abs(w0))), (d, t)
+
+
+def pin_toy_quadratic_sparse_converges(lib):
+    """Section 3.2: with top-s sparsification GMC still approaches the
+    optimum w* = 0 from (-1, 2) (d = 2, s = d/2)."""
+    d = 2
+    wl = synth.Workload("toy", [d], K=2, ratio=0.5, beta=0.9, eta=0.005, steps=3000,
+                        compressor="topk", dist="normal")
+    recs = _run(lib, wl, 0.5, wl.steps, grad_fn=_toy_grads(d), w0=[-1.0, 2.0])
+    dist = [float(np.linalg.norm(r["w_next"])) for r in recs]
+    assert dist[-1] < 0.1 * math.sqrt(5.0)
+    assert max(dist[-200:]) < 0.2 * math.sqrt(5.0)
+
+
+ALL_PINS = [pin_count_rule, pin_constants, pin_topk_bruteforce, pin_delta_approximation,
+            pin_error_feedback_identity, pin_msgd_reduction, pin_update_rule_eq8, pin_lemma1,
+            pin_aggregate_single_worker, pin_aggregate_sum, pin_splitmix64_vectors,
+            pin_rbgs_blocks, pin_rbgs_step_and_cost, pin_toy_quadratic_closed_form,
+            pin_toy_quadratic_sparse_converges]

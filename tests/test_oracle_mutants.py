@@ -1,0 +1,63 @@
+"""Plants plausible mistakes in copies of the oracle (CPU only) and checks
+that the pins catch every one: a dropped term, a wrong sign, a swapped
+operand, a wrong index, a reversed order.  The oracle source itself is never
+changed; each mutant is a text substitution compiled into a temporary
+library."""
+import os
+import tempfile
+
+import pytest
+
+import oracle
+from oracle_pins import ALL_PINS
+
+MUTANTS = {
+    "momentum_sign": ("u[j] = acc - mom;", "u[j] = acc + mom;"),
+    "momentum_dropped": ("u[j] = acc - mom;", "u[j] = acc;"),
+    "diff_swapped": ("float diff = w_t[j] - w_prev[j];", "float diff = w_prev[j] - w_t[j];"),
+    "error_feedback_dropped": ("float acc = e[j] + g[j];", "float acc = g[j];"),
+    "gradient_dropped": ("float acc = e[j] + g[j];", "float acc = e[j];"),
+    "momentum_coeff_beta": ("*c = (float)(beta / eta);", "*c = (float)beta;"),
+    "server_scale_dropped": ("delta[j] = -(s * acc[j]);", "delta[j] = -acc[j];"),
+    "server_sign": ("delta[j] = -(s * acc[j]);", "delta[j] = s * acc[j];"),
+    "server_scale_no_K": ("*s = (float)(eta / (double)K);", "*s = (float)eta;"),
+    "server_worker_index": ("acc[idx[k][i]] = acc[idx[k][i]] + val[k][i];",
+                            "acc[idx[k][i]] = acc[idx[k][i]] + val[0][i];"),
+    "residual_not_cleared": ("u[idx[i]] = u[idx[i]] - sent;", "u[idx[i]] = u[idx[i]];"),
+    "topk_smallest": ("if (x->key != y->key) return x->key > y->key ? -1 : 1;",
+                      "if (x->key != y->key) return x->key < y->key ? -1 : 1;"),
+    "topk_tie_high_index": ("if (x->pos != y->pos) return x->pos < y->pos ? -1 : 1;",
+                            "if (x->pos != y->pos) return x->pos > y->pos ? -1 : 1;"),
+    "topk_signed_key": ("return b & 0x7fffffffu;", "return b;"),
+    "count_floor": ("int64_t k = (int64_t)ceil(x);", "int64_t k = (int64_t)floor(x);"),
+    "apply_sign": ("w[j] = w[j] + delta[j];", "w[j] = w[j] - delta[j];"),
+    "floyd_no_dedup": ("blocks[have++] = dup ? (int32_t)J : r;", "blocks[have++] = r;"),
+    "rbgs_short_block": ("int64_t lo = (int64_t)blocks[q] * B, hi = lo + B;",
+                         "int64_t lo = (int64_t)blocks[q] * B, hi = lo + B - 1;"),
+    "splitmix_shift": ("z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;",
+                       "z = (z ^ (z >> 28)) * 0x94d049bb133111ebULL;"),
+}
+
+
+@pytest.fixture(scope="module")
+def source():
+    with open(os.path.join(os.path.dirname(oracle.__file__), "gmc_oracle.c")) as f:
+        return f.read()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name, source):
+    old, new = MUTANTS[name]
+    assert source.count(old) == 1, "mutation anchor not found: " + old
+    with tempfile.TemporaryDirectory() as tmp:
+        src = os.path.join(tmp, "m.c")
+        with open(src, "w") as f:
+            f.write(source.replace(old, new))
+        lib = oracle.load(oracle.build(force=True, src=src, out=os.path.join(tmp, "m.so")))
+        caught = []
+        for pin in ALL_PINS:
+            try:
+                pin(lib)
+            except (AssertionError, ValueError, IndexError, KeyError):
+                caught.append(pin.__name__)
+        assert caught, "no pin caught mutant " + name
