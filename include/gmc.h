@@ -1,0 +1,202 @@
+/*
+ * gmc.h -- C ABI of the MI355X (gfx950) library for the data-parallel hot
+ * path of Global Momentum Compression (GMC, Algorithm 1; its RBGS variant as
+ * used by GMC+, Algorithm 2).
+ *
+ * One call sequence is one iteration t of Algorithm 1 for K workers that
+ * live on one GPU as K device-resident vectors:
+ *
+ *   gmc_step       each worker k forms u_k = e_{t,k} + g_{t,k}
+ *                  - (beta/eta)(w_t - w_{t-1}), compresses it (top-s or RBGS)
+ *                  into a sparse message C(u_k), and keeps the residual
+ *                  e_{t+1,k} = u_k - C(u_k)                 (Algorithm 1, workers)
+ *   gmc_aggregate  the server's update w_{t+1} - w_t = -(eta/K) sum_k C(u_k),
+ *                  materialised as a dense vector          (Algorithm 1, server)
+ *   gmc_apply      w_{t+1} = w_t + (w_{t+1} - w_t)          (Algorithm 1, workers)
+ *
+ * Conventions shared by every entry point:
+ *   - Arguments named *_dev are device pointers to memory the caller owns
+ *     (e.g. PyTorch tensors).  The context owns only its scratch memory.
+ *   - All device work is enqueued on the context's stream (gmc_set_stream;
+ *     default: the null stream) and is asynchronous: outputs are valid once
+ *     that stream has been synchronised.  Host arrays passed in are read
+ *     before the call returns.
+ *   - Arithmetic is IEEE binary32 with one rounding per operation and no
+ *     fused multiply-add contraction; denormals are kept.  c = fl32(beta/eta)
+ *     and s = fl32(eta/K) are formed in binary64 and rounded once.
+ *     u = fl(fl(e + g) - fl(c * fl(w_t - w_prev))).  The server sums the K
+ *     messages in worker order 0..K-1 starting from +0.0f and writes
+ *     update = -(s * sum); components no worker sent get -(s * +0) = -0.0f,
+ *     so w + update equals w - s * sum bit for bit everywhere.
+ *   - top-s keeps, per segment of n components, k = min(n, max(1,
+ *     ceil(ratio * n))) components (the product in binary64), ranked by the
+ *     magnitude bits bits(u) & 0x7FFFFFFF (NaN above Inf, -0 equal to +0),
+ *     ties broken towards the lower index.  A kept component leaves
+ *     u - u behind in the residual (+0.0f for finite u).
+ *   - RBGS keeps whole blocks: block b covers [b*B, min((b+1)*B, d)); n_sel =
+ *     min(nb, max(1, ceil(ratio * nb))) of the nb = ceil(d/B) blocks are
+ *     drawn by Floyd's sampling algorithm from a SplitMix64 stream whose state
+ *     starts at seed XOR mix64(t + 1); every worker uses the same blocks
+ *     (Section 4: same random seed on all workers), so only values travel.
+ *   - Indices are int32: d must be below 2^31.
+ *   - Every call returns a gmc_status; on failure gmc_last_error() describes
+ *     the cause.  Invalid arguments never reach the device.
+ *   - A context is not thread safe; calls on one context must not overlap.
+ */
+#ifndef GMC_H
+#define GMC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct gmc_ctx gmc_ctx;
+
+typedef enum {
+    GMC_TOPK_GLOBAL = 0,    /* top-s over the whole vector (one segment)          */
+    GMC_TOPK_SEGMENTED = 1, /* top-s per segment (per tensor), see gmc_set_segments */
+    GMC_RBGS = 2            /* random blocks shared by all workers                */
+} gmc_compressor;
+
+typedef enum {
+    GMC_OK = 0,
+    GMC_EINVAL = -1,  /* an argument is out of range, NULL or misaligned      */
+    GMC_ENOMEM = -2,  /* device or host allocation failed                      */
+    GMC_EDEVICE = -3, /* a HIP runtime call failed                             */
+    GMC_ESTATE = -4   /* call out of order (e.g. configuration after a step)   */
+} gmc_status;
+
+#define GMC_MAX_WORKERS 64
+
+/*
+ * Create a context for d parameters and K workers (Algorithm 1, "Input":
+ * compressor, K, w_0 is the caller's, eta, beta).
+ *   d      1 <= d < 2^31
+ *   K      1 <= K <= GMC_MAX_WORKERS
+ *   compressor  a gmc_compressor value
+ *   ratio  (0, 1]: fraction kept per segment (top-s) or of blocks (RBGS)
+ *   beta   momentum coefficient, [0, 1)
+ *   eta    learning rate, > 0 and finite
+ *   seed   RBGS seed (ignored by top-s)
+ * The step counter t starts at 0 (w_{-1} = w_0 and e_{0,k} = 0 are the
+ * caller's initial buffers).  Allocates the context's scratch on the current
+ * HIP device.  *out is set to NULL on failure.
+ */
+gmc_status gmc_init(gmc_ctx** out, int64_t d, int32_t K, int32_t compressor, double ratio,
+                    double beta, double eta, uint64_t seed);
+
+/*
+ * GMC_TOPK_SEGMENTED only: set the segments (tensors) top-s works on.
+ * seg_off is a host array of n_seg+1 strictly increasing offsets, seg_off[0]
+ * = 0, seg_off[n_seg] = d.  Before the first step only (GMC_ESTATE after).
+ * Default: one segment [0, d).
+ */
+gmc_status gmc_set_segments(gmc_ctx* ctx, int32_t n_seg, const int64_t* seg_off);
+
+/* GMC_RBGS only: block length B (1 <= B <= d, multiple of 4 for the vector
+ * path; any B is accepted).  Before the first step only.  Default 4096. */
+gmc_status gmc_set_block(gmc_ctx* ctx, int32_t block);
+
+/* Stream all later calls enqueue on (a hipStream_t; NULL = null stream). */
+gmc_status gmc_set_stream(gmc_ctx* ctx, void* hip_stream);
+
+/* Per-worker message capacity the caller must provide, in elements:
+ * top-s: k_tot = sum over segments of k; RBGS: n_sel * B. */
+int64_t gmc_message_len(const gmc_ctx* ctx);
+
+/* Per-worker index capacity: top-s: k_tot (element indices);
+ * RBGS: n_sel (block ids). */
+int64_t gmc_index_len(const gmc_ctx* ctx);
+
+/*
+ * One worker-side pass of Algorithm 1 for all K workers at step t, then
+ * t <- t + 1.
+ *   w_t_dev, w_prev_dev   [d] fp32: w_t and w_{t-1}; read only
+ *   grads_dev             host array of K device pointers, each [d] fp32:
+ *                         g_{t,k}; read only
+ *   err_dev               host array of K device pointers, each [d] fp32:
+ *                         e_{t,k} in, e_{t+1,k} = u - C(u) out (in place)
+ *   idx_dev               [K][gmc_index_len] int32 out: top-s: ascending
+ *                         element indices, segment after segment; RBGS:
+ *                         ascending block ids, the same row for every worker
+ *   val_dev               [K][gmc_message_len] fp32 out: u_k at the kept
+ *                         components, in idx order (RBGS: block after block)
+ *   msg_len_dev           [K] int64 out: values written per worker
+ * Device buffers must not overlap each other.  Pointers that are not 16-byte
+ * aligned are accepted (slower path).  w is never written.
+ */
+gmc_status gmc_step(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev,
+                    const float* const* grads_dev, float* const* err_dev,
+                    int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev);
+
+/*
+ * The server's update (Algorithm 1, server): update_dev[j] =
+ * -(s * sum_k val_k(j)) over the workers whose message holds j, in worker
+ * order; -0.0f where no worker sent j.  idx/val/msg_len are K messages in the
+ * layout gmc_step writes (top-s rows must be strictly ascending and in
+ * [0, d); RBGS rows are the block ids of the last gmc_step).
+ *   update_dev  [d] fp32 out, dense
+ */
+gmc_status gmc_aggregate(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev,
+                         const int64_t* msg_len_dev, float* update_dev);
+
+/*
+ * Workers' apply (Algorithm 1): w_prev_out_dev[j] = w_dev[j] (when not NULL),
+ * then w_dev[j] = w_dev[j] + update_dev[j], for every j in [0, d).
+ *   w_dev           [d] fp32 in/out
+ *   w_prev_out_dev  [d] fp32 out or NULL; may not alias w_dev
+ *   update_dev      [d] fp32 in
+ */
+gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const float* update_dev);
+
+/* Step counter t (RBGS draws depend on (seed, t)); for checkpoint/resume. */
+gmc_status gmc_get_step(const gmc_ctx* ctx, int64_t* t);
+gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
+
+/*
+ * Tuning and test options (value semantics per option):
+ *   GMC_OPT_FORCE_FULL_SELECT  1: every top-s selection takes the full-data
+ *                              path (no speculative candidates)
+ *   GMC_OPT_CAND_MARGIN        candidate target as a multiple of k (>= 1)
+ *   GMC_OPT_CAND_CAP_MULT      candidate capacity as a multiple of k (>= 1);
+ *                              reallocates scratch; before the first step
+ *   GMC_OPT_PROFILE            1: time the stage kernels with HIP events
+ */
+enum {
+    GMC_OPT_FORCE_FULL_SELECT = 1,
+    GMC_OPT_CAND_MARGIN = 2,
+    GMC_OPT_CAND_CAP_MULT = 3,
+    GMC_OPT_PROFILE = 4
+};
+gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value);
+
+/*
+ * Diagnostics, synchronising the context's stream first.  Writes up to n of:
+ *   [0] steps taken  [1] top-s segment selections resolved from candidates
+ *   [2] selections that took the full-data path  [3] candidates collected
+ *   [4] selections whose count check failed (must stay 0)
+ */
+gmc_status gmc_stats(gmc_ctx* ctx, int64_t* out, int32_t n);
+
+/*
+ * Stage timings when GMC_OPT_PROFILE is on: for each stage i < n, total
+ * milliseconds and launch count since the option was set.  Stage order:
+ * 0 fused worker pass, 1 selection, 2 emit, 3 aggregate, 4 apply.
+ * Synchronises the context's stream.
+ */
+gmc_status gmc_profile_read(gmc_ctx* ctx, double* ms, int64_t* launches, int32_t n);
+
+/* Message for the last non-OK status of this context (or of gmc_init when
+ * ctx is NULL); never NULL. */
+const char* gmc_last_error(const gmc_ctx* ctx);
+
+/* Free the context and its scratch (synchronises its stream).  NULL is a no-op. */
+void gmc_destroy(gmc_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GMC_H */

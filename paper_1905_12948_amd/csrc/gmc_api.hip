@@ -1,0 +1,598 @@
+// C ABI of the GMC device library (declared in include/gmc.h): argument
+// checks, the context and its device scratch, and the launch order of one
+// iteration of Algorithm 1.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/gmc.h"
+#include "gmc_internal.h"
+
+using namespace gmc;
+
+namespace {
+
+constexpr int kStages = 5;  // fused pass, selection, emit, aggregate, apply
+constexpr int64_t kMaxPendingEvents = 4096;
+
+thread_local std::string g_init_error = "no error";
+
+}  // namespace
+
+struct gmc_ctx {
+    // problem
+    int64_t d = 0;
+    int32_t K = 0;
+    int32_t comp = 0;
+    double ratio = 0, beta = 0, eta = 0;
+    uint64_t seed = 0;
+    float c = 0, s = 0;
+    int64_t t = 0;
+    hipStream_t stream = nullptr;
+    int device = 0;
+    bool started = false;
+    std::string err = "no error";
+
+    // configuration
+    std::vector<int64_t> seg_off;  // top-s segments (host)
+    int32_t block = 4096;          // RBGS block length
+    int force_full = 0;
+    int margin = 4;
+    int cap_mult = 16;
+
+    // derived
+    std::vector<int32_t> seg_k;
+    int64_t k_tot = 0;
+    int32_t nb = 0, n_sel = 0;
+
+    // device scratch (one allocation, carved)
+    bool prepared = false;
+    void* mem = nullptr;
+    size_t mem_bytes = 0;
+    TopkGeometry geo{};
+    TopkScratch scr{};
+    int32_t* rowptr = nullptr;
+    int32_t n_ranges = 0;
+    int32_t* gen_list = nullptr;   // chunks the vector pass cannot take
+    int32_t n_gen = 0;
+    uint32_t* rbgs_bitmap = nullptr;
+    int32_t* rbgs_blocks = nullptr;
+    int32_t* rbgs_slot = nullptr;
+    int64_t* stats = nullptr;
+
+    // profiling
+    bool profile = false;
+    double prof_ms[kStages] = {0};
+    int64_t prof_n[kStages] = {0};
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> pending[kStages];
+};
+
+namespace {
+
+gmc_status fail(gmc_ctx* ctx, gmc_status st, const std::string& msg) {
+    if (ctx) ctx->err = msg; else g_init_error = msg;
+    return st;
+}
+
+gmc_status hip_fail(gmc_ctx* ctx, hipError_t e, const char* what) {
+    std::string m = std::string(what) + ": " + hipGetErrorString(e);
+    return fail(ctx, GMC_EDEVICE, m);
+}
+
+#define GMC_HIP(ctx, call)                                  \
+    do {                                                    \
+        hipError_t e_ = (call);                             \
+        if (e_ != hipSuccess) return hip_fail(ctx, e_, #call); \
+    } while (0)
+
+int64_t count_for(int64_t n, double ratio) {
+    const double x = ratio * (double)n;
+    int64_t k = (int64_t)std::ceil(x);
+    if (k < 1) k = 1;
+    if (k > n) k = n;
+    return k;
+}
+
+void release(gmc_ctx* ctx) {
+    if (ctx->mem) {
+        (void)hipSetDevice(ctx->device);
+        (void)hipDeviceSynchronize();
+        (void)hipFree(ctx->mem);
+    }
+    ctx->mem = nullptr;
+    ctx->mem_bytes = 0;
+    ctx->prepared = false;
+}
+
+struct Carver {
+    char* base;
+    size_t off = 0;
+    template <class T>
+    T* take(size_t n) {
+        off = (off + 255) & ~(size_t)255;
+        T* p = reinterpret_cast<T*>(base + off);
+        off += n * sizeof(T);
+        return p;
+    }
+};
+
+// Host-side tables of the top-s geometry.
+struct TopkTables {
+    std::vector<int32_t> chunk_start, chunk_len, chunk_seg;
+    std::vector<int32_t> item_seg, item_lo, item_hi, item_rank;
+    std::vector<int32_t> seg_items, seg_item_lo, seg_out;
+    std::vector<int32_t> pair_k, pair_cap;
+    std::vector<int64_t> pair_cand;
+    std::vector<int32_t> gen_list;  // partial chunks and chunks with an unaligned start
+    int64_t cand_total = 0;
+};
+
+TopkTables build_tables(const gmc_ctx* ctx) {
+    TopkTables T;
+    const int n_seg = (int)ctx->seg_off.size() - 1;
+    int64_t out = 0;
+    for (int sg = 0; sg < n_seg; ++sg) {
+        const int64_t lo = ctx->seg_off[sg], hi = ctx->seg_off[sg + 1];
+        const int32_t first_chunk = (int32_t)T.chunk_start.size();
+        for (int64_t a = lo; a < hi; a += kChunk) {
+            const int32_t len = (int32_t)std::min<int64_t>(kChunk, hi - a);
+            if ((a & 3) != 0 || len != kChunk) T.gen_list.push_back((int32_t)T.chunk_start.size());
+            T.chunk_start.push_back((int32_t)a);
+            T.chunk_len.push_back(len);
+            T.chunk_seg.push_back(sg);
+        }
+        const int32_t last_chunk = (int32_t)T.chunk_start.size();
+        T.seg_item_lo.push_back((int32_t)T.item_seg.size());
+        int32_t rank = 0;
+        for (int32_t c = first_chunk; c < last_chunk; c += kItemChunks) {
+            T.item_seg.push_back(sg);
+            T.item_lo.push_back(c);
+            T.item_hi.push_back(std::min(c + kItemChunks, last_chunk));
+            T.item_rank.push_back(rank++);
+        }
+        T.seg_items.push_back(rank);
+        T.seg_out.push_back((int32_t)out);
+        out += ctx->seg_k[sg];
+    }
+    for (int k = 0; k < ctx->K; ++k) {
+        for (int sg = 0; sg < n_seg; ++sg) {
+            const int64_t n = ctx->seg_off[sg + 1] - ctx->seg_off[sg];
+            const int64_t kk = ctx->seg_k[sg];
+            const int64_t cap = std::min<int64_t>(n, (int64_t)ctx->cap_mult * kk + 2048);
+            T.pair_k.push_back((int32_t)kk);
+            T.pair_cap.push_back((int32_t)cap);
+            T.pair_cand.push_back(T.cand_total);
+            T.cand_total += cap;
+        }
+    }
+    return T;
+}
+
+gmc_status prepare(gmc_ctx* ctx) {
+    if (ctx->prepared) return GMC_OK;
+    release(ctx);
+    GMC_HIP(ctx, hipSetDevice(ctx->device));
+    const int32_t K = ctx->K;
+    const int64_t d = ctx->d;
+    ctx->n_ranges = (int32_t)((d + kAggRange - 1) / kAggRange);
+
+    TopkTables T;
+    size_t bytes = 0;
+    auto add = [&](size_t n, size_t sz) { bytes = ((bytes + 255) & ~(size_t)255) + n * sz; };
+    add(8, sizeof(int64_t));  // stats
+    if (ctx->comp == GMC_RBGS) {
+        add((size_t)(ctx->nb + 31) / 32, 4);
+        add((size_t)ctx->n_sel, 4);
+        add((size_t)ctx->nb, 4);
+    } else {
+        T = build_tables(ctx);
+        const size_t nc = T.chunk_start.size(), ni = T.item_seg.size(), ns = T.seg_items.size();
+        const size_t np = (size_t)K * ns;
+        add(nc, 4); add(nc, 4); add(nc, 4);
+        add(ni, 4); add(ni, 4); add(ni, 4); add(ni, 4);
+        add(ns, 4); add(ns, 4); add(ns, 4);
+        add(np, 4); add(np, 4); add(np, 8);
+        add(np, sizeof(PairState));
+        add(np * kBins, 4);
+        add((size_t)K * nc, 4); add((size_t)K * nc, 4);
+        add((size_t)T.cand_total, 4); add((size_t)T.cand_total, 4);
+        for (int q = 0; q < 4; ++q) add((size_t)K * ni, 4);
+        add((size_t)K * (ctx->n_ranges + 1), 4);
+        add(T.gen_list.size() + 1, 4);
+    }
+    bytes += 256;
+    void* mem = nullptr;
+    hipError_t e = hipMalloc(&mem, bytes);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(ctx, GMC_ENOMEM, "hipMalloc of " + std::to_string(bytes) + " bytes of scratch failed");
+    }
+    ctx->mem = mem;
+    ctx->mem_bytes = bytes;
+    GMC_HIP(ctx, hipMemset(mem, 0, bytes));
+    Carver cv{reinterpret_cast<char*>(mem)};
+    ctx->stats = cv.take<int64_t>(8);
+    if (ctx->comp == GMC_RBGS) {
+        ctx->rbgs_bitmap = cv.take<uint32_t>((ctx->nb + 31) / 32);
+        ctx->rbgs_blocks = cv.take<int32_t>(ctx->n_sel);
+        ctx->rbgs_slot = cv.take<int32_t>(ctx->nb);
+    } else {
+        const size_t nc = T.chunk_start.size(), ni = T.item_seg.size(), ns = T.seg_items.size();
+        const size_t np = (size_t)K * ns;
+        auto up = [&](auto* dst, const auto& v) -> hipError_t {
+            return hipMemcpy(dst, v.data(), v.size() * sizeof(v[0]), hipMemcpyHostToDevice);
+        };
+        int32_t* cs = cv.take<int32_t>(nc); int32_t* cl = cv.take<int32_t>(nc); int32_t* cg = cv.take<int32_t>(nc);
+        int32_t* is = cv.take<int32_t>(ni); int32_t* il = cv.take<int32_t>(ni); int32_t* ih = cv.take<int32_t>(ni);
+        int32_t* ir = cv.take<int32_t>(ni);
+        int32_t* si = cv.take<int32_t>(ns); int32_t* sl = cv.take<int32_t>(ns); int32_t* so = cv.take<int32_t>(ns);
+        int32_t* pk = cv.take<int32_t>(np); int32_t* pc = cv.take<int32_t>(np); int64_t* pcd = cv.take<int64_t>(np);
+        GMC_HIP(ctx, up(cs, T.chunk_start)); GMC_HIP(ctx, up(cl, T.chunk_len)); GMC_HIP(ctx, up(cg, T.chunk_seg));
+        GMC_HIP(ctx, up(is, T.item_seg)); GMC_HIP(ctx, up(il, T.item_lo)); GMC_HIP(ctx, up(ih, T.item_hi));
+        GMC_HIP(ctx, up(ir, T.item_rank));
+        GMC_HIP(ctx, up(si, T.seg_items)); GMC_HIP(ctx, up(sl, T.seg_item_lo)); GMC_HIP(ctx, up(so, T.seg_out));
+        GMC_HIP(ctx, up(pk, T.pair_k)); GMC_HIP(ctx, up(pc, T.pair_cap)); GMC_HIP(ctx, up(pcd, T.pair_cand));
+        TopkGeometry& g = ctx->geo;
+        g.K = K;
+        g.n_seg = (int32_t)ns;
+        g.n_chunks = (int32_t)nc;
+        g.n_items = (int32_t)ni;
+        g.chunk_start = cs; g.chunk_len = cl; g.chunk_seg = cg;
+        g.item_seg = is; g.item_chunk_lo = il; g.item_chunk_hi = ih; g.item_rank = ir;
+        g.seg_items = si; g.seg_item_lo = sl; g.seg_out = so;
+        g.pair_k = pk; g.pair_cap = pc; g.pair_cand = pcd;
+        TopkScratch& s = ctx->scr;
+        s.pair = cv.take<PairState>(np);
+        std::vector<PairState> init(np);
+        for (auto& ps : init) {
+            std::memset(&ps, 0, sizeof ps);
+            ps.tau = kNoThreshold;
+        }
+        GMC_HIP(ctx, up(s.pair, init));
+        s.hist = cv.take<uint32_t>(np * kBins);
+        s.run_off = cv.take<uint32_t>((size_t)K * nc);
+        s.run_cnt = cv.take<uint32_t>((size_t)K * nc);
+        s.cand_idx = cv.take<int32_t>((size_t)T.cand_total);
+        s.cand_val = cv.take<float>((size_t)T.cand_total);
+        s.item_above = cv.take<uint32_t>((size_t)K * ni);
+        s.item_ties = cv.take<uint32_t>((size_t)K * ni);
+        s.item_out = cv.take<uint32_t>((size_t)K * ni);
+        s.item_tiebase = cv.take<uint32_t>((size_t)K * ni);
+        s.stats = ctx->stats;
+        ctx->rowptr = cv.take<int32_t>((size_t)K * (ctx->n_ranges + 1));
+        ctx->gen_list = cv.take<int32_t>(T.gen_list.size() + 1);
+        ctx->n_gen = (int32_t)T.gen_list.size();
+        if (ctx->n_gen) GMC_HIP(ctx, up(ctx->gen_list, T.gen_list));
+    }
+    if (cv.off > bytes) return fail(ctx, GMC_ENOMEM, "internal: scratch layout overflow");
+    ctx->prepared = true;
+    return GMC_OK;
+}
+
+// -- profiling ---------------------------------------------------------------
+
+gmc_status prof_begin(gmc_ctx* ctx, hipEvent_t* ev) {
+    *ev = nullptr;
+    if (!ctx->profile) return GMC_OK;
+    GMC_HIP(ctx, hipEventCreate(ev));
+    GMC_HIP(ctx, hipEventRecord(*ev, ctx->stream));
+    return GMC_OK;
+}
+
+gmc_status prof_fold(gmc_ctx* ctx, int stage) {
+    for (auto& pr : ctx->pending[stage]) {
+        GMC_HIP(ctx, hipEventSynchronize(pr.second));
+        float ms = 0.f;
+        GMC_HIP(ctx, hipEventElapsedTime(&ms, pr.first, pr.second));
+        ctx->prof_ms[stage] += ms;
+        ctx->prof_n[stage] += 1;
+        (void)hipEventDestroy(pr.first);
+        (void)hipEventDestroy(pr.second);
+    }
+    ctx->pending[stage].clear();
+    return GMC_OK;
+}
+
+gmc_status prof_end(gmc_ctx* ctx, int stage, hipEvent_t start) {
+    if (!ctx->profile || !start) return GMC_OK;
+    hipEvent_t stop;
+    GMC_HIP(ctx, hipEventCreate(&stop));
+    GMC_HIP(ctx, hipEventRecord(stop, ctx->stream));
+    ctx->pending[stage].emplace_back(start, stop);
+    if ((int64_t)ctx->pending[stage].size() >= kMaxPendingEvents) return prof_fold(ctx, stage);
+    return GMC_OK;
+}
+
+void prof_clear(gmc_ctx* ctx) {
+    for (int s = 0; s < kStages; ++s) {
+        for (auto& pr : ctx->pending[s]) {
+            (void)hipEventDestroy(pr.first);
+            (void)hipEventDestroy(pr.second);
+        }
+        ctx->pending[s].clear();
+        ctx->prof_ms[s] = 0;
+        ctx->prof_n[s] = 0;
+    }
+}
+
+#define GMC_LAUNCH(ctx, call)                                  \
+    do {                                                       \
+        hipError_t e_ = (call);                                \
+        if (e_ != hipSuccess) return hip_fail(ctx, e_, #call); \
+    } while (0)
+
+#define GMC_TRY(x)                       \
+    do {                                 \
+        gmc_status st_ = (x);            \
+        if (st_ != GMC_OK) return st_;   \
+    } while (0)
+
+}  // namespace
+
+// ============================================================================
+// C ABI
+// ============================================================================
+
+extern "C" {
+
+gmc_status gmc_init(gmc_ctx** out, int64_t d, int32_t K, int32_t compressor, double ratio, double beta,
+                    double eta, uint64_t seed) {
+    if (!out) return fail(nullptr, GMC_EINVAL, "gmc_init: out is NULL");
+    *out = nullptr;
+    if (d < 1 || d > 0x7fffffffLL) return fail(nullptr, GMC_EINVAL, "gmc_init: d must be in [1, 2^31)");
+    if (K < 1 || K > GMC_MAX_WORKERS) return fail(nullptr, GMC_EINVAL, "gmc_init: K must be in [1, 64]");
+    if (compressor != GMC_TOPK_GLOBAL && compressor != GMC_TOPK_SEGMENTED && compressor != GMC_RBGS)
+        return fail(nullptr, GMC_EINVAL, "gmc_init: unknown compressor");
+    if (!(ratio > 0.0 && ratio <= 1.0)) return fail(nullptr, GMC_EINVAL, "gmc_init: ratio must be in (0, 1]");
+    if (!(beta >= 0.0 && beta < 1.0)) return fail(nullptr, GMC_EINVAL, "gmc_init: beta must be in [0, 1)");
+    if (!(eta > 0.0 && std::isfinite(eta))) return fail(nullptr, GMC_EINVAL, "gmc_init: eta must be > 0 and finite");
+    gmc_ctx* ctx = new (std::nothrow) gmc_ctx;
+    if (!ctx) return fail(nullptr, GMC_ENOMEM, "gmc_init: host allocation failed");
+    ctx->d = d;
+    ctx->K = K;
+    ctx->comp = compressor;
+    ctx->ratio = ratio;
+    ctx->beta = beta;
+    ctx->eta = eta;
+    ctx->seed = seed;
+    ctx->c = (float)(beta / eta);
+    ctx->s = (float)(eta / (double)K);
+    ctx->seg_off = {0, d};
+    ctx->seg_k = {(int32_t)count_for(d, ratio)};
+    ctx->k_tot = ctx->seg_k[0];
+    if (compressor == GMC_RBGS) {
+        ctx->block = (int32_t)std::min<int64_t>(4096, d);
+        ctx->nb = (int32_t)((d + ctx->block - 1) / ctx->block);
+        ctx->n_sel = (int32_t)count_for(ctx->nb, ratio);
+    }
+    hipError_t e = hipGetDevice(&ctx->device);
+    if (e != hipSuccess) {
+        delete ctx;
+        return fail(nullptr, GMC_EDEVICE, std::string("gmc_init: hipGetDevice: ") + hipGetErrorString(e));
+    }
+    gmc_status st = prepare(ctx);
+    if (st != GMC_OK) {
+        g_init_error = ctx->err;
+        release(ctx);
+        delete ctx;
+        return st;
+    }
+    *out = ctx;
+    return GMC_OK;
+}
+
+gmc_status gmc_set_segments(gmc_ctx* ctx, int32_t n_seg, const int64_t* seg_off) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_set_segments: ctx is NULL");
+    if (ctx->started) return fail(ctx, GMC_ESTATE, "gmc_set_segments: segments are fixed after the first step");
+    if (ctx->comp == GMC_RBGS) return fail(ctx, GMC_EINVAL, "gmc_set_segments: not a top-s context");
+    if (!seg_off || n_seg < 1 || n_seg > ctx->d) return fail(ctx, GMC_EINVAL, "gmc_set_segments: bad n_seg or NULL table");
+    if (ctx->comp == GMC_TOPK_GLOBAL && n_seg != 1)
+        return fail(ctx, GMC_EINVAL, "gmc_set_segments: GMC_TOPK_GLOBAL has exactly one segment");
+    if (seg_off[0] != 0 || seg_off[n_seg] != ctx->d)
+        return fail(ctx, GMC_EINVAL, "gmc_set_segments: offsets must start at 0 and end at d");
+    for (int32_t i = 0; i < n_seg; ++i)
+        if (seg_off[i + 1] <= seg_off[i]) return fail(ctx, GMC_EINVAL, "gmc_set_segments: offsets must increase strictly");
+    ctx->seg_off.assign(seg_off, seg_off + n_seg + 1);
+    ctx->seg_k.clear();
+    ctx->k_tot = 0;
+    for (int32_t i = 0; i < n_seg; ++i) {
+        const int64_t k = count_for(seg_off[i + 1] - seg_off[i], ctx->ratio);
+        ctx->seg_k.push_back((int32_t)k);
+        ctx->k_tot += k;
+    }
+    ctx->prepared = false;
+    return prepare(ctx);
+}
+
+gmc_status gmc_set_block(gmc_ctx* ctx, int32_t block) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_set_block: ctx is NULL");
+    if (ctx->started) return fail(ctx, GMC_ESTATE, "gmc_set_block: the block length is fixed after the first step");
+    if (ctx->comp != GMC_RBGS) return fail(ctx, GMC_EINVAL, "gmc_set_block: not an RBGS context");
+    if (block < 1 || block > ctx->d) return fail(ctx, GMC_EINVAL, "gmc_set_block: block must be in [1, d]");
+    ctx->block = block;
+    ctx->nb = (int32_t)((ctx->d + block - 1) / block);
+    ctx->n_sel = (int32_t)count_for(ctx->nb, ctx->ratio);
+    ctx->prepared = false;
+    return prepare(ctx);
+}
+
+gmc_status gmc_set_stream(gmc_ctx* ctx, void* hip_stream) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_set_stream: ctx is NULL");
+    ctx->stream = reinterpret_cast<hipStream_t>(hip_stream);
+    return GMC_OK;
+}
+
+int64_t gmc_message_len(const gmc_ctx* ctx) {
+    if (!ctx) return -1;
+    return ctx->comp == GMC_RBGS ? (int64_t)ctx->n_sel * ctx->block : ctx->k_tot;
+}
+
+int64_t gmc_index_len(const gmc_ctx* ctx) {
+    if (!ctx) return -1;
+    return ctx->comp == GMC_RBGS ? (int64_t)ctx->n_sel : ctx->k_tot;
+}
+
+gmc_status gmc_step(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev, const float* const* grads_dev,
+                    float* const* err_dev, int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_step: ctx is NULL");
+    if (!w_t_dev || !w_prev_dev || !grads_dev || !err_dev || !idx_dev || !val_dev || !msg_len_dev)
+        return fail(ctx, GMC_EINVAL, "gmc_step: NULL argument");
+    StepArgs a{};
+    a.w_t = w_t_dev;
+    a.w_prev = w_prev_dev;
+    a.c = ctx->c;
+    a.d = (int32_t)ctx->d;
+    for (int k = 0; k < ctx->K; ++k) {
+        if (!grads_dev[k] || !err_dev[k]) return fail(ctx, GMC_EINVAL, "gmc_step: NULL worker pointer");
+        a.wp.g[k] = grads_dev[k];
+        a.wp.e[k] = err_dev[k];
+    }
+    GMC_TRY(prepare(ctx));
+    GMC_HIP(ctx, hipSetDevice(ctx->device));
+    ctx->started = true;
+    const int64_t row_i = gmc_index_len(ctx), row_v = gmc_message_len(ctx);
+    hipEvent_t ev;
+    if (ctx->comp == GMC_RBGS) {
+        GMC_TRY(prof_begin(ctx, &ev));
+        GMC_LAUNCH(ctx, launch_rbgs_sample(ctx->seed, (uint64_t)ctx->t, ctx->nb, ctx->n_sel, (int32_t)ctx->d,
+                                           ctx->block, ctx->K, ctx->rbgs_bitmap, ctx->rbgs_blocks, ctx->rbgs_slot,
+                                           idx_dev, row_i, msg_len_dev, ctx->stream));
+        GMC_TRY(prof_end(ctx, 1, ev));
+        GMC_TRY(prof_begin(ctx, &ev));
+        GMC_LAUNCH(ctx, launch_rbgs_fused(a, ctx->K, ctx->block, ctx->rbgs_slot, val_dev, row_v, ctx->stream));
+        GMC_TRY(prof_end(ctx, 0, ev));
+    } else {
+        // worker k takes the vector pass when its rows and w_t, w_prev are 16-byte aligned
+        uint64_t vec_mask = 0;
+        const bool w_ok = ((uintptr_t)w_t_dev & 15u) == 0 && ((uintptr_t)w_prev_dev & 15u) == 0;
+        for (int k = 0; k < ctx->K && w_ok; ++k)
+            if ((((uintptr_t)grads_dev[k] | (uintptr_t)err_dev[k]) & 15u) == 0) vec_mask |= 1ull << k;
+        const uint64_t all = ctx->K == 64 ? ~0ull : ((1ull << ctx->K) - 1ull);
+        const int32_t* gl = vec_mask == all ? ctx->gen_list : nullptr;
+        const int32_t ng = vec_mask == all ? ctx->n_gen : ctx->geo.n_chunks;
+        GMC_TRY(prof_begin(ctx, &ev));
+        GMC_LAUNCH(ctx, launch_topk_fused(a, ctx->geo, ctx->scr, vec_mask, gl, ng, ctx->stream));
+        GMC_TRY(prof_end(ctx, 0, ev));
+        GMC_TRY(prof_begin(ctx, &ev));
+        for (int pass = 1; pass <= 3; ++pass)
+            GMC_LAUNCH(ctx, launch_topk_hist(pass, a, ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
+        GMC_LAUNCH(ctx, launch_topk_count(a, ctx->geo, ctx->scr, msg_len_dev, ctx->k_tot, ctx->stream));
+        GMC_TRY(prof_end(ctx, 1, ev));
+        GMC_TRY(prof_begin(ctx, &ev));
+        GMC_LAUNCH(ctx, launch_topk_emit(a, ctx->geo, ctx->scr, idx_dev, val_dev, row_v, ctx->stream));
+        GMC_TRY(prof_end(ctx, 2, ev));
+    }
+    ctx->t += 1;
+    return GMC_OK;
+}
+
+gmc_status gmc_aggregate(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev, const int64_t* msg_len_dev,
+                         float* update_dev) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_aggregate: ctx is NULL");
+    if (!idx_dev || !val_dev || !msg_len_dev || !update_dev) return fail(ctx, GMC_EINVAL, "gmc_aggregate: NULL argument");
+    GMC_TRY(prepare(ctx));
+    GMC_HIP(ctx, hipSetDevice(ctx->device));
+    const int64_t row_i = gmc_index_len(ctx), row_v = gmc_message_len(ctx);
+    hipEvent_t ev;
+    GMC_TRY(prof_begin(ctx, &ev));
+    if (ctx->comp == GMC_RBGS) {
+        GMC_LAUNCH(ctx, launch_agg_rbgs(ctx->K, (int32_t)ctx->d, ctx->block, ctx->s, idx_dev, ctx->n_sel, val_dev,
+                                        row_v, update_dev, ctx->stream));
+    } else {
+        GMC_LAUNCH(ctx, launch_agg_rowptr(ctx->K, (int32_t)ctx->d, idx_dev, row_i, msg_len_dev, ctx->rowptr,
+                                          ctx->n_ranges, ctx->stream));
+        GMC_LAUNCH(ctx, launch_agg_topk(ctx->K, (int32_t)ctx->d, ctx->s, idx_dev, row_i, val_dev, row_v, ctx->rowptr,
+                                        ctx->n_ranges, update_dev, ctx->stream));
+    }
+    GMC_TRY(prof_end(ctx, 3, ev));
+    return GMC_OK;
+}
+
+gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const float* update_dev) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_apply: ctx is NULL");
+    if (!w_dev || !update_dev) return fail(ctx, GMC_EINVAL, "gmc_apply: NULL argument");
+    if (w_prev_out_dev == w_dev) return fail(ctx, GMC_EINVAL, "gmc_apply: w_prev_out may not alias w");
+    GMC_HIP(ctx, hipSetDevice(ctx->device));
+    hipEvent_t ev;
+    GMC_TRY(prof_begin(ctx, &ev));
+    GMC_LAUNCH(ctx, launch_apply((int32_t)ctx->d, w_dev, w_prev_out_dev, update_dev, ctx->stream));
+    GMC_TRY(prof_end(ctx, 4, ev));
+    return GMC_OK;
+}
+
+gmc_status gmc_get_step(const gmc_ctx* ctx, int64_t* t) {
+    if (!ctx || !t) return fail(nullptr, GMC_EINVAL, "gmc_get_step: NULL argument");
+    *t = ctx->t;
+    return GMC_OK;
+}
+
+gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_set_step: ctx is NULL");
+    if (t < 0) return fail(ctx, GMC_EINVAL, "gmc_set_step: t must be >= 0");
+    ctx->t = t;
+    return GMC_OK;
+}
+
+gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_set_option: ctx is NULL");
+    switch (option) {
+        case GMC_OPT_FORCE_FULL_SELECT:
+            ctx->force_full = value ? 1 : 0;
+            return GMC_OK;
+        case GMC_OPT_CAND_MARGIN:
+            if (value < 1 || value > 1024) return fail(ctx, GMC_EINVAL, "gmc_set_option: margin must be in [1, 1024]");
+            ctx->margin = (int)value;
+            return GMC_OK;
+        case GMC_OPT_CAND_CAP_MULT:
+            if (value < 1 || value > 1024) return fail(ctx, GMC_EINVAL, "gmc_set_option: cap multiple must be in [1, 1024]");
+            if (ctx->started) return fail(ctx, GMC_ESTATE, "gmc_set_option: capacity is fixed after the first step");
+            ctx->cap_mult = (int)value;
+            ctx->prepared = false;
+            return prepare(ctx);
+        case GMC_OPT_PROFILE:
+            if (ctx->profile) GMC_HIP(ctx, hipStreamSynchronize(ctx->stream));
+            prof_clear(ctx);
+            ctx->profile = value != 0;
+            return GMC_OK;
+        default:
+            return fail(ctx, GMC_EINVAL, "gmc_set_option: unknown option");
+    }
+}
+
+gmc_status gmc_stats(gmc_ctx* ctx, int64_t* out, int32_t n) {
+    if (!ctx || !out || n < 0) return fail(ctx, GMC_EINVAL, "gmc_stats: bad argument");
+    GMC_HIP(ctx, hipSetDevice(ctx->device));
+    GMC_HIP(ctx, hipStreamSynchronize(ctx->stream));
+    int64_t host[8] = {0};
+    if (ctx->stats) GMC_HIP(ctx, hipMemcpy(host, ctx->stats, sizeof host, hipMemcpyDeviceToHost));
+    host[0] = ctx->t;
+    for (int32_t i = 0; i < n && i < 8; ++i) out[i] = host[i];
+    return GMC_OK;
+}
+
+gmc_status gmc_profile_read(gmc_ctx* ctx, double* ms, int64_t* launches, int32_t n) {
+    if (!ctx || !ms || !launches || n < 0) return fail(ctx, GMC_EINVAL, "gmc_profile_read: bad argument");
+    GMC_HIP(ctx, hipSetDevice(ctx->device));
+    for (int s = 0; s < kStages; ++s) GMC_TRY(prof_fold(ctx, s));
+    for (int32_t i = 0; i < n && i < kStages; ++i) {
+        ms[i] = ctx->prof_ms[i];
+        launches[i] = ctx->prof_n[i];
+    }
+    return GMC_OK;
+}
+
+const char* gmc_last_error(const gmc_ctx* ctx) {
+    return ctx ? ctx->err.c_str() : g_init_error.c_str();
+}
+
+void gmc_destroy(gmc_ctx* ctx) {
+    if (!ctx) return;
+    prof_clear(ctx);
+    release(ctx);
+    delete ctx;
+}
+
+}  // extern "C"

@@ -1,0 +1,125 @@
+// Internal declarations of the GMC device library: launch geometry, the
+// device-side scratch layout and the kernel launchers.  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gmc {
+
+constexpr int kMaxWorkers = 64;
+
+// Fused worker pass: a workgroup of 4 wavefronts; each wavefront owns one
+// chunk of kChunk consecutive elements (64 lanes x 4 floats x 8 iterations).
+constexpr int kWave = 64;
+constexpr int kWavesPerGroup = 4;
+constexpr int kGroup = kWave * kWavesPerGroup;  // 256 threads
+constexpr int kVecIters = 8;
+constexpr int kChunk = kWave * 4 * kVecIters;   // 2048 elements
+
+// Selection works on "items": runs of up to kItemChunks chunks of one segment.
+constexpr int kItemChunks = 32;
+
+// Radix select over the 31-bit magnitude key in three digits: 11 + 11 + 9.
+constexpr int kBins = 2048;
+constexpr int kShift1 = 20, kShift2 = 9;
+
+// Aggregation range per workgroup.
+constexpr int kAggRange = 2048;
+
+constexpr uint32_t kNoThreshold = 0xffffffffu;  // no speculative candidates
+
+struct WorkerPtrs {
+    const float* g[kMaxWorkers];
+    float* e[kMaxWorkers];
+};
+
+// Per (worker, segment) pair state, kept in device memory across kernels.
+struct PairState {
+    uint32_t tau;       // candidate threshold key of the next fused pass
+    uint32_t cand;      // candidates appended by the fused pass (atomic)
+    int32_t mode;       // 0 = resolve from candidates, 1 = full data
+    uint32_t prefix;    // radix digits fixed so far
+    int32_t need;       // components still to take below the prefix
+    uint32_t T;         // threshold key: k-th largest magnitude key
+    int32_t r;          // components with key == T to take (lowest index)
+    uint32_t done;      // finished workgroups of the current kernel
+};
+
+// Static geometry of the top-s selection (built on the host at init).
+struct TopkGeometry {
+    int32_t K, n_seg, n_chunks, n_items;
+    const int32_t* chunk_start;   // [n_chunks]
+    const int32_t* chunk_len;     // [n_chunks]
+    const int32_t* chunk_seg;     // [n_chunks]
+    const int32_t* item_seg;      // [n_items]
+    const int32_t* item_chunk_lo; // [n_items]
+    const int32_t* item_chunk_hi; // [n_items]
+    const int32_t* item_rank;     // [n_items] index of the item within its segment
+    const int32_t* seg_items;     // [n_seg] items per segment
+    const int32_t* seg_item_lo;   // [n_seg] first item of the segment
+    const int32_t* seg_out;       // [n_seg] offset of the segment in a message row
+    const int32_t* pair_k;        // [K*n_seg]
+    const int32_t* pair_cap;      // [K*n_seg]
+    const int64_t* pair_cand;     // [K*n_seg] start of the pair's candidate region
+};
+
+struct TopkScratch {
+    PairState* pair;              // [K*n_seg]
+    uint32_t* hist;               // [K*n_seg][kBins]
+    uint32_t* run_off;            // [K*n_chunks]
+    uint32_t* run_cnt;            // [K*n_chunks]
+    int32_t* cand_idx;            // [sum cap]
+    float* cand_val;              // [sum cap]
+    uint32_t* item_above;         // [K*n_items]
+    uint32_t* item_ties;          // [K*n_items]
+    uint32_t* item_out;           // [K*n_items]
+    uint32_t* item_tiebase;       // [K*n_items]
+    int64_t* stats;               // [8]
+};
+
+struct StepArgs {
+    const float* w_t;
+    const float* w_prev;
+    WorkerPtrs wp;
+    float c;
+    int32_t d;
+};
+
+// ----------------------------------------------------------------------------
+// launchers (gmc_kernels.hip); each returns the launch status
+// ----------------------------------------------------------------------------
+// vec_mask: bit k set when worker k's rows (and w_t, w_prev) are 16-byte
+// aligned.  gen_list/n_gen: chunks the element-wise kernel visits (NULL list:
+// chunks 0..n_gen-1).
+hipError_t launch_topk_fused(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
+                             uint64_t vec_mask, const int32_t* gen_list, int32_t n_gen,
+                             hipStream_t st);
+hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
+                            const TopkScratch& s, int force_full, int margin, hipStream_t st);
+hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
+                             int64_t* msg_len, int64_t msg_total, hipStream_t st);
+hipError_t launch_topk_emit(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
+                            int32_t* idx, float* val, int64_t row_len, hipStream_t st);
+
+hipError_t launch_rbgs_sample(uint64_t seed, uint64_t t, int32_t nb, int32_t n_sel, int32_t d,
+                              int32_t B, int32_t K, uint32_t* bitmap, int32_t* blocks,
+                              int32_t* block_slot, int32_t* idx, int64_t idx_row,
+                              int64_t* msg_len, hipStream_t st);
+hipError_t launch_rbgs_fused(const StepArgs& a, int32_t K, int32_t B, const int32_t* block_slot,
+                             float* val, int64_t val_row, hipStream_t st);
+
+hipError_t launch_agg_rowptr(int32_t K, int32_t d, const int32_t* idx, int64_t idx_row,
+                             const int64_t* msg_len, int32_t* rowptr, int32_t n_ranges,
+                             hipStream_t st);
+hipError_t launch_agg_topk(int32_t K, int32_t d, float s, const int32_t* idx, int64_t idx_row,
+                           const float* val, int64_t val_row, const int32_t* rowptr,
+                           int32_t n_ranges, float* update, hipStream_t st);
+hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, float s, const int32_t* blocks,
+                           int32_t n_sel, const float* val, int64_t val_row, float* update,
+                           hipStream_t st);
+
+hipError_t launch_apply(int32_t d, float* w, float* w_prev_out, const float* update,
+                        hipStream_t st);
+
+}  // namespace gmc

@@ -1,0 +1,238 @@
+"""ctypes binding of libgmc.so (include/gmc.h), one call per C entry point.
+
+The binding only marshals arguments: it checks dtype, device, shape and
+contiguity of the torch tensors, passes their device pointers and the current
+HIP stream, and raises GmcError on a non-OK status.  Every step of the path
+runs in the library's HIP kernels; there is no fallback of any kind, and
+importing this module fails loudly when libgmc.so has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence, Tuple, Union
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgmc.so")
+
+GMC_TOPK_GLOBAL, GMC_TOPK_SEGMENTED, GMC_RBGS = 0, 1, 2
+GMC_OK, GMC_EINVAL, GMC_ENOMEM, GMC_EDEVICE, GMC_ESTATE = 0, -1, -2, -3, -4
+GMC_OPT_FORCE_FULL_SELECT, GMC_OPT_CAND_MARGIN, GMC_OPT_CAND_CAP_MULT, GMC_OPT_PROFILE = 1, 2, 3, 4
+MAX_WORKERS = 64
+STAGES = ("fused", "select", "emit", "aggregate", "apply")
+
+COMPRESSORS = {"topk": GMC_TOPK_GLOBAL, "topk_seg": GMC_TOPK_SEGMENTED, "rbgs": GMC_RBGS}
+
+# every entry point include/gmc.h declares
+EXPORTS = ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "gmc_message_len",
+           "gmc_index_len", "gmc_step", "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step",
+           "gmc_set_option", "gmc_stats", "gmc_profile_read", "gmc_last_error", "gmc_destroy")
+
+
+class GmcError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("gmc status %d: %s" % (status, msg))
+        self.status = status
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libgmc.so from the package directory (built by
+    ``__graft_entry__.build()``); raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libgmc.so is not built: run __graft_entry__.build() "
+                          "(hipcc --offload-arch=gfx950)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, u64, dbl = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_double
+    lib.gmc_init.argtypes = [ctypes.POINTER(P), i64, i32, i32, dbl, dbl, dbl, u64]
+    lib.gmc_set_segments.argtypes = [P, i32, P]
+    lib.gmc_set_block.argtypes = [P, i32]
+    lib.gmc_set_stream.argtypes = [P, P]
+    lib.gmc_message_len.argtypes = [P]
+    lib.gmc_message_len.restype = i64
+    lib.gmc_index_len.argtypes = [P]
+    lib.gmc_index_len.restype = i64
+    lib.gmc_step.argtypes = [P, P, P, P, P, P, P, P]
+    lib.gmc_aggregate.argtypes = [P, P, P, P, P]
+    lib.gmc_apply.argtypes = [P, P, P, P]
+    lib.gmc_get_step.argtypes = [P, ctypes.POINTER(i64)]
+    lib.gmc_set_step.argtypes = [P, i64]
+    lib.gmc_set_option.argtypes = [P, i32, i64]
+    lib.gmc_stats.argtypes = [P, P, i32]
+    lib.gmc_profile_read.argtypes = [P, P, P, i32]
+    lib.gmc_last_error.argtypes = [P]
+    lib.gmc_last_error.restype = ctypes.c_char_p
+    lib.gmc_destroy.argtypes = [P]
+    lib.gmc_destroy.restype = None
+    for name in ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "gmc_step",
+                 "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step", "gmc_set_option",
+                 "gmc_stats", "gmc_profile_read"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _check(t, dtype, numel: Optional[int] = None, name: str = "tensor"):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if t.device.type != "cuda":
+        raise ValueError("%s must be on a GPU device" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if numel is not None and t.numel() < numel:
+        raise ValueError("%s needs at least %d elements, has %d" % (name, numel, t.numel()))
+    return t.data_ptr()
+
+
+def _rows(x, d: int, K: int, name: str) -> List[int]:
+    """K device pointers from a [K, >=d] tensor (row stride may exceed d) or
+    a sequence of K [d] tensors."""
+    torch = _torch()
+    if isinstance(x, torch.Tensor):
+        if x.dim() != 2 or x.shape[0] != K or x.shape[1] < d:
+            raise ValueError("%s must be [K, >=d]" % name)
+        if x.dtype != torch.float32 or x.device.type != "cuda" or x.stride(1) != 1:
+            raise ValueError("%s must be a float32 GPU tensor with unit inner stride" % name)
+        return [x[k].data_ptr() for k in range(K)]
+    if len(x) != K:
+        raise ValueError("%s must hold K=%d tensors" % (name, K))
+    return [_check(t, torch.float32, d, "%s[%d]" % (name, k)) for k, t in enumerate(x)]
+
+
+class Gmc:
+    """One GMC context: ``step`` (workers), ``aggregate`` (server), ``apply``.
+
+    compressor: "topk" (global top-s), "topk_seg" (top-s per segment; pass
+    ``segments`` as the n_seg+1 offsets) or "rbgs" (``block`` elements per
+    block).  Calls run on torch's current stream of the tensors' device.
+    """
+
+    def __init__(self, d: int, K: int, compressor: str = "topk", ratio: float = 0.001,
+                 beta: float = 0.9, eta: float = 0.1, seed: int = 0,
+                 segments: Optional[Sequence[int]] = None, block: Optional[int] = None):
+        self._lib = load()
+        self.d, self.K, self.compressor = int(d), int(K), compressor
+        if compressor not in COMPRESSORS:
+            raise ValueError("compressor must be one of %s" % list(COMPRESSORS))
+        ctx = ctypes.c_void_p()
+        st = self._lib.gmc_init(ctypes.byref(ctx), self.d, self.K, COMPRESSORS[compressor],
+                                float(ratio), float(beta), float(eta), int(seed) & (2 ** 64 - 1))
+        if st != GMC_OK:
+            raise GmcError(st, self._lib.gmc_last_error(None).decode())
+        self._ctx = ctx
+        if segments is not None:
+            off = (ctypes.c_int64 * len(segments))(*[int(x) for x in segments])
+            self._call(self._lib.gmc_set_segments(self._ctx, len(segments) - 1, off))
+        if block is not None:
+            self._call(self._lib.gmc_set_block(self._ctx, int(block)))
+
+    # -- plumbing -------------------------------------------------------
+    def _call(self, st: int):
+        if st != GMC_OK:
+            raise GmcError(st, self._lib.gmc_last_error(self._ctx).decode())
+
+    def _stream(self, device):
+        torch = _torch()
+        s = torch.cuda.current_stream(device)
+        self._call(self._lib.gmc_set_stream(self._ctx, ctypes.c_void_p(s.cuda_stream)))
+
+    def close(self):
+        if getattr(self, "_ctx", None):
+            self._lib.gmc_destroy(self._ctx)
+            self._ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- sizes ------------------------------------------------------------
+    @property
+    def message_len(self) -> int:
+        return int(self._lib.gmc_message_len(self._ctx))
+
+    @property
+    def index_len(self) -> int:
+        return int(self._lib.gmc_index_len(self._ctx))
+
+    def alloc_messages(self, device="cuda"):
+        """Fresh (idx int32 [K, index_len], val fp32 [K, message_len],
+        msg_len int64 [K]) buffers."""
+        torch = _torch()
+        return (torch.zeros((self.K, self.index_len), dtype=torch.int32, device=device),
+                torch.zeros((self.K, self.message_len), dtype=torch.float32, device=device),
+                torch.zeros((self.K,), dtype=torch.int64, device=device))
+
+    # -- the three calls of one iteration ---------------------------------
+    def step(self, w_t, w_prev, grads, err, idx, val, msg_len):
+        torch = _torch()
+        d, K = self.d, self.K
+        pw = _check(w_t, torch.float32, d, "w_t")
+        pp = _check(w_prev, torch.float32, d, "w_prev")
+        gp = (ctypes.c_void_p * K)(*_rows(grads, d, K, "grads"))
+        ep = (ctypes.c_void_p * K)(*_rows(err, d, K, "err"))
+        pi = _check(idx, torch.int32, K * self.index_len, "idx")
+        pv = _check(val, torch.float32, K * self.message_len, "val")
+        pl = _check(msg_len, torch.int64, K, "msg_len")
+        self._stream(w_t.device)
+        self._call(self._lib.gmc_step(self._ctx, pw, pp, gp, ep, pi, pv, pl))
+
+    def aggregate(self, idx, val, msg_len, update):
+        torch = _torch()
+        pi = _check(idx, torch.int32, self.K * self.index_len, "idx")
+        pv = _check(val, torch.float32, self.K * self.message_len, "val")
+        pl = _check(msg_len, torch.int64, self.K, "msg_len")
+        pu = _check(update, torch.float32, self.d, "update")
+        self._stream(update.device)
+        self._call(self._lib.gmc_aggregate(self._ctx, pi, pv, pl, pu))
+
+    def apply(self, w, update, w_prev_out=None):
+        torch = _torch()
+        pw = _check(w, torch.float32, self.d, "w")
+        pu = _check(update, torch.float32, self.d, "update")
+        pp = None if w_prev_out is None else _check(w_prev_out, torch.float32, self.d, "w_prev_out")
+        self._stream(w.device)
+        self._call(self._lib.gmc_apply(self._ctx, pw, pp, pu))
+
+    # -- state and diagnostics ---------------------------------------------
+    @property
+    def t(self) -> int:
+        v = ctypes.c_int64()
+        self._call(self._lib.gmc_get_step(self._ctx, ctypes.byref(v)))
+        return v.value
+
+    @t.setter
+    def t(self, value: int):
+        self._call(self._lib.gmc_set_step(self._ctx, int(value)))
+
+    def set_option(self, option: int, value: int):
+        self._call(self._lib.gmc_set_option(self._ctx, int(option), int(value)))
+
+    def stats(self) -> dict:
+        out = (ctypes.c_int64 * 8)()
+        self._call(self._lib.gmc_stats(self._ctx, out, 8))
+        keys = ("steps", "from_candidates", "full_data", "candidates", "count_errors")
+        return {k: int(out[i]) for i, k in enumerate(keys)}
+
+    def profile(self, on: bool = True):
+        self.set_option(GMC_OPT_PROFILE, 1 if on else 0)
+
+    def profile_read(self) -> dict:
+        ms = (ctypes.c_double * len(STAGES))()
+        n = (ctypes.c_int64 * len(STAGES))()
+        self._call(self._lib.gmc_profile_read(self._ctx, ms, n, len(STAGES)))
+        return {name: (ms[i], int(n[i])) for i, name in enumerate(STAGES)}

@@ -1,0 +1,113 @@
+"""Device library vs the CPU oracle, element by element, on the same seeded
+inputs: every workload shape (shrunk so the oracle finishes in seconds while
+still spanning many chunks, items and ragged tails), both selection paths,
+misaligned rows and the degenerate cases of the method."""
+import numpy as np
+import pytest
+
+import synth
+from gpu_harness import Case, run_lockstep
+
+pytestmark = pytest.mark.gpu
+
+OPT_FULL, OPT_MARGIN, OPT_CAP = 1, 2, 3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def W(name):
+    return synth.workload(name)
+
+
+def test_tiny_full_size():
+    st = run_lockstep(Case(W("tiny"), steps=5, label="tiny"))
+    assert st["full_data"] >= 4          # step 0 has no threshold yet
+    assert st["from_candidates"] >= 8    # later steps resolve from candidates
+
+
+def test_resnet18_shape_shrunk():
+    run_lockstep(Case(W("resnet18").shrunk(16), steps=4, label="resnet18/16"))
+
+
+def test_resnet50_shape_shrunk():
+    run_lockstep(Case(W("resnet50").shrunk(32), steps=4, label="resnet50/32"))
+
+
+def test_rbgs_shrunk():
+    run_lockstep(Case(W("rbgs").shrunk(16), steps=5, label="rbgs/16"))
+
+
+def test_gpt2_per_tensor_shrunk():
+    run_lockstep(Case(W("gpt2").shrunk(64), steps=3, label="gpt2/64"))
+
+
+def test_forced_full_data_path():
+    st = run_lockstep(Case(W("resnet50").shrunk(32, K=6), steps=3, options=((OPT_FULL, 1),),
+                           label="full-data"))
+    assert st["from_candidates"] == 0
+
+
+def test_candidate_overflow_takes_full_data_path():
+    st = run_lockstep(Case(W("resnet18").shrunk(16, K=4), steps=4,
+                           options=((OPT_CAP, 1), (OPT_MARGIN, 64)), label="overflow"))
+    assert st["full_data"] > 0
+
+
+def test_misaligned_rows():
+    wl = synth.Workload("odd", [5000, 3, 77777, 2048 * 3 + 1], K=3, ratio=0.01, beta=0.9, eta=0.1,
+                        steps=3, compressor="topk_seg", dist="normal")
+    run_lockstep(Case(wl, steps=3, row_pad=1, label="misaligned"))
+
+
+def test_no_compression_is_momentum_sgd():
+    wl = synth.Workload("dense", [1000, 24], K=1, ratio=1.0, beta=0.9, eta=0.1, steps=3,
+                        compressor="topk", dist="normal")
+    run_lockstep(Case(wl, steps=3, label="ratio=1,K=1"))
+    wl = synth.Workload("dense4", [4099], K=4, ratio=1.0, beta=0.5, eta=0.3, steps=3,
+                        compressor="topk", dist="normal")
+    run_lockstep(Case(wl, steps=3, label="ratio=1,K=4"))
+
+
+@pytest.mark.parametrize("sizes,K,ratio", [([1], 3, 0.5), ([3], 2, 0.5), ([2, 1, 5], 2, 0.3),
+                                           ([2048], 1, 1e-6), ([2049], 2, 0.999)])
+def test_degenerate_sizes(sizes, K, ratio):
+    wl = synth.Workload("small", sizes, K=K, ratio=ratio, beta=0.9, eta=0.1, steps=3,
+                        compressor="topk_seg", dist="normal")
+    run_lockstep(Case(wl, steps=3, label="small%s" % sizes))
+
+
+def test_heavy_ties_lowest_index_wins():
+    def quantise(t, g):
+        return np.sign(np.round(g)).astype(np.float32)          # values in {-1, 0, 1}
+    wl = W("tiny").shrunk(8)
+    run_lockstep(Case(wl, steps=4, grad_hook=quantise, label="ties"))
+
+
+def test_all_zero_gradients():
+    wl = W("tiny").shrunk(32, K=2)
+    run_lockstep(Case(wl, steps=2, grad_hook=lambda t, g: np.zeros_like(g), label="zeros"))
+
+
+def test_infinities_rank_first():
+    def inject(t, g):
+        if t == 1:
+            g = g.copy()
+            g[0, [5, 900]] = np.inf
+            g[1, 17] = -np.inf
+        return g
+    wl = W("tiny").shrunk(64, K=2)
+    run_lockstep(Case(wl, steps=2, grad_hook=inject, label="inf"))
+
+
+def test_rbgs_partial_last_block_and_small_blocks():
+    wl = synth.Workload("rb", [10000 + 1234], K=3, ratio=0.5, beta=0.9, eta=0.1, steps=6,
+                        compressor="rbgs", dist="normal", block=1000)
+    run_lockstep(Case(wl, steps=6, label="rbgs-partial"))
+    wl = synth.Workload("rb7", [999], K=2, ratio=0.3, beta=0.9, eta=0.1, steps=3,
+                        compressor="rbgs", dist="normal", block=7)
+    run_lockstep(Case(wl, steps=3, label="rbgs-block7"))
