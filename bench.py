@@ -1,0 +1,246 @@
+#!/usr/bin/env python
+"""GMC step throughput on one MI355X.
+
+One step is one full iteration of Algorithm 1 for K simulated workers:
+gmc_step (global momentum + error feedback + compression + residual for all
+K workers) and gmc_aggregate_apply (server sum in worker order and the
+apply, w_{t+1} = w_t + update written over w_{t-1}'s buffer, the two
+parameter buffers swapping roles every step).  Inputs are resident in HBM
+before the timed region; each step takes the next of a few pre-generated
+gradient batches.
+
+Prints one JSON line (stdout): G worker-elements/s (K*d per step), ms/step,
+the fraction of HBM peak the step's algorithmic bytes reach, a `roofline`
+object for the dominant kernel (the fused worker pass, timed with HIP events
+on its own stream inside the timed region) and a `cpu_baseline` object (the
+CPU oracle timed on a bounded sample of the same workload).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload resnet50]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "GMC step throughput: G worker-elements/s and % of HBM peak, d=25.6M K=16"
+UNIT = "G worker-elements/s"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E peak, GB/s
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "topk_fused_vec_resnet50_pmc.txt")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_1905_12948_amd", "csrc", f)
+                  for f in ("gmc_kernels.hip", "gmc_internal.h")]
+
+DESCRIPTIONS = {
+    "resnet50": "ResNet-50-sized GMC step: d=25,557,032 fp32 in 161 tensors, K=16 workers, global "
+                "top-k 0.1% (k=25,558 per worker), Student-t(3) gradients with per-tensor "
+                "log-uniform scales in [1e-5,1e-1], beta=0.9, eta=0.1",
+    "resnet18": "ResNet-18-sized GMC step: d=11,173,962 fp32 in 62 tensors, K=8, global top-k 1%, "
+                "non-IID Gaussian gradients",
+    "rbgs": "GMC+ RBGS step: d=25,557,032 fp32, K=8, 1% of 4096-element blocks per step",
+    "gpt2": "Transformer-sized GMC step: d=124,439,808 fp32 in 148 tensors, K=8, per-tensor top-k "
+            "0.1%, Student-t(4) gradients",
+    "tiny": "Tiny GMC step: d=2^20, K=4, global top-k 1%",
+}
+
+
+def log(msg: str):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def algorithmic_bytes(wl, msg_len: int) -> dict:
+    """Bytes one step must move (per step, whole job), and those of the fused
+    worker pass alone.  top-s: read g, read e, write e (12 B per worker-
+    element); read w_t, w_prev for the momentum term and read + write w in
+    the apply (16 B per element); write (idx, val) and read them back in the
+    aggregation (16 B per message entry).  RBGS sends values only (8 B)."""
+    K, d = wl.K, wl.d
+    if wl.compressor == "rbgs":
+        step = 12 * K * d + 16 * d + 8 * K * msg_len
+        fused = 12 * K * d + 8 * d + 4 * K * msg_len
+    else:
+        step = 12 * K * d + 16 * d + 16 * K * msg_len
+        fused = 12 * K * d + 8 * d
+    return {"step": step, "fused": fused}
+
+
+def read_pmc_summary():
+    """Per-dispatch HBM traffic of the fused kernel from the committed
+    rocprofv3 counter summary, scaled by the copy-kernel calibration; None if
+    absent or taken on different kernel sources."""
+    if not os.path.exists(PMC_SUMMARY):
+        return None
+    kv = {}
+    with open(PMC_SUMMARY) as f:
+        for line in f:
+            if "=" in line and not line.lstrip().startswith("#"):
+                k, v = line.split("=", 1)
+                kv[k.strip()] = v.strip()
+    try:
+        if kv.get("kernel_source_sha256") != kernel_source_hash():
+            return None
+        fs = float(kv["copy_bytes"]) / (float(kv["copy_fetch_kib"]) * 1024.0)
+        ws = float(kv["copy_bytes"]) / (float(kv["copy_write_kib"]) * 1024.0)
+        return (float(kv["fused_fetch_kib"]) * 1024.0 * fs + float(kv["fused_write_kib"]) * 1024.0 * ws)
+    except (KeyError, ValueError, ZeroDivisionError):
+        return None
+
+
+def cpu_baseline(wl, workers: int, steps: int) -> dict:
+    """The CPU oracle (single-threaded C, as it stands) on a bounded sample
+    of the workload: `workers` of the K workers at the full d for `steps`
+    iterations, with host-generated inputs of the same recipe."""
+    import numpy as np
+    import oracle
+    import synth
+    import dataclasses
+    sub = dataclasses.replace(wl, K=workers)
+    seg = sub.topk_segments() if sub.compressor == "topk_seg" else None
+    orc = oracle.GmcOracle(sub.d, workers, "rbgs" if sub.compressor == "rbgs" else "topk",
+                           sub.ratio, sub.beta, sub.eta, seed=sub.seed, seg_off=seg, block=sub.block)
+    w = sub.w0()
+    wp = w.copy()
+    err = np.zeros((workers, sub.d), np.float32)
+    batches = [sub.grads(t) for t in range(steps)]
+    t0 = time.perf_counter()
+    for t in range(steps):
+        idx, val, ln = orc.step(w, wp, batches[t], err)
+        delta = orc.aggregate(idx, val, ln)
+        wn = w.copy()
+        orc.apply(wn, delta)
+        wp, w = w, wn
+    dt = time.perf_counter() - t0
+    return {"value": workers * sub.d * steps / dt / 1e9, "unit": UNIT, "cores": 1, "kind": "oracle",
+            "sample": "%d of the %d workers at the full d=%d for %d steps (oracle compression, "
+                      "aggregation of those %d messages and apply each step), %.1f s of CPU time"
+                      % (workers, wl.K, wl.d, steps, workers, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="resnet50", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--grad-batches", type=int, default=4)
+    ap.add_argument("--cpu-workers", type=int, default=2)
+    ap.add_argument("--cpu-steps", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib", action="store_true",
+                    help="also run the plain copy kernel (memory-counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the K workers are simulated on a single MI355X and "
+              "nothing in this build uses a second GPU (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import synth.device as sdev
+    from paper_1905_12948_amd import Gmc
+    from paper_1905_12948_amd.gmc import calib_copy
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    wl = synth.workload(args.workload)
+    d, K = wl.d, wl.K
+    seg = wl.topk_segments().tolist() if wl.compressor == "topk_seg" else None
+    gm = Gmc(d, K, wl.compressor, wl.ratio, wl.beta, wl.eta, seed=wl.seed, segments=seg,
+             block=wl.block if wl.compressor == "rbgs" else None)
+    log("workload %s: d=%d K=%d %s ratio=%g; generating %d gradient batches on the GPU"
+        % (wl.name, d, K, wl.compressor, wl.ratio, args.grad_batches))
+    w = sdev.w0(wl, dev)
+    wp = w.clone()
+    err = torch.zeros((K, d), dtype=torch.float32, device=dev)
+    G = [sdev.grads(wl, t, dev) for t in range(args.grad_batches)]
+    idx, val, ln = gm.alloc_messages(dev)
+    if args.calib:
+        cal_src = torch.ones(1 << 28, dtype=torch.float32, device=dev)     # 1 GiB
+        cal_dst = torch.empty_like(cal_src)
+    torch.cuda.synchronize()
+
+    # w_t and w_{t-1} live in two buffers whose roles swap every step:
+    # gmc_aggregate_apply writes w_{t+1} = w_t + update over w_{t-1}'s buffer
+    bufs = [w, wp]
+    step_no = [0]
+
+    def one_step():
+        cur, prev = bufs[step_no[0] % 2], bufs[(step_no[0] + 1) % 2]
+        gm.step(cur, prev, G[step_no[0] % len(G)], err, idx, val, ln)
+        gm.aggregate_apply(idx, val, ln, cur, prev)
+        step_no[0] += 1
+
+    log("warmup %d steps" % args.warmup)
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    stats0 = gm.stats()
+    gm.profile(["fused_vec"])
+
+    log("timing %d steps" % args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        one_step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = gm.profile_read()
+    stats1 = gm.stats()
+    gm.profile([])
+    if args.calib:
+        for _ in range(3):
+            calib_copy(cal_dst, cal_src)
+        torch.cuda.synchronize()
+
+    ms_step = elapsed * 1e3 / args.steps
+    msg_len = int(ln[0].item())
+    ab = algorithmic_bytes(wl, msg_len)
+    fused_ms_total, fused_n = prof["fused_vec"]
+    fused_ms = fused_ms_total / max(fused_n, 1)
+    achieved = ab["fused"] / (fused_ms * 1e-3) / 1e9
+    traffic = read_pmc_summary()
+    roofline = {"kernel": "topk_fused_vec_kernel" if wl.compressor != "rbgs" else "rbgs_fused_kernel",
+                "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": None if traffic is None else int(traffic),
+                "alg_bytes_per_launch": ab["fused"], "avg_ms": round(fused_ms, 4)}
+    value = K * d / (ms_step * 1e-3) / 1e9
+    sel = {k: stats1[k] - stats0[k] for k in ("from_candidates", "full_data", "candidates")}
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": UNIT, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": DESCRIPTIONS[wl.name], "d": d, "K": K, "compressor": wl.compressor,
+                   "ratio": wl.ratio, "message_len": msg_len, "grad_batches": len(G)},
+        "hbm_peak_frac": round(ab["step"] / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "alg_bytes_per_step": ab["step"],
+        "selection": sel,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline: oracle on %d workers x %d steps" % (args.cpu_workers, args.cpu_steps))
+        del G
+        torch.cuda.empty_cache()
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_workers, args.cpu_steps)
+    gm.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

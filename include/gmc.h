@@ -143,6 +143,21 @@ gmc_status gmc_aggregate(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_
                          const int64_t* msg_len_dev, float* update_dev);
 
 /*
+ * The server's update and the workers' apply in one pass (Algorithm 1,
+ * server and workers): with update = -(s * sum_k C(u_k)) exactly as
+ * gmc_aggregate computes it,
+ *   w_out_dev[j] = w_dev[j] + update[j]   for every j in [0, d),
+ * and update_dev[j] = update[j] when update_dev is not NULL.  w_out_dev may
+ * equal w_dev (in place); otherwise the two must not overlap.  Out of place
+ * the caller keeps w_{t+1} in w_out_dev and w_t in w_dev, i.e. swaps the
+ * roles of its two parameter buffers for the next gmc_step instead of
+ * copying w into w_prev.  update_dev may not alias either.
+ */
+gmc_status gmc_aggregate_apply(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev,
+                               const int64_t* msg_len_dev, const float* w_dev, float* w_out_dev,
+                               float* update_dev);
+
+/*
  * Workers' apply (Algorithm 1): w_prev_out_dev[j] = w_dev[j] (when not NULL),
  * then w_dev[j] = w_dev[j] + update_dev[j], for every j in [0, d).
  *   w_dev           [d] fp32 in/out
@@ -162,7 +177,9 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
  *   GMC_OPT_CAND_MARGIN        candidate target as a multiple of k (>= 1)
  *   GMC_OPT_CAND_CAP_MULT      candidate capacity as a multiple of k (>= 1);
  *                              reallocates scratch; before the first step
- *   GMC_OPT_PROFILE            1: time the stage kernels with HIP events
+ *   GMC_OPT_PROFILE            bit mask of the stages to time with HIP events
+ *                              on the context's stream (0: off); see
+ *                              gmc_profile_read for the stage numbers
  */
 enum {
     GMC_OPT_FORCE_FULL_SELECT = 1,
@@ -181,12 +198,20 @@ gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value);
 gmc_status gmc_stats(gmc_ctx* ctx, int64_t* out, int32_t n);
 
 /*
- * Stage timings when GMC_OPT_PROFILE is on: for each stage i < n, total
- * milliseconds and launch count since the option was set.  Stage order:
- * 0 fused worker pass, 1 selection, 2 emit, 3 aggregate, 4 apply.
- * Synchronises the context's stream.
+ * Stage timings of the stages GMC_OPT_PROFILE selects: for each stage i < n,
+ * total milliseconds and timed launches since the option was last set.
+ * Stages: 0 fused worker pass (vector kernel; RBGS: its fused gather pass),
+ * 1 fused worker pass (element-wise kernel), 2 selection (RBGS: block draw),
+ * 3 emit, 4 aggregate, 5 apply.  Synchronises the context's stream.
  */
 gmc_status gmc_profile_read(gmc_ctx* ctx, double* ms, int64_t* launches, int32_t n);
+
+/*
+ * Measurement support, not part of the method: a plain copy of n floats
+ * (dst_dev[i] = src_dev[i]) on hip_stream, the reference kernel of known
+ * traffic against which memory counters are scaled.  Buffers must not overlap.
+ */
+gmc_status gmc_calib_copy(void* hip_stream, float* dst_dev, const float* src_dev, int64_t n);
 
 /* Message for the last non-OK status of this context (or of gmc_init when
  * ctx is NULL); never NULL. */

@@ -15,7 +15,9 @@ using namespace gmc;
 
 namespace {
 
-constexpr int kStages = 5;  // fused pass, selection, emit, aggregate, apply
+// profiled stages: fused pass (vector kernel), fused pass (element-wise
+// kernel), selection, emit, aggregate, apply
+constexpr int kStages = 6;
 constexpr int64_t kMaxPendingEvents = 4096;
 
 thread_local std::string g_init_error = "no error";
@@ -64,7 +66,7 @@ struct gmc_ctx {
     int64_t* stats = nullptr;
 
     // profiling
-    bool profile = false;
+    uint32_t profile = 0;  // bit i: time stage i
     double prof_ms[kStages] = {0};
     int64_t prof_n[kStages] = {0};
     std::vector<std::pair<hipEvent_t, hipEvent_t>> pending[kStages];
@@ -127,6 +129,7 @@ struct TopkTables {
     std::vector<int32_t> pair_k, pair_cap;
     std::vector<int64_t> pair_cand;
     std::vector<int32_t> gen_list;  // partial chunks and chunks with an unaligned start
+    std::vector<int32_t> seg_start, slice_seg, slice_rank, seg_slices;
     int64_t cand_total = 0;
 };
 
@@ -144,6 +147,13 @@ TopkTables build_tables(const gmc_ctx* ctx) {
             T.chunk_len.push_back(len);
             T.chunk_seg.push_back(sg);
         }
+        // pad with empty chunks so that a workgroup's chunks never straddle segments
+        while (T.chunk_start.size() % kWavesPerGroup) {
+            T.gen_list.push_back((int32_t)T.chunk_start.size());
+            T.chunk_start.push_back((int32_t)hi);
+            T.chunk_len.push_back(0);
+            T.chunk_seg.push_back(sg);
+        }
         const int32_t last_chunk = (int32_t)T.chunk_start.size();
         T.seg_item_lo.push_back((int32_t)T.item_seg.size());
         int32_t rank = 0;
@@ -156,6 +166,18 @@ TopkTables build_tables(const gmc_ctx* ctx) {
         T.seg_items.push_back(rank);
         T.seg_out.push_back((int32_t)out);
         out += ctx->seg_k[sg];
+    }
+    for (int sg = 0; sg <= n_seg; ++sg) T.seg_start.push_back((int32_t)ctx->seg_off[sg]);
+    for (int sg = 0; sg < n_seg; ++sg) {
+        const int64_t n = ctx->seg_off[sg + 1] - ctx->seg_off[sg];
+        const int64_t cap = std::min<int64_t>(n, (int64_t)ctx->cap_mult * ctx->seg_k[sg] + 2048);
+        int64_t w = std::max((n + kSliceElems - 1) / kSliceElems, (cap + kSliceCands - 1) / kSliceCands);
+        w = std::max<int64_t>(1, std::min<int64_t>(w, kMaxSlices));
+        T.seg_slices.push_back((int32_t)w);
+        for (int32_t r = 0; r < w; ++r) {
+            T.slice_seg.push_back(sg);
+            T.slice_rank.push_back(r);
+        }
     }
     for (int k = 0; k < ctx->K; ++k) {
         for (int sg = 0; sg < n_seg; ++sg) {
@@ -195,6 +217,8 @@ gmc_status prepare(gmc_ctx* ctx) {
         add(ni, 4); add(ni, 4); add(ni, 4); add(ni, 4);
         add(ns, 4); add(ns, 4); add(ns, 4);
         add(np, 4); add(np, 4); add(np, 8);
+        add(T.seg_start.size(), 4); add(T.slice_seg.size(), 4); add(T.slice_rank.size(), 4);
+        add(T.seg_slices.size(), 4);
         add(np, sizeof(PairState));
         add(np * kBins, 4);
         add((size_t)K * nc, 4); add((size_t)K * nc, 4);
@@ -235,6 +259,10 @@ gmc_status prepare(gmc_ctx* ctx) {
         GMC_HIP(ctx, up(ir, T.item_rank));
         GMC_HIP(ctx, up(si, T.seg_items)); GMC_HIP(ctx, up(sl, T.seg_item_lo)); GMC_HIP(ctx, up(so, T.seg_out));
         GMC_HIP(ctx, up(pk, T.pair_k)); GMC_HIP(ctx, up(pc, T.pair_cap)); GMC_HIP(ctx, up(pcd, T.pair_cand));
+        int32_t* sst = cv.take<int32_t>(T.seg_start.size()); int32_t* sls = cv.take<int32_t>(T.slice_seg.size());
+        int32_t* slr = cv.take<int32_t>(T.slice_rank.size()); int32_t* ssl = cv.take<int32_t>(T.seg_slices.size());
+        GMC_HIP(ctx, up(sst, T.seg_start)); GMC_HIP(ctx, up(sls, T.slice_seg));
+        GMC_HIP(ctx, up(slr, T.slice_rank)); GMC_HIP(ctx, up(ssl, T.seg_slices));
         TopkGeometry& g = ctx->geo;
         g.K = K;
         g.n_seg = (int32_t)ns;
@@ -244,6 +272,8 @@ gmc_status prepare(gmc_ctx* ctx) {
         g.item_seg = is; g.item_chunk_lo = il; g.item_chunk_hi = ih; g.item_rank = ir;
         g.seg_items = si; g.seg_item_lo = sl; g.seg_out = so;
         g.pair_k = pk; g.pair_cap = pc; g.pair_cand = pcd;
+        g.n_slices = (int32_t)T.slice_seg.size();
+        g.seg_start = sst; g.slice_seg = sls; g.slice_rank = slr; g.seg_slices = ssl;
         TopkScratch& s = ctx->scr;
         s.pair = cv.take<PairState>(np);
         std::vector<PairState> init(np);
@@ -274,9 +304,9 @@ gmc_status prepare(gmc_ctx* ctx) {
 
 // -- profiling ---------------------------------------------------------------
 
-gmc_status prof_begin(gmc_ctx* ctx, hipEvent_t* ev) {
+gmc_status prof_begin(gmc_ctx* ctx, int stage, hipEvent_t* ev) {
     *ev = nullptr;
-    if (!ctx->profile) return GMC_OK;
+    if (!((ctx->profile >> stage) & 1u)) return GMC_OK;
     GMC_HIP(ctx, hipEventCreate(ev));
     GMC_HIP(ctx, hipEventRecord(*ev, ctx->stream));
     return GMC_OK;
@@ -297,7 +327,7 @@ gmc_status prof_fold(gmc_ctx* ctx, int stage) {
 }
 
 gmc_status prof_end(gmc_ctx* ctx, int stage, hipEvent_t start) {
-    if (!ctx->profile || !start) return GMC_OK;
+    if (!start) return GMC_OK;
     hipEvent_t stop;
     GMC_HIP(ctx, hipEventCreate(&stop));
     GMC_HIP(ctx, hipEventRecord(stop, ctx->stream));
@@ -456,12 +486,12 @@ gmc_status gmc_step(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev,
     const int64_t row_i = gmc_index_len(ctx), row_v = gmc_message_len(ctx);
     hipEvent_t ev;
     if (ctx->comp == GMC_RBGS) {
-        GMC_TRY(prof_begin(ctx, &ev));
+        GMC_TRY(prof_begin(ctx, 2, &ev));
         GMC_LAUNCH(ctx, launch_rbgs_sample(ctx->seed, (uint64_t)ctx->t, ctx->nb, ctx->n_sel, (int32_t)ctx->d,
                                            ctx->block, ctx->K, ctx->rbgs_bitmap, ctx->rbgs_blocks, ctx->rbgs_slot,
                                            idx_dev, row_i, msg_len_dev, ctx->stream));
-        GMC_TRY(prof_end(ctx, 1, ev));
-        GMC_TRY(prof_begin(ctx, &ev));
+        GMC_TRY(prof_end(ctx, 2, ev));
+        GMC_TRY(prof_begin(ctx, 0, &ev));
         GMC_LAUNCH(ctx, launch_rbgs_fused(a, ctx->K, ctx->block, ctx->rbgs_slot, val_dev, row_v, ctx->stream));
         GMC_TRY(prof_end(ctx, 0, ev));
     } else {
@@ -473,42 +503,73 @@ gmc_status gmc_step(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev,
         const uint64_t all = ctx->K == 64 ? ~0ull : ((1ull << ctx->K) - 1ull);
         const int32_t* gl = vec_mask == all ? ctx->gen_list : nullptr;
         const int32_t ng = vec_mask == all ? ctx->n_gen : ctx->geo.n_chunks;
-        GMC_TRY(prof_begin(ctx, &ev));
-        GMC_LAUNCH(ctx, launch_topk_fused(a, ctx->geo, ctx->scr, vec_mask, gl, ng, ctx->stream));
-        GMC_TRY(prof_end(ctx, 0, ev));
-        GMC_TRY(prof_begin(ctx, &ev));
+        if (vec_mask) {
+            GMC_TRY(prof_begin(ctx, 0, &ev));
+            GMC_LAUNCH(ctx, launch_topk_fused_vec(a, ctx->geo, ctx->scr, vec_mask, ctx->stream));
+            GMC_TRY(prof_end(ctx, 0, ev));
+        }
+        if (ng > 0) {
+            GMC_TRY(prof_begin(ctx, 1, &ev));
+            GMC_LAUNCH(ctx, launch_topk_fused_gen(a, ctx->geo, ctx->scr, vec_mask, gl, ng, ctx->stream));
+            GMC_TRY(prof_end(ctx, 1, ev));
+        }
+        GMC_TRY(prof_begin(ctx, 2, &ev));
         for (int pass = 1; pass <= 3; ++pass)
             GMC_LAUNCH(ctx, launch_topk_hist(pass, a, ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
         GMC_LAUNCH(ctx, launch_topk_count(a, ctx->geo, ctx->scr, msg_len_dev, ctx->k_tot, ctx->stream));
-        GMC_TRY(prof_end(ctx, 1, ev));
-        GMC_TRY(prof_begin(ctx, &ev));
-        GMC_LAUNCH(ctx, launch_topk_emit(a, ctx->geo, ctx->scr, idx_dev, val_dev, row_v, ctx->stream));
         GMC_TRY(prof_end(ctx, 2, ev));
+        GMC_TRY(prof_begin(ctx, 3, &ev));
+        GMC_LAUNCH(ctx, launch_topk_emit(a, ctx->geo, ctx->scr, idx_dev, val_dev, row_v, ctx->stream));
+        GMC_TRY(prof_end(ctx, 3, ev));
     }
     ctx->t += 1;
     return GMC_OK;
 }
 
-gmc_status gmc_aggregate(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev, const int64_t* msg_len_dev,
-                         float* update_dev) {
-    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_aggregate: ctx is NULL");
-    if (!idx_dev || !val_dev || !msg_len_dev || !update_dev) return fail(ctx, GMC_EINVAL, "gmc_aggregate: NULL argument");
+}  // extern "C"
+
+namespace {
+
+gmc_status aggregate_impl(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev, const int64_t* msg_len_dev,
+                          float* update_dev, const float* w_in, float* w_out) {
     GMC_TRY(prepare(ctx));
     GMC_HIP(ctx, hipSetDevice(ctx->device));
     const int64_t row_i = gmc_index_len(ctx), row_v = gmc_message_len(ctx);
     hipEvent_t ev;
-    GMC_TRY(prof_begin(ctx, &ev));
+    GMC_TRY(prof_begin(ctx, 4, &ev));
     if (ctx->comp == GMC_RBGS) {
         GMC_LAUNCH(ctx, launch_agg_rbgs(ctx->K, (int32_t)ctx->d, ctx->block, ctx->s, idx_dev, ctx->n_sel, val_dev,
-                                        row_v, update_dev, ctx->stream));
+                                        row_v, update_dev, w_in, w_out, ctx->stream));
     } else {
         GMC_LAUNCH(ctx, launch_agg_rowptr(ctx->K, (int32_t)ctx->d, idx_dev, row_i, msg_len_dev, ctx->rowptr,
                                           ctx->n_ranges, ctx->stream));
         GMC_LAUNCH(ctx, launch_agg_topk(ctx->K, (int32_t)ctx->d, ctx->s, idx_dev, row_i, val_dev, row_v, ctx->rowptr,
-                                        ctx->n_ranges, update_dev, ctx->stream));
+                                        ctx->n_ranges, update_dev, w_in, w_out, ctx->stream));
     }
-    GMC_TRY(prof_end(ctx, 3, ev));
+    GMC_TRY(prof_end(ctx, 4, ev));
     return GMC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+gmc_status gmc_aggregate(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev, const int64_t* msg_len_dev,
+                         float* update_dev) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_aggregate: ctx is NULL");
+    if (!idx_dev || !val_dev || !msg_len_dev || !update_dev) return fail(ctx, GMC_EINVAL, "gmc_aggregate: NULL argument");
+    return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, update_dev, nullptr, nullptr);
+}
+
+gmc_status gmc_aggregate_apply(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev,
+                               const int64_t* msg_len_dev, const float* w_dev, float* w_out_dev,
+                               float* update_dev) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_aggregate_apply: ctx is NULL");
+    if (!idx_dev || !val_dev || !msg_len_dev || !w_dev || !w_out_dev)
+        return fail(ctx, GMC_EINVAL, "gmc_aggregate_apply: NULL argument");
+    if (update_dev && (update_dev == w_out_dev || update_dev == w_dev))
+        return fail(ctx, GMC_EINVAL, "gmc_aggregate_apply: update may not alias w or w_out");
+    return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, update_dev, w_dev, w_out_dev);
 }
 
 gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const float* update_dev) {
@@ -517,9 +578,9 @@ gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const fl
     if (w_prev_out_dev == w_dev) return fail(ctx, GMC_EINVAL, "gmc_apply: w_prev_out may not alias w");
     GMC_HIP(ctx, hipSetDevice(ctx->device));
     hipEvent_t ev;
-    GMC_TRY(prof_begin(ctx, &ev));
+    GMC_TRY(prof_begin(ctx, 5, &ev));
     GMC_LAUNCH(ctx, launch_apply((int32_t)ctx->d, w_dev, w_prev_out_dev, update_dev, ctx->stream));
-    GMC_TRY(prof_end(ctx, 4, ev));
+    GMC_TRY(prof_end(ctx, 5, ev));
     return GMC_OK;
 }
 
@@ -555,7 +616,7 @@ gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value) {
         case GMC_OPT_PROFILE:
             if (ctx->profile) GMC_HIP(ctx, hipStreamSynchronize(ctx->stream));
             prof_clear(ctx);
-            ctx->profile = value != 0;
+            ctx->profile = (uint32_t)value & ((1u << kStages) - 1u);
             return GMC_OK;
         default:
             return fail(ctx, GMC_EINVAL, "gmc_set_option: unknown option");
@@ -593,6 +654,14 @@ void gmc_destroy(gmc_ctx* ctx) {
     prof_clear(ctx);
     release(ctx);
     delete ctx;
+}
+
+gmc_status gmc_calib_copy(void* hip_stream, float* dst_dev, const float* src_dev, int64_t n) {
+    if (!dst_dev || !src_dev || n < 0) return fail(nullptr, GMC_EINVAL, "gmc_calib_copy: bad argument");
+    if (n == 0) return GMC_OK;
+    hipError_t e = launch_calib_copy(dst_dev, src_dev, n, reinterpret_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return hip_fail(nullptr, e, "gmc_calib_copy");
+    return GMC_OK;
 }
 
 }  // extern "C"

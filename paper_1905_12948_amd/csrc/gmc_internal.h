@@ -17,8 +17,13 @@ constexpr int kGroup = kWave * kWavesPerGroup;  // 256 threads
 constexpr int kVecIters = 8;
 constexpr int kChunk = kWave * 4 * kVecIters;   // 2048 elements
 
-// Selection works on "items": runs of up to kItemChunks chunks of one segment.
+// Selection works on "items": runs of up to kItemChunks chunks of one segment
+// (one workgroup each in the emit pass), and on "slices": a segment's
+// selection input split evenly over seg_slices workgroups.
 constexpr int kItemChunks = 32;
+constexpr int64_t kSliceElems = 1 << 19;   // full-data elements per slice (at most)
+constexpr int64_t kSliceCands = 8192;      // candidate capacity per slice (at most)
+constexpr int kMaxSlices = 256;
 
 // Radix select over the 31-bit magnitude key in three digits: 11 + 11 + 9.
 constexpr int kBins = 2048;
@@ -44,11 +49,17 @@ struct PairState {
     uint32_t T;         // threshold key: k-th largest magnitude key
     int32_t r;          // components with key == T to take (lowest index)
     uint32_t done;      // finished workgroups of the current kernel
+    uint32_t cand_used; // candidates of this step (cand is reset for the next)
+    uint32_t pad[7];
 };
 
 // Static geometry of the top-s selection (built on the host at init).
 struct TopkGeometry {
-    int32_t K, n_seg, n_chunks, n_items;
+    int32_t K, n_seg, n_chunks, n_items, n_slices;
+    const int32_t* seg_start;     // [n_seg+1] segment offsets
+    const int32_t* slice_seg;     // [n_slices] segment of each histogram/count slice
+    const int32_t* slice_rank;    // [n_slices] index of the slice within its segment
+    const int32_t* seg_slices;    // [n_seg] slices per segment
     const int32_t* chunk_start;   // [n_chunks]
     const int32_t* chunk_len;     // [n_chunks]
     const int32_t* chunk_seg;     // [n_chunks]
@@ -92,9 +103,11 @@ struct StepArgs {
 // vec_mask: bit k set when worker k's rows (and w_t, w_prev) are 16-byte
 // aligned.  gen_list/n_gen: chunks the element-wise kernel visits (NULL list:
 // chunks 0..n_gen-1).
-hipError_t launch_topk_fused(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
-                             uint64_t vec_mask, const int32_t* gen_list, int32_t n_gen,
-                             hipStream_t st);
+hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
+                                 uint64_t vec_mask, hipStream_t st);
+hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
+                                 uint64_t vec_mask, const int32_t* gen_list, int32_t n_gen,
+                                 hipStream_t st);
 hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
                             const TopkScratch& s, int force_full, int margin, hipStream_t st);
 hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
@@ -112,14 +125,19 @@ hipError_t launch_rbgs_fused(const StepArgs& a, int32_t K, int32_t B, const int3
 hipError_t launch_agg_rowptr(int32_t K, int32_t d, const int32_t* idx, int64_t idx_row,
                              const int64_t* msg_len, int32_t* rowptr, int32_t n_ranges,
                              hipStream_t st);
+// update (nullable) = -(s * sum); with w_out: w_out = w_in + update as well
 hipError_t launch_agg_topk(int32_t K, int32_t d, float s, const int32_t* idx, int64_t idx_row,
                            const float* val, int64_t val_row, const int32_t* rowptr,
-                           int32_t n_ranges, float* update, hipStream_t st);
+                           int32_t n_ranges, float* update, const float* w_in, float* w_out,
+                           hipStream_t st);
 hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, float s, const int32_t* blocks,
                            int32_t n_sel, const float* val, int64_t val_row, float* update,
-                           hipStream_t st);
+                           const float* w_in, float* w_out, hipStream_t st);
 
 hipError_t launch_apply(int32_t d, float* w, float* w_prev_out, const float* update,
                         hipStream_t st);
+
+// plain copy of n floats (memory-counter calibration)
+hipError_t launch_calib_copy(float* dst, const float* src, int64_t n, hipStream_t st);
 
 }  // namespace gmc

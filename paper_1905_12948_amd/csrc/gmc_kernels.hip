@@ -82,6 +82,31 @@ __device__ __forceinline__ uint32_t block_scan_excl(uint32_t v, uint32_t* total,
     return before + x - v;
 }
 
+// Cross-workgroup hand-off without cache flushes.  Everything one workgroup
+// hands to another inside a kernel travels through agent-scope atomics
+// (read-modify-writes, or loads/stores that bypass the non-coherent caches);
+// these two helpers only order them: the producer waits until its atomics
+// have completed before it signals, the consumer issues its reads only after
+// it has seen the signal.  (An agent-scope fence would write back and
+// invalidate the whole L2 in every workgroup.)
+__device__ __forceinline__ void order_release() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));  // vmcnt(0)
+}
+
+__device__ __forceinline__ void order_acquire() {
+    __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));  // vmcnt(0)
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+__device__ __forceinline__ uint32_t load_agent(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void store_agent(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 }  // namespace
 
 // ============================================================================
@@ -149,181 +174,378 @@ __device__ __forceinline__ void append_candidates(Flags flags, const float* e, i
     }
 }
 
-// Vector path: full chunks whose start is a multiple of 4, workers
-// whose g/e rows are 16-byte aligned (bit k of vec_mask), w_t/w_prev aligned.
-__global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
+// ---------------------------------------------------------------------------
+// Vector path with workgroup-level candidate staging.
+//
+// A workgroup owns 4 consecutive chunks of one segment (the chunk table pads
+// each segment to a multiple of 4).  Each wavefront streams its chunk for
+// every worker; a worker's candidates go to a per-worker region of LDS, so
+// the wavefront never waits on a global atomic in the streaming loop.  At the
+// end the workgroup reserves global candidate space with one atomic per
+// worker (all workers' atomics issued together) and copies the staged runs
+// out.  A wavefront whose candidates do not fit in the staging region
+// appends them straight to global memory instead.
+// ---------------------------------------------------------------------------
+
+constexpr int kStageEntries = 4096;             // 32 KiB of (index, value) pairs
+constexpr uint32_t kRunDirect = 0xffffffffu;    // run written straight to global memory
+constexpr uint32_t kRunSkip = 0xfffffffeu;      // chunk owned by the element-wise kernel
+
+struct StageShared {
+    int32_t idx[kStageEntries];
+    float val[kStageEntries];
+    uint32_t used[kMaxWorkers];                 // entries reserved per worker
+    uint32_t run_off[kMaxWorkers][kWavesPerGroup];
+    uint32_t run_cnt[kMaxWorkers][kWavesPerGroup];
+    uint32_t gbase[kMaxWorkers];
+};
+
+__global__ __launch_bounds__(kGroup) __attribute__((amdgpu_waves_per_eu(4))) void topk_fused_vec_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                                 uint64_t vec_mask) {
+    __shared__ StageShared sh;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x >> 6;
+    const int K = g.K;
+    const uint32_t per = kStageEntries / K;     // staging entries per worker
     const int chunk = blockIdx.x * kWavesPerGroup + wave;
-    if (chunk >= g.n_chunks) return;  // wave-uniform; no workgroup barrier below
     const int start = g.chunk_start[chunk];
     const int len = g.chunk_len[chunk];
-    if ((start & 3) != 0 || len != kChunk) return;  // handled by the element-wise kernel
-    const int seg = g.chunk_seg[chunk];
-    const float c = a.c;
-    const float* wt_p = a.w_t + start + lane * 4;
-    const float* wp_p = a.w_prev + start + lane * 4;
+    const int seg = g.chunk_seg[chunk];         // the same for the whole workgroup
+    const bool mine = (start & 3) == 0 && len == kChunk;  // other chunks: element-wise kernel
+    for (int i = threadIdx.x; i < K; i += kGroup) sh.used[i] = 0u;
+    __syncthreads();
 
-    float4 m4[kVecIters];
+    if (mine) {
+        const float c = a.c;
+        const float* wt_p = a.w_t + start + lane * 4;
+        const float* wp_p = a.w_prev + start + lane * 4;
+        float4 m4[kVecIters];
 #pragma unroll
-    for (int i = 0; i < kVecIters; ++i) {
-        const float4 wt = ld4(wt_p + i * (kWave * 4)), wp = ld4(wp_p + i * (kWave * 4));
-        m4[i] = make_float4(c * (wt.x - wp.x), c * (wt.y - wp.y), c * (wt.z - wp.z), c * (wt.w - wp.w));
-    }
+        for (int i = 0; i < kVecIters; ++i) {
+            const float4 wt = ld4(wt_p + i * (kWave * 4)), wp = ld4(wp_p + i * (kWave * 4));
+            m4[i] = make_float4(c * (wt.x - wp.x), c * (wt.y - wp.y), c * (wt.z - wp.z), c * (wt.w - wp.w));
+        }
 #pragma unroll 1
-    for (int k = 0; k < g.K; ++k) {
-        if (!((vec_mask >> k) & 1ull)) continue;
+        for (int k = 0; k < K; ++k) {
+            if (!((vec_mask >> k) & 1ull)) {
+                if (lane == 0) sh.run_off[k][wave] = kRunSkip;
+                continue;
+            }
+            const int p = k * g.n_seg + seg;
+            const uint32_t tau = s.pair[p].tau;
+            float* ep = a.wp.e[k] + start + lane * 4;
+            const float* gp = a.wp.g[k] + start + lane * 4;
+            float4 u[kVecIters], gv[kVecIters];
+#pragma unroll
+            for (int i = 0; i < kVecIters; ++i) {
+                u[i] = ld4(ep + i * (kWave * 4));
+                gv[i] = ld4(gp + i * (kWave * 4));
+            }
+            uint32_t flags = 0;
+#pragma unroll
+            for (int i = 0; i < kVecIters; ++i) {
+                u[i].x = precompress(u[i].x, gv[i].x, m4[i].x);
+                u[i].y = precompress(u[i].y, gv[i].y, m4[i].y);
+                u[i].z = precompress(u[i].z, gv[i].z, m4[i].z);
+                u[i].w = precompress(u[i].w, gv[i].w, m4[i].w);
+                st4(ep + i * (kWave * 4), u[i]);
+                flags |= (key_of(u[i].x) >= tau ? 1u : 0u) << (i * 4 + 0);
+                flags |= (key_of(u[i].y) >= tau ? 1u : 0u) << (i * 4 + 1);
+                flags |= (key_of(u[i].z) >= tau ? 1u : 0u) << (i * 4 + 2);
+                flags |= (key_of(u[i].w) >= tau ? 1u : 0u) << (i * 4 + 3);
+            }
+            if (ballot(flags != 0u) == 0ull) {
+                if (lane == 0) {
+                    sh.run_off[k][wave] = 0u;
+                    sh.run_cnt[k][wave] = 0u;
+                }
+                continue;
+            }
+            // iteration-major order = ascending element index
+            uint32_t lane_pre[kVecIters];
+            uint32_t total = 0;
+#pragma unroll
+            for (int i = 0; i < kVecIters; ++i) {
+                uint32_t tot;
+                const uint32_t pre = wave_prefix_small((uint32_t)__popc((flags >> (i * 4)) & 0xfu), &tot);
+                lane_pre[i] = total + pre;
+                total += tot;
+            }
+            uint32_t off = 0;
+            if (lane == 0) off = atomicAdd(&sh.used[k], total);
+            off = __shfl(off, 0, kWave);
+            if (off + total <= per) {
+                const uint32_t base = (uint32_t)k * per + off;
+                if (lane == 0) {
+                    sh.run_off[k][wave] = base;
+                    sh.run_cnt[k][wave] = total;
+                }
+#pragma unroll
+                for (int i = 0; i < kVecIters; ++i) {
+                    const uint32_t bits = (flags >> (i * 4)) & 0xfu;
+                    uint32_t pos = base + lane_pre[i];
+                    const int j = start + i * (kWave * 4) + lane * 4;
+                    if (bits & 1u) { sh.idx[pos] = j + 0; sh.val[pos] = u[i].x; ++pos; }
+                    if (bits & 2u) { sh.idx[pos] = j + 1; sh.val[pos] = u[i].y; ++pos; }
+                    if (bits & 4u) { sh.idx[pos] = j + 2; sh.val[pos] = u[i].z; ++pos; }
+                    if (bits & 8u) { sh.idx[pos] = j + 3; sh.val[pos] = u[i].w; }
+                }
+            } else {
+                // staging full: append this run to global memory directly
+                uint32_t goff = 0;
+                if (lane == 0) goff = atomicAdd(&s.pair[p].cand, total);
+                goff = __shfl(goff, 0, kWave);
+                const size_t slot = (size_t)k * g.n_chunks + chunk;
+                if (lane == 0) {
+                    s.run_off[slot] = goff;
+                    s.run_cnt[slot] = total;
+                    sh.run_off[k][wave] = kRunDirect;
+                    sh.run_cnt[k][wave] = total;
+                }
+                const uint32_t cap = (uint32_t)g.pair_cap[p];
+                if (goff > cap || total > cap - goff) continue;  // overflow: full-data selection
+                int32_t* ci = s.cand_idx + g.pair_cand[p] + goff;
+                float* cv = s.cand_val + g.pair_cand[p] + goff;
+                const float* e = a.wp.e[k];
+#pragma unroll 1
+                for (int i = 0; i < kVecIters; ++i) {
+                    uint32_t bits = (flags >> (i * 4)) & 0xfu;
+                    uint32_t pos = lane_pre[i];
+                    while (bits) {
+                        const int q = __ffs(bits) - 1;
+                        bits &= bits - 1u;
+                        const int j = start + i * (kWave * 4) + lane * 4 + q;
+                        ci[pos] = j;
+                        cv[pos] = e[j];  // re-read of this lane's own store
+                        ++pos;
+                    }
+                }
+            }
+        }
+    } else if (lane == 0) {
+        for (int k = 0; k < K; ++k) sh.run_off[k][wave] = kRunSkip;
+    }
+    __syncthreads();
+
+    // one global reservation per worker for all staged runs of the workgroup
+    if (threadIdx.x < K) {
+        const int k = threadIdx.x;
+        uint32_t staged = 0;
+        for (int w = 0; w < kWavesPerGroup; ++w)
+            if (sh.run_off[k][w] < kRunSkip) staged += sh.run_cnt[k][w];
+        sh.gbase[k] = staged ? atomicAdd(&s.pair[k * g.n_seg + seg].cand, staged) : 0u;
+    }
+    __syncthreads();
+    if (threadIdx.x < K * kWavesPerGroup) {
+        const int k = threadIdx.x / kWavesPerGroup, w = threadIdx.x % kWavesPerGroup;
+        const uint32_t ro = sh.run_off[k][w];
+        if (ro < kRunSkip) {
+            uint32_t pre = 0;
+            for (int q = 0; q < w; ++q)
+                if (sh.run_off[k][q] < kRunSkip) pre += sh.run_cnt[k][q];
+            const size_t slot = (size_t)k * g.n_chunks + blockIdx.x * kWavesPerGroup + w;
+            s.run_off[slot] = sh.gbase[k] + pre;
+            s.run_cnt[slot] = sh.run_cnt[k][w];
+        }
+    }
+    for (int k = 0; k < K; ++k) {
+        uint32_t cnt[kWavesPerGroup], pre[kWavesPerGroup + 1];
+        pre[0] = 0;
+#pragma unroll
+        for (int w = 0; w < kWavesPerGroup; ++w) {
+            const bool staged = sh.run_off[k][w] < kRunSkip;
+            cnt[w] = staged ? sh.run_cnt[k][w] : 0u;
+            pre[w + 1] = pre[w] + cnt[w];
+        }
+        const uint32_t n = pre[kWavesPerGroup];
+        if (n == 0) continue;
         const int p = k * g.n_seg + seg;
-        const uint32_t tau = s.pair[p].tau;
-        float* e = a.wp.e[k];
-        float* ep = e + start + lane * 4;
-        const float* gp = a.wp.g[k] + start + lane * 4;
-        float4 ev[kVecIters], gv[kVecIters];
-#pragma unroll
-        for (int i = 0; i < kVecIters; ++i) {
-            ev[i] = ld4(ep + i * (kWave * 4));
-            gv[i] = ld4(gp + i * (kWave * 4));
+        const uint32_t base = sh.gbase[k], cap = (uint32_t)g.pair_cap[p];
+        if (base > cap || n > cap - base) continue;  // overflow: full-data selection
+        int32_t* ci = s.cand_idx + g.pair_cand[p] + base;
+        float* cv = s.cand_val + g.pair_cand[p] + base;
+        for (uint32_t i = threadIdx.x; i < n; i += kGroup) {
+            int w = 0;
+            while (i >= pre[w + 1]) ++w;
+            const uint32_t src = sh.run_off[k][w] + (i - pre[w]);
+            ci[i] = sh.idx[src];
+            cv[i] = sh.val[src];
         }
-        uint32_t flags = 0;
-#pragma unroll
-        for (int i = 0; i < kVecIters; ++i) {
-            float4 u;
-            u.x = precompress(ev[i].x, gv[i].x, m4[i].x);
-            u.y = precompress(ev[i].y, gv[i].y, m4[i].y);
-            u.z = precompress(ev[i].z, gv[i].z, m4[i].z);
-            u.w = precompress(ev[i].w, gv[i].w, m4[i].w);
-            st4(ep + i * (kWave * 4), u);
-            flags |= (key_of(u.x) >= tau ? 1u : 0u) << (i * 4 + 0);
-            flags |= (key_of(u.y) >= tau ? 1u : 0u) << (i * 4 + 1);
-            flags |= (key_of(u.z) >= tau ? 1u : 0u) << (i * 4 + 2);
-            flags |= (key_of(u.w) >= tau ? 1u : 0u) << (i * 4 + 3);
-        }
-        append_candidates<kVecIters, 4>(flags, e, start, lane, g, s, k, chunk, p);
     }
 }
 
 // Element-wise path for the (chunk, worker) pairs the vector kernel skips:
-// partial chunks (a segment's last) and chunks with an unaligned start, and
-// workers (or w) whose rows are not 16-byte aligned.  `list` holds the
-// chunk ids to visit (NULL: every chunk).
+// partial chunks (a segment's last), chunks with an unaligned start, and
+// workers (or w) whose rows are not 16-byte aligned.  One wavefront per (chunk, worker);
+// `list` holds the chunk ids to visit (NULL: every chunk).
 __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                                 uint64_t vec_mask, const int32_t* list,
                                                                 int32_t n_list) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x >> 6;
-    const int li = blockIdx.x * kWavesPerGroup + wave;
-    if (li >= n_list) return;
+    const int64_t wid = (int64_t)blockIdx.x * kWavesPerGroup + wave;
+    if (wid >= (int64_t)n_list * g.K) return;  // wave-uniform; no workgroup barrier below
+    const int li = (int)(wid / g.K), k = (int)(wid % g.K);
     const int chunk = list ? list[li] : li;
     const int start = g.chunk_start[chunk];
     const int len = g.chunk_len[chunk];
-    const bool regular = (start & 3) == 0 && len == kChunk;
+    if ((start & 3) == 0 && len == kChunk && ((vec_mask >> k) & 1ull)) return;  // the vector kernel's
     const int seg = g.chunk_seg[chunk];
     const float c = a.c;
     constexpr int kIt = kChunk / kWave;  // 32
-    for (int k = 0; k < g.K; ++k) {
-        if (regular && ((vec_mask >> k) & 1ull)) continue;  // the vector kernel did this one
-        const int p = k * g.n_seg + seg;
-        const uint32_t tau = s.pair[p].tau;
-        float* e = a.wp.e[k];
-        const float* gr = a.wp.g[k];
-        uint32_t flags = 0;
+    const int p = k * g.n_seg + seg;
+    const uint32_t tau = s.pair[p].tau;
+    float* e = a.wp.e[k];
+    const float* gr = a.wp.g[k];
+    uint32_t flags = 0;
 #pragma unroll 4
-        for (int i = 0; i < kIt; ++i) {
-            const int o = i * kWave + lane;
-            if (o < len) {
-                const int j = start + o;
-                const float m = c * (a.w_t[j] - a.w_prev[j]);
-                const float u = precompress(e[j], gr[j], m);
-                e[j] = u;
-                flags |= (key_of(u) >= tau ? 1u : 0u) << i;
-            }
+    for (int i = 0; i < kIt; ++i) {
+        const int o = i * kWave + lane;
+        if (o < len) {
+            const int j = start + o;
+            const float m = c * (a.w_t[j] - a.w_prev[j]);
+            const float u = precompress(e[j], gr[j], m);
+            e[j] = u;
+            flags |= (key_of(u) >= tau ? 1u : 0u) << i;
         }
-        append_candidates<kIt, 1>(flags, e, start, lane, g, s, k, chunk, p);
     }
+    append_candidates<kIt, 1>(flags, e, start, lane, g, s, k, chunk, p);
 }
 
-hipError_t launch_topk_fused(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, uint64_t vec_mask,
-                             const int32_t* gen_list, int32_t n_gen, hipStream_t st) {
-    if (vec_mask) {
-        const int grid = (g.n_chunks + kWavesPerGroup - 1) / kWavesPerGroup;
-        hipLaunchKernelGGL(topk_fused_vec_kernel, dim3(grid), dim3(kGroup), 0, st, a, g, s, vec_mask);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    if (n_gen > 0) {
-        const int grid = (n_gen + kWavesPerGroup - 1) / kWavesPerGroup;
-        hipLaunchKernelGGL(topk_fused_gen_kernel, dim3(grid), dim3(kGroup), 0, st, a, g, s, vec_mask, gen_list,
-                           n_gen);
-    }
+hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
+                                 uint64_t vec_mask, hipStream_t st) {
+    const int grid = (g.n_chunks + kWavesPerGroup - 1) / kWavesPerGroup;
+    hipLaunchKernelGGL(topk_fused_vec_kernel, dim3(grid), dim3(kGroup), 0, st, a, g, s, vec_mask);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
+                                 uint64_t vec_mask, const int32_t* gen_list, int32_t n_gen, hipStream_t st) {
+    const int64_t waves = (int64_t)n_gen * g.K;
+    const int grid = (int)((waves + kWavesPerGroup - 1) / kWavesPerGroup);
+    hipLaunchKernelGGL(topk_fused_gen_kernel, dim3(grid), dim3(kGroup), 0, st, a, g, s, vec_mask, gen_list,
+                       n_gen);
     return hipGetLastError();
 }
 
 // ============================================================================
-// selection: item iteration helpers
+// selection
+//
+// The input of a (worker, segment) pair's selection is either its candidate
+// list (mode 0: the fused pass collected every component whose key reaches
+// the speculative threshold, and there are at least k and at most the
+// capacity of them) or all of the segment's u (mode 1, the full-data path).
+// Histogram and count passes read it as flat slices, one workgroup per
+// slice, in no particular order; the emit pass walks it item by item in
+// index order (an item is kItemChunks consecutive chunks of a segment).
 // ============================================================================
 
 namespace {
 
-// The elements of one item in ascending index order: either the candidate
-// runs of its chunks (mode 0) or the raw residual range (mode 1).
-struct ItemView {
-    int mode;
-    int32_t total;          // elements in the item
-    // mode 0
-    const int32_t* cidx;    // candidate region of the pair
-    const float* cval;
-    // mode 1
-    const float* u;         // worker's u (held in e)
-    int32_t lo;             // first element index of the item
-    int32_t nch;            // chunks in the item
+constexpr int kItemShift = 16;       // log2(kChunk * kItemChunks): elements per item
+constexpr int kSliceLoads = 16;      // independent loads in flight per thread
+constexpr int kMaxSegItems = 4096;   // per-item counters kept in LDS (segments up to 2^28)
+constexpr int kEmitStage = kGroup * kSliceLoads;  // candidates staged in LDS per round
+static_assert((1 << kItemShift) == kChunk * kItemChunks, "item geometry");
+
+// A workgroup's slice of a pair's selection input.
+struct Slice {
+    int64_t lo, hi;          // positions in the input array
+    const float* val;        // mode 0: candidate values; mode 1: u of the segment (held in e)
+    const int32_t* idx;      // mode 0: candidate indices; mode 1: NULL (index = seg_lo + position)
+    int32_t seg_lo;
 };
 
-// Shared memory for an item's run table (mode 0).
+__device__ __forceinline__ Slice open_slice(int mode, uint32_t cand, int k, int seg, int p, int w, int W,
+                                            const StepArgs& a, const TopkGeometry& g, const TopkScratch& s) {
+    Slice v;
+    v.seg_lo = g.seg_start[seg];
+    const int64_t total = mode == 0 ? (int64_t)cand : (int64_t)(g.seg_start[seg + 1] - v.seg_lo);
+    v.lo = total * w / W;
+    v.hi = total * (w + 1) / W;
+    if (mode == 0) {
+        v.val = s.cand_val + g.pair_cand[p];
+        v.idx = s.cand_idx + g.pair_cand[p];
+    } else {
+        v.val = a.wp.e[k] + v.seg_lo;
+        v.idx = nullptr;
+    }
+    return v;
+}
+
+// f(key, index) for every element of the slice; loads are issued
+// kSliceLoads at a time per thread.
+template <bool kNeedIdx, class F>
+__device__ __forceinline__ void for_slice(const Slice& v, F f) {
+    for (int64_t b = v.lo; b < v.hi; b += (int64_t)kGroup * kSliceLoads) {
+        float x[kSliceLoads];
+        int32_t j[kSliceLoads];
+#pragma unroll
+        for (int i = 0; i < kSliceLoads; ++i) {
+            const int64_t pos = b + (int64_t)i * kGroup + threadIdx.x;
+            x[i] = 0.0f;
+            j[i] = 0;
+            if (pos < v.hi) {
+                x[i] = v.val[pos];
+                if (kNeedIdx) j[i] = v.idx ? v.idx[pos] : v.seg_lo + (int32_t)pos;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < kSliceLoads; ++i) {
+            const int64_t pos = b + (int64_t)i * kGroup + threadIdx.x;
+            if (pos < v.hi) f(key_of(x[i]), j[i]);
+        }
+    }
+}
+
+// Runs of an item's chunks in the candidate buffer (mode 0).
 struct ItemShared {
-    uint32_t flat[kItemChunks + 1];  // exclusive prefix of run counts
+    uint32_t flat[kItemChunks + 1];  // exclusive prefix of the runs' counts
     uint32_t roff[kItemChunks];
     uint32_t wsum[kWavesPerGroup];
 };
 
+// An item's elements in ascending index order: its chunks' candidate runs
+// (mode 0) or its range of u (mode 1).
+struct ItemView {
+    int mode;
+    int32_t total;
+    const int32_t* cidx;
+    const float* cval;
+    const float* u;
+    int32_t lo;
+    int32_t nch;
+};
+
 __device__ ItemView open_item(int mode, int k, int it, int p, const StepArgs& a, const TopkGeometry& g,
                               const TopkScratch& s, ItemShared& sh) {
+    static_assert(kItemChunks <= kGroup, "one run per thread");
     ItemView v;
     v.mode = mode;
     const int clo = g.item_chunk_lo[it], chi = g.item_chunk_hi[it];
     v.nch = chi - clo;
+    v.cidx = s.cand_idx + g.pair_cand[p];
+    v.cval = s.cand_val + g.pair_cand[p];
+    v.u = a.wp.e[k];
+    v.lo = g.chunk_start[clo];
     if (mode == 0) {
-        v.cidx = s.cand_idx + g.pair_cand[p];
-        v.cval = s.cand_val + g.pair_cand[p];
-        v.u = nullptr;
-        v.lo = 0;
-        if (threadIdx.x < kWave) {
-            const int lane = threadIdx.x;
-            uint32_t cnt = 0, off = 0;
-            if (lane < v.nch) {
-                const size_t slot = (size_t)k * g.n_chunks + clo + lane;
-                cnt = s.run_cnt[slot];
-                off = s.run_off[slot];
-            }
-            uint32_t x = cnt;
-#pragma unroll
-            for (int o = 1; o < kWave; o <<= 1) {
-                const uint32_t y = __shfl_up(x, o, kWave);
-                if (lane >= o) x += y;
-            }
-            if (lane < v.nch) {
-                sh.flat[lane] = x - cnt;
-                sh.roff[lane] = off;
-            }
-            if (lane == v.nch - 1) sh.flat[v.nch] = x;
+        const int t = threadIdx.x;
+        uint32_t cnt = 0, off = 0;
+        if (t < v.nch) {
+            const size_t slot = (size_t)k * g.n_chunks + clo + t;
+            cnt = s.run_cnt[slot];
+            off = s.run_off[slot];
         }
+        uint32_t total;
+        const uint32_t pre = block_scan_excl(cnt, &total, sh.wsum);
+        if (t < v.nch) {
+            sh.flat[t] = pre;
+            sh.roff[t] = off;
+        }
+        if (t == 0) sh.flat[v.nch] = total;
         __syncthreads();
-        v.total = (int32_t)sh.flat[v.nch];
+        v.total = (int32_t)total;
     } else {
-        v.cidx = nullptr;
-        v.cval = nullptr;
-        v.u = a.wp.e[k];
-        v.lo = g.chunk_start[clo];
         v.total = g.chunk_start[chi - 1] + g.chunk_len[chi - 1] - v.lo;
     }
     return v;
@@ -335,8 +557,7 @@ __device__ __forceinline__ float item_get(const ItemView& v, const ItemShared& s
         *j = v.lo + pos;
         return v.u[v.lo + pos];
     }
-    // largest c with flat[c] <= pos
-    int lo = 0, hi = v.nch - 1;
+    int lo = 0, hi = v.nch - 1;  // largest run c with flat[c] <= pos
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
         if (sh.flat[mid] <= (uint32_t)pos) lo = mid; else hi = mid - 1;
@@ -346,37 +567,24 @@ __device__ __forceinline__ float item_get(const ItemView& v, const ItemShared& s
     return v.cval[cpos];
 }
 
-// Finds the bin b (scanning from the top) with above(b) < need <= above(b) +
-// h[b], where above(b) = sum of bins above b.  h is in shared memory with
-// nbins entries (a multiple of kGroup).  Returns b and *above (all threads).
-__device__ int find_bin(const uint32_t* h, int nbins, uint32_t need, uint32_t* above_out,
-                        uint32_t* sh_scan, int* sh_res) {
+// The bin b (scanning from the top) with above(b) < need <= above(b) + h[b],
+// above(b) = sum of the bins above b; h in LDS, nbins a multiple of kGroup.
+// Returns -1 if the bins hold fewer than need elements.
+__device__ int find_bin(const uint32_t* h, int nbins, uint32_t need, uint32_t* above_out, uint32_t* sh_wsum,
+                        int* sh_res) {
     const int per = nbins / kGroup;
-    // thread t owns bins [t*per, (t+1)*per); suffix order: thread 255 first
     const int t = threadIdx.x;
+    const int rt = kGroup - 1 - t;  // thread rt owns the per bins ending (from the top) at rank rt
     uint32_t mine = 0;
-    for (int q = 0; q < per; ++q) mine += h[t * per + q];
-    // exclusive scan in reverse thread order
-    const int rt = kGroup - 1 - t;
-    // scan over reversed index: use LDS array
-    sh_scan[rt] = mine;
-    __syncthreads();
-    if (t == 0) {
-        uint32_t run = 0;
-        for (int i = 0; i < kGroup; ++i) {
-            const uint32_t x = sh_scan[i];
-            sh_scan[i] = run;
-            run += x;
-        }
-    }
-    __syncthreads();
-    uint32_t above = sh_scan[rt];
+    for (int q = 0; q < per; ++q) mine += h[rt * per + q];
+    uint32_t total;
+    uint32_t above = block_scan_excl(mine, &total, sh_wsum);  // bins above this thread's, in reverse order
     if (t == 0) sh_res[0] = -1;
     __syncthreads();
     for (int q = per - 1; q >= 0; --q) {
-        const uint32_t hb = h[t * per + q];
+        const uint32_t hb = h[rt * per + q];
         if (above < need && need <= above + hb) {
-            sh_res[0] = t * per + q;
+            sh_res[0] = rt * per + q;
             sh_res[1] = (int)above;
         }
         above += hb;
@@ -388,46 +596,61 @@ __device__ int find_bin(const uint32_t* h, int nbins, uint32_t need, uint32_t* a
     return b;
 }
 
+// Workgroup -> (worker, segment, slice) of the histogram and count passes.
+struct SliceId {
+    int k, seg, p, w, W;
+};
+
+__device__ __forceinline__ SliceId slice_id(const TopkGeometry& g) {
+    SliceId id;
+    id.k = blockIdx.x / g.n_slices;
+    const int r = blockIdx.x % g.n_slices;
+    id.seg = g.slice_seg[r];
+    id.w = g.slice_rank[r];
+    id.W = g.seg_slices[id.seg];
+    id.p = id.k * g.n_seg + id.seg;
+    return id;
+}
+
+// Signals that this workgroup's contribution (global atomics) is complete;
+// true in exactly one workgroup of the pair, the last to finish.
+__device__ __forceinline__ bool finish_slice(uint32_t* done, int W, int* sh_flag) {
+    order_release();
+    __syncthreads();
+    if (threadIdx.x == 0) *sh_flag = atomicAdd(done, 1u) == (uint32_t)W - 1u;
+    __syncthreads();
+    if (!*sh_flag) return false;
+    order_acquire();
+    return true;
+}
+
 }  // namespace
 
-// ============================================================================
-// selection: histogram passes
-// ============================================================================
+// ----------------------------------------------------------------------------
+// histogram passes: 11 + 11 + 9 bits of the 31-bit magnitude key
+// ----------------------------------------------------------------------------
 
 template <int PASS>
 __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                            int force_full, int margin) {
     constexpr int nbins = PASS == 3 ? 512 : kBins;
     __shared__ uint32_t h[kBins];
-    __shared__ ItemShared ish;
-    __shared__ uint32_t sh_scan[kGroup];
+    __shared__ uint32_t sh_wsum[kWavesPerGroup];
     __shared__ int sh_res[2];
     __shared__ int sh_last;
 
-    const int k = blockIdx.x / g.n_items;
-    const int it = blockIdx.x % g.n_items;
-    const int seg = g.item_seg[it];
-    const int p = k * g.n_seg + seg;
-    PairState* ps = &s.pair[p];
-    const int kp = g.pair_k[p];
-
-    int mode;
-    uint32_t cand = 0;
-    if (PASS == 1) {
-        cand = ps->cand;
-        mode = (force_full || cand < (uint32_t)kp || cand > (uint32_t)g.pair_cap[p]) ? 1 : 0;
-    } else {
-        mode = ps->mode;
-    }
+    const SliceId id = slice_id(g);
+    PairState* ps = &s.pair[id.p];
+    const int kp = g.pair_k[id.p];
+    const uint32_t cand = PASS == 1 ? ps->cand : ps->cand_used;
+    const int mode = PASS == 1 ? ((force_full || cand < (uint32_t)kp || cand > (uint32_t)g.pair_cap[id.p]) ? 1 : 0)
+                               : ps->mode;
     const uint32_t prefix = PASS == 1 ? 0u : ps->prefix;
 
     for (int b = threadIdx.x; b < nbins; b += kGroup) h[b] = 0u;
-    ItemView v = open_item(mode, k, it, p, a, g, s, ish);  // contains a barrier
     __syncthreads();
-
-    for (int32_t pos = threadIdx.x; pos < v.total; pos += kGroup) {
-        int32_t j;
-        const uint32_t key = key_of(item_get(v, ish, pos, &j));
+    const Slice v = open_slice(mode, cand, id.k, id.seg, id.p, id.w, id.W, a, g, s);
+    for_slice<false>(v, [&](uint32_t key, int32_t) {
         if (PASS == 1) {
             atomicAdd(&h[key >> kShift1], 1u);
         } else if (PASS == 2) {
@@ -435,66 +658,47 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
         } else {
             if ((key >> kShift2) == prefix) atomicAdd(&h[key & 511u], 1u);
         }
-    }
+    });
     __syncthreads();
-
-    uint32_t* gh = s.hist + (size_t)p * kBins;
+    uint32_t* gh = s.hist + (size_t)id.p * kBins;
     for (int b = threadIdx.x; b < nbins; b += kGroup)
         if (h[b]) atomicAdd(&gh[b], h[b]);
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const uint32_t prev = atomicAdd(&ps->done, 1u);
-        sh_last = prev == (uint32_t)g.seg_items[seg] - 1u;
-    }
-    __syncthreads();
-    if (!sh_last) return;
-    __threadfence();
+    if (!finish_slice(&ps->done, id.W, &sh_last)) return;
 
-    // last workgroup of this (worker, segment): read and clear the histogram
+    // last workgroup of the pair: read and clear the histogram, pick the digit
     for (int b = threadIdx.x; b < nbins; b += kGroup) {
-        h[b] = __hip_atomic_load(&gh[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&gh[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        h[b] = load_agent(&gh[b]);
+        store_agent(&gh[b], 0u);
     }
     __syncthreads();
     const uint32_t need = PASS == 1 ? (uint32_t)kp : (uint32_t)ps->need;
     uint32_t above = 0;
-    const int bin = find_bin(h, nbins, need, &above, sh_scan, sh_res);
+    const int bin = find_bin(h, nbins, need, &above, sh_wsum, sh_res);
 
     if (PASS == 1) {
-        // speculative threshold for the next step: the lowest bin down to
+        // speculative threshold of the next step: the lowest bin down to
         // which at least margin*k components were counted this step
-        uint32_t total = 0;
-        for (int b = threadIdx.x; b < nbins; b += kGroup) total += h[b];
-        // reduce total across the block (reuse sh_scan)
-        sh_scan[threadIdx.x] = total;
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            uint32_t t = 0;
-            for (int i = 0; i < kGroup; ++i) t += sh_scan[i];
-            sh_scan[0] = t;
-        }
-        __syncthreads();
-        total = sh_scan[0];
-        __syncthreads();
+        uint32_t mine = 0;
+        for (int b = threadIdx.x; b < nbins; b += kGroup) mine += h[b];
+        uint32_t total;
+        block_scan_excl(mine, &total, sh_wsum);
         const uint64_t want64 = (uint64_t)margin * (uint64_t)kp;
         const uint32_t want = (uint32_t)(want64 < total ? want64 : total);
         uint32_t ab2 = 0;
-        int tb = find_bin(h, nbins, want, &ab2, sh_scan, sh_res);
+        int tb = find_bin(h, nbins, want, &ab2, sh_wsum, sh_res);
         if (threadIdx.x == 0) {
             if (want64 > total && tb > 0) --tb;  // too few counted: widen by one bin
             if (tb < 0) tb = 0;
             ps->tau = (uint32_t)tb << kShift1;
             ps->mode = mode;
-            ps->cand = 0u;
+            ps->cand_used = cand;
+            ps->cand = 0u;  // every workgroup of the pair has read it
             atomicAdd((unsigned long long*)&s.stats[mode == 0 ? 1 : 2], 1ull);
             if (mode == 0) atomicAdd((unsigned long long*)&s.stats[3], (unsigned long long)cand);
         }
     }
     if (threadIdx.x == 0) {
-        if (bin < 0) {
-            atomicAdd((unsigned long long*)&s.stats[4], 1ull);  // cannot happen for valid counts
-        }
+        if (bin < 0) atomicAdd((unsigned long long*)&s.stats[4], 1ull);  // cannot happen for valid counts
         const uint32_t b = bin < 0 ? 0u : (uint32_t)bin;
         if (PASS == 1) {
             ps->prefix = b;
@@ -506,13 +710,13 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
             ps->T = (prefix << 9) | b;
             ps->r = (int32_t)(need - above);
         }
-        __hip_atomic_store(&ps->done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        store_agent(&ps->done, 0u);
     }
 }
 
 hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
                             const TopkScratch& s, int force_full, int margin, hipStream_t st) {
-    const int grid = g.K * g.n_items;
+    const int grid = g.K * g.n_slices;
     if (pass == 1)
         hipLaunchKernelGGL(topk_hist_kernel<1>, dim3(grid), dim3(kGroup), 0, st, a, g, s, force_full, margin);
     else if (pass == 2)
@@ -522,91 +726,73 @@ hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
     return hipGetLastError();
 }
 
-// ============================================================================
-// selection: per-item counts and the scan over a segment's items
-// ============================================================================
+// ----------------------------------------------------------------------------
+// per-item counts above / at the threshold, then the scan over the items
+// ----------------------------------------------------------------------------
 
 __global__ __launch_bounds__(kGroup) void topk_count_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                             int64_t* msg_len, int64_t msg_total) {
-    __shared__ ItemShared ish;
-    __shared__ uint32_t red[2][kWavesPerGroup];
+    __shared__ uint32_t c_above[kMaxSegItems];
+    __shared__ uint32_t c_ties[kMaxSegItems];
+    __shared__ uint32_t sh_wsum[kWavesPerGroup];
     __shared__ int sh_last;
-    __shared__ uint32_t carry[3];
+    __shared__ uint32_t carry[2];
 
-    const int k = blockIdx.x / g.n_items;
-    const int it = blockIdx.x % g.n_items;
-    const int seg = g.item_seg[it];
-    const int p = k * g.n_seg + seg;
-    PairState* ps = &s.pair[p];
+    const SliceId id = slice_id(g);
+    PairState* ps = &s.pair[id.p];
     const int mode = ps->mode;
     const uint32_t T = ps->T;
-
-    ItemView v = open_item(mode, k, it, p, a, g, s, ish);
-    uint32_t above = 0, ties = 0;
-    for (int32_t pos = threadIdx.x; pos < v.total; pos += kGroup) {
-        int32_t j;
-        const uint32_t key = key_of(item_get(v, ish, pos, &j));
-        above += key > T;
-        ties += key == T;
-    }
-    // block reduce
-    for (int o = kWave / 2; o > 0; o >>= 1) {
-        above += __shfl_down(above, o, kWave);
-        ties += __shfl_down(ties, o, kWave);
-    }
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
-    if (lane == 0) {
-        red[0][wave] = above;
-        red[1][wave] = ties;
+    const int n_it = g.seg_items[id.seg];
+    const bool in_lds = n_it <= kMaxSegItems;
+    const size_t base = (size_t)id.k * g.n_items + g.seg_item_lo[id.seg];
+    for (int i = threadIdx.x; i < n_it && in_lds; i += kGroup) {
+        c_above[i] = 0u;
+        c_ties[i] = 0u;
     }
     __syncthreads();
-    const size_t slot = (size_t)k * g.n_items + it;
-    if (threadIdx.x == 0) {
-        uint32_t A = 0, Ti = 0;
-        for (int w = 0; w < kWavesPerGroup; ++w) {
-            A += red[0][w];
-            Ti += red[1][w];
+    const Slice v = open_slice(mode, mode == 0 ? ps->cand_used : 0u, id.k, id.seg, id.p, id.w, id.W, a, g, s);
+    for_slice<true>(v, [&](uint32_t key, int32_t j) {
+        const int item = (j - v.seg_lo) >> kItemShift;
+        if (in_lds) {
+            if (key > T) atomicAdd(&c_above[item], 1u);
+            else if (key == T) atomicAdd(&c_ties[item], 1u);
+        } else {
+            if (key > T) atomicAdd(&s.item_above[base + item], 1u);
+            else if (key == T) atomicAdd(&s.item_ties[base + item], 1u);
         }
-        s.item_above[slot] = A;
-        s.item_ties[slot] = Ti;
-    }
-    __threadfence();
+    });
     __syncthreads();
-    if (threadIdx.x == 0) {
-        const uint32_t prev = atomicAdd(&ps->done, 1u);
-        sh_last = prev == (uint32_t)g.seg_items[seg] - 1u;
+    for (int i = threadIdx.x; i < n_it && in_lds; i += kGroup) {
+        if (c_above[i]) atomicAdd(&s.item_above[base + i], c_above[i]);
+        if (c_ties[i]) atomicAdd(&s.item_ties[base + i], c_ties[i]);
     }
-    __syncthreads();
-    if (!sh_last) return;
-    __threadfence();
+    if (!finish_slice(&ps->done, id.W, &sh_last)) return;
 
     // last workgroup of the pair: scan the segment's items in index order
-    const int n = g.seg_items[seg];
-    const size_t base = (size_t)k * g.n_items + g.seg_item_lo[seg];
     const int32_t r = ps->r;
     if (threadIdx.x == 0) {
         carry[0] = 0;  // ties before
-        carry[1] = 0;  // selected before
-        carry[2] = 0;
+        carry[1] = 0;  // kept before
     }
     __syncthreads();
-    __shared__ uint32_t wsum[kWavesPerGroup];
-    for (int c0 = 0; c0 < n; c0 += kGroup) {
+    for (int c0 = 0; c0 < n_it; c0 += kGroup) {
         const int i = c0 + threadIdx.x;
         uint32_t A = 0, Ti = 0;
-        if (i < n) {
-            A = __hip_atomic_load(&s.item_above[base + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            Ti = __hip_atomic_load(&s.item_ties[base + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (i < n_it) {
+            A = load_agent(&s.item_above[base + i]);
+            Ti = load_agent(&s.item_ties[base + i]);
+            store_agent(&s.item_above[base + i], 0u);
+            store_agent(&s.item_ties[base + i], 0u);
         }
         uint32_t tot_t;
-        const uint32_t tie_pre = carry[0] + block_scan_excl(Ti, &tot_t, wsum);
+        const uint32_t tie_pre = carry[0] + block_scan_excl(Ti, &tot_t, sh_wsum);
         int64_t take = (int64_t)r - (int64_t)tie_pre;
         if (take < 0) take = 0;
         if (take > (int64_t)Ti) take = Ti;
         const uint32_t sel = A + (uint32_t)take;
         uint32_t tot_s;
-        const uint32_t sel_pre = carry[1] + block_scan_excl(sel, &tot_s, wsum);
-        if (i < n) {
+        const uint32_t sel_pre = carry[1] + block_scan_excl(sel, &tot_s, sh_wsum);
+        if (i < n_it) {
             s.item_tiebase[base + i] = tie_pre;
             s.item_out[base + i] = sel_pre;
         }
@@ -618,27 +804,38 @@ __global__ __launch_bounds__(kGroup) void topk_count_kernel(StepArgs a, TopkGeom
         __syncthreads();
     }
     if (threadIdx.x == 0) {
-        if (carry[1] != (uint32_t)g.pair_k[p]) atomicAdd((unsigned long long*)&s.stats[4], 1ull);
-        if (seg == 0) msg_len[k] = msg_total;
-        __hip_atomic_store(&ps->done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (carry[1] != (uint32_t)g.pair_k[id.p]) atomicAdd((unsigned long long*)&s.stats[4], 1ull);
+        if (id.seg == 0) msg_len[id.k] = msg_total;
+        store_agent(&ps->done, 0u);
     }
 }
 
 hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                              int64_t* msg_len, int64_t msg_total, hipStream_t st) {
-    hipLaunchKernelGGL(topk_count_kernel, dim3(g.K * g.n_items), dim3(kGroup), 0, st, a, g, s,
-                       msg_len, msg_total);
+    hipLaunchKernelGGL(topk_count_kernel, dim3(g.K * g.n_slices), dim3(kGroup), 0, st, a, g, s, msg_len,
+                       msg_total);
     return hipGetLastError();
 }
 
-// ============================================================================
-// selection: ordered emission of the kept components
-// ============================================================================
+// ----------------------------------------------------------------------------
+// ordered emission of the kept components
+// ----------------------------------------------------------------------------
+
+// One workgroup per item.  The item's elements are staged in LDS in rounds
+// of kEmitStage with all loads in flight together; in a round each thread
+// owns kSliceLoads consecutive elements, one block-wide scan of its
+// (above, tie) counts places them, and the thread writes its kept ones in
+// order.  LDS rows are padded by one word per kSliceLoads entries so the
+// threads' strided reads hit distinct banks.
+__device__ __forceinline__ int stage_slot(int q) { return q + (q >> 4); }
 
 __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                            int32_t* idx, float* val, int64_t row_len) {
+    static_assert(kSliceLoads == 16, "stage_slot pads every 16 entries");
+    constexpr int kStageSlots = kEmitStage + kEmitStage / 16;
     __shared__ ItemShared ish;
-    __shared__ uint32_t wcnt[2][kWavesPerGroup];
+    __shared__ int32_t st_idx[kStageSlots];
+    __shared__ float st_val[kStageSlots];
 
     const int k = blockIdx.x / g.n_items;
     const int it = blockIdx.x % g.n_items;
@@ -651,59 +848,68 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
     const size_t slot = (size_t)k * g.n_items + it;
     const uint32_t out0 = s.item_out[slot];
     const int64_t tiebase = s.item_tiebase[slot];
-    int64_t ties_quota = r - tiebase;
-    if (ties_quota < 0) ties_quota = 0;
+    int64_t quota = r - tiebase;  // ties this item may still take, in index order
+    if (quota < 0) quota = 0;
 
     const uint32_t kseg = (uint32_t)g.pair_k[p];
     int32_t* irow = idx + (size_t)k * row_len + g.seg_out[seg];
     float* vrow = val + (size_t)k * row_len + g.seg_out[seg];
     float* e = a.wp.e[k];
 
-    ItemView v = open_item(mode, k, it, p, a, g, s, ish);
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
-    uint32_t run_above = 0, run_ties = 0;
-    for (int32_t b0 = 0; b0 < v.total; b0 += kGroup) {
-        const int32_t pos = b0 + threadIdx.x;
-        bool is_above = false, is_tie = false;
-        int32_t j = 0;
-        float x = 0.0f;
-        if (pos < v.total) {
-            x = item_get(v, ish, pos, &j);
-            const uint32_t key = key_of(x);
-            is_above = key > T;
-            is_tie = key == T;
-        }
-        const uint64_t am = ballot(is_above), tm = ballot(is_tie);
-        if (lane == 0) {
-            wcnt[0][wave] = popc64(am);
-            wcnt[1][wave] = popc64(tm);
-        }
-        __syncthreads();
-        uint32_t a_before = run_above + popc64(am & lanemask_lt());
-        uint32_t t_before = run_ties + popc64(tm & lanemask_lt());
-        uint32_t a_tot = 0, t_tot = 0;
+    const ItemView v = open_item(mode, k, it, p, a, g, s, ish);
+    uint32_t run_above = 0, run_ties = 0;  // over the earlier rounds
+    for (int32_t s0 = 0; s0 < v.total; s0 += kEmitStage) {
+        const int32_t ns = v.total - s0 < kEmitStage ? v.total - s0 : kEmitStage;
 #pragma unroll
-        for (int w = 0; w < kWavesPerGroup; ++w) {
-            if (w < wave) {
-                a_before += wcnt[0][w];
-                t_before += wcnt[1][w];
+        for (int i = 0; i < kSliceLoads; ++i) {
+            const int32_t q = i * kGroup + threadIdx.x;
+            if (q < ns) {
+                int32_t j;
+                const float x = item_get(v, ish, s0 + q, &j);
+                st_idx[stage_slot(q)] = j;
+                st_val[stage_slot(q)] = x;
             }
-            a_tot += wcnt[0][w];
-            t_tot += wcnt[1][w];
         }
         __syncthreads();
-        const bool take = is_above || (is_tie && (int64_t)t_before < ties_quota);
-        if (take) {
-            const int64_t taken_ties = (int64_t)t_before < ties_quota ? (int64_t)t_before : ties_quota;
-            const uint32_t o = out0 + a_before + (uint32_t)taken_ties;
-            if (o < kseg) {  // always true when the counts are consistent
+        const int32_t q0 = threadIdx.x * kSliceLoads;
+        uint32_t na = 0, nt = 0;
+#pragma unroll
+        for (int i = 0; i < kSliceLoads; ++i) {
+            if (q0 + i < ns) {
+                const uint32_t key = key_of(st_val[stage_slot(q0 + i)]);
+                na += key > T;
+                nt += key == T;
+            }
+        }
+        uint32_t tot;
+        const uint32_t pre = block_scan_excl((na << 16) | nt, &tot, ish.wsum);  // counts < 2^16
+        uint32_t a_before = run_above + (pre >> 16), t_before = run_ties + (pre & 0xffffu);
+#pragma unroll
+        for (int i = 0; i < kSliceLoads; ++i) {
+            if (q0 + i >= ns) break;
+            const float x = st_val[stage_slot(q0 + i)];
+            const uint32_t key = key_of(x);
+            bool take = false;
+            uint32_t o = 0;
+            if (key > T) {
+                take = true;
+                o = out0 + a_before + (uint32_t)((int64_t)t_before < quota ? (int64_t)t_before : quota);
+                ++a_before;
+            } else if (key == T) {
+                take = (int64_t)t_before < quota;
+                o = out0 + a_before + t_before;
+                ++t_before;
+            }
+            if (take && o < kseg) {  // o < kseg always holds when the counts are consistent
+                const int32_t j = st_idx[stage_slot(q0 + i)];
                 irow[o] = j;
                 vrow[o] = x;
                 e[j] = x - x;  // residual u - C(u) at a kept component
             }
         }
-        run_above += a_tot;
-        run_ties += t_tot;
+        run_above += tot >> 16;
+        run_ties += tot & 0xffffu;
+        __syncthreads();
     }
 }
 
@@ -784,7 +990,7 @@ __global__ __launch_bounds__(kGroup) void rbgs_sample_kernel(uint64_t seed, uint
         if (threadIdx.x == 0) carry += tot;
         __syncthreads();
     }
-    __threadfence();
+    __threadfence_block();
     __syncthreads();
     // message length: all selected blocks are full except possibly block nb-1
     const int32_t last = blocks[n_sel - 1];
@@ -892,115 +1098,217 @@ hipError_t launch_rbgs_fused(const StepArgs& a, int32_t K, int32_t B, const int3
 // server: sum over workers in worker order, dense update
 // ============================================================================
 
-// rowptr[k][r] = first message position of worker k whose index falls in
-// range r (ranges of kAggRange elements); rowptr[k][n_ranges] = length.
-// Out-of-range or non-ascending indices cannot make it write outside rowptr.
+// Writes update = -(s * acc) for the n components of a range starting at base
+// (when update is not NULL) and, with kApply, w_out = w_in + update.
+template <bool kApply>
+__device__ __forceinline__ void write_update(const float* acc, float s, int64_t base, int64_t n, float* update,
+                                             const float* w_in, float* w_out) {
+    const bool vec = n == kAggRange && (base & 3) == 0 && (update == nullptr || aligned16(update)) &&
+                     (!kApply || (aligned16(w_in) && aligned16(w_out)));
+    if (vec) {
+        for (int q = threadIdx.x * 4; q < kAggRange; q += kGroup * 4) {
+            const float4 dl = make_float4(-(s * acc[q]), -(s * acc[q + 1]), -(s * acc[q + 2]), -(s * acc[q + 3]));
+            if (update) st4(update + base + q, dl);
+            if (kApply) {
+                const float4 x = ld4(w_in + base + q);
+                st4(w_out + base + q, make_float4(x.x + dl.x, x.y + dl.y, x.z + dl.z, x.w + dl.w));
+            }
+        }
+    } else {
+        for (int q = threadIdx.x; q < n; q += kGroup) {
+            const float dl = -(s * acc[q]);
+            if (update) update[base + q] = dl;
+            if (kApply) w_out[base + q] = w_in[base + q] + dl;
+        }
+    }
+}
+
+// rowptr[k][r] = first message position of worker k whose index is >= r*R
+// (a lower bound by binary search over the worker's ascending row);
+// rowptr[k][n_ranges] = the row's length.  Any row content keeps every entry
+// within [0, length].
 __global__ __launch_bounds__(kGroup) void agg_rowptr_kernel(int32_t K, int32_t d, const int32_t* idx,
                                                             int64_t idx_row, const int64_t* msg_len,
                                                             int32_t* rowptr, int32_t n_ranges) {
     const int k = blockIdx.y;
-    const int64_t i = (int64_t)blockIdx.x * kGroup + threadIdx.x;
+    const int32_t r = blockIdx.x * kGroup + threadIdx.x;
+    if (r > n_ranges) return;
     int64_t L = msg_len[k];
     if (L < 0) L = 0;
     if (L > idx_row) L = idx_row;
     int32_t* rp = rowptr + (size_t)k * (n_ranges + 1);
-    auto range_of = [&](int64_t q) -> int64_t {
-        int64_t x = idx[(size_t)k * idx_row + q];
-        if (x < 0) x = 0;
-        if (x >= d) x = d - 1;
-        return x / kAggRange;
-    };
-    if (L == 0) {
-        if (i == 0)
-            for (int32_t rr = 0; rr <= n_ranges; ++rr) rp[rr] = 0;
+    if (r == n_ranges) {
+        rp[r] = (int32_t)L;
         return;
     }
-    if (i >= L) return;
-    const int64_t rc = range_of(i);
-    const int64_t rprev = i == 0 ? -1 : range_of(i - 1);
-    for (int64_t rr = rprev + 1; rr <= rc; ++rr) rp[rr] = (int32_t)i;
-    if (i == L - 1)
-        for (int64_t rr = (rc > rprev ? rc : rprev) + 1; rr <= n_ranges; ++rr) rp[rr] = (int32_t)L;
+    const int64_t target = (int64_t)r * kAggRange;
+    const int32_t* row = idx + (size_t)k * idx_row;
+    int64_t lo = 0, hi = L;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if ((int64_t)row[mid] < target) lo = mid + 1; else hi = mid;
+    }
+    rp[r] = (int32_t)lo;
 }
 
 hipError_t launch_agg_rowptr(int32_t K, int32_t d, const int32_t* idx, int64_t idx_row,
                              const int64_t* msg_len, int32_t* rowptr, int32_t n_ranges,
                              hipStream_t st) {
-    const int gx = (int)((idx_row + kGroup - 1) / kGroup);
-    hipLaunchKernelGGL(agg_rowptr_kernel, dim3(gx > 0 ? gx : 1, K), dim3(kGroup), 0, st, K, d, idx, idx_row,
-                       msg_len, rowptr, n_ranges);
+    const int gx = (n_ranges + 1 + kGroup - 1) / kGroup;
+    hipLaunchKernelGGL(agg_rowptr_kernel, dim3(gx, K), dim3(kGroup), 0, st, K, d, idx, idx_row, msg_len,
+                       rowptr, n_ranges);
     return hipGetLastError();
 }
 
+// One workgroup per range of kAggRange components.  The workgroup first
+// issues its loads of w (fused apply), then fetches the K workers' entries of
+// the range into LDS together (one round of loads) and adds them to the
+// range's accumulator one worker after the other; a range with more entries
+// than the staging holds reads them worker by worker instead.
+constexpr int kAggStage = 1024;
+
+template <bool kApply>
 __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, float s, const int32_t* idx,
                                                           int64_t idx_row, const float* val, int64_t val_row,
                                                           const int32_t* rowptr, int32_t n_ranges,
-                                                          float* update) {
+                                                          float* update, const float* w_in, float* w_out) {
+    static_assert(kAggRange == kGroup * 8, "8 components per thread");
     __shared__ float acc[kAggRange];
+    __shared__ int32_t st_idx[kAggStage];
+    __shared__ float st_val[kAggStage];
+    __shared__ int32_t src[kMaxWorkers];
+    __shared__ int32_t pre[kMaxWorkers + 1];
     const int r = blockIdx.x;
     const int64_t base = (int64_t)r * kAggRange;
-    for (int q = threadIdx.x; q < kAggRange; q += kGroup) acc[q] = 0.0f;
-    __syncthreads();
-    for (int k = 0; k < K; ++k) {
-        const int32_t* rp = rowptr + (size_t)k * (n_ranges + 1);
-        int32_t lo = rp[r], hi = rp[r + 1];
-        for (int32_t i = lo + threadIdx.x; i < hi; i += kGroup) {
-            const int64_t j = (int64_t)idx[(size_t)k * idx_row + i] - base;
-            if (j >= 0 && j < kAggRange) acc[j] = acc[j] + val[(size_t)k * val_row + i];
-        }
-        __syncthreads();  // worker k's additions land before worker k+1's
-    }
     const int64_t n = (int64_t)d - base < kAggRange ? (int64_t)d - base : kAggRange;
-    if (n == kAggRange && aligned16(update) && (base & 3) == 0) {
-        for (int q = threadIdx.x * 4; q < kAggRange; q += kGroup * 4)
-            st4(update + base + q, make_float4(-(s * acc[q]), -(s * acc[q + 1]), -(s * acc[q + 2]), -(s * acc[q + 3])));
+    const bool vec = n == kAggRange && (update == nullptr || aligned16(update)) &&
+                     (!kApply || (aligned16(w_in) && aligned16(w_out)));
+    // this thread's components: [base + 4t, +4) and [base + 1024 + 4t, +4)
+    const int q0 = threadIdx.x * 4, q1 = kGroup * 4 + threadIdx.x * 4;
+    float4 w0 = make_float4(0.f, 0.f, 0.f, 0.f), w1 = w0;
+    if (kApply && vec) {
+        w0 = ld4(w_in + base + q0);
+        w1 = ld4(w_in + base + q1);
+    }
+    for (int q = threadIdx.x; q < kAggRange; q += kGroup) acc[q] = 0.0f;
+    if (threadIdx.x < K) {
+        const int32_t* rp = rowptr + (size_t)threadIdx.x * (n_ranges + 1);
+        const int32_t lo = rp[r], hi = rp[r + 1];
+        src[threadIdx.x] = lo;
+        pre[threadIdx.x + 1] = hi > lo ? hi - lo : 0;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        pre[0] = 0;
+        for (int k = 0; k < K; ++k) pre[k + 1] += pre[k];
+    }
+    __syncthreads();
+    const int32_t total = pre[K];
+    if (total <= kAggStage) {
+        for (int32_t i = threadIdx.x; i < total; i += kGroup) {
+            int k = 0;
+            while (i >= pre[k + 1]) ++k;
+            const int64_t q = (int64_t)src[k] + (i - pre[k]);
+            st_idx[i] = idx[(size_t)k * idx_row + q];
+            st_val[i] = val[(size_t)k * val_row + q];
+        }
+        __syncthreads();
+        for (int k = 0; k < K; ++k) {
+            if (pre[k + 1] > pre[k]) {
+                for (int32_t i = pre[k] + threadIdx.x; i < pre[k + 1]; i += kGroup) {
+                    const int64_t j = (int64_t)st_idx[i] - base;
+                    if (j >= 0 && j < kAggRange) acc[j] = acc[j] + st_val[i];
+                }
+                __syncthreads();  // worker k's additions land before worker k+1's
+            }
+        }
     } else {
-        for (int q = threadIdx.x; q < n; q += kGroup) update[base + q] = -(s * acc[q]);
+        for (int k = 0; k < K; ++k) {
+            for (int32_t i = threadIdx.x; i < pre[k + 1] - pre[k]; i += kGroup) {
+                const int64_t q = (int64_t)src[k] + i;
+                const int64_t j = (int64_t)idx[(size_t)k * idx_row + q] - base;
+                if (j >= 0 && j < kAggRange) acc[j] = acc[j] + val[(size_t)k * val_row + q];
+            }
+            __syncthreads();
+        }
+    }
+    __syncthreads();
+    if (vec) {
+        const float4 d0 = make_float4(-(s * acc[q0]), -(s * acc[q0 + 1]), -(s * acc[q0 + 2]), -(s * acc[q0 + 3]));
+        const float4 d1 = make_float4(-(s * acc[q1]), -(s * acc[q1 + 1]), -(s * acc[q1 + 2]), -(s * acc[q1 + 3]));
+        if (update) {
+            st4(update + base + q0, d0);
+            st4(update + base + q1, d1);
+        }
+        if (kApply) {
+            st4(w_out + base + q0, make_float4(w0.x + d0.x, w0.y + d0.y, w0.z + d0.z, w0.w + d0.w));
+            st4(w_out + base + q1, make_float4(w1.x + d1.x, w1.y + d1.y, w1.z + d1.z, w1.w + d1.w));
+        }
+    } else {
+        write_update<kApply>(acc, s, base, n, update, w_in, w_out);
     }
 }
 
 hipError_t launch_agg_topk(int32_t K, int32_t d, float s, const int32_t* idx, int64_t idx_row,
                            const float* val, int64_t val_row, const int32_t* rowptr,
-                           int32_t n_ranges, float* update, hipStream_t st) {
-    hipLaunchKernelGGL(agg_topk_kernel, dim3(n_ranges), dim3(kGroup), 0, st, K, d, s, idx, idx_row, val,
-                       val_row, rowptr, n_ranges, update);
+                           int32_t n_ranges, float* update, const float* w_in, float* w_out,
+                           hipStream_t st) {
+    if (w_out)
+        hipLaunchKernelGGL(agg_topk_kernel<true>, dim3(n_ranges), dim3(kGroup), 0, st, K, d, s, idx, idx_row, val,
+                           val_row, rowptr, n_ranges, update, w_in, w_out);
+    else
+        hipLaunchKernelGGL(agg_topk_kernel<false>, dim3(n_ranges), dim3(kGroup), 0, st, K, d, s, idx, idx_row, val,
+                           val_row, rowptr, n_ranges, update, w_in, w_out);
     return hipGetLastError();
 }
 
 // RBGS: every worker sent the same blocks (ascending ids in blocks[0..n_sel));
-// a component of block blocks[q] sits at q*B + offset in each message.
+// a component of block blocks[q] sits at q*B + offset in each message.  One
+// workgroup per range of kAggRange components, like the top-s kernel.
+template <bool kApply>
 __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, int32_t B, float s,
                                                           const int32_t* blocks, int32_t n_sel,
                                                           const float* val, int64_t val_row,
-                                                          float* update) {
-    const int64_t j = (int64_t)blockIdx.x * kGroup + threadIdx.x;
-    if (j >= d) return;
-    const int32_t b = (int32_t)(j / B);
-    // binary search for b among the ascending block ids
-    int lo = 0, hi = n_sel - 1, slot = -1;
-    while (lo <= hi) {
-        const int mid = (lo + hi) >> 1;
-        const int32_t x = blocks[mid];
-        if (x == b) {
-            slot = mid;
-            break;
+                                                          float* update, const float* w_in, float* w_out) {
+    __shared__ float acc[kAggRange];
+    const int64_t base = (int64_t)blockIdx.x * kAggRange;
+    const int64_t n = (int64_t)d - base < kAggRange ? (int64_t)d - base : kAggRange;
+    for (int q = threadIdx.x; q < kAggRange; q += kGroup) {
+        float a = 0.0f;
+        if (q < n) {
+            const int64_t j = base + q;
+            const int32_t b = (int32_t)(j / B);
+            int lo = 0, hi = n_sel - 1, slot = -1;
+            while (lo <= hi) {  // ascending block ids
+                const int mid = (lo + hi) >> 1;
+                const int32_t x = blocks[mid];
+                if (x == b) {
+                    slot = mid;
+                    break;
+                }
+                if (x < b) lo = mid + 1; else hi = mid - 1;
+            }
+            if (slot >= 0) {
+                const int64_t vpos = (int64_t)slot * B + (j - (int64_t)b * B);
+                for (int k = 0; k < K; ++k) a = a + val[(size_t)k * val_row + vpos];
+            }
         }
-        if (x < b) lo = mid + 1; else hi = mid - 1;
+        acc[q] = a;
     }
-    float acc = 0.0f;
-    if (slot >= 0) {
-        const int64_t vpos = (int64_t)slot * B + (j - (int64_t)b * B);
-        for (int k = 0; k < K; ++k) acc = acc + val[(size_t)k * val_row + vpos];
-    }
-    update[j] = -(s * acc);
+    __syncthreads();
+    write_update<kApply>(acc, s, base, n, update, w_in, w_out);
 }
 
 hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, float s, const int32_t* blocks,
                            int32_t n_sel, const float* val, int64_t val_row, float* update,
-                           hipStream_t st) {
-    const int grid = (int)(((int64_t)d + kGroup - 1) / kGroup);
-    hipLaunchKernelGGL(agg_rbgs_kernel, dim3(grid), dim3(kGroup), 0, st, K, d, B, s, blocks, n_sel, val, val_row,
-                       update);
+                           const float* w_in, float* w_out, hipStream_t st) {
+    const int grid = (int)(((int64_t)d + kAggRange - 1) / kAggRange);
+    if (w_out)
+        hipLaunchKernelGGL(agg_rbgs_kernel<true>, dim3(grid), dim3(kGroup), 0, st, K, d, B, s, blocks, n_sel, val,
+                           val_row, update, w_in, w_out);
+    else
+        hipLaunchKernelGGL(agg_rbgs_kernel<false>, dim3(grid), dim3(kGroup), 0, st, K, d, B, s, blocks, n_sel, val,
+                           val_row, update, w_in, w_out);
     return hipGetLastError();
 }
 
@@ -1031,6 +1339,26 @@ hipError_t launch_apply(int32_t d, float* w, float* w_prev_out, const float* upd
     const int64_t threads = ((int64_t)d + 3) / 4;
     const int grid = (int)((threads + kGroup - 1) / kGroup);
     hipLaunchKernelGGL(apply_kernel, dim3(grid), dim3(kGroup), 0, st, d, w, w_prev_out, update);
+    return hipGetLastError();
+}
+
+// ============================================================================
+// plain copy, the reference for memory-counter calibration
+// ============================================================================
+
+__global__ __launch_bounds__(kGroup) void calib_copy_kernel(float* dst, const float* src, int64_t n) {
+    const int64_t i = ((int64_t)blockIdx.x * kGroup + threadIdx.x) * 4;
+    if (i + 4 <= n && aligned16(dst) && aligned16(src)) {
+        st4(dst + i, ld4(src + i));
+        return;
+    }
+    for (int64_t q = i; q < i + 4 && q < n; ++q) dst[q] = src[q];
+}
+
+hipError_t launch_calib_copy(float* dst, const float* src, int64_t n, hipStream_t st) {
+    const int64_t threads = (n + 3) / 4;
+    const int grid = (int)((threads + kGroup - 1) / kGroup);
+    hipLaunchKernelGGL(calib_copy_kernel, dim3(grid), dim3(kGroup), 0, st, dst, src, n);
     return hipGetLastError();
 }
 

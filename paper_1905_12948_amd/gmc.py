@@ -19,14 +19,15 @@ GMC_TOPK_GLOBAL, GMC_TOPK_SEGMENTED, GMC_RBGS = 0, 1, 2
 GMC_OK, GMC_EINVAL, GMC_ENOMEM, GMC_EDEVICE, GMC_ESTATE = 0, -1, -2, -3, -4
 GMC_OPT_FORCE_FULL_SELECT, GMC_OPT_CAND_MARGIN, GMC_OPT_CAND_CAP_MULT, GMC_OPT_PROFILE = 1, 2, 3, 4
 MAX_WORKERS = 64
-STAGES = ("fused", "select", "emit", "aggregate", "apply")
+STAGES = ("fused_vec", "fused_gen", "select", "emit", "aggregate", "apply")
 
 COMPRESSORS = {"topk": GMC_TOPK_GLOBAL, "topk_seg": GMC_TOPK_SEGMENTED, "rbgs": GMC_RBGS}
 
 # every entry point include/gmc.h declares
 EXPORTS = ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "gmc_message_len",
            "gmc_index_len", "gmc_step", "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step",
-           "gmc_set_option", "gmc_stats", "gmc_profile_read", "gmc_last_error", "gmc_destroy")
+           "gmc_set_option", "gmc_stats", "gmc_profile_read", "gmc_last_error", "gmc_destroy",
+           "gmc_calib_copy", "gmc_aggregate_apply")
 
 
 class GmcError(RuntimeError):
@@ -69,9 +70,11 @@ def load() -> ctypes.CDLL:
     lib.gmc_last_error.restype = ctypes.c_char_p
     lib.gmc_destroy.argtypes = [P]
     lib.gmc_destroy.restype = None
+    lib.gmc_calib_copy.argtypes = [P, P, P, i64]
+    lib.gmc_aggregate_apply.argtypes = [P, P, P, P, P, P, P]
     for name in ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "gmc_step",
                  "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step", "gmc_set_option",
-                 "gmc_stats", "gmc_profile_read"):
+                 "gmc_stats", "gmc_profile_read", "gmc_calib_copy", "gmc_aggregate_apply"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -110,6 +113,19 @@ def _rows(x, d: int, K: int, name: str) -> List[int]:
     if len(x) != K:
         raise ValueError("%s must hold K=%d tensors" % (name, K))
     return [_check(t, torch.float32, d, "%s[%d]" % (name, k)) for k, t in enumerate(x)]
+
+
+def calib_copy(dst, src):
+    """Plain device copy dst[:] = src[:] (fp32), the reference kernel for
+    memory-counter calibration."""
+    torch = _torch()
+    n = src.numel()
+    pd = _check(dst, torch.float32, n, "dst")
+    ps = _check(src, torch.float32, n, "src")
+    lib = load()
+    st = lib.gmc_calib_copy(ctypes.c_void_p(torch.cuda.current_stream(src.device).cuda_stream), pd, ps, n)
+    if st != GMC_OK:
+        raise GmcError(st, lib.gmc_last_error(None).decode())
 
 
 class Gmc:
@@ -200,6 +216,19 @@ class Gmc:
         self._stream(update.device)
         self._call(self._lib.gmc_aggregate(self._ctx, pi, pv, pl, pu))
 
+    def aggregate_apply(self, idx, val, msg_len, w, w_out, update=None):
+        """w_out = w + update (update = the server's dense update, written to
+        `update` when given); w_out may be w itself."""
+        torch = _torch()
+        pi = _check(idx, torch.int32, self.K * self.index_len, "idx")
+        pv = _check(val, torch.float32, self.K * self.message_len, "val")
+        pl = _check(msg_len, torch.int64, self.K, "msg_len")
+        pw = _check(w, torch.float32, self.d, "w")
+        po = _check(w_out, torch.float32, self.d, "w_out")
+        pu = None if update is None else _check(update, torch.float32, self.d, "update")
+        self._stream(w.device)
+        self._call(self._lib.gmc_aggregate_apply(self._ctx, pi, pv, pl, pw, po, pu))
+
     def apply(self, w, update, w_prev_out=None):
         torch = _torch()
         pw = _check(w, torch.float32, self.d, "w")
@@ -228,8 +257,15 @@ class Gmc:
         keys = ("steps", "from_candidates", "full_data", "candidates", "count_errors")
         return {k: int(out[i]) for i, k in enumerate(keys)}
 
-    def profile(self, on: bool = True):
-        self.set_option(GMC_OPT_PROFILE, 1 if on else 0)
+    def profile(self, stages=None):
+        """Time the given stage names (None: all; []: off) with HIP events."""
+        if stages is None:
+            mask = (1 << len(STAGES)) - 1
+        else:
+            mask = 0
+            for name in stages:
+                mask |= 1 << STAGES.index(name)
+        self.set_option(GMC_OPT_PROFILE, mask)
 
     def profile_read(self) -> dict:
         ms = (ctypes.c_double * len(STAGES))()

@@ -44,6 +44,8 @@ class Case:
     row_pad: int = 0              # extra floats between worker rows (misaligned rows)
     grad_hook: Optional[Callable] = None   # (t, grads) -> grads, host side
     label: str = ""
+    fused_apply: bool = False     # gmc_aggregate_apply out of place, buffers swapped
+    write_update: bool = True     # with fused_apply: also materialise the update
 
 
 def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
@@ -88,8 +90,12 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
         for k in range(K):
             g_rows[k].copy_(torch.from_numpy(gr[k]))
         g.step(w, wp, g_rows, e_rows, idx, val, ln)
-        g.aggregate(idx, val, ln, upd)
-        g.apply(w, upd, w_prev_out=wp)
+        if case.fused_apply:
+            g.aggregate_apply(idx, val, ln, w, wp, update=upd if case.write_update else None)
+            w, wp = wp, w
+        else:
+            g.aggregate(idx, val, ln, upd)
+            g.apply(w, upd, w_prev_out=wp)
 
         oi, ov, ol = orc.step(w_h, wp_h, gr, e_h)
         od = orc.aggregate(oi, ov, ol)
@@ -111,7 +117,8 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
             m = int(ol[k])
             assert_same_f32(gv[k, :m], ov[k, :m], tag + ": values of worker %d" % k)
             assert_same_f32(e_rows[k].cpu().numpy(), e_h[k], tag + ": residual of worker %d" % k)
-        assert_same_f32(upd.cpu().numpy(), od, tag + ": update")
+        if case.write_update or not case.fused_apply:
+            assert_same_f32(upd.cpu().numpy(), od, tag + ": update")
         assert_same_f32(w.cpu().numpy(), w_h, tag + ": w")
         assert_same_f32(wp.cpu().numpy(), wp_h, tag + ": w_prev")
         if verbose:

@@ -111,3 +111,20 @@ def test_rbgs_partial_last_block_and_small_blocks():
     wl = synth.Workload("rb7", [999], K=2, ratio=0.3, beta=0.9, eta=0.1, steps=3,
                         compressor="rbgs", dist="normal", block=7)
     run_lockstep(Case(wl, steps=3, label="rbgs-block7"))
+
+
+def test_many_workers_overflow_the_staging():
+    # K = 64 leaves 64 staging entries per worker and workgroup; a generous
+    # candidate margin pushes wavefronts onto the direct global append
+    wl = W("resnet50").shrunk(256, K=64)
+    run_lockstep(Case(wl, steps=3, options=((OPT_MARGIN, 200),), label="K=64"))
+
+
+@pytest.mark.parametrize("name,shrink,steps", [("resnet50", 32, 4), ("rbgs", 16, 4), ("gpt2", 64, 3)])
+def test_fused_aggregate_apply_swapping_buffers(name, shrink, steps):
+    run_lockstep(Case(W(name).shrunk(shrink), steps=steps, fused_apply=True, label="fused/" + name))
+
+
+def test_fused_aggregate_apply_without_update():
+    run_lockstep(Case(W("resnet18").shrunk(16, K=4), steps=3, fused_apply=True, write_update=False,
+                      label="fused-no-update"))
