@@ -136,6 +136,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="resnet50", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--grad-batches", type=int, default=4)
+    ap.add_argument("--margin", type=int, default=None,
+                    help="candidate margin (multiple of k) of the speculative selection")
     ap.add_argument("--cpu-workers", type=int, default=2)
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -162,6 +164,9 @@ def main():
     seg = wl.topk_segments().tolist() if wl.compressor == "topk_seg" else None
     gm = Gmc(d, K, wl.compressor, wl.ratio, wl.beta, wl.eta, seed=wl.seed, segments=seg,
              block=wl.block if wl.compressor == "rbgs" else None)
+    if args.margin is not None:
+        from paper_1905_12948_amd import GMC_OPT_CAND_MARGIN
+        gm.set_option(GMC_OPT_CAND_MARGIN, args.margin)
     log("workload %s: d=%d K=%d %s ratio=%g; generating %d gradient batches on the GPU"
         % (wl.name, d, K, wl.compressor, wl.ratio, args.grad_batches))
     w = sdev.w0(wl, dev)

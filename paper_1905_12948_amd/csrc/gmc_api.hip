@@ -42,7 +42,7 @@ struct gmc_ctx {
     std::vector<int64_t> seg_off;  // top-s segments (host)
     int32_t block = 4096;          // RBGS block length
     int force_full = 0;
-    int margin = 4;
+    int margin = 2;
     int cap_mult = 16;
 
     // derived
@@ -90,6 +90,12 @@ gmc_status hip_fail(gmc_ctx* ctx, hipError_t e, const char* what) {
         if (e_ != hipSuccess) return hip_fail(ctx, e_, #call); \
     } while (0)
 
+#define GMC_TRY(x)                       \
+    do {                                 \
+        gmc_status st_ = (x);            \
+        if (st_ != GMC_OK) return st_;   \
+    } while (0)
+
 int64_t count_for(int64_t n, double ratio) {
     const double x = ratio * (double)n;
     int64_t k = (int64_t)std::ceil(x);
@@ -123,22 +129,28 @@ struct Carver {
 
 // Host-side tables of the top-s geometry.
 struct TopkTables {
+    std::vector<int32_t> seg_start, seg_out;
     std::vector<int32_t> chunk_start, chunk_len, chunk_seg;
-    std::vector<int32_t> item_seg, item_lo, item_hi, item_rank;
-    std::vector<int32_t> seg_items, seg_item_lo, seg_out;
+    std::vector<int32_t> cgrp_lo, cgrp_hi, cgrp_seg, cgrp_rank, seg_cgrp_lo, seg_cgrps;
+    std::vector<int32_t> slice_seg, slice_rank, seg_slices, seg_slice_lo;
     std::vector<int32_t> pair_k, pair_cap;
     std::vector<int64_t> pair_cand;
     std::vector<int32_t> gen_list;  // partial chunks and chunks with an unaligned start
-    std::vector<int32_t> seg_start, slice_seg, slice_rank, seg_slices;
     int64_t cand_total = 0;
 };
+
+int64_t pair_capacity(const gmc_ctx* ctx, int64_t n, int64_t k) {
+    return std::min<int64_t>(n, (int64_t)ctx->cap_mult * k + 2048);
+}
 
 TopkTables build_tables(const gmc_ctx* ctx) {
     TopkTables T;
     const int n_seg = (int)ctx->seg_off.size() - 1;
     int64_t out = 0;
+    for (int sg = 0; sg <= n_seg; ++sg) T.seg_start.push_back((int32_t)ctx->seg_off[sg]);
     for (int sg = 0; sg < n_seg; ++sg) {
-        const int64_t lo = ctx->seg_off[sg], hi = ctx->seg_off[sg + 1];
+        const int64_t lo = ctx->seg_off[sg], hi = ctx->seg_off[sg + 1], n = hi - lo;
+        // chunks of kChunk elements
         const int32_t first_chunk = (int32_t)T.chunk_start.size();
         for (int64_t a = lo; a < hi; a += kChunk) {
             const int32_t len = (int32_t)std::min<int64_t>(kChunk, hi - a);
@@ -147,44 +159,35 @@ TopkTables build_tables(const gmc_ctx* ctx) {
             T.chunk_len.push_back(len);
             T.chunk_seg.push_back(sg);
         }
-        // pad with empty chunks so that a workgroup's chunks never straddle segments
-        while (T.chunk_start.size() % kWavesPerGroup) {
-            T.gen_list.push_back((int32_t)T.chunk_start.size());
-            T.chunk_start.push_back((int32_t)hi);
-            T.chunk_len.push_back(0);
-            T.chunk_seg.push_back(sg);
-        }
         const int32_t last_chunk = (int32_t)T.chunk_start.size();
-        T.seg_item_lo.push_back((int32_t)T.item_seg.size());
+        // compaction groups
+        T.seg_cgrp_lo.push_back((int32_t)T.cgrp_lo.size());
         int32_t rank = 0;
-        for (int32_t c = first_chunk; c < last_chunk; c += kItemChunks) {
-            T.item_seg.push_back(sg);
-            T.item_lo.push_back(c);
-            T.item_hi.push_back(std::min(c + kItemChunks, last_chunk));
-            T.item_rank.push_back(rank++);
+        for (int32_t c = first_chunk; c < last_chunk; c += kCompactChunks) {
+            T.cgrp_lo.push_back(c);
+            T.cgrp_hi.push_back(std::min(c + kCompactChunks, last_chunk));
+            T.cgrp_seg.push_back(sg);
+            T.cgrp_rank.push_back(rank++);
         }
-        T.seg_items.push_back(rank);
-        T.seg_out.push_back((int32_t)out);
-        out += ctx->seg_k[sg];
-    }
-    for (int sg = 0; sg <= n_seg; ++sg) T.seg_start.push_back((int32_t)ctx->seg_off[sg]);
-    for (int sg = 0; sg < n_seg; ++sg) {
-        const int64_t n = ctx->seg_off[sg + 1] - ctx->seg_off[sg];
-        const int64_t cap = std::min<int64_t>(n, (int64_t)ctx->cap_mult * ctx->seg_k[sg] + 2048);
+        T.seg_cgrps.push_back(rank);
+        // slices of the selection passes
+        const int64_t cap = pair_capacity(ctx, n, ctx->seg_k[sg]);
         int64_t w = std::max((n + kSliceElems - 1) / kSliceElems, (cap + kSliceCands - 1) / kSliceCands);
         w = std::max<int64_t>(1, std::min<int64_t>(w, kMaxSlices));
+        T.seg_slice_lo.push_back((int32_t)T.slice_seg.size());
         T.seg_slices.push_back((int32_t)w);
         for (int32_t r = 0; r < w; ++r) {
             T.slice_seg.push_back(sg);
             T.slice_rank.push_back(r);
         }
+        T.seg_out.push_back((int32_t)out);
+        out += ctx->seg_k[sg];
     }
     for (int k = 0; k < ctx->K; ++k) {
         for (int sg = 0; sg < n_seg; ++sg) {
             const int64_t n = ctx->seg_off[sg + 1] - ctx->seg_off[sg];
-            const int64_t kk = ctx->seg_k[sg];
-            const int64_t cap = std::min<int64_t>(n, (int64_t)ctx->cap_mult * kk + 2048);
-            T.pair_k.push_back((int32_t)kk);
+            const int64_t cap = pair_capacity(ctx, n, ctx->seg_k[sg]);
+            T.pair_k.push_back(ctx->seg_k[sg]);
             T.pair_cap.push_back((int32_t)cap);
             T.pair_cand.push_back(T.cand_total);
             T.cand_total += cap;
@@ -211,21 +214,21 @@ gmc_status prepare(gmc_ctx* ctx) {
         add((size_t)ctx->nb, 4);
     } else {
         T = build_tables(ctx);
-        const size_t nc = T.chunk_start.size(), ni = T.item_seg.size(), ns = T.seg_items.size();
-        const size_t np = (size_t)K * ns;
+        const size_t nc = T.chunk_start.size(), ng = T.cgrp_lo.size(), nsl = T.slice_seg.size();
+        const size_t ns = T.seg_out.size(), np = (size_t)K * ns;
+        add(ns + 1, 4); add(ns, 4);
         add(nc, 4); add(nc, 4); add(nc, 4);
-        add(ni, 4); add(ni, 4); add(ni, 4); add(ni, 4);
-        add(ns, 4); add(ns, 4); add(ns, 4);
+        add(ng, 4); add(ng, 4); add(ng, 4); add(ng, 4); add(ns, 4); add(ns, 4);
+        add(nsl, 4); add(nsl, 4); add(ns, 4); add(ns, 4);
         add(np, 4); add(np, 4); add(np, 8);
-        add(T.seg_start.size(), 4); add(T.slice_seg.size(), 4); add(T.slice_rank.size(), 4);
-        add(T.seg_slices.size(), 4);
+        add(T.gen_list.size() + 1, 4);
         add(np, sizeof(PairState));
         add(np * kBins, 4);
-        add((size_t)K * nc, 4); add((size_t)K * nc, 4);
+        add((size_t)K * nc, 4); add((size_t)K * nc, 4); add((size_t)K * ng, 4);
+        add((size_t)K * nc * kChunk, 4); add((size_t)K * nc * kChunk, 4);
         add((size_t)T.cand_total, 4); add((size_t)T.cand_total, 4);
-        for (int q = 0; q < 4; ++q) add((size_t)K * ni, 4);
+        for (int q = 0; q < 4; ++q) add((size_t)K * nsl, 4);
         add((size_t)K * (ctx->n_ranges + 1), 4);
-        add(T.gen_list.size() + 1, 4);
     }
     bytes += 256;
     void* mem = nullptr;
@@ -244,58 +247,66 @@ gmc_status prepare(gmc_ctx* ctx) {
         ctx->rbgs_blocks = cv.take<int32_t>(ctx->n_sel);
         ctx->rbgs_slot = cv.take<int32_t>(ctx->nb);
     } else {
-        const size_t nc = T.chunk_start.size(), ni = T.item_seg.size(), ns = T.seg_items.size();
-        const size_t np = (size_t)K * ns;
-        auto up = [&](auto* dst, const auto& v) -> hipError_t {
-            return hipMemcpy(dst, v.data(), v.size() * sizeof(v[0]), hipMemcpyHostToDevice);
+        const size_t nc = T.chunk_start.size(), ng = T.cgrp_lo.size(), nsl = T.slice_seg.size();
+        const size_t ns = T.seg_out.size(), np = (size_t)K * ns;
+        auto put = [&](const std::vector<int32_t>& v, const int32_t** dst) -> gmc_status {
+            int32_t* d = cv.take<int32_t>(v.size() + (v.empty() ? 1 : 0));
+            if (!v.empty()) GMC_HIP(ctx, hipMemcpy(d, v.data(), v.size() * 4, hipMemcpyHostToDevice));
+            *dst = d;
+            return GMC_OK;
         };
-        int32_t* cs = cv.take<int32_t>(nc); int32_t* cl = cv.take<int32_t>(nc); int32_t* cg = cv.take<int32_t>(nc);
-        int32_t* is = cv.take<int32_t>(ni); int32_t* il = cv.take<int32_t>(ni); int32_t* ih = cv.take<int32_t>(ni);
-        int32_t* ir = cv.take<int32_t>(ni);
-        int32_t* si = cv.take<int32_t>(ns); int32_t* sl = cv.take<int32_t>(ns); int32_t* so = cv.take<int32_t>(ns);
-        int32_t* pk = cv.take<int32_t>(np); int32_t* pc = cv.take<int32_t>(np); int64_t* pcd = cv.take<int64_t>(np);
-        GMC_HIP(ctx, up(cs, T.chunk_start)); GMC_HIP(ctx, up(cl, T.chunk_len)); GMC_HIP(ctx, up(cg, T.chunk_seg));
-        GMC_HIP(ctx, up(is, T.item_seg)); GMC_HIP(ctx, up(il, T.item_lo)); GMC_HIP(ctx, up(ih, T.item_hi));
-        GMC_HIP(ctx, up(ir, T.item_rank));
-        GMC_HIP(ctx, up(si, T.seg_items)); GMC_HIP(ctx, up(sl, T.seg_item_lo)); GMC_HIP(ctx, up(so, T.seg_out));
-        GMC_HIP(ctx, up(pk, T.pair_k)); GMC_HIP(ctx, up(pc, T.pair_cap)); GMC_HIP(ctx, up(pcd, T.pair_cand));
-        int32_t* sst = cv.take<int32_t>(T.seg_start.size()); int32_t* sls = cv.take<int32_t>(T.slice_seg.size());
-        int32_t* slr = cv.take<int32_t>(T.slice_rank.size()); int32_t* ssl = cv.take<int32_t>(T.seg_slices.size());
-        GMC_HIP(ctx, up(sst, T.seg_start)); GMC_HIP(ctx, up(sls, T.slice_seg));
-        GMC_HIP(ctx, up(slr, T.slice_rank)); GMC_HIP(ctx, up(ssl, T.seg_slices));
         TopkGeometry& g = ctx->geo;
         g.K = K;
         g.n_seg = (int32_t)ns;
         g.n_chunks = (int32_t)nc;
-        g.n_items = (int32_t)ni;
-        g.chunk_start = cs; g.chunk_len = cl; g.chunk_seg = cg;
-        g.item_seg = is; g.item_chunk_lo = il; g.item_chunk_hi = ih; g.item_rank = ir;
-        g.seg_items = si; g.seg_item_lo = sl; g.seg_out = so;
-        g.pair_k = pk; g.pair_cap = pc; g.pair_cand = pcd;
-        g.n_slices = (int32_t)T.slice_seg.size();
-        g.seg_start = sst; g.slice_seg = sls; g.slice_rank = slr; g.seg_slices = ssl;
-        TopkScratch& s = ctx->scr;
-        s.pair = cv.take<PairState>(np);
+        g.n_cgroups = (int32_t)ng;
+        g.n_slices = (int32_t)nsl;
+        GMC_TRY(put(T.seg_start, &g.seg_start));
+        GMC_TRY(put(T.seg_out, &g.seg_out));
+        GMC_TRY(put(T.chunk_start, &g.chunk_start));
+        GMC_TRY(put(T.chunk_len, &g.chunk_len));
+        GMC_TRY(put(T.chunk_seg, &g.chunk_seg));
+        GMC_TRY(put(T.cgrp_lo, &g.cgrp_lo));
+        GMC_TRY(put(T.cgrp_hi, &g.cgrp_hi));
+        GMC_TRY(put(T.cgrp_seg, &g.cgrp_seg));
+        GMC_TRY(put(T.cgrp_rank, &g.cgrp_rank));
+        GMC_TRY(put(T.seg_cgrp_lo, &g.seg_cgrp_lo));
+        GMC_TRY(put(T.seg_cgrps, &g.seg_cgrps));
+        GMC_TRY(put(T.slice_seg, &g.slice_seg));
+        GMC_TRY(put(T.slice_rank, &g.slice_rank));
+        GMC_TRY(put(T.seg_slices, &g.seg_slices));
+        GMC_TRY(put(T.seg_slice_lo, &g.seg_slice_lo));
+        GMC_TRY(put(T.pair_k, &g.pair_k));
+        GMC_TRY(put(T.pair_cap, &g.pair_cap));
+        int64_t* pcd = cv.take<int64_t>(np);
+        GMC_HIP(ctx, hipMemcpy(pcd, T.pair_cand.data(), np * 8, hipMemcpyHostToDevice));
+        g.pair_cand = pcd;
+        const int32_t* gl = nullptr;
+        GMC_TRY(put(T.gen_list, &gl));
+        ctx->gen_list = const_cast<int32_t*>(gl);
+        ctx->n_gen = (int32_t)T.gen_list.size();
+        TopkScratch& sc = ctx->scr;
+        sc.pair = cv.take<PairState>(np);
         std::vector<PairState> init(np);
         for (auto& ps : init) {
             std::memset(&ps, 0, sizeof ps);
             ps.tau = kNoThreshold;
         }
-        GMC_HIP(ctx, up(s.pair, init));
-        s.hist = cv.take<uint32_t>(np * kBins);
-        s.run_off = cv.take<uint32_t>((size_t)K * nc);
-        s.run_cnt = cv.take<uint32_t>((size_t)K * nc);
-        s.cand_idx = cv.take<int32_t>((size_t)T.cand_total);
-        s.cand_val = cv.take<float>((size_t)T.cand_total);
-        s.item_above = cv.take<uint32_t>((size_t)K * ni);
-        s.item_ties = cv.take<uint32_t>((size_t)K * ni);
-        s.item_out = cv.take<uint32_t>((size_t)K * ni);
-        s.item_tiebase = cv.take<uint32_t>((size_t)K * ni);
-        s.stats = ctx->stats;
+        GMC_HIP(ctx, hipMemcpy(sc.pair, init.data(), np * sizeof(PairState), hipMemcpyHostToDevice));
+        sc.hist = cv.take<uint32_t>(np * kBins);
+        sc.run_cnt = cv.take<uint32_t>((size_t)K * nc);
+        sc.run_pre = cv.take<uint32_t>((size_t)K * nc);
+        sc.grp_total = cv.take<uint32_t>((size_t)K * ng);
+        sc.slot_idx = cv.take<int32_t>((size_t)K * nc * kChunk);
+        sc.slot_val = cv.take<float>((size_t)K * nc * kChunk);
+        sc.cand_idx = cv.take<int32_t>((size_t)T.cand_total);
+        sc.cand_val = cv.take<float>((size_t)T.cand_total);
+        sc.sl_above = cv.take<uint32_t>((size_t)K * nsl);
+        sc.sl_ties = cv.take<uint32_t>((size_t)K * nsl);
+        sc.sl_out = cv.take<uint32_t>((size_t)K * nsl);
+        sc.sl_tiebase = cv.take<uint32_t>((size_t)K * nsl);
+        sc.stats = ctx->stats;
         ctx->rowptr = cv.take<int32_t>((size_t)K * (ctx->n_ranges + 1));
-        ctx->gen_list = cv.take<int32_t>(T.gen_list.size() + 1);
-        ctx->n_gen = (int32_t)T.gen_list.size();
-        if (ctx->n_gen) GMC_HIP(ctx, up(ctx->gen_list, T.gen_list));
     }
     if (cv.off > bytes) return fail(ctx, GMC_ENOMEM, "internal: scratch layout overflow");
     ctx->prepared = true;
@@ -354,11 +365,6 @@ void prof_clear(gmc_ctx* ctx) {
         if (e_ != hipSuccess) return hip_fail(ctx, e_, #call); \
     } while (0)
 
-#define GMC_TRY(x)                       \
-    do {                                 \
-        gmc_status st_ = (x);            \
-        if (st_ != GMC_OK) return st_;   \
-    } while (0)
 
 }  // namespace
 
@@ -514,6 +520,7 @@ gmc_status gmc_step(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev,
             GMC_TRY(prof_end(ctx, 1, ev));
         }
         GMC_TRY(prof_begin(ctx, 2, &ev));
+        GMC_LAUNCH(ctx, launch_topk_compact(ctx->geo, ctx->scr, ctx->stream));
         for (int pass = 1; pass <= 3; ++pass)
             GMC_LAUNCH(ctx, launch_topk_hist(pass, a, ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
         GMC_LAUNCH(ctx, launch_topk_count(a, ctx->geo, ctx->scr, msg_len_dev, ctx->k_tot, ctx->stream));

@@ -9,18 +9,23 @@ namespace gmc {
 
 constexpr int kMaxWorkers = 64;
 
-// Fused worker pass: a workgroup of 4 wavefronts; each wavefront owns one
-// chunk of kChunk consecutive elements (64 lanes x 4 floats x 8 iterations).
+// Fused worker pass: chunks of kChunk consecutive elements of a segment; the
+// vector kernel gives one workgroup (256 threads x 8 floats) to each (chunk,
+// worker), the element-wise kernel one wavefront.
 constexpr int kWave = 64;
 constexpr int kWavesPerGroup = 4;
 constexpr int kGroup = kWave * kWavesPerGroup;  // 256 threads
 constexpr int kVecIters = 8;
 constexpr int kChunk = kWave * 4 * kVecIters;   // 2048 elements
 
-// Selection works on "items": runs of up to kItemChunks chunks of one segment
-// (one workgroup each in the emit pass), and on "slices": a segment's
-// selection input split evenly over seg_slices workgroups.
-constexpr int kItemChunks = 32;
+// Selection: the fused pass leaves each (worker, chunk)'s candidates in the
+// chunk's own staging slot; compaction groups of kCompactChunks chunks pack
+// them, in index order, into the pair's candidate list (each group's copy is
+// split over kCompactParts workgroups).  The histogram, count and emit passes
+// read the list (or, on the full-data path, the segment's u) as "slices":
+// seg_slices even shares, one workgroup each.
+constexpr int kCompactChunks = 256;        // chunks per compaction group (one per thread)
+constexpr int kCompactParts = 8;
 constexpr int64_t kSliceElems = 1 << 19;   // full-data elements per slice (at most)
 constexpr int64_t kSliceCands = 8192;      // candidate capacity per slice (at most)
 constexpr int kMaxSlices = 256;
@@ -55,37 +60,41 @@ struct PairState {
 
 // Static geometry of the top-s selection (built on the host at init).
 struct TopkGeometry {
-    int32_t K, n_seg, n_chunks, n_items, n_slices;
+    int32_t K, n_seg, n_chunks, n_cgroups, n_slices;
     const int32_t* seg_start;     // [n_seg+1] segment offsets
-    const int32_t* slice_seg;     // [n_slices] segment of each histogram/count slice
-    const int32_t* slice_rank;    // [n_slices] index of the slice within its segment
-    const int32_t* seg_slices;    // [n_seg] slices per segment
+    const int32_t* seg_out;       // [n_seg] offset of the segment in a message row
     const int32_t* chunk_start;   // [n_chunks]
     const int32_t* chunk_len;     // [n_chunks]
     const int32_t* chunk_seg;     // [n_chunks]
-    const int32_t* item_seg;      // [n_items]
-    const int32_t* item_chunk_lo; // [n_items]
-    const int32_t* item_chunk_hi; // [n_items]
-    const int32_t* item_rank;     // [n_items] index of the item within its segment
-    const int32_t* seg_items;     // [n_seg] items per segment
-    const int32_t* seg_item_lo;   // [n_seg] first item of the segment
-    const int32_t* seg_out;       // [n_seg] offset of the segment in a message row
+    const int32_t* cgrp_lo;       // [n_cgroups] first chunk of the group
+    const int32_t* cgrp_hi;       // [n_cgroups] one past its last chunk
+    const int32_t* cgrp_seg;      // [n_cgroups] its segment
+    const int32_t* cgrp_rank;     // [n_cgroups] its index within the segment
+    const int32_t* seg_cgrp_lo;   // [n_seg] first group of the segment
+    const int32_t* seg_cgrps;     // [n_seg] groups of the segment
+    const int32_t* slice_seg;     // [n_slices] segment of the slice
+    const int32_t* slice_rank;    // [n_slices] index of the slice within its segment
+    const int32_t* seg_slices;    // [n_seg] slices of the segment
+    const int32_t* seg_slice_lo;  // [n_seg] first slice of the segment
     const int32_t* pair_k;        // [K*n_seg]
     const int32_t* pair_cap;      // [K*n_seg]
-    const int64_t* pair_cand;     // [K*n_seg] start of the pair's candidate region
+    const int64_t* pair_cand;     // [K*n_seg] start of the pair's candidate list
 };
 
 struct TopkScratch {
     PairState* pair;              // [K*n_seg]
     uint32_t* hist;               // [K*n_seg][kBins]
-    uint32_t* run_off;            // [K*n_chunks]
-    uint32_t* run_cnt;            // [K*n_chunks]
-    int32_t* cand_idx;            // [sum cap]
+    uint32_t* run_cnt;            // [K*n_chunks] candidates of (worker, chunk)
+    uint32_t* run_pre;            // [K*n_chunks] exclusive prefix of run_cnt within the group
+    uint32_t* grp_total;          // [K*n_cgroups]
+    int32_t* slot_idx;            // [K*n_chunks][kChunk] candidates of (worker, chunk), index order
+    float* slot_val;              // [K*n_chunks][kChunk]
+    int32_t* cand_idx;            // [sum cap] candidate lists, ascending index
     float* cand_val;              // [sum cap]
-    uint32_t* item_above;         // [K*n_items]
-    uint32_t* item_ties;          // [K*n_items]
-    uint32_t* item_out;           // [K*n_items]
-    uint32_t* item_tiebase;       // [K*n_items]
+    uint32_t* sl_above;           // [K*n_slices] kept-above-threshold count of each slice
+    uint32_t* sl_ties;            // [K*n_slices] at-threshold count
+    uint32_t* sl_out;             // [K*n_slices] message offset of the slice's first kept component
+    uint32_t* sl_tiebase;         // [K*n_slices] at-threshold components in earlier slices
     int64_t* stats;               // [8]
 };
 
@@ -108,6 +117,7 @@ hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const
 hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                                  uint64_t vec_mask, const int32_t* gen_list, int32_t n_gen,
                                  hipStream_t st);
+hipError_t launch_topk_compact(const TopkGeometry& g, const TopkScratch& s, hipStream_t st);  // count + copy
 hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
                             const TopkScratch& s, int force_full, int margin, hipStream_t st);
 hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,

@@ -4,13 +4,14 @@
 //
 //   topk_fused   u_k = (e_k + g_k) - c (w_t - w_prev) for every worker, written
 //                over e_k; components whose magnitude key reaches the pair's
-//                speculative threshold are appended to a candidate list
+//                speculative threshold are kept as candidates
+//   topk_compact packs each pair's candidates into a list in index order
 //   topk_hist    three radix-select passes (11 + 11 + 9 bits of the key) over
 //                the candidates, or over all of u when the candidates cannot
 //                prove they hold the top k; the last workgroup of each
 //                (worker, segment) picks the digit
-//   topk_count   per item counts above / at the threshold, then a scan over
-//                the segment's items (last workgroup)
+//   topk_count   per-slice counts above / at the threshold, then a scan over
+//                the segment's slices (last workgroup)
 //   topk_emit    ordered compaction of the kept components into the message,
 //                residual u - u at the kept components
 //   rbgs_*       shared block draw and the fused pass that gathers whole blocks
@@ -46,6 +47,23 @@ __device__ __forceinline__ uint32_t wave_prefix_small(uint32_t v, uint32_t* tota
 
 __device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 __device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+
+// Streaming (nontemporal) access for data touched once per step: the K
+// workers' g and e rows are gigabytes, far beyond any cache level.
+__device__ __forceinline__ float4 ld4_stream(const float* p) {
+    float4 v;
+    v.x = __builtin_nontemporal_load(p + 0);
+    v.y = __builtin_nontemporal_load(p + 1);
+    v.z = __builtin_nontemporal_load(p + 2);
+    v.w = __builtin_nontemporal_load(p + 3);
+    return v;
+}
+__device__ __forceinline__ void st4_stream(float* p, float4 v) {
+    __builtin_nontemporal_store(v.x, p + 0);
+    __builtin_nontemporal_store(v.y, p + 1);
+    __builtin_nontemporal_store(v.z, p + 2);
+    __builtin_nontemporal_store(v.w, p + 3);
+}
 
 __device__ __forceinline__ bool aligned16(const void* p) {
     return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
@@ -113,265 +131,191 @@ __device__ __forceinline__ void store_agent(uint32_t* p, uint32_t v) {
 // fused worker pass for top-s
 // ============================================================================
 
-// Candidate append of one wavefront-chunk for worker k.  `flags` holds, per
-// lane, kIters*kPer bits (iteration-major) of components to append; the
-// component of bit (i, q) is element `start + i*kWave*kPer + lane*kPer + q`,
-// whose u value has just been stored to e[j] by this lane.
-template <int kIters, int kPer, class Flags>
-__device__ __forceinline__ void append_candidates(Flags flags, const float* e, int start, int lane,
-                                                  const TopkGeometry& g, const TopkScratch& s, int k,
-                                                  int chunk, int p) {
+// ---------------------------------------------------------------------------
+// Vector path: one workgroup per (chunk, worker), 8 components per thread.
+//
+// Consecutive workgroups take the K workers of one chunk, so w_t and w_prev
+// of the chunk are fetched from memory once and re-read from cache by the
+// other K-1 workgroups.  g and e are streamed with nontemporal accesses.  A
+// worker's candidates of the chunk go, in index order, to the chunk's own
+// slot in the staging area (kChunk entries, so it can never overflow): the
+// streaming pass takes no atomics; the compaction kernel packs the slots.
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
+                                                                uint64_t vec_mask) {
+    __shared__ uint32_t wtot[2][kWavesPerGroup];
+    const int chunk = blockIdx.x / g.K, k = blockIdx.x % g.K;
+    if (!((vec_mask >> k) & 1ull)) return;  // the element-wise kernel's
+    const int start = g.chunk_start[chunk];
+    const int len = g.chunk_len[chunk];
+    if ((start & 3) != 0 || len != kChunk) return;  // the element-wise kernel's
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+    const int seg = g.chunk_seg[chunk];
+    const int p = k * g.n_seg + seg;
+    const uint32_t tau = s.pair[p].tau;
+    const float c = a.c;
+    const int o0 = threadIdx.x * 4;               // components o0..o0+3 and 1024+o0..1024+o0+3
+    float* ep = a.wp.e[k] + start + o0;
+    const float* gp = a.wp.g[k] + start + o0;
+    const float* wt_p = a.w_t + start + o0;
+    const float* wp_p = a.w_prev + start + o0;
+    float4 u[2], gv[2], wt[2], wv[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        u[i] = ld4_stream(ep + i * (kGroup * 4));
+        gv[i] = ld4_stream(gp + i * (kGroup * 4));
+        wt[i] = ld4(wt_p + i * (kGroup * 4));
+        wv[i] = ld4(wp_p + i * (kGroup * 4));
+    }
+    uint32_t flags = 0;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const float4 m = make_float4(c * (wt[i].x - wv[i].x), c * (wt[i].y - wv[i].y), c * (wt[i].z - wv[i].z),
+                                     c * (wt[i].w - wv[i].w));
+        u[i].x = precompress(u[i].x, gv[i].x, m.x);
+        u[i].y = precompress(u[i].y, gv[i].y, m.y);
+        u[i].z = precompress(u[i].z, gv[i].z, m.z);
+        u[i].w = precompress(u[i].w, gv[i].w, m.w);
+        st4_stream(ep + i * (kGroup * 4), u[i]);
+        flags |= (key_of(u[i].x) >= tau ? 1u : 0u) << (i * 4 + 0);
+        flags |= (key_of(u[i].y) >= tau ? 1u : 0u) << (i * 4 + 1);
+        flags |= (key_of(u[i].z) >= tau ? 1u : 0u) << (i * 4 + 2);
+        flags |= (key_of(u[i].w) >= tau ? 1u : 0u) << (i * 4 + 3);
+    }
     const size_t run_slot = (size_t)k * g.n_chunks + chunk;
-    if (ballot(flags != 0) == 0ull) {
-        if (lane == 0) {
-            s.run_off[run_slot] = 0u;
-            s.run_cnt[run_slot] = 0u;
-        }
+    if (__syncthreads_or(flags != 0u) == 0) {
+        if (threadIdx.x == 0) s.run_cnt[run_slot] = 0u;
         return;
     }
-    // per-iteration exclusive lane prefix and iteration bases
-    uint32_t lane_pre[kIters];
-    uint32_t base = 0;
+    // position in index order: (i, thread, q)
+    uint32_t pre[2];
 #pragma unroll
-    for (int i = 0; i < kIters; ++i) {
-        const uint32_t bits = (uint32_t)(flags >> (i * kPer)) & ((1u << kPer) - 1u);
-        const uint32_t cnt = (uint32_t)__popc(bits);
-        uint32_t tot, pre;
-        if (kPer == 1) {
-            const uint64_t b = ballot(cnt != 0u);
-            pre = popc64(b & lanemask_lt());
-            tot = popc64(b);
-        } else {
-            pre = wave_prefix_small(cnt, &tot);
+    for (int i = 0; i < 2; ++i) {
+        uint32_t tot;
+        pre[i] = wave_prefix_small((uint32_t)__popc((flags >> (i * 4)) & 0xfu), &tot);
+        if (lane == 0) wtot[i][wave] = tot;
+    }
+    __syncthreads();
+    uint32_t total = 0, pos[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        uint32_t before = 0;
+#pragma unroll
+        for (int w = 0; w < kWavesPerGroup; ++w) {
+            if (w < wave) before += wtot[i][w];
         }
-        lane_pre[i] = base + pre;
-        base += tot;
-    }
-    const uint32_t total = base;
-    uint32_t off = 0;
-    if (lane == 0) off = atomicAdd(&s.pair[p].cand, total);
-    off = __shfl(off, 0, kWave);
-    if (lane == 0) {
-        s.run_off[run_slot] = off;
-        s.run_cnt[run_slot] = total;
-    }
-    const uint32_t cap = (uint32_t)g.pair_cap[p];
-    if (off > cap || total > cap - off) return;  // overflow: the selection takes the full-data path
-    int32_t* ci = s.cand_idx + g.pair_cand[p];
-    float* cv = s.cand_val + g.pair_cand[p];
+        pos[i] = total + before + pre[i];
 #pragma unroll
-    for (int i = 0; i < kIters; ++i) {
-        uint32_t bits = (uint32_t)(flags >> (i * kPer)) & ((1u << kPer) - 1u);
-        uint32_t pos = off + lane_pre[i];
-        while (bits) {
-            const int q = __ffs(bits) - 1;
-            bits &= bits - 1u;
-            const int j = start + i * (kWave * kPer) + lane * kPer + q;
-            ci[pos] = j;
-            cv[pos] = e[j];  // re-read of this lane's own store
-            ++pos;
+        for (int w = 0; w < kWavesPerGroup; ++w) total += wtot[i][w];
+    }
+    if (threadIdx.x == 0) s.run_cnt[run_slot] = total;
+    int32_t* si = s.slot_idx + run_slot * kChunk;
+    float* sv = s.slot_val + run_slot * kChunk;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const uint32_t bits = (flags >> (i * 4)) & 0xfu;
+        uint32_t q = pos[i];
+        const int j = start + o0 + i * (kGroup * 4);
+        if (bits & 1u) { si[q] = j + 0; sv[q] = u[i].x; ++q; }
+        if (bits & 2u) { si[q] = j + 1; sv[q] = u[i].y; ++q; }
+        if (bits & 4u) { si[q] = j + 2; sv[q] = u[i].z; ++q; }
+        if (bits & 8u) { si[q] = j + 3; sv[q] = u[i].w; }
+    }
+}
+
+// Compaction, first half: the exclusive prefix of the run counts of each
+// group of kCompactChunks chunks, and the group's total.
+__global__ __launch_bounds__(kGroup) void topk_compact_count_kernel(TopkGeometry g, TopkScratch s) {
+    static_assert(kCompactChunks == kGroup, "one chunk per thread");
+    __shared__ uint32_t wsum[kWavesPerGroup];
+    const int k = blockIdx.x / g.n_cgroups;
+    const int cg = blockIdx.x % g.n_cgroups;
+    const int clo = g.cgrp_lo[cg], nch = g.cgrp_hi[cg] - clo;
+    const size_t slot0 = (size_t)k * g.n_chunks + clo;
+    const uint32_t cnt = threadIdx.x < nch ? s.run_cnt[slot0 + threadIdx.x] : 0u;
+    uint32_t total;
+    const uint32_t pre = block_scan_excl(cnt, &total, wsum);
+    if (threadIdx.x < nch) s.run_pre[slot0 + threadIdx.x] = pre;
+    if (threadIdx.x == 0) s.grp_total[(size_t)k * g.n_cgroups + cg] = total;
+}
+
+// Compaction, second half: group cg of a segment starts at the sum of the
+// totals of the segment's earlier groups, so the pair's candidate list comes
+// out in ascending index order.  Each group's copy is split over
+// kCompactParts workgroups.  The first workgroup of a segment also publishes
+// the pair's candidate count.  A pair whose candidates exceed its capacity
+// is not copied (it takes the full-data path).
+__global__ __launch_bounds__(kGroup) void topk_compact_copy_kernel(TopkGeometry g, TopkScratch s) {
+    __shared__ uint32_t pre[kCompactChunks + 1];
+    __shared__ uint32_t wsum[kWavesPerGroup];
+    const int part = blockIdx.x % kCompactParts;
+    const int rest = blockIdx.x / kCompactParts;
+    const int k = rest / g.n_cgroups;
+    const int cg = rest % g.n_cgroups;
+    const int seg = g.cgrp_seg[cg];
+    const int p = k * g.n_seg + seg;
+    const int rank = g.cgrp_rank[cg];
+    const size_t grp0 = (size_t)k * g.n_cgroups + g.seg_cgrp_lo[seg];
+    uint32_t before = 0, all = 0;
+    for (int r0 = 0; r0 < g.seg_cgrps[seg]; r0 += kGroup) {
+        const int r = r0 + threadIdx.x;
+        const uint32_t t = r < g.seg_cgrps[seg] ? s.grp_total[grp0 + r] : 0u;
+        uint32_t tot;
+        const uint32_t ex = block_scan_excl(t, &tot, wsum);
+        if (r == rank) pre[kCompactChunks] = all + ex;  // temporarily: this group's base
+        all += tot;
+    }
+    __syncthreads();
+    before = pre[kCompactChunks];
+    if (rank == 0 && part == 0 && threadIdx.x == 0) s.pair[p].cand = all;
+    const uint32_t total = s.grp_total[grp0 + rank];
+    if (all > (uint32_t)g.pair_cap[p] || total == 0) return;
+    const uint32_t lo = (uint32_t)((uint64_t)total * part / kCompactParts);
+    const uint32_t hi = (uint32_t)((uint64_t)total * (part + 1) / kCompactParts);
+    if (lo == hi) return;
+    const int clo = g.cgrp_lo[cg], nch = g.cgrp_hi[cg] - clo;
+    const size_t slot0 = (size_t)k * g.n_chunks + clo;
+    __syncthreads();
+    if (threadIdx.x < nch) pre[threadIdx.x] = s.run_pre[slot0 + threadIdx.x];
+    __syncthreads();
+    int32_t* ci = s.cand_idx + g.pair_cand[p] + before;
+    float* cv = s.cand_val + g.pair_cand[p] + before;
+    for (uint32_t q0 = lo; q0 < hi; q0 += kGroup * 8) {
+        int32_t jv[8];
+        float xv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t q = q0 + i * kGroup + threadIdx.x;
+            if (q < hi) {
+                int a = 0, b = nch - 1;  // chunk c with pre[c] <= q < pre[c+1]
+                while (a < b) {
+                    const int mid = (a + b + 1) >> 1;
+                    if (pre[mid] <= q) a = mid; else b = mid - 1;
+                }
+                const size_t src = (slot0 + a) * kChunk + (q - pre[a]);
+                jv[i] = s.slot_idx[src];
+                xv[i] = s.slot_val[src];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t q = q0 + i * kGroup + threadIdx.x;
+            if (q < hi) {
+                ci[q] = jv[i];
+                cv[q] = xv[i];
+            }
         }
     }
 }
 
-// ---------------------------------------------------------------------------
-// Vector path with workgroup-level candidate staging.
-//
-// A workgroup owns 4 consecutive chunks of one segment (the chunk table pads
-// each segment to a multiple of 4).  Each wavefront streams its chunk for
-// every worker; a worker's candidates go to a per-worker region of LDS, so
-// the wavefront never waits on a global atomic in the streaming loop.  At the
-// end the workgroup reserves global candidate space with one atomic per
-// worker (all workers' atomics issued together) and copies the staged runs
-// out.  A wavefront whose candidates do not fit in the staging region
-// appends them straight to global memory instead.
-// ---------------------------------------------------------------------------
-
-constexpr int kStageEntries = 4096;             // 32 KiB of (index, value) pairs
-constexpr uint32_t kRunDirect = 0xffffffffu;    // run written straight to global memory
-constexpr uint32_t kRunSkip = 0xfffffffeu;      // chunk owned by the element-wise kernel
-
-struct StageShared {
-    int32_t idx[kStageEntries];
-    float val[kStageEntries];
-    uint32_t used[kMaxWorkers];                 // entries reserved per worker
-    uint32_t run_off[kMaxWorkers][kWavesPerGroup];
-    uint32_t run_cnt[kMaxWorkers][kWavesPerGroup];
-    uint32_t gbase[kMaxWorkers];
-};
-
-__global__ __launch_bounds__(kGroup) __attribute__((amdgpu_waves_per_eu(4))) void topk_fused_vec_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
-                                                                uint64_t vec_mask) {
-    __shared__ StageShared sh;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x >> 6;
-    const int K = g.K;
-    const uint32_t per = kStageEntries / K;     // staging entries per worker
-    const int chunk = blockIdx.x * kWavesPerGroup + wave;
-    const int start = g.chunk_start[chunk];
-    const int len = g.chunk_len[chunk];
-    const int seg = g.chunk_seg[chunk];         // the same for the whole workgroup
-    const bool mine = (start & 3) == 0 && len == kChunk;  // other chunks: element-wise kernel
-    for (int i = threadIdx.x; i < K; i += kGroup) sh.used[i] = 0u;
-    __syncthreads();
-
-    if (mine) {
-        const float c = a.c;
-        const float* wt_p = a.w_t + start + lane * 4;
-        const float* wp_p = a.w_prev + start + lane * 4;
-        float4 m4[kVecIters];
-#pragma unroll
-        for (int i = 0; i < kVecIters; ++i) {
-            const float4 wt = ld4(wt_p + i * (kWave * 4)), wp = ld4(wp_p + i * (kWave * 4));
-            m4[i] = make_float4(c * (wt.x - wp.x), c * (wt.y - wp.y), c * (wt.z - wp.z), c * (wt.w - wp.w));
-        }
-#pragma unroll 1
-        for (int k = 0; k < K; ++k) {
-            if (!((vec_mask >> k) & 1ull)) {
-                if (lane == 0) sh.run_off[k][wave] = kRunSkip;
-                continue;
-            }
-            const int p = k * g.n_seg + seg;
-            const uint32_t tau = s.pair[p].tau;
-            float* ep = a.wp.e[k] + start + lane * 4;
-            const float* gp = a.wp.g[k] + start + lane * 4;
-            float4 u[kVecIters], gv[kVecIters];
-#pragma unroll
-            for (int i = 0; i < kVecIters; ++i) {
-                u[i] = ld4(ep + i * (kWave * 4));
-                gv[i] = ld4(gp + i * (kWave * 4));
-            }
-            uint32_t flags = 0;
-#pragma unroll
-            for (int i = 0; i < kVecIters; ++i) {
-                u[i].x = precompress(u[i].x, gv[i].x, m4[i].x);
-                u[i].y = precompress(u[i].y, gv[i].y, m4[i].y);
-                u[i].z = precompress(u[i].z, gv[i].z, m4[i].z);
-                u[i].w = precompress(u[i].w, gv[i].w, m4[i].w);
-                st4(ep + i * (kWave * 4), u[i]);
-                flags |= (key_of(u[i].x) >= tau ? 1u : 0u) << (i * 4 + 0);
-                flags |= (key_of(u[i].y) >= tau ? 1u : 0u) << (i * 4 + 1);
-                flags |= (key_of(u[i].z) >= tau ? 1u : 0u) << (i * 4 + 2);
-                flags |= (key_of(u[i].w) >= tau ? 1u : 0u) << (i * 4 + 3);
-            }
-            if (ballot(flags != 0u) == 0ull) {
-                if (lane == 0) {
-                    sh.run_off[k][wave] = 0u;
-                    sh.run_cnt[k][wave] = 0u;
-                }
-                continue;
-            }
-            // iteration-major order = ascending element index
-            uint32_t lane_pre[kVecIters];
-            uint32_t total = 0;
-#pragma unroll
-            for (int i = 0; i < kVecIters; ++i) {
-                uint32_t tot;
-                const uint32_t pre = wave_prefix_small((uint32_t)__popc((flags >> (i * 4)) & 0xfu), &tot);
-                lane_pre[i] = total + pre;
-                total += tot;
-            }
-            uint32_t off = 0;
-            if (lane == 0) off = atomicAdd(&sh.used[k], total);
-            off = __shfl(off, 0, kWave);
-            if (off + total <= per) {
-                const uint32_t base = (uint32_t)k * per + off;
-                if (lane == 0) {
-                    sh.run_off[k][wave] = base;
-                    sh.run_cnt[k][wave] = total;
-                }
-#pragma unroll
-                for (int i = 0; i < kVecIters; ++i) {
-                    const uint32_t bits = (flags >> (i * 4)) & 0xfu;
-                    uint32_t pos = base + lane_pre[i];
-                    const int j = start + i * (kWave * 4) + lane * 4;
-                    if (bits & 1u) { sh.idx[pos] = j + 0; sh.val[pos] = u[i].x; ++pos; }
-                    if (bits & 2u) { sh.idx[pos] = j + 1; sh.val[pos] = u[i].y; ++pos; }
-                    if (bits & 4u) { sh.idx[pos] = j + 2; sh.val[pos] = u[i].z; ++pos; }
-                    if (bits & 8u) { sh.idx[pos] = j + 3; sh.val[pos] = u[i].w; }
-                }
-            } else {
-                // staging full: append this run to global memory directly
-                uint32_t goff = 0;
-                if (lane == 0) goff = atomicAdd(&s.pair[p].cand, total);
-                goff = __shfl(goff, 0, kWave);
-                const size_t slot = (size_t)k * g.n_chunks + chunk;
-                if (lane == 0) {
-                    s.run_off[slot] = goff;
-                    s.run_cnt[slot] = total;
-                    sh.run_off[k][wave] = kRunDirect;
-                    sh.run_cnt[k][wave] = total;
-                }
-                const uint32_t cap = (uint32_t)g.pair_cap[p];
-                if (goff > cap || total > cap - goff) continue;  // overflow: full-data selection
-                int32_t* ci = s.cand_idx + g.pair_cand[p] + goff;
-                float* cv = s.cand_val + g.pair_cand[p] + goff;
-                const float* e = a.wp.e[k];
-#pragma unroll 1
-                for (int i = 0; i < kVecIters; ++i) {
-                    uint32_t bits = (flags >> (i * 4)) & 0xfu;
-                    uint32_t pos = lane_pre[i];
-                    while (bits) {
-                        const int q = __ffs(bits) - 1;
-                        bits &= bits - 1u;
-                        const int j = start + i * (kWave * 4) + lane * 4 + q;
-                        ci[pos] = j;
-                        cv[pos] = e[j];  // re-read of this lane's own store
-                        ++pos;
-                    }
-                }
-            }
-        }
-    } else if (lane == 0) {
-        for (int k = 0; k < K; ++k) sh.run_off[k][wave] = kRunSkip;
-    }
-    __syncthreads();
-
-    // one global reservation per worker for all staged runs of the workgroup
-    if (threadIdx.x < K) {
-        const int k = threadIdx.x;
-        uint32_t staged = 0;
-        for (int w = 0; w < kWavesPerGroup; ++w)
-            if (sh.run_off[k][w] < kRunSkip) staged += sh.run_cnt[k][w];
-        sh.gbase[k] = staged ? atomicAdd(&s.pair[k * g.n_seg + seg].cand, staged) : 0u;
-    }
-    __syncthreads();
-    if (threadIdx.x < K * kWavesPerGroup) {
-        const int k = threadIdx.x / kWavesPerGroup, w = threadIdx.x % kWavesPerGroup;
-        const uint32_t ro = sh.run_off[k][w];
-        if (ro < kRunSkip) {
-            uint32_t pre = 0;
-            for (int q = 0; q < w; ++q)
-                if (sh.run_off[k][q] < kRunSkip) pre += sh.run_cnt[k][q];
-            const size_t slot = (size_t)k * g.n_chunks + blockIdx.x * kWavesPerGroup + w;
-            s.run_off[slot] = sh.gbase[k] + pre;
-            s.run_cnt[slot] = sh.run_cnt[k][w];
-        }
-    }
-    for (int k = 0; k < K; ++k) {
-        uint32_t cnt[kWavesPerGroup], pre[kWavesPerGroup + 1];
-        pre[0] = 0;
-#pragma unroll
-        for (int w = 0; w < kWavesPerGroup; ++w) {
-            const bool staged = sh.run_off[k][w] < kRunSkip;
-            cnt[w] = staged ? sh.run_cnt[k][w] : 0u;
-            pre[w + 1] = pre[w] + cnt[w];
-        }
-        const uint32_t n = pre[kWavesPerGroup];
-        if (n == 0) continue;
-        const int p = k * g.n_seg + seg;
-        const uint32_t base = sh.gbase[k], cap = (uint32_t)g.pair_cap[p];
-        if (base > cap || n > cap - base) continue;  // overflow: full-data selection
-        int32_t* ci = s.cand_idx + g.pair_cand[p] + base;
-        float* cv = s.cand_val + g.pair_cand[p] + base;
-        for (uint32_t i = threadIdx.x; i < n; i += kGroup) {
-            int w = 0;
-            while (i >= pre[w + 1]) ++w;
-            const uint32_t src = sh.run_off[k][w] + (i - pre[w]);
-            ci[i] = sh.idx[src];
-            cv[i] = sh.val[src];
-        }
-    }
+hipError_t launch_topk_compact(const TopkGeometry& g, const TopkScratch& s, hipStream_t st) {
+    hipLaunchKernelGGL(topk_compact_count_kernel, dim3(g.K * g.n_cgroups), dim3(kGroup), 0, st, g, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(topk_compact_copy_kernel, dim3(g.K * g.n_cgroups * kCompactParts), dim3(kGroup), 0, st, g,
+                       s);
+    return hipGetLastError();
 }
 
 // Element-wise path for the (chunk, worker) pairs the vector kernel skips:
@@ -409,12 +353,28 @@ __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, Topk
             flags |= (key_of(u) >= tau ? 1u : 0u) << i;
         }
     }
-    append_candidates<kIt, 1>(flags, e, start, lane, g, s, k, chunk, p);
+    // the chunk's slot, in index order (iteration-major, then lane)
+    const size_t run_slot = (size_t)k * g.n_chunks + chunk;
+    int32_t* si = s.slot_idx + run_slot * kChunk;
+    float* sv = s.slot_val + run_slot * kChunk;
+    const uint64_t lt = lanemask_lt();
+    uint32_t base = 0;
+    for (int i = 0; i < kIt; ++i) {
+        const uint64_t b = ballot((flags >> i) & 1u);
+        if ((flags >> i) & 1u) {
+            const uint32_t q = base + popc64(b & lt);
+            const int j = start + i * kWave + lane;
+            si[q] = j;
+            sv[q] = e[j];  // re-read of this lane's own store
+        }
+        base += popc64(b);
+    }
+    if (lane == 0) s.run_cnt[run_slot] = base;
 }
 
 hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                                  uint64_t vec_mask, hipStream_t st) {
-    const int grid = (g.n_chunks + kWavesPerGroup - 1) / kWavesPerGroup;
+    const int grid = g.n_chunks * g.K;
     hipLaunchKernelGGL(topk_fused_vec_kernel, dim3(grid), dim3(kGroup), 0, st, a, g, s, vec_mask);
     return hipGetLastError();
 }
@@ -435,18 +395,17 @@ hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const
 // list (mode 0: the fused pass collected every component whose key reaches
 // the speculative threshold, and there are at least k and at most the
 // capacity of them) or all of the segment's u (mode 1, the full-data path).
-// Histogram and count passes read it as flat slices, one workgroup per
-// slice, in no particular order; the emit pass walks it item by item in
-// index order (an item is kItemChunks consecutive chunks of a segment).
+// Both are in ascending index order.  The histogram, count and emit passes
+// read them as flat slices, one workgroup per slice; the count pass scans
+// the slices' counts so that each emit workgroup knows where its kept
+// components go.
 // ============================================================================
 
 namespace {
 
-constexpr int kItemShift = 16;       // log2(kChunk * kItemChunks): elements per item
 constexpr int kSliceLoads = 16;      // independent loads in flight per thread
-constexpr int kMaxSegItems = 4096;   // per-item counters kept in LDS (segments up to 2^28)
-constexpr int kEmitStage = kGroup * kSliceLoads;  // candidates staged in LDS per round
-static_assert((1 << kItemShift) == kChunk * kItemChunks, "item geometry");
+constexpr int kEmitLoads = 4;        // staged elements per thread in the emit pass
+constexpr int kEmitStage = kGroup * kEmitLoads;  // elements staged in LDS per round
 
 // A workgroup's slice of a pair's selection input.
 struct Slice {
@@ -496,75 +455,6 @@ __device__ __forceinline__ void for_slice(const Slice& v, F f) {
             if (pos < v.hi) f(key_of(x[i]), j[i]);
         }
     }
-}
-
-// Runs of an item's chunks in the candidate buffer (mode 0).
-struct ItemShared {
-    uint32_t flat[kItemChunks + 1];  // exclusive prefix of the runs' counts
-    uint32_t roff[kItemChunks];
-    uint32_t wsum[kWavesPerGroup];
-};
-
-// An item's elements in ascending index order: its chunks' candidate runs
-// (mode 0) or its range of u (mode 1).
-struct ItemView {
-    int mode;
-    int32_t total;
-    const int32_t* cidx;
-    const float* cval;
-    const float* u;
-    int32_t lo;
-    int32_t nch;
-};
-
-__device__ ItemView open_item(int mode, int k, int it, int p, const StepArgs& a, const TopkGeometry& g,
-                              const TopkScratch& s, ItemShared& sh) {
-    static_assert(kItemChunks <= kGroup, "one run per thread");
-    ItemView v;
-    v.mode = mode;
-    const int clo = g.item_chunk_lo[it], chi = g.item_chunk_hi[it];
-    v.nch = chi - clo;
-    v.cidx = s.cand_idx + g.pair_cand[p];
-    v.cval = s.cand_val + g.pair_cand[p];
-    v.u = a.wp.e[k];
-    v.lo = g.chunk_start[clo];
-    if (mode == 0) {
-        const int t = threadIdx.x;
-        uint32_t cnt = 0, off = 0;
-        if (t < v.nch) {
-            const size_t slot = (size_t)k * g.n_chunks + clo + t;
-            cnt = s.run_cnt[slot];
-            off = s.run_off[slot];
-        }
-        uint32_t total;
-        const uint32_t pre = block_scan_excl(cnt, &total, sh.wsum);
-        if (t < v.nch) {
-            sh.flat[t] = pre;
-            sh.roff[t] = off;
-        }
-        if (t == 0) sh.flat[v.nch] = total;
-        __syncthreads();
-        v.total = (int32_t)total;
-    } else {
-        v.total = g.chunk_start[chi - 1] + g.chunk_len[chi - 1] - v.lo;
-    }
-    return v;
-}
-
-// Element at flat position pos (< total): value and global index.
-__device__ __forceinline__ float item_get(const ItemView& v, const ItemShared& sh, int32_t pos, int32_t* j) {
-    if (v.mode == 1) {
-        *j = v.lo + pos;
-        return v.u[v.lo + pos];
-    }
-    int lo = 0, hi = v.nch - 1;  // largest run c with flat[c] <= pos
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (sh.flat[mid] <= (uint32_t)pos) lo = mid; else hi = mid - 1;
-    }
-    const uint32_t cpos = sh.roff[lo] + ((uint32_t)pos - sh.flat[lo]);
-    *j = v.cidx[cpos];
-    return v.cval[cpos];
 }
 
 // The bin b (scanning from the top) with above(b) < need <= above(b) + h[b],
@@ -727,13 +617,12 @@ hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
 }
 
 // ----------------------------------------------------------------------------
-// per-item counts above / at the threshold, then the scan over the items
+// per-slice counts above / at the threshold, then the scan over the slices
 // ----------------------------------------------------------------------------
 
 __global__ __launch_bounds__(kGroup) void topk_count_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                             int64_t* msg_len, int64_t msg_total) {
-    __shared__ uint32_t c_above[kMaxSegItems];
-    __shared__ uint32_t c_ties[kMaxSegItems];
+    __shared__ uint32_t red[2][kWavesPerGroup];
     __shared__ uint32_t sh_wsum[kWavesPerGroup];
     __shared__ int sh_last;
     __shared__ uint32_t carry[2];
@@ -742,47 +631,47 @@ __global__ __launch_bounds__(kGroup) void topk_count_kernel(StepArgs a, TopkGeom
     PairState* ps = &s.pair[id.p];
     const int mode = ps->mode;
     const uint32_t T = ps->T;
-    const int n_it = g.seg_items[id.seg];
-    const bool in_lds = n_it <= kMaxSegItems;
-    const size_t base = (size_t)id.k * g.n_items + g.seg_item_lo[id.seg];
-    for (int i = threadIdx.x; i < n_it && in_lds; i += kGroup) {
-        c_above[i] = 0u;
-        c_ties[i] = 0u;
+    const Slice v = open_slice(mode, ps->cand_used, id.k, id.seg, id.p, id.w, id.W, a, g, s);
+    uint32_t above = 0, ties = 0;
+    for_slice<false>(v, [&](uint32_t key, int32_t) {
+        above += key > T;
+        ties += key == T;
+    });
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        above += __shfl_down(above, o, kWave);
+        ties += __shfl_down(ties, o, kWave);
+    }
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+    if (lane == 0) {
+        red[0][wave] = above;
+        red[1][wave] = ties;
     }
     __syncthreads();
-    const Slice v = open_slice(mode, mode == 0 ? ps->cand_used : 0u, id.k, id.seg, id.p, id.w, id.W, a, g, s);
-    for_slice<true>(v, [&](uint32_t key, int32_t j) {
-        const int item = (j - v.seg_lo) >> kItemShift;
-        if (in_lds) {
-            if (key > T) atomicAdd(&c_above[item], 1u);
-            else if (key == T) atomicAdd(&c_ties[item], 1u);
-        } else {
-            if (key > T) atomicAdd(&s.item_above[base + item], 1u);
-            else if (key == T) atomicAdd(&s.item_ties[base + item], 1u);
+    const size_t base = (size_t)id.k * g.n_slices + g.seg_slice_lo[id.seg];
+    if (threadIdx.x == 0) {
+        uint32_t A = 0, Ti = 0;
+        for (int w = 0; w < kWavesPerGroup; ++w) {
+            A += red[0][w];
+            Ti += red[1][w];
         }
-    });
-    __syncthreads();
-    for (int i = threadIdx.x; i < n_it && in_lds; i += kGroup) {
-        if (c_above[i]) atomicAdd(&s.item_above[base + i], c_above[i]);
-        if (c_ties[i]) atomicAdd(&s.item_ties[base + i], c_ties[i]);
+        store_agent(&s.sl_above[base + id.w], A);
+        store_agent(&s.sl_ties[base + id.w], Ti);
     }
     if (!finish_slice(&ps->done, id.W, &sh_last)) return;
 
-    // last workgroup of the pair: scan the segment's items in index order
+    // last workgroup of the pair: scan the segment's slices in index order
     const int32_t r = ps->r;
     if (threadIdx.x == 0) {
         carry[0] = 0;  // ties before
         carry[1] = 0;  // kept before
     }
     __syncthreads();
-    for (int c0 = 0; c0 < n_it; c0 += kGroup) {
+    for (int c0 = 0; c0 < id.W; c0 += kGroup) {
         const int i = c0 + threadIdx.x;
         uint32_t A = 0, Ti = 0;
-        if (i < n_it) {
-            A = load_agent(&s.item_above[base + i]);
-            Ti = load_agent(&s.item_ties[base + i]);
-            store_agent(&s.item_above[base + i], 0u);
-            store_agent(&s.item_ties[base + i], 0u);
+        if (i < id.W) {
+            A = load_agent(&s.sl_above[base + i]);
+            Ti = load_agent(&s.sl_ties[base + i]);
         }
         uint32_t tot_t;
         const uint32_t tie_pre = carry[0] + block_scan_excl(Ti, &tot_t, sh_wsum);
@@ -792,9 +681,9 @@ __global__ __launch_bounds__(kGroup) void topk_count_kernel(StepArgs a, TopkGeom
         const uint32_t sel = A + (uint32_t)take;
         uint32_t tot_s;
         const uint32_t sel_pre = carry[1] + block_scan_excl(sel, &tot_s, sh_wsum);
-        if (i < n_it) {
-            s.item_tiebase[base + i] = tie_pre;
-            s.item_out[base + i] = sel_pre;
+        if (i < id.W) {
+            s.sl_tiebase[base + i] = tie_pre;
+            s.sl_out[base + i] = sel_pre;
         }
         __syncthreads();
         if (threadIdx.x == 0) {
@@ -819,62 +708,56 @@ hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const Top
 
 // ----------------------------------------------------------------------------
 // ordered emission of the kept components
+//
+// One workgroup per slice.  The slice's elements are staged in LDS in rounds
+// of kEmitStage (coalesced loads, all in flight together); in a round each
+// thread owns kEmitLoads consecutive elements, one block-wide scan of its
+// (above, tie) counts places them, and the thread writes its kept ones in
+// order.  LDS rows are padded by one word per kEmitLoads entries so that the
+// threads' strided reads hit distinct banks.
 // ----------------------------------------------------------------------------
 
-// One workgroup per item.  The item's elements are staged in LDS in rounds
-// of kEmitStage with all loads in flight together; in a round each thread
-// owns kSliceLoads consecutive elements, one block-wide scan of its
-// (above, tie) counts places them, and the thread writes its kept ones in
-// order.  LDS rows are padded by one word per kSliceLoads entries so the
-// threads' strided reads hit distinct banks.
-__device__ __forceinline__ int stage_slot(int q) { return q + (q >> 4); }
+__device__ __forceinline__ int stage_slot(int q) { return q + (q >> 2); }
 
 __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                            int32_t* idx, float* val, int64_t row_len) {
-    static_assert(kSliceLoads == 16, "stage_slot pads every 16 entries");
-    constexpr int kStageSlots = kEmitStage + kEmitStage / 16;
-    __shared__ ItemShared ish;
+    static_assert(kEmitLoads == 4, "stage_slot pads every 4 entries");
+    constexpr int kStageSlots = kEmitStage + kEmitStage / 4;
     __shared__ int32_t st_idx[kStageSlots];
     __shared__ float st_val[kStageSlots];
+    __shared__ uint32_t sh_wsum[kWavesPerGroup];
 
-    const int k = blockIdx.x / g.n_items;
-    const int it = blockIdx.x % g.n_items;
-    const int seg = g.item_seg[it];
-    const int p = k * g.n_seg + seg;
-    const PairState* ps = &s.pair[p];
+    const SliceId id = slice_id(g);
+    const PairState* ps = &s.pair[id.p];
     const int mode = ps->mode;
     const uint32_t T = ps->T;
     const int64_t r = ps->r;
-    const size_t slot = (size_t)k * g.n_items + it;
-    const uint32_t out0 = s.item_out[slot];
-    const int64_t tiebase = s.item_tiebase[slot];
-    int64_t quota = r - tiebase;  // ties this item may still take, in index order
+    const size_t sl = (size_t)id.k * g.n_slices + g.seg_slice_lo[id.seg] + id.w;
+    const uint32_t out0 = s.sl_out[sl];
+    int64_t quota = r - (int64_t)s.sl_tiebase[sl];  // ties this slice may still take, in index order
     if (quota < 0) quota = 0;
+    const uint32_t kseg = (uint32_t)g.pair_k[id.p];
+    int32_t* irow = idx + (size_t)id.k * row_len + g.seg_out[id.seg];
+    float* vrow = val + (size_t)id.k * row_len + g.seg_out[id.seg];
+    float* e = a.wp.e[id.k];
 
-    const uint32_t kseg = (uint32_t)g.pair_k[p];
-    int32_t* irow = idx + (size_t)k * row_len + g.seg_out[seg];
-    float* vrow = val + (size_t)k * row_len + g.seg_out[seg];
-    float* e = a.wp.e[k];
-
-    const ItemView v = open_item(mode, k, it, p, a, g, s, ish);
+    const Slice v = open_slice(mode, ps->cand_used, id.k, id.seg, id.p, id.w, id.W, a, g, s);
     uint32_t run_above = 0, run_ties = 0;  // over the earlier rounds
-    for (int32_t s0 = 0; s0 < v.total; s0 += kEmitStage) {
-        const int32_t ns = v.total - s0 < kEmitStage ? v.total - s0 : kEmitStage;
+    for (int64_t s0 = v.lo; s0 < v.hi; s0 += kEmitStage) {
+        const int32_t ns = (int32_t)(v.hi - s0 < kEmitStage ? v.hi - s0 : kEmitStage);
 #pragma unroll
-        for (int i = 0; i < kSliceLoads; ++i) {
+        for (int i = 0; i < kEmitLoads; ++i) {
             const int32_t q = i * kGroup + threadIdx.x;
             if (q < ns) {
-                int32_t j;
-                const float x = item_get(v, ish, s0 + q, &j);
-                st_idx[stage_slot(q)] = j;
-                st_val[stage_slot(q)] = x;
+                st_val[stage_slot(q)] = v.val[s0 + q];
+                st_idx[stage_slot(q)] = v.idx ? v.idx[s0 + q] : v.seg_lo + (int32_t)(s0 + q);
             }
         }
         __syncthreads();
-        const int32_t q0 = threadIdx.x * kSliceLoads;
+        const int32_t q0 = threadIdx.x * kEmitLoads;
         uint32_t na = 0, nt = 0;
 #pragma unroll
-        for (int i = 0; i < kSliceLoads; ++i) {
+        for (int i = 0; i < kEmitLoads; ++i) {
             if (q0 + i < ns) {
                 const uint32_t key = key_of(st_val[stage_slot(q0 + i)]);
                 na += key > T;
@@ -882,10 +765,10 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
             }
         }
         uint32_t tot;
-        const uint32_t pre = block_scan_excl((na << 16) | nt, &tot, ish.wsum);  // counts < 2^16
+        const uint32_t pre = block_scan_excl((na << 16) | nt, &tot, sh_wsum);  // counts < 2^16
         uint32_t a_before = run_above + (pre >> 16), t_before = run_ties + (pre & 0xffffu);
 #pragma unroll
-        for (int i = 0; i < kSliceLoads; ++i) {
+        for (int i = 0; i < kEmitLoads; ++i) {
             if (q0 + i >= ns) break;
             const float x = st_val[stage_slot(q0 + i)];
             const uint32_t key = key_of(x);
@@ -915,7 +798,7 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
 
 hipError_t launch_topk_emit(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                             int32_t* idx, float* val, int64_t row_len, hipStream_t st) {
-    hipLaunchKernelGGL(topk_emit_kernel, dim3(g.K * g.n_items), dim3(kGroup), 0, st, a, g, s, idx, val,
+    hipLaunchKernelGGL(topk_emit_kernel, dim3(g.K * g.n_slices), dim3(kGroup), 0, st, a, g, s, idx, val,
                        row_len);
     return hipGetLastError();
 }
