@@ -147,11 +147,13 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
     __shared__ uint32_t wtot[2][kWavesPerGroup];
     const int chunk = blockIdx.x / g.K, k = blockIdx.x % g.K;
     if (!((vec_mask >> k) & 1ull)) return;  // the element-wise kernel's
-    const int start = g.chunk_start[chunk];
-    const int len = g.chunk_len[chunk];
+    // one segment (global top-s): the chunk's place is arithmetic, no table lookup
+    const bool one = g.n_seg == 1;
+    const int start = one ? chunk * kChunk : g.chunk_start[chunk];
+    const int len = one ? min(kChunk, a.d - start) : g.chunk_len[chunk];
     if ((start & 3) != 0 || len != kChunk) return;  // the element-wise kernel's
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
-    const int seg = g.chunk_seg[chunk];
+    const int seg = one ? 0 : g.chunk_seg[chunk];
     const int p = k * g.n_seg + seg;
     const uint32_t tau = s.pair[p].tau;
     const float c = a.c;
