@@ -171,7 +171,8 @@ def main():
         % (wl.name, d, K, wl.compressor, wl.ratio, args.grad_batches))
     w = sdev.w0(wl, dev)
     wp = w.clone()
-    err = torch.zeros((K, d), dtype=torch.float32, device=dev)
+    # K per-worker rows packed with a 128-byte-aligned pitch (sdev.rows)
+    err = sdev.rows(K, d, dev, zero=True)
     G = [sdev.grads(wl, t, dev) for t in range(args.grad_batches)]
     idx, val, ln = gm.alloc_messages(dev)
     if args.calib:

@@ -225,7 +225,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         add(np, sizeof(PairState));
         add(np * kBins, 4);
         add((size_t)K * nc, 4); add((size_t)K * nc, 4); add((size_t)K * ng, 4);
-        add((size_t)K * nc * kChunk, 4); add((size_t)K * nc * kChunk, 4);
+        add((size_t)K * nc * kChunk, sizeof(int2));
         add((size_t)T.cand_total, 4); add((size_t)T.cand_total, 4);
         for (int q = 0; q < 4; ++q) add((size_t)K * nsl, 4);
         add((size_t)K * (ctx->n_ranges + 1), 4);
@@ -297,8 +297,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         sc.run_cnt = cv.take<uint32_t>((size_t)K * nc);
         sc.run_pre = cv.take<uint32_t>((size_t)K * nc);
         sc.grp_total = cv.take<uint32_t>((size_t)K * ng);
-        sc.slot_idx = cv.take<int32_t>((size_t)K * nc * kChunk);
-        sc.slot_val = cv.take<float>((size_t)K * nc * kChunk);
+        sc.slot = cv.take<int2>((size_t)K * nc * kChunk);
         sc.cand_idx = cv.take<int32_t>((size_t)T.cand_total);
         sc.cand_val = cv.take<float>((size_t)T.cand_total);
         sc.sl_above = cv.take<uint32_t>((size_t)K * nsl);

@@ -87,8 +87,8 @@ struct TopkScratch {
     uint32_t* run_cnt;            // [K*n_chunks] candidates of (worker, chunk)
     uint32_t* run_pre;            // [K*n_chunks] exclusive prefix of run_cnt within the group
     uint32_t* grp_total;          // [K*n_cgroups]
-    int32_t* slot_idx;            // [K*n_chunks][kChunk] candidates of (worker, chunk), index order
-    float* slot_val;              // [K*n_chunks][kChunk]
+    int2* slot;                   // [K*n_chunks][kChunk] candidates of (worker, chunk) in index
+                                  // order: (index, bit pattern of u)
     int32_t* cand_idx;            // [sum cap] candidate lists, ascending index
     float* cand_val;              // [sum cap]
     uint32_t* sl_above;           // [K*n_slices] kept-above-threshold count of each slice

@@ -145,6 +145,7 @@ __device__ __forceinline__ void store_agent(uint32_t* p, uint32_t v) {
 __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                                 uint64_t vec_mask) {
     __shared__ uint32_t wtot[2][kWavesPerGroup];
+    __shared__ int2 stage[kChunk];
     const int chunk = blockIdx.x / g.K, k = blockIdx.x % g.K;
     if (!((vec_mask >> k) & 1ull)) return;  // the element-wise kernel's
     // one segment (global top-s): the chunk's place is arithmetic, no table lookup
@@ -212,18 +213,22 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
         for (int w = 0; w < kWavesPerGroup; ++w) total += wtot[i][w];
     }
     if (threadIdx.x == 0) s.run_cnt[run_slot] = total;
-    int32_t* si = s.slot_idx + run_slot * kChunk;
-    float* sv = s.slot_val + run_slot * kChunk;
+    // gather the candidates in LDS, then write the slot with consecutive
+    // threads on consecutive entries (a few whole lines instead of one
+    // partial line per candidate)
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const uint32_t bits = (flags >> (i * 4)) & 0xfu;
         uint32_t q = pos[i];
         const int j = start + o0 + i * (kGroup * 4);
-        if (bits & 1u) { si[q] = j + 0; sv[q] = u[i].x; ++q; }
-        if (bits & 2u) { si[q] = j + 1; sv[q] = u[i].y; ++q; }
-        if (bits & 4u) { si[q] = j + 2; sv[q] = u[i].z; ++q; }
-        if (bits & 8u) { si[q] = j + 3; sv[q] = u[i].w; }
+        if (bits & 1u) { stage[q] = make_int2(j + 0, __float_as_int(u[i].x)); ++q; }
+        if (bits & 2u) { stage[q] = make_int2(j + 1, __float_as_int(u[i].y)); ++q; }
+        if (bits & 4u) { stage[q] = make_int2(j + 2, __float_as_int(u[i].z)); ++q; }
+        if (bits & 8u) { stage[q] = make_int2(j + 3, __float_as_int(u[i].w)); }
     }
+    __syncthreads();
+    int2* sp = s.slot + run_slot * kChunk;
+    for (uint32_t q = threadIdx.x; q < total; q += kGroup) sp[q] = stage[q];
 }
 
 // Compaction, first half: the exclusive prefix of the run counts of each
@@ -295,9 +300,9 @@ __global__ __launch_bounds__(kGroup) void topk_compact_copy_kernel(TopkGeometry 
                     const int mid = (a + b + 1) >> 1;
                     if (pre[mid] <= q) a = mid; else b = mid - 1;
                 }
-                const size_t src = (slot0 + a) * kChunk + (q - pre[a]);
-                jv[i] = s.slot_idx[src];
-                xv[i] = s.slot_val[src];
+                const int2 c = s.slot[(slot0 + a) * kChunk + (q - pre[a])];
+                jv[i] = c.x;
+                xv[i] = __int_as_float(c.y);
             }
         }
 #pragma unroll
@@ -357,8 +362,7 @@ __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, Topk
     }
     // the chunk's slot, in index order (iteration-major, then lane)
     const size_t run_slot = (size_t)k * g.n_chunks + chunk;
-    int32_t* si = s.slot_idx + run_slot * kChunk;
-    float* sv = s.slot_val + run_slot * kChunk;
+    int2* sp = s.slot + run_slot * kChunk;
     const uint64_t lt = lanemask_lt();
     uint32_t base = 0;
     for (int i = 0; i < kIt; ++i) {
@@ -366,8 +370,7 @@ __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, Topk
         if ((flags >> i) & 1u) {
             const uint32_t q = base + popc64(b & lt);
             const int j = start + i * kWave + lane;
-            si[q] = j;
-            sv[q] = e[j];  // re-read of this lane's own store
+            sp[q] = make_int2(j, __float_as_int(e[j]));  // re-read of this lane's own store
         }
         base += popc64(b);
     }

@@ -32,13 +32,26 @@ def _draw(wl: Workload, shape, gen) -> torch.Tensor:
     return torch.randn(shape, generator=gen, device=dev, dtype=torch.float32)
 
 
+ROW_ALIGN = 32   # floats: 128 bytes, one cache line
+
+
+def rows(K: int, d: int, device, zero: bool = False) -> torch.Tensor:
+    """A [K, d] fp32 view whose rows start on 128-byte boundaries (row pitch
+    rounded up to a multiple of 32 floats), the layout of K per-worker
+    buffers packed into one allocation."""
+    pitch = (d + ROW_ALIGN - 1) // ROW_ALIGN * ROW_ALIGN
+    buf = (torch.zeros if zero else torch.empty)((K, pitch), dtype=torch.float32, device=device)
+    return buf[:, :d]
+
+
 def grads(wl: Workload, t: int, device, out: torch.Tensor = None) -> torch.Tensor:
-    """g_{t,k} for all K workers as fp32 [K, d] on `device`."""
+    """g_{t,k} for all K workers as fp32 [K, d] on `device` (by default in
+    the line-aligned row layout of `rows`)."""
     device = torch.device(device)
     gen = torch.Generator(device=device)
     gen.manual_seed((wl.seed * 1_000_003 + 7919 * (t + 1)) & 0x7FFFFFFFFFFFFFFF)
     if out is None:
-        out = torch.empty((wl.K, wl.d), dtype=torch.float32, device=device)
+        out = rows(wl.K, wl.d, device)
     scale = _scale_vector(wl, device)
     for k in range(wl.K):
         x = _draw(wl, (wl.d,), gen)

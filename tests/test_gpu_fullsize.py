@@ -73,7 +73,7 @@ def test_full_size_workload(name, steps):
     print("full size %s: d=%d K=%d %s" % (name, d, K, wl.compressor), flush=True)
     bufs = [sdev.w0(wl, dev), None]
     bufs[1] = bufs[0].clone()
-    err = torch.zeros((K, d), dtype=torch.float32, device=dev)
+    err = sdev.rows(K, d, dev, zero=True)
     idx, val, ln = g.alloc_messages(dev)
     upd = torch.empty(d, dtype=torch.float32, device=dev)
     check = [0, K - 1]
