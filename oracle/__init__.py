@@ -1,5 +1,7 @@
 """GMC oracle: a plain, slow, single-threaded CPU implementation of one GMC
-iteration (Algorithm 1) and of the RBGS variant used by GMC+ (Algorithm 2).
+iteration (Algorithm 1), of GMC+'s RBGS compressor and detached point
+(Algorithm 2), and of the two alternative update rules of the appendix
+(momentum on the server; learning rate inside the residual).
 
 TEST INFRASTRUCTURE.  Only the test suite, ``__graft_entry__.smoke()`` and the
 bench's ``cpu_baseline`` leg may import this package.  The device library does
@@ -62,6 +64,19 @@ def _bind(lib):
     lib.orc_aggregate.restype = ctypes.c_int
     lib.orc_apply.argtypes = [c_i64, c_vp, c_vp]
     lib.orc_apply.restype = None
+    lib.orc_detach_constant.argtypes = [ctypes.c_double, ctypes.c_double]
+    lib.orc_detach_constant.restype = c_f
+    lib.orc_detach.argtypes = [c_i64, c_f, c_vp, c_vp, c_vp]
+    lib.orc_detach.restype = None
+    lib.orc_variant_constants.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_int,
+                                          ctypes.POINTER(c_f), ctypes.POINTER(c_f), ctypes.POINTER(c_f)]
+    lib.orc_variant_constants.restype = None
+    lib.orc_precompress_plain.argtypes = [c_i64, c_vp, c_vp, c_vp]
+    lib.orc_precompress_plain.restype = None
+    lib.orc_precompress_lr.argtypes = [c_i64, c_f, c_f, c_vp, c_vp, c_vp, c_vp, c_vp]
+    lib.orc_precompress_lr.restype = None
+    lib.orc_apply_server_momentum.argtypes = [c_i64, c_f, c_vp, c_vp, c_vp, c_vp]
+    lib.orc_apply_server_momentum.restype = None
     return lib
 
 
@@ -176,6 +191,52 @@ def apply(w: np.ndarray, delta, lib=None) -> None:
     (lib or load()).orc_apply(w.size, _ptr(w), _ptr(delta))
 
 
+def detach_constant(lam: float, eta: float, lib=None) -> np.float32:
+    return np.float32((lib or load()).orc_detach_constant(lam, eta))
+
+
+def detach(q, w_next, e_next, lib=None) -> np.ndarray:
+    """w_{t+1,k} = w_{t+1} - q e_{t+1,k} (Algorithm 2), q = fl32(lambda eta)."""
+    w_next, e_next = _f32(w_next), _f32(e_next)
+    out = np.empty_like(w_next)
+    (lib or load()).orc_detach(w_next.size, ctypes.c_float(float(q)), _ptr(w_next), _ptr(e_next), _ptr(out))
+    return out
+
+
+VARIANTS = {"gmc": 0, "server_momentum": 1, "lr_in_residual": 2}
+
+
+def variant_constants(variant: str, beta: float, eta: float, K: int, lib=None):
+    """(c, s, h) of an update rule: see ``orc_variant_constants``."""
+    c, s, h = ctypes.c_float(), ctypes.c_float(), ctypes.c_float()
+    (lib or load()).orc_variant_constants(VARIANTS[variant], beta, eta, K, ctypes.byref(c), ctypes.byref(s),
+                                          ctypes.byref(h))
+    return np.float32(c.value), np.float32(s.value), np.float32(h.value)
+
+
+def precompress_plain(g, e, lib=None) -> np.ndarray:
+    g, e = _f32(g), _f32(e)
+    u = np.empty_like(g)
+    (lib or load()).orc_precompress_plain(g.size, _ptr(g), _ptr(e), _ptr(u))
+    return u
+
+
+def precompress_lr(h, b, w_t, w_prev, g, e, lib=None) -> np.ndarray:
+    w_t, w_prev, g, e = map(_f32, (w_t, w_prev, g, e))
+    u = np.empty_like(w_t)
+    (lib or load()).orc_precompress_lr(w_t.size, ctypes.c_float(float(h)), ctypes.c_float(float(b)), _ptr(w_t),
+                                       _ptr(w_prev), _ptr(g), _ptr(e), _ptr(u))
+    return u
+
+
+def apply_server_momentum(b, w_t, w_prev, delta, lib=None) -> np.ndarray:
+    w_t, w_prev, delta = map(_f32, (w_t, w_prev, delta))
+    out = np.empty_like(w_t)
+    (lib or load()).orc_apply_server_momentum(w_t.size, ctypes.c_float(float(b)), _ptr(w_t), _ptr(w_prev),
+                                              _ptr(delta), _ptr(out))
+    return out
+
+
 # ---------------------------------------------------------------------------
 # one GMC iteration for K workers, in the message layout of the device ABI
 # ---------------------------------------------------------------------------
@@ -190,11 +251,13 @@ class GmcOracle:
     """
 
     def __init__(self, d: int, K: int, compressor: str, ratio: float, beta: float, eta: float,
-                 seed: int = 0, seg_off=None, block: int = 4096, lib=None):
+                 seed: int = 0, seg_off=None, block: int = 4096, lib=None, variant: str = "gmc",
+                 lam: float = 0.0):
         self.lib = lib or load()
         self.d, self.K, self.compressor = d, K, compressor
         self.ratio = ratio
-        self.c, self.s = constants(beta, eta, K, self.lib)
+        self.variant, self.beta, self.lam = variant, beta, lam
+        self.set_eta(eta)
         self.seed, self.block, self.t = seed, block, 0
         if seg_off is None:
             seg_off = [0, d]
@@ -210,7 +273,17 @@ class GmcOracle:
             self.seg_k = np.array(ks, dtype=np.int64)
             self.index_len = self.message_len = int(sum(ks))
 
+    def set_eta(self, eta: float) -> None:
+        """The learning rate of the following iterations (a schedule)."""
+        self.eta = eta
+        self.c, self.s, self.h = variant_constants(self.variant, self.beta, eta, self.K, self.lib)
+        self.q = detach_constant(self.lam, eta, self.lib)
+
     def precompress(self, w_t, w_prev, g, e) -> np.ndarray:
+        if self.variant == "server_momentum":
+            return precompress_plain(g, e, self.lib)
+        if self.variant == "lr_in_residual":
+            return precompress_lr(self.h, self.c, w_t, w_prev, g, e, self.lib)
         return precompress(self.c, w_t, w_prev, g, e, self.lib)
 
     def step(self, w_t, w_prev, grads, err):
@@ -252,3 +325,17 @@ class GmcOracle:
 
     def apply(self, w: np.ndarray, delta) -> None:
         apply(w, delta, self.lib)
+
+    def next_params(self, w_t, w_prev, delta) -> np.ndarray:
+        """w_{t+1} from the server's sum: w_t + delta, or with momentum on
+        the server (w_t + delta) + beta (w_t - w_{t-1})."""
+        if self.variant == "server_momentum":
+            return apply_server_momentum(self.c, w_t, w_prev, delta, self.lib)
+        w = _f32(w_t).copy()
+        apply(w, delta, self.lib)
+        return w
+
+    def detach(self, w_next, err) -> np.ndarray:
+        """GMC+'s detached points w_{t+1,k} = w_{t+1} - (lambda eta) e_{t+1,k},
+        [K, d] (Algorithm 2)."""
+        return np.stack([detach(self.q, w_next, err[k], self.lib) for k in range(self.K)])

@@ -266,3 +266,98 @@ void orc_apply(int64_t d, float* w, const float* delta)
 {
     for (int64_t j = 0; j < d; ++j) w[j] = w[j] + delta[j];
 }
+
+/* ------------------------------------------------------------------------- */
+/* GMC+: the detached point (Algorithm 2)                                     */
+/* ------------------------------------------------------------------------- */
+
+/* lambda * eta, the coefficient of the residual in the detach step, formed
+ * in double and rounded once. */
+float orc_detach_constant(double lambda, double eta)
+{
+    return (float)(lambda * eta);
+}
+
+/*
+ * w_{t+1,k} = w_{t+1} - (lambda eta) e_{t+1,k}        (Algorithm 2, detach)
+ *
+ * GMC+ takes worker k's next stochastic gradient at this point instead of at
+ * w_{t+1}; with lambda = 0 the point is w_{t+1} and GMC+ is GMC.  q is
+ * orc_detach_constant(lambda, eta).
+ */
+void orc_detach(int64_t d, float q, const float* w_next, const float* e_next, float* w_k)
+{
+    for (int64_t j = 0; j < d; ++j) {
+        float r = q * e_next[j];
+        w_k[j] = w_next[j] - r;
+    }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Other ways of combining momentum and error feedback (appendix)             */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * Constants of the three update rules, each formed in double and rounded
+ * once to binary32:
+ *   variant 0, GMC (Algorithm 1):        c = beta/eta (worker), s = eta/K, h = 1;
+ *   variant 1, momentum on the server:   c = beta (server), s = eta/K, h = 1;
+ *   variant 2, lr inside the residual:   c = beta (worker), s = 1/K, h = eta.
+ * A learning-rate schedule changes eta between iterations; the constants are
+ * then those of the iteration's eta.
+ */
+void orc_variant_constants(int variant, double beta, double eta, int K, float* c, float* s, float* h)
+{
+    float c_gmc, s_gmc;
+    orc_constants(beta, eta, K, &c_gmc, &s_gmc);
+    const float b = (float)beta;
+    if (variant == 1) {
+        *c = b;
+        *s = s_gmc;
+        *h = 1.0f;
+    } else if (variant == 2) {
+        *c = (float)beta;
+        *s = (float)(1.0 / (double)K);
+        *h = (float)eta;
+    } else {
+        *c = c_gmc;
+        *s = s_gmc;
+        *h = 1.0f;
+    }
+}
+
+/* Momentum on the server: the worker's vector carries no momentum term,
+ * u = e_{t,k} + g_{t,k}. */
+void orc_precompress_plain(int64_t d, const float* g, const float* e, float* u)
+{
+    for (int64_t j = 0; j < d; ++j) u[j] = e[j] + g[j];
+}
+
+/* Learning rate inside the residual:
+ * u = e_{t,k} + eta g_{t,k} - beta (w_t - w_{t-1}), left to right, with
+ * h = eta and b = beta in binary32. */
+void orc_precompress_lr(int64_t d, float h, float b, const float* w_t, const float* w_prev,
+                        const float* g, const float* e, float* u)
+{
+    for (int64_t j = 0; j < d; ++j) {
+        float dw = w_t[j] - w_prev[j];
+        float pull = b * dw;
+        float sg = h * g[j];
+        float sum = e[j] + sg;
+        u[j] = sum - pull;
+    }
+}
+
+/* Momentum on the server: w_{t+1} = w_t - (eta/K) sum_k C(u_k) + beta (w_t - w_{t-1}),
+ * left to right: (w_t + delta) + b (w_t - w_{t-1}) with delta from
+ * orc_aggregate and b = beta in binary32. */
+void orc_apply_server_momentum(int64_t d, float b, const float* w_t, const float* w_prev,
+                               const float* delta, float* w_next)
+{
+    for (int64_t j = 0; j < d; ++j) {
+        float moved = w_t[j] + delta[j];
+        float back = w_t[j] - w_prev[j];
+        float push = b * back;
+        w_next[j] = moved + push;
+    }
+}

@@ -70,6 +70,31 @@ def _run(lib, wl: synth.Workload, ratio: float, steps: int, grad_fn=None, w0=Non
     return recs
 
 
+def _run_rule(lib, wl: synth.Workload, ratio: float, steps: int, variant: str = "gmc", lam: float = 0.0,
+              eta_fn=None, compressor: str = "topk", block: int = 4096):
+    """Like ``_run`` for any of the update rules, an eta schedule and GMC+'s
+    detached points (``wk``: w_{t+1,k} after each step)."""
+    orc = oracle.GmcOracle(wl.d, wl.K, compressor, ratio, wl.beta, wl.eta, seg_off=[0, wl.d], lib=lib,
+                           variant=variant, lam=lam, block=block)
+    w = wl.w0().copy()
+    w_prev = w.copy()
+    err = np.zeros((wl.K, wl.d), np.float32)
+    recs = []
+    for t in range(steps):
+        eta = wl.eta if eta_fn is None else eta_fn(t)
+        orc.set_eta(eta)
+        g = wl.grads(t)
+        e_before = err.copy()
+        us = np.stack([orc.precompress(w, w_prev, g[k], err[k]) for k in range(wl.K)])
+        idx, val, ln = orc.step(w, w_prev, g, err)
+        delta = orc.aggregate(idx, val, ln)
+        w_next = orc.next_params(w, w_prev, delta)
+        recs.append(dict(w_prev=w_prev, w=w, w_next=w_next, g=g, e=e_before, e_next=err.copy(), u=us,
+                         idx=idx, val=val, ln=ln, delta=delta, eta=eta, wk=orc.detach(w_next, err)))
+        w_prev, w = w, w_next
+    return recs
+
+
 # ---------------------------------------------------------------------------
 # counts and constants
 # ---------------------------------------------------------------------------
@@ -392,8 +417,147 @@ def pin_toy_quadratic_sparse_converges(lib):
     assert max(dist[-200:]) < 0.2 * math.sqrt(5.0)
 
 
+# ---------------------------------------------------------------------------
+# GMC+ (Algorithm 2): the detached point
+# ---------------------------------------------------------------------------
+
+def pin_detach_lambda_zero(lib):
+    """lambda = 0: every worker's point is w_{t+1} itself, bit for bit, so
+    GMC+ is GMC (Section 4)."""
+    rng = np.random.default_rng(21)
+    w = rng.standard_normal(3000).astype(np.float32)
+    e = (rng.standard_normal(3000) * 10.0 ** rng.integers(-40, 3, 3000)).astype(np.float32)
+    e[:4] = [0.0, -0.0, 1e-45, -3e-42]
+    for eta in (0.1, 0.05, 1.0):
+        q = oracle.detach_constant(0.0, eta, lib)
+        assert np.array_equal(_bits(oracle.detach(q, w, e, lib)), _bits(w))
+
+
+def _bar(recs, key):
+    return [np.asarray(r[key], np.float64).mean(0) for r in recs]
+
+
+def pin_gmcplus_average_rule(lib):
+    """Section 4: with wbar_t the mean of the detached points and ebar_t that
+    of the residuals, wbar_{t+1} = wbar_t + beta (wbar_t - wbar_{t-1})
+    + eta (1 - lambda)(ebar_{t+1} - ebar_t) + beta lambda eta (ebar_t - ebar_{t-1})
+    - eta gbar_t, for top-s and RBGS, checked within the binary32 rounding of
+    the operations involved."""
+    for comp, lam, ratio in [("topk", 0.5, 0.03), ("rbgs", 0.3, 0.25), ("topk", 1.0, 0.01)]:
+        wl = synth.Workload("gmcplus", [3000, 1096], K=3, ratio=ratio, beta=0.9, eta=0.1, steps=8,
+                            compressor=comp, dist="normal", scale_lo=1e-2, scale_hi=1.0)
+        recs = _run_rule(lib, wl, ratio, wl.steps, lam=lam, compressor=comp, block=512)
+        b, eta = wl.beta, wl.eta
+        f = lambda a: np.asarray(a, np.float64)
+        wbar = [f(recs[0]["w"])] + [f(r["wk"]).mean(0) for r in recs]      # wbar_0 = w_0
+        ebar = [np.zeros(wl.d)] + [f(r["e_next"]).mean(0) for r in recs]  # ebar_0 = 0
+        for t in range(1, len(recs)):
+            r = recs[t]
+            gbar = f(r["g"]).mean(0)
+            rhs = (wbar[t] + b * (wbar[t] - wbar[t - 1]) + eta * (1 - lam) * (ebar[t + 1] - ebar[t])
+                   + b * lam * eta * (ebar[t] - ebar[t - 1]) - eta * gbar)
+            scale = (np.abs(f(r["w_next"])) + np.abs(f(r["w"])) + np.abs(f(r["w_prev"]))
+                     + eta * (np.abs(f(r["g"])).mean(0) + np.abs(f(r["e"])).mean(0)
+                              + np.abs(f(r["e_next"])).mean(0) + wl.K * np.abs(f(r["u"])).mean(0)))
+            assert np.all(np.abs(wbar[t + 1] - rhs) <= 64 * EPS32 * scale + 1e-30), (comp, lam, t)
+
+
+def pin_gmcplus_lemma(lib):
+    """The auxiliary sequence of GMC+ (Section 4):
+    zbar_t = wbar_t + beta/(1-beta)(wbar_t - wbar_{t-1})
+             - [(1-lambda) eta ebar_t + beta lambda eta ebar_{t-1}]/(1-beta)
+    moves by -eta/(1-beta) gbar_t per iteration."""
+    lam = 0.5
+    wl = synth.Workload("gmcplus", [2048, 77], K=4, ratio=0.05, beta=0.9, eta=0.1, steps=8,
+                        compressor="topk", dist="student_t", nu=3, scale_lo=1e-3, scale_hi=1.0)
+    recs = _run_rule(lib, wl, wl.ratio, wl.steps, lam=lam)
+    b, eta = wl.beta, wl.eta
+    f = lambda a: np.asarray(a, np.float64)
+    wbar = [f(recs[0]["w"]), f(recs[0]["w"])] + [f(r["wk"]).mean(0) for r in recs]  # wbar_{-1}, wbar_0, ...
+    ebar = [np.zeros(wl.d), np.zeros(wl.d)] + [f(r["e_next"]).mean(0) for r in recs]
+
+    def z(i):  # i = t + 1 in the lists above
+        return (wbar[i] + b / (1 - b) * (wbar[i] - wbar[i - 1])
+                - ((1 - lam) * eta * ebar[i] + b * lam * eta * ebar[i - 1]) / (1 - b))
+    for t, r in enumerate(recs):
+        gbar = f(r["g"]).mean(0)
+        scale = (np.abs(f(r["w_next"])) + np.abs(f(r["w"])) + np.abs(f(r["w_prev"]))
+                 + eta * (np.abs(f(r["g"])).mean(0) + np.abs(f(r["e"])).mean(0)
+                          + np.abs(f(r["e_next"])).mean(0) + wl.K * np.abs(f(r["u"])).mean(0)))
+        assert np.all(np.abs(z(t + 2) - (z(t + 1) - eta / (1 - b) * gbar))
+                      <= 256 / (1 - b) * EPS32 * scale + 1e-30), t
+
+
+# ---------------------------------------------------------------------------
+# the appendix's other update rules, and a learning-rate schedule
+# ---------------------------------------------------------------------------
+
+def _eq8_check(recs, wl, bound_mult=16):
+    f = lambda a: np.asarray(a, np.float64)
+    for r in recs:
+        eta = r["eta"]
+        gbar, ebar, ebar1 = _eq8_terms(r, wl)
+        w, wp, wn = f(r["w"]), f(r["w_prev"]), f(r["w_next"])
+        rhs = w - eta * gbar - eta * ebar + eta * ebar1 + wl.beta * (w - wp)
+        scale = (np.abs(w) + np.abs(wn) + wl.beta * np.abs(w - wp)
+                 + eta * (np.abs(f(r["g"])).mean(0) + np.abs(f(r["e"])).mean(0)
+                          + wl.K * np.abs(f(r["u"])).mean(0)) + np.abs(f(r["e"])).mean(0))
+        assert np.all(np.abs(wn - rhs) <= bound_mult * EPS32 * scale + 1e-30)
+
+
+def pin_server_momentum_rule(lib):
+    """Momentum on the server (appendix): without compression it is momentum
+    SGD, and with it eq. 8 still holds (the appendix derives the same update
+    rule once C is eliminated)."""
+    wl = synth.Workload("srv", [3000, 17], K=3, ratio=1.0, beta=0.9, eta=0.1, steps=12,
+                        compressor="topk", dist="normal")
+    recs = _run_rule(lib, wl, 1.0, wl.steps, variant="server_momentum")
+    m = np.zeros(wl.d)
+    w = np.asarray(recs[0]["w"], np.float64)
+    for r in recs:
+        m = wl.beta * m + wl.eta * np.asarray(r["g"], np.float64).mean(0)
+        w = w - m
+        assert np.all(_bits(r["e_next"]) == 0)
+        assert np.max(np.abs(np.asarray(r["w_next"], np.float64) - w)) <= 2e-5 * (1 + np.max(np.abs(w)))
+    wl = synth.Workload("srv", [2500, 1500, 96], K=4, ratio=0.02, beta=0.9, eta=0.1, steps=12,
+                        compressor="topk", dist="normal", scale_lo=1e-2, scale_hi=1.0)
+    _eq8_check(_run_rule(lib, wl, wl.ratio, wl.steps, variant="server_momentum"), wl)
+
+
+def pin_lr_in_residual_equals_gmc(lib):
+    """Learning rate inside the residual (appendix) is GMC when eta is
+    constant.  With eta a power of two every scaling by eta is exact in
+    binary32, so the residuals and messages are exactly eta times GMC's and
+    the parameters are identical, bit for bit."""
+    eta = 0.125
+    wl = synth.Workload("lr", [3000, 1096], K=3, ratio=0.03, beta=0.9, eta=eta, steps=6,
+                        compressor="topk", dist="normal", scale_lo=1e-2, scale_hi=1.0)
+    a = _run_rule(lib, wl, wl.ratio, wl.steps)
+    b = _run_rule(lib, wl, wl.ratio, wl.steps, variant="lr_in_residual")
+    e = np.float32(eta)
+    for ra, rb in zip(a, b):
+        assert np.array_equal(ra["idx"], rb["idx"])
+        assert np.array_equal(_bits(ra["val"] * e), _bits(rb["val"]))
+        assert np.array_equal(_bits(ra["e_next"] * e), _bits(rb["e_next"]))
+        assert np.array_equal(_bits(ra["w_next"]), _bits(rb["w_next"]))
+
+
+def pin_eta_schedule_eq8(lib):
+    """Under the cosine schedule of Section 5.1 (eta_t = eta (1 + cos(pi t/T))/2),
+    GMC's iterates satisfy eq. 8 with eta_t in every term, which holds only if
+    the momentum coefficient of iteration t is beta/eta_t and the server's
+    scale eta_t/K."""
+    wl = synth.Workload("cos", [2500, 1500, 96], K=4, ratio=0.02, beta=0.9, eta=0.1, steps=12,
+                        compressor="topk", dist="normal", scale_lo=1e-2, scale_hi=1.0)
+    T = 16
+    sched = lambda t: wl.eta * 0.5 * (1 + math.cos(math.pi * t / T))
+    _eq8_check(_run_rule(lib, wl, wl.ratio, wl.steps, eta_fn=sched), wl)
+
+
 ALL_PINS = [pin_count_rule, pin_constants, pin_topk_bruteforce, pin_delta_approximation,
             pin_error_feedback_identity, pin_msgd_reduction, pin_update_rule_eq8, pin_lemma1,
             pin_aggregate_single_worker, pin_aggregate_sum, pin_splitmix64_vectors,
             pin_rbgs_blocks, pin_rbgs_step_and_cost, pin_toy_quadratic_closed_form,
-            pin_toy_quadratic_sparse_converges]
+            pin_toy_quadratic_sparse_converges, pin_detach_lambda_zero, pin_gmcplus_average_rule,
+            pin_gmcplus_lemma, pin_server_momentum_rule, pin_lr_in_residual_equals_gmc,
+            pin_eta_schedule_eq8]

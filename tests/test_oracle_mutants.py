@@ -36,6 +36,17 @@ MUTANTS = {
                          "int64_t lo = (int64_t)blocks[q] * B, hi = lo + B - 1;"),
     "splitmix_shift": ("z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;",
                        "z = (z ^ (z >> 28)) * 0x94d049bb133111ebULL;"),
+    "detach_sign": ("w_k[j] = w_next[j] - r;", "w_k[j] = w_next[j] + r;"),
+    "detach_lambda_over_eta": ("return (float)(lambda * eta);", "return (float)(lambda / eta);"),
+    "detach_eta_dropped": ("return (float)(lambda * eta);", "return (float)lambda;"),
+    "plain_feedback_dropped": ("u[j] = e[j] + g[j];", "u[j] = g[j];"),
+    "lr_gradient_unscaled": ("float sg = h * g[j];", "float sg = g[j];"),
+    "lr_momentum_sign": ("u[j] = sum - pull;", "u[j] = sum + pull;"),
+    "lr_coeff_over_eta": ("*c = (float)beta;", "*c = c_gmc;"),
+    "lr_server_scale": ("*s = (float)(1.0 / (double)K);", "*s = s_gmc;"),
+    "server_momentum_sign": ("w_next[j] = moved + push;", "w_next[j] = moved - push;"),
+    "server_momentum_dropped": ("w_next[j] = moved + push;", "w_next[j] = moved;"),
+    "server_coeff_over_eta": ("*c = b;", "*c = c_gmc;"),
 }
 
 
