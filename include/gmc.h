@@ -1,7 +1,8 @@
 /*
  * gmc.h -- C ABI of the MI355X (gfx950) library for the data-parallel hot
- * path of Global Momentum Compression (GMC, Algorithm 1; its RBGS variant as
- * used by GMC+, Algorithm 2).
+ * path of Global Momentum Compression (GMC, Algorithm 1), of GMC+ (Algorithm
+ * 2: RBGS and the detached points), and of the two other ways of combining
+ * momentum with error feedback that the paper's appendix compares GMC with.
  *
  * One call sequence is one iteration t of Algorithm 1 for K workers that
  * live on one GPU as K device-resident vectors:
@@ -13,6 +14,10 @@
  *   gmc_aggregate  the server's update w_{t+1} - w_t = -(eta/K) sum_k C(u_k),
  *                  materialised as a dense vector          (Algorithm 1, server)
  *   gmc_apply      w_{t+1} = w_t + (w_{t+1} - w_t)          (Algorithm 1, workers)
+ *
+ * gmc_aggregate_apply and gmc_finish fuse the last two; gmc_step_detach,
+ * gmc_finish and gmc_detach also produce GMC+'s detached points
+ * w_{t+1,k} = w_{t+1} - lambda eta e_{t+1,k} (Algorithm 2).
  *
  * Conventions shared by every entry point:
  *   - Arguments named *_dev are device pointers to memory the caller owns
@@ -151,7 +156,8 @@ gmc_status gmc_aggregate(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_
  * equal w_dev (in place); otherwise the two must not overlap.  Out of place
  * the caller keeps w_{t+1} in w_out_dev and w_t in w_dev, i.e. swaps the
  * roles of its two parameter buffers for the next gmc_step instead of
- * copying w into w_prev.  update_dev may not alias either.
+ * copying w into w_prev.  update_dev may not alias either.  Not with
+ * GMC_RULE_SERVER_MOMENTUM (GMC_EINVAL; use gmc_finish).
  */
 gmc_status gmc_aggregate_apply(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev,
                                const int64_t* msg_len_dev, const float* w_dev, float* w_out_dev,
@@ -159,12 +165,79 @@ gmc_status gmc_aggregate_apply(gmc_ctx* ctx, const int32_t* idx_dev, const float
 
 /*
  * Workers' apply (Algorithm 1): w_prev_out_dev[j] = w_dev[j] (when not NULL),
- * then w_dev[j] = w_dev[j] + update_dev[j], for every j in [0, d).
+ * then w_dev[j] = w_dev[j] + update_dev[j], for every j in [0, d).  Not with
+ * GMC_RULE_SERVER_MOMENTUM (GMC_EINVAL; gmc_finish applies that rule).
  *   w_dev           [d] fp32 in/out
  *   w_prev_out_dev  [d] fp32 out or NULL; may not alias w_dev
  *   update_dev      [d] fp32 in
  */
 gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const float* update_dev);
+
+/*
+ * Update rules (before the first step only; default GMC_RULE_GMC):
+ *   GMC_RULE_GMC              Algorithm 1: u = (e + g) - c (w_t - w_{t-1}) with
+ *                             c = fl32(beta/eta); update = -(fl32(eta/K) * sum)
+ *   GMC_RULE_SERVER_MOMENTUM  appendix, momentum on the server: u = e + g;
+ *                             update = -(fl32(eta/K) * sum) and
+ *                             w_{t+1} = (w_t + update) + fl32(beta) (w_t - w_{t-1}),
+ *                             so the apply needs w_{t-1} (gmc_finish only)
+ *   GMC_RULE_LR_IN_RESIDUAL   appendix, learning rate inside the residual:
+ *                             u = (e + fl32(eta) g) - fl32(beta) (w_t - w_{t-1});
+ *                             update = -(fl32(1/K) * sum)
+ * Each operation is one binary32 rounding, left to right as written.
+ */
+enum { GMC_RULE_GMC = 0, GMC_RULE_SERVER_MOMENTUM = 1, GMC_RULE_LR_IN_RESIDUAL = 2 };
+gmc_status gmc_set_rule(gmc_ctx* ctx, int32_t rule);
+
+/* Learning rate of the following iterations (eta > 0, finite), e.g. the
+ * cosine schedule of Section 5.1; the rule's constants are re-derived from
+ * it (in binary64, rounded once).  Any time between iterations. */
+gmc_status gmc_set_eta(gmc_ctx* ctx, double eta);
+
+/* GMC+'s detach coefficient lambda in [0, 1] (Algorithm 2; default 0, which
+ * makes the detached points equal to w_{t+1}).  q = fl32(lambda * eta) at the
+ * current eta.  Any time between iterations. */
+gmc_status gmc_set_lambda(gmc_ctx* ctx, double lambda);
+
+/*
+ * gmc_step for GMC+ (Algorithm 2): the same worker pass, and in the same
+ * streaming pass w_k_dev[k][j] = w_t[j] - q u_k[j], which is already the
+ * detached point w_{t+1,k}[j] = w_{t+1}[j] - q e_{t+1,k}[j] at every component
+ * that no worker sends (there e_{t+1,k} = u_k and w_{t+1} = w_t, bit for bit).
+ * gmc_finish with the same w_k_dev completes the others.
+ *   w_k_dev  host array of K device pointers, each [d] fp32 out
+ * Not with GMC_RULE_SERVER_MOMENTUM (w_{t+1} differs from w_t everywhere):
+ * GMC_EINVAL; use gmc_detach there.
+ */
+gmc_status gmc_step_detach(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev,
+                           const float* const* grads_dev, float* const* err_dev, float* const* w_k_dev,
+                           int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev);
+
+/*
+ * The server pass of an iteration under the context's rule (the sum as in
+ * gmc_aggregate, then the apply), and optionally the completion of GMC+'s
+ * detached points:
+ *   w_dev       [d] fp32 in: w_t
+ *   w_prev_dev  [d] fp32 in: w_{t-1}; required by GMC_RULE_SERVER_MOMENTUM,
+ *               ignored (may be NULL) otherwise; may equal w_out_dev (the
+ *               caller's buffer swap), not w_dev
+ *   w_out_dev   [d] fp32 out: w_{t+1}; may equal w_dev (in place)
+ *   update_dev  [d] fp32 out or NULL: -(s * sum), the sparse part
+ *   err_dev, w_k_dev  NULL, or host arrays of K device pointers: e_{t+1,k}
+ *               (as gmc_step_detach left them) and the detached points that
+ *               gmc_step_detach started; every component some worker sent
+ *               gets w_k[j] = w_{t+1}[j] - q e_{t+1,k}[j] (Algorithm 2)
+ */
+gmc_status gmc_finish(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev, const int64_t* msg_len_dev,
+                      const float* w_dev, const float* w_prev_dev, float* w_out_dev, float* update_dev,
+                      const float* const* err_dev, float* const* w_k_dev);
+
+/*
+ * GMC+'s detached points as one dense pass (Algorithm 2, detach):
+ * w_k_dev[k][j] = w_dev[j] - q err_dev[k][j] for every worker and component,
+ * with w_dev = w_{t+1} and err = e_{t+1,k}; any rule.
+ */
+gmc_status gmc_detach(gmc_ctx* ctx, const float* w_dev, const float* const* err_dev, float* const* w_k_dev);
 
 /* Step counter t (RBGS draws depend on (seed, t)); for checkpoint/resume. */
 gmc_status gmc_get_step(const gmc_ctx* ctx, int64_t* t);

@@ -30,8 +30,10 @@ struct gmc_ctx {
     int32_t K = 0;
     int32_t comp = 0;
     double ratio = 0, beta = 0, eta = 0;
+    double lambda = 0;             // GMC+ detach coefficient
+    int32_t rule = kRuleGmc;       // update rule
     uint64_t seed = 0;
-    float c = 0, s = 0;
+    float c = 0, s = 0, h = 1, b = 0, q = 0;  // see derive_constants
     int64_t t = 0;
     hipStream_t stream = nullptr;
     int device = 0;
@@ -95,6 +97,29 @@ gmc_status hip_fail(gmc_ctx* ctx, hipError_t e, const char* what) {
         gmc_status st_ = (x);            \
         if (st_ != GMC_OK) return st_;   \
     } while (0)
+
+// Constants of the update rule at the current eta, each formed in binary64
+// and rounded once: c multiplies w_t - w_{t-1} in the workers' vector, h the
+// gradient, s the server's sum, b the server's momentum term, q the residual
+// in GMC+'s detach.
+void derive_constants(gmc_ctx* ctx) {
+    const double beta = ctx->beta, eta = ctx->eta, K = (double)ctx->K;
+    ctx->h = 1.0f;
+    ctx->b = 0.0f;
+    if (ctx->rule == kRuleServerMomentum) {
+        ctx->c = 0.0f;
+        ctx->s = (float)(eta / K);
+        ctx->b = (float)beta;
+    } else if (ctx->rule == kRuleLrInResidual) {
+        ctx->c = (float)beta;
+        ctx->s = (float)(1.0 / K);
+        ctx->h = (float)eta;
+    } else {
+        ctx->c = (float)(beta / eta);
+        ctx->s = (float)(eta / K);
+    }
+    ctx->q = (float)(ctx->lambda * eta);
+}
 
 int64_t count_for(int64_t n, double ratio) {
     const double x = ratio * (double)n;
@@ -393,8 +418,7 @@ gmc_status gmc_init(gmc_ctx** out, int64_t d, int32_t K, int32_t compressor, dou
     ctx->beta = beta;
     ctx->eta = eta;
     ctx->seed = seed;
-    ctx->c = (float)(beta / eta);
-    ctx->s = (float)(eta / (double)K);
+    derive_constants(ctx);
     ctx->seg_off = {0, d};
     ctx->seg_k = {(int32_t)count_for(d, ratio)};
     ctx->k_tot = ctx->seg_k[0];
@@ -470,20 +494,28 @@ int64_t gmc_index_len(const gmc_ctx* ctx) {
     return ctx->comp == GMC_RBGS ? (int64_t)ctx->n_sel : ctx->k_tot;
 }
 
-gmc_status gmc_step(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev, const float* const* grads_dev,
-                    float* const* err_dev, int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev) {
-    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_step: ctx is NULL");
-    if (!w_t_dev || !w_prev_dev || !grads_dev || !err_dev || !idx_dev || !val_dev || !msg_len_dev)
-        return fail(ctx, GMC_EINVAL, "gmc_step: NULL argument");
+}  // extern "C"
+
+namespace {
+
+gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev, const float* const* grads_dev,
+                     float* const* err_dev, float* const* y_dev, int32_t* idx_dev, float* val_dev,
+                     int64_t* msg_len_dev) {
     StepArgs a{};
     a.w_t = w_t_dev;
     a.w_prev = w_prev_dev;
     a.c = ctx->c;
+    a.h = ctx->h;
+    a.q = ctx->q;
+    a.rule = ctx->rule;
+    a.detach = y_dev ? 1 : 0;
     a.d = (int32_t)ctx->d;
     for (int k = 0; k < ctx->K; ++k) {
-        if (!grads_dev[k] || !err_dev[k]) return fail(ctx, GMC_EINVAL, "gmc_step: NULL worker pointer");
+        if (!grads_dev[k] || !err_dev[k] || (y_dev && !y_dev[k]))
+            return fail(ctx, GMC_EINVAL, "gmc_step: NULL worker pointer");
         a.wp.g[k] = grads_dev[k];
         a.wp.e[k] = err_dev[k];
+        a.wp.y[k] = y_dev ? y_dev[k] : nullptr;
     }
     GMC_TRY(prepare(ctx));
     GMC_HIP(ctx, hipSetDevice(ctx->device));
@@ -504,7 +536,8 @@ gmc_status gmc_step(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev,
         uint64_t vec_mask = 0;
         const bool w_ok = ((uintptr_t)w_t_dev & 15u) == 0 && ((uintptr_t)w_prev_dev & 15u) == 0;
         for (int k = 0; k < ctx->K && w_ok; ++k)
-            if ((((uintptr_t)grads_dev[k] | (uintptr_t)err_dev[k]) & 15u) == 0) vec_mask |= 1ull << k;
+            if ((((uintptr_t)grads_dev[k] | (uintptr_t)err_dev[k] | (uintptr_t)a.wp.y[k]) & 15u) == 0)
+                vec_mask |= 1ull << k;
         const uint64_t all = ctx->K == 64 ? ~0ull : ((1ull << ctx->K) - 1ull);
         const int32_t* gl = vec_mask == all ? ctx->gen_list : nullptr;
         const int32_t ng = vec_mask == all ? ctx->n_gen : ctx->geo.n_chunks;
@@ -532,25 +565,53 @@ gmc_status gmc_step(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev,
     return GMC_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+gmc_status gmc_step(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev, const float* const* grads_dev,
+                    float* const* err_dev, int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_step: ctx is NULL");
+    if (!w_t_dev || !w_prev_dev || !grads_dev || !err_dev || !idx_dev || !val_dev || !msg_len_dev)
+        return fail(ctx, GMC_EINVAL, "gmc_step: NULL argument");
+    return step_impl(ctx, w_t_dev, w_prev_dev, grads_dev, err_dev, nullptr, idx_dev, val_dev, msg_len_dev);
+}
+
+gmc_status gmc_step_detach(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev,
+                           const float* const* grads_dev, float* const* err_dev, float* const* w_k_dev,
+                           int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_step_detach: ctx is NULL");
+    if (!w_t_dev || !w_prev_dev || !grads_dev || !err_dev || !w_k_dev || !idx_dev || !val_dev || !msg_len_dev)
+        return fail(ctx, GMC_EINVAL, "gmc_step_detach: NULL argument");
+    if (ctx->rule == kRuleServerMomentum)
+        return fail(ctx, GMC_EINVAL,
+                    "gmc_step_detach: with momentum on the server w_{t+1} differs from w_t everywhere; "
+                    "use gmc_detach after the apply");
+    return step_impl(ctx, w_t_dev, w_prev_dev, grads_dev, err_dev, w_k_dev, idx_dev, val_dev, msg_len_dev);
+}
+
 }  // extern "C"
 
 namespace {
 
 gmc_status aggregate_impl(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev, const int64_t* msg_len_dev,
-                          float* update_dev, const float* w_in, float* w_out) {
+                          FinishArgs& f) {
     GMC_TRY(prepare(ctx));
     GMC_HIP(ctx, hipSetDevice(ctx->device));
+    f.s = ctx->s;
+    f.b = ctx->b;
+    f.q = ctx->q;
     const int64_t row_i = gmc_index_len(ctx), row_v = gmc_message_len(ctx);
     hipEvent_t ev;
     GMC_TRY(prof_begin(ctx, 4, &ev));
     if (ctx->comp == GMC_RBGS) {
-        GMC_LAUNCH(ctx, launch_agg_rbgs(ctx->K, (int32_t)ctx->d, ctx->block, ctx->s, idx_dev, ctx->n_sel, val_dev,
-                                        row_v, update_dev, w_in, w_out, ctx->stream));
+        GMC_LAUNCH(ctx, launch_agg_rbgs(ctx->K, (int32_t)ctx->d, ctx->block, idx_dev, ctx->n_sel, val_dev, row_v, f,
+                                        ctx->stream));
     } else {
         GMC_LAUNCH(ctx, launch_agg_rowptr(ctx->K, (int32_t)ctx->d, idx_dev, row_i, msg_len_dev, ctx->rowptr,
                                           ctx->n_ranges, ctx->stream));
-        GMC_LAUNCH(ctx, launch_agg_topk(ctx->K, (int32_t)ctx->d, ctx->s, idx_dev, row_i, val_dev, row_v, ctx->rowptr,
-                                        ctx->n_ranges, update_dev, w_in, w_out, ctx->stream));
+        GMC_LAUNCH(ctx, launch_agg_topk(ctx->K, (int32_t)ctx->d, idx_dev, row_i, val_dev, row_v, ctx->rowptr,
+                                        ctx->n_ranges, f, ctx->stream));
     }
     GMC_TRY(prof_end(ctx, 4, ev));
     return GMC_OK;
@@ -564,7 +625,9 @@ gmc_status gmc_aggregate(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_
                          float* update_dev) {
     if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_aggregate: ctx is NULL");
     if (!idx_dev || !val_dev || !msg_len_dev || !update_dev) return fail(ctx, GMC_EINVAL, "gmc_aggregate: NULL argument");
-    return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, update_dev, nullptr, nullptr);
+    FinishArgs f{};
+    f.update = update_dev;
+    return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, f);
 }
 
 gmc_status gmc_aggregate_apply(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev,
@@ -575,18 +638,99 @@ gmc_status gmc_aggregate_apply(gmc_ctx* ctx, const int32_t* idx_dev, const float
         return fail(ctx, GMC_EINVAL, "gmc_aggregate_apply: NULL argument");
     if (update_dev && (update_dev == w_out_dev || update_dev == w_dev))
         return fail(ctx, GMC_EINVAL, "gmc_aggregate_apply: update may not alias w or w_out");
-    return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, update_dev, w_dev, w_out_dev);
+    if (ctx->rule == kRuleServerMomentum)
+        return fail(ctx, GMC_EINVAL, "gmc_aggregate_apply: momentum on the server needs w_{t-1}; use gmc_finish");
+    FinishArgs f{};
+    f.w_in = w_dev;
+    f.w_out = w_out_dev;
+    f.update = update_dev;
+    return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, f);
+}
+
+gmc_status gmc_finish(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev, const int64_t* msg_len_dev,
+                      const float* w_dev, const float* w_prev_dev, float* w_out_dev, float* update_dev,
+                      const float* const* err_dev, float* const* w_k_dev) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_finish: ctx is NULL");
+    if (!idx_dev || !val_dev || !msg_len_dev || !w_dev || !w_out_dev)
+        return fail(ctx, GMC_EINVAL, "gmc_finish: NULL argument");
+    if (update_dev && (update_dev == w_out_dev || update_dev == w_dev || update_dev == w_prev_dev))
+        return fail(ctx, GMC_EINVAL, "gmc_finish: update may not alias w, w_prev or w_out");
+    if (ctx->rule == kRuleServerMomentum && !w_prev_dev)
+        return fail(ctx, GMC_EINVAL, "gmc_finish: momentum on the server needs w_prev");
+    if (w_prev_dev && w_prev_dev == w_dev) return fail(ctx, GMC_EINVAL, "gmc_finish: w_prev may not alias w");
+    FinishArgs f{};
+    f.w_in = w_dev;
+    f.w_prev = ctx->rule == kRuleServerMomentum ? w_prev_dev : nullptr;
+    f.w_out = w_out_dev;
+    f.update = update_dev;
+    if (w_k_dev) {
+        if (ctx->rule == kRuleServerMomentum)
+            return fail(ctx, GMC_EINVAL, "gmc_finish: detached points with momentum on the server: use gmc_detach");
+        if (!err_dev) return fail(ctx, GMC_EINVAL, "gmc_finish: detached points need err");
+        f.detach = 1;
+        for (int k = 0; k < ctx->K; ++k) {
+            if (!err_dev[k] || !w_k_dev[k]) return fail(ctx, GMC_EINVAL, "gmc_finish: NULL worker pointer");
+            f.e[k] = err_dev[k];
+            f.y[k] = w_k_dev[k];
+        }
+    }
+    return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, f);
+}
+
+gmc_status gmc_detach(gmc_ctx* ctx, const float* w_dev, const float* const* err_dev, float* const* w_k_dev) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_detach: ctx is NULL");
+    if (!w_dev || !err_dev || !w_k_dev) return fail(ctx, GMC_EINVAL, "gmc_detach: NULL argument");
+    DetachArgs a{};
+    a.w = w_dev;
+    a.q = ctx->q;
+    a.d = (int32_t)ctx->d;
+    for (int k = 0; k < ctx->K; ++k) {
+        if (!err_dev[k] || !w_k_dev[k]) return fail(ctx, GMC_EINVAL, "gmc_detach: NULL worker pointer");
+        a.e[k] = err_dev[k];
+        a.y[k] = w_k_dev[k];
+    }
+    GMC_HIP(ctx, hipSetDevice(ctx->device));
+    GMC_LAUNCH(ctx, launch_detach(a, ctx->K, ctx->stream));
+    return GMC_OK;
 }
 
 gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const float* update_dev) {
     if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_apply: ctx is NULL");
     if (!w_dev || !update_dev) return fail(ctx, GMC_EINVAL, "gmc_apply: NULL argument");
     if (w_prev_out_dev == w_dev) return fail(ctx, GMC_EINVAL, "gmc_apply: w_prev_out may not alias w");
+    if (ctx->rule == kRuleServerMomentum)
+        return fail(ctx, GMC_EINVAL, "gmc_apply: momentum on the server needs w_{t-1}; use gmc_finish");
     GMC_HIP(ctx, hipSetDevice(ctx->device));
     hipEvent_t ev;
     GMC_TRY(prof_begin(ctx, 5, &ev));
     GMC_LAUNCH(ctx, launch_apply((int32_t)ctx->d, w_dev, w_prev_out_dev, update_dev, ctx->stream));
     GMC_TRY(prof_end(ctx, 5, ev));
+    return GMC_OK;
+}
+
+gmc_status gmc_set_rule(gmc_ctx* ctx, int32_t rule) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_set_rule: ctx is NULL");
+    if (rule != kRuleGmc && rule != kRuleServerMomentum && rule != kRuleLrInResidual)
+        return fail(ctx, GMC_EINVAL, "gmc_set_rule: unknown rule");
+    if (ctx->started) return fail(ctx, GMC_ESTATE, "gmc_set_rule: the rule is fixed after the first step");
+    ctx->rule = rule;
+    derive_constants(ctx);
+    return GMC_OK;
+}
+
+gmc_status gmc_set_eta(gmc_ctx* ctx, double eta) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_set_eta: ctx is NULL");
+    if (!(eta > 0.0 && std::isfinite(eta))) return fail(ctx, GMC_EINVAL, "gmc_set_eta: eta must be > 0 and finite");
+    ctx->eta = eta;
+    derive_constants(ctx);
+    return GMC_OK;
+}
+
+gmc_status gmc_set_lambda(gmc_ctx* ctx, double lambda) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_set_lambda: ctx is NULL");
+    if (!(lambda >= 0.0 && lambda <= 1.0)) return fail(ctx, GMC_EINVAL, "gmc_set_lambda: lambda must be in [0, 1]");
+    ctx->lambda = lambda;
+    derive_constants(ctx);
     return GMC_OK;
 }
 

@@ -39,9 +39,16 @@ constexpr int kAggRange = 2048;
 
 constexpr uint32_t kNoThreshold = 0xffffffffu;  // no speculative candidates
 
+// Update rules: GMC (Algorithm 1) and the two other ways of combining
+// momentum with error feedback that the appendix compares it with.
+constexpr int kRuleGmc = 0;             // u = (e + g) - (beta/eta)(w_t - w_{t-1})
+constexpr int kRuleServerMomentum = 1;  // u = e + g; the server adds beta (w_t - w_{t-1})
+constexpr int kRuleLrInResidual = 2;    // u = (e + eta g) - beta (w_t - w_{t-1})
+
 struct WorkerPtrs {
     const float* g[kMaxWorkers];
     float* e[kMaxWorkers];
+    float* y[kMaxWorkers];  // GMC+ detached points (written when StepArgs::detach)
 };
 
 // Per (worker, segment) pair state, kept in device memory across kernels.
@@ -102,8 +109,37 @@ struct StepArgs {
     const float* w_t;
     const float* w_prev;
     WorkerPtrs wp;
-    float c;
+    float c;         // coefficient of w_t - w_{t-1} in u (beta/eta; lr-in-residual: beta)
+    float h;         // coefficient of g in u (1; lr-in-residual: eta)
+    float q;         // lambda*eta of GMC+'s detach
+    int32_t rule;    // kRule*
+    int32_t detach;  // 1: also write y_k = w_t - q u_k (completed by the server pass)
     int32_t d;
+};
+
+// The server pass after the sum over workers: update = -(s * sum), the
+// apply rule, and the completion of GMC+'s detached points at the components
+// some worker sent (where w_{t+1} differs from w_t).
+struct FinishArgs {
+    const float* w_in;    // w_t; NULL: no apply
+    const float* w_prev;  // w_{t-1} for momentum on the server, else NULL
+    float* w_out;         // w_{t+1}; NULL: no apply
+    float* update;        // nullable
+    float s;              // server scale (eta/K; lr-in-residual: 1/K)
+    float b;              // server momentum coefficient (beta) when w_prev is set
+    float q;              // lambda*eta
+    int32_t detach;       // 1: y_k = w_{t+1} - q e_k at the sent components
+    const float* e[kMaxWorkers];  // e_{t+1,k}
+    float* y[kMaxWorkers];        // w_{t+1,k}
+};
+
+// Dense detached points: y_k = w - q e_k for every component and worker.
+struct DetachArgs {
+    const float* w;
+    float q;
+    int32_t d;
+    const float* e[kMaxWorkers];
+    float* y[kMaxWorkers];
 };
 
 // ----------------------------------------------------------------------------
@@ -135,14 +171,15 @@ hipError_t launch_rbgs_fused(const StepArgs& a, int32_t K, int32_t B, const int3
 hipError_t launch_agg_rowptr(int32_t K, int32_t d, const int32_t* idx, int64_t idx_row,
                              const int64_t* msg_len, int32_t* rowptr, int32_t n_ranges,
                              hipStream_t st);
-// update (nullable) = -(s * sum); with w_out: w_out = w_in + update as well
-hipError_t launch_agg_topk(int32_t K, int32_t d, float s, const int32_t* idx, int64_t idx_row,
+// update (nullable) = -(s * sum); with w_out: w_out = w_in + update (plus
+// b (w_in - w_prev) with w_prev) as well; see FinishArgs
+hipError_t launch_agg_topk(int32_t K, int32_t d, const int32_t* idx, int64_t idx_row,
                            const float* val, int64_t val_row, const int32_t* rowptr,
-                           int32_t n_ranges, float* update, const float* w_in, float* w_out,
+                           int32_t n_ranges, const FinishArgs& f, hipStream_t st);
+hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, const int32_t* blocks,
+                           int32_t n_sel, const float* val, int64_t val_row, const FinishArgs& f,
                            hipStream_t st);
-hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, float s, const int32_t* blocks,
-                           int32_t n_sel, const float* val, int64_t val_row, float* update,
-                           const float* w_in, float* w_out, hipStream_t st);
+hipError_t launch_detach(const DetachArgs& a, int32_t K, hipStream_t st);
 
 hipError_t launch_apply(int32_t d, float* w, float* w_prev_out, const float* update,
                         hipStream_t st);

@@ -75,6 +75,34 @@ __device__ __forceinline__ float precompress(float e, float g, float m) {
     return acc - m;
 }
 
+// u under an update rule, from e, g and the two parameter vectors:
+//   GMC (Algorithm 1)         (e + g) - c (w_t - w_prev)
+//   momentum on the server    e + g
+//   lr inside the residual    (e + h g) - c (w_t - w_prev)
+template <int kRule>
+__device__ __forceinline__ float rule_u(float e, float g, float wt, float wp, float c, float h) {
+    if (kRule == kRuleServerMomentum) return e + g;
+    const float m = c * (wt - wp);
+    if (kRule == kRuleLrInResidual) {
+        const float sg = h * g;
+        const float acc = e + sg;
+        return acc - m;
+    }
+    return precompress(e, g, m);
+}
+
+__device__ __forceinline__ float rule_u_rt(int rule, float e, float g, float wt, float wp, float c, float h) {
+    if (rule == kRuleServerMomentum) return rule_u<kRuleServerMomentum>(e, g, wt, wp, c, h);
+    if (rule == kRuleLrInResidual) return rule_u<kRuleLrInResidual>(e, g, wt, wp, c, h);
+    return rule_u<kRuleGmc>(e, g, wt, wp, c, h);
+}
+
+// GMC+'s detached point from w and the residual: w - q e (Algorithm 2).
+__device__ __forceinline__ float detached(float w, float e, float q) {
+    const float r = q * e;
+    return w - r;
+}
+
 // Block-wide (256 threads) exclusive scan of one uint32 per thread; returns
 // the thread's exclusive prefix and writes the total to *total.
 __device__ __forceinline__ uint32_t block_scan_excl(uint32_t v, uint32_t* total, uint32_t* sh /*[kWavesPerGroup]*/) {
@@ -142,6 +170,7 @@ __device__ __forceinline__ void store_agent(uint32_t* p, uint32_t v) {
 // streaming pass takes no atomics; the compaction kernel packs the slots.
 // ---------------------------------------------------------------------------
 
+template <int kRule, bool kDetach>
 __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                                 uint64_t vec_mask) {
     __shared__ uint32_t wtot[2][kWavesPerGroup];
@@ -157,30 +186,39 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
     const int seg = one ? 0 : g.chunk_seg[chunk];
     const int p = k * g.n_seg + seg;
     const uint32_t tau = s.pair[p].tau;
-    const float c = a.c;
+    const float c = a.c, h = a.h;
     const int o0 = threadIdx.x * 4;               // components o0..o0+3 and 1024+o0..1024+o0+3
     float* ep = a.wp.e[k] + start + o0;
     const float* gp = a.wp.g[k] + start + o0;
     const float* wt_p = a.w_t + start + o0;
     const float* wp_p = a.w_prev + start + o0;
+    constexpr bool kNeedW = kRule != kRuleServerMomentum || kDetach;
     float4 u[2], gv[2], wt[2], wv[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         u[i] = ld4_stream(ep + i * (kGroup * 4));
         gv[i] = ld4_stream(gp + i * (kGroup * 4));
-        wt[i] = ld4(wt_p + i * (kGroup * 4));
-        wv[i] = ld4(wp_p + i * (kGroup * 4));
+        if (kNeedW) {
+            wt[i] = ld4(wt_p + i * (kGroup * 4));
+            wv[i] = ld4(wp_p + i * (kGroup * 4));
+        } else {
+            wt[i] = wv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
     }
     uint32_t flags = 0;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-        const float4 m = make_float4(c * (wt[i].x - wv[i].x), c * (wt[i].y - wv[i].y), c * (wt[i].z - wv[i].z),
-                                     c * (wt[i].w - wv[i].w));
-        u[i].x = precompress(u[i].x, gv[i].x, m.x);
-        u[i].y = precompress(u[i].y, gv[i].y, m.y);
-        u[i].z = precompress(u[i].z, gv[i].z, m.z);
-        u[i].w = precompress(u[i].w, gv[i].w, m.w);
+        u[i].x = rule_u<kRule>(u[i].x, gv[i].x, wt[i].x, wv[i].x, c, h);
+        u[i].y = rule_u<kRule>(u[i].y, gv[i].y, wt[i].y, wv[i].y, c, h);
+        u[i].z = rule_u<kRule>(u[i].z, gv[i].z, wt[i].z, wv[i].z, c, h);
+        u[i].w = rule_u<kRule>(u[i].w, gv[i].w, wt[i].w, wv[i].w, c, h);
         st4_stream(ep + i * (kGroup * 4), u[i]);
+        if (kDetach) {
+            const float q = a.q;
+            st4_stream(a.wp.y[k] + start + o0 + i * (kGroup * 4),
+                       make_float4(detached(wt[i].x, u[i].x, q), detached(wt[i].y, u[i].y, q),
+                                   detached(wt[i].z, u[i].z, q), detached(wt[i].w, u[i].w, q)));
+        }
         flags |= (key_of(u[i].x) >= tau ? 1u : 0u) << (i * 4 + 0);
         flags |= (key_of(u[i].y) >= tau ? 1u : 0u) << (i * 4 + 1);
         flags |= (key_of(u[i].z) >= tau ? 1u : 0u) << (i * 4 + 2);
@@ -354,9 +392,9 @@ __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, Topk
         const int o = i * kWave + lane;
         if (o < len) {
             const int j = start + o;
-            const float m = c * (a.w_t[j] - a.w_prev[j]);
-            const float u = precompress(e[j], gr[j], m);
+            const float u = rule_u_rt(a.rule, e[j], gr[j], a.w_t[j], a.w_prev[j], c, a.h);
             e[j] = u;
+            if (a.detach) a.wp.y[k][j] = detached(a.w_t[j], u, a.q);
             flags |= (key_of(u) >= tau ? 1u : 0u) << i;
         }
     }
@@ -380,7 +418,25 @@ __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, Topk
 hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                                  uint64_t vec_mask, hipStream_t st) {
     const int grid = g.n_chunks * g.K;
-    hipLaunchKernelGGL(topk_fused_vec_kernel, dim3(grid), dim3(kGroup), 0, st, a, g, s, vec_mask);
+    if (a.rule == kRuleServerMomentum) {
+        if (a.detach) return hipErrorInvalidValue;  // the detached points need w_{t+1} = w_t off the sent set
+        hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleServerMomentum, false>), dim3(grid), dim3(kGroup), 0, st, a,
+                           g, s, vec_mask);
+    } else if (a.rule == kRuleLrInResidual) {
+        if (a.detach)
+            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleLrInResidual, true>), dim3(grid), dim3(kGroup), 0, st, a,
+                               g, s, vec_mask);
+        else
+            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleLrInResidual, false>), dim3(grid), dim3(kGroup), 0, st,
+                               a, g, s, vec_mask);
+    } else {
+        if (a.detach)
+            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleGmc, true>), dim3(grid), dim3(kGroup), 0, st, a, g, s,
+                               vec_mask);
+        else
+            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleGmc, false>), dim3(grid), dim3(kGroup), 0, st, a, g, s,
+                               vec_mask);
+    }
     return hipGetLastError();
 }
 
@@ -911,7 +967,8 @@ __global__ __launch_bounds__(kGroup) void rbgs_fused_kernel(StepArgs a, int32_t 
     const int32_t d = a.d;
     const int64_t j0 = ((int64_t)blockIdx.x * kGroup + threadIdx.x) * 4;
     if (j0 >= d) return;
-    const float c = a.c;
+    const float c = a.c, h = a.h, qd = a.q;
+    const int rule = a.rule;
     const bool full = j0 + 4 <= d;
     const bool vec = full && (B & 3) == 0 && aligned16(a.w_t) && aligned16(a.w_prev) && aligned16(val) &&
                      (val_row & 3) == 0;
@@ -920,33 +977,38 @@ __global__ __launch_bounds__(kGroup) void rbgs_fused_kernel(StepArgs a, int32_t 
         const int32_t b = j / B;
         const int32_t slot = block_slot[b];
         const float4 wt = ld4(a.w_t + j), wp = ld4(a.w_prev + j);
-        const float4 m = make_float4(c * (wt.x - wp.x), c * (wt.y - wp.y), c * (wt.z - wp.z), c * (wt.w - wp.w));
         const int64_t vpos = (int64_t)slot * B + (j - (int64_t)b * B);
         for (int k = 0; k < K; ++k) {
             float* e = a.wp.e[k];
             const float* gr = a.wp.g[k];
-            if (aligned16(e) && aligned16(gr)) {
+            float* y = a.wp.y[k];
+            if (aligned16(e) && aligned16(gr) && (!a.detach || aligned16(y))) {
                 const float4 ev = ld4(e + j), gv = ld4(gr + j);
                 float4 u;
-                u.x = precompress(ev.x, gv.x, m.x);
-                u.y = precompress(ev.y, gv.y, m.y);
-                u.z = precompress(ev.z, gv.z, m.z);
-                u.w = precompress(ev.w, gv.w, m.w);
+                u.x = rule_u_rt(rule, ev.x, gv.x, wt.x, wp.x, c, h);
+                u.y = rule_u_rt(rule, ev.y, gv.y, wt.y, wp.y, c, h);
+                u.z = rule_u_rt(rule, ev.z, gv.z, wt.z, wp.z, c, h);
+                u.w = rule_u_rt(rule, ev.w, gv.w, wt.w, wp.w, c, h);
                 if (slot >= 0) {
                     st4(val + (size_t)k * val_row + vpos, u);
                     st4(e + j, make_float4(u.x - u.x, u.y - u.y, u.z - u.z, u.w - u.w));
                 } else {
                     st4(e + j, u);
+                    // unsent: e_{t+1} = u and w_{t+1} = w_t here, so this is final
+                    if (a.detach)
+                        st4(y + j, make_float4(detached(wt.x, u.x, qd), detached(wt.y, u.y, qd),
+                                               detached(wt.z, u.z, qd), detached(wt.w, u.w, qd)));
                 }
             } else {
-                const float mm[4] = {m.x, m.y, m.z, m.w};
+                const float wtq[4] = {wt.x, wt.y, wt.z, wt.w}, wpq[4] = {wp.x, wp.y, wp.z, wp.w};
                 for (int q = 0; q < 4; ++q) {
-                    const float u = precompress(e[j + q], gr[j + q], mm[q]);
+                    const float u = rule_u_rt(rule, e[j + q], gr[j + q], wtq[q], wpq[q], c, h);
                     if (slot >= 0) {
                         val[(size_t)k * val_row + vpos + q] = u;
                         e[j + q] = u - u;
                     } else {
                         e[j + q] = u;
+                        if (a.detach) y[j + q] = detached(wtq[q], u, qd);
                     }
                 }
             }
@@ -959,16 +1021,17 @@ __global__ __launch_bounds__(kGroup) void rbgs_fused_kernel(StepArgs a, int32_t 
         const int32_t j = (int32_t)jj;
         const int32_t b = j / B;
         const int32_t slot = block_slot[b];
-        const float m = c * (a.w_t[j] - a.w_prev[j]);
+        const float wtj = a.w_t[j], wpj = a.w_prev[j];
         const int64_t vpos = (int64_t)slot * B + (j - (int64_t)b * B);
         for (int k = 0; k < K; ++k) {
             float* e = a.wp.e[k];
-            const float u = precompress(e[j], a.wp.g[k][j], m);
+            const float u = rule_u_rt(rule, e[j], a.wp.g[k][j], wtj, wpj, c, h);
             if (slot >= 0) {
                 val[(size_t)k * val_row + vpos] = u;
                 e[j] = u - u;
             } else {
                 e[j] = u;
+                if (a.detach) a.wp.y[k][j] = detached(wtj, u, qd);
             }
         }
     }
@@ -986,28 +1049,64 @@ hipError_t launch_rbgs_fused(const StepArgs& a, int32_t K, int32_t B, const int3
 // server: sum over workers in worker order, dense update
 // ============================================================================
 
+// w_{t+1} at one component: w_t + update, or with momentum on the server
+// (w_t + update) + b (w_t - w_{t-1}).
+__device__ __forceinline__ float next_w(float x, float dl, const float* w_prev, int64_t j, float b) {
+    const float moved = x + dl;
+    if (!w_prev) return moved;
+    const float back = x - w_prev[j];
+    const float push = b * back;
+    return moved + push;
+}
+
 // Writes update = -(s * acc) for the n components of a range starting at base
-// (when update is not NULL) and, with kApply, w_out = w_in + update.
+// (when f.update is not NULL) and, with kApply, w_out = next_w(w_in, update).
 template <bool kApply>
-__device__ __forceinline__ void write_update(const float* acc, float s, int64_t base, int64_t n, float* update,
-                                             const float* w_in, float* w_out) {
-    const bool vec = n == kAggRange && (base & 3) == 0 && (update == nullptr || aligned16(update)) &&
-                     (!kApply || (aligned16(w_in) && aligned16(w_out)));
+__device__ __forceinline__ void write_update(const float* acc, int64_t base, int64_t n, const FinishArgs& f) {
+    const float s = f.s;
+    const bool vec = n == kAggRange && (base & 3) == 0 && (f.update == nullptr || aligned16(f.update)) &&
+                     (!kApply || (aligned16(f.w_in) && aligned16(f.w_out) &&
+                                  (f.w_prev == nullptr || aligned16(f.w_prev))));
     if (vec) {
         for (int q = threadIdx.x * 4; q < kAggRange; q += kGroup * 4) {
+            const int64_t j = base + q;
             const float4 dl = make_float4(-(s * acc[q]), -(s * acc[q + 1]), -(s * acc[q + 2]), -(s * acc[q + 3]));
-            if (update) st4(update + base + q, dl);
+            if (f.update) st4(f.update + j, dl);
             if (kApply) {
-                const float4 x = ld4(w_in + base + q);
-                st4(w_out + base + q, make_float4(x.x + dl.x, x.y + dl.y, x.z + dl.z, x.w + dl.w));
+                const float4 x = ld4(f.w_in + j);
+                float4 nx = make_float4(x.x + dl.x, x.y + dl.y, x.z + dl.z, x.w + dl.w);
+                if (f.w_prev) {  // momentum on the server
+                    const float4 p = ld4(f.w_prev + j);
+                    const float b = f.b;
+                    nx = make_float4(nx.x + b * (x.x - p.x), nx.y + b * (x.y - p.y), nx.z + b * (x.z - p.z),
+                                     nx.w + b * (x.w - p.w));
+                }
+                st4(f.w_out + j, nx);
             }
         }
-    } else {
-        for (int q = threadIdx.x; q < n; q += kGroup) {
-            const float dl = -(s * acc[q]);
-            if (update) update[base + q] = dl;
-            if (kApply) w_out[base + q] = w_in[base + q] + dl;
-        }
+        return;
+    }
+    for (int q = threadIdx.x; q < n; q += kGroup) {
+        const int64_t j = base + q;
+        const float dl = -(s * acc[q]);
+        if (f.update) f.update[j] = dl;
+        if (kApply) f.w_out[j] = next_w(f.w_in[j], dl, f.w_prev, j, f.b);
+    }
+}
+
+// GMC+: the detached points at the components of the range some worker sent
+// (hit[q] != 0), where w_{t+1} may differ from w_t: y_k = w_{t+1} - q e_{t+1,k}
+// for every worker k, with w_{t+1} read back from w_out after the
+// workgroup's writes (w_out may alias w_in or w_prev).  Elsewhere the fused
+// worker pass already wrote the final value w_t - q u_k.
+__device__ __forceinline__ void finish_detach(const unsigned char* hit, int64_t base, int64_t n, int32_t K,
+                                              const FinishArgs& f) {
+    __syncthreads();  // this workgroup's w_out writes are visible to all its threads
+    for (int q = threadIdx.x; q < n; q += kGroup) {
+        if (!hit[q]) continue;
+        const int64_t j = base + q;
+        const float wn = f.w_out[j];
+        for (int k = 0; k < K; ++k) f.y[k][j] = detached(wn, f.e[k][j], f.q);
     }
 }
 
@@ -1056,12 +1155,12 @@ hipError_t launch_agg_rowptr(int32_t K, int32_t d, const int32_t* idx, int64_t i
 constexpr int kAggStage = 1024;
 
 template <bool kApply>
-__global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, float s, const int32_t* idx,
+__global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, const int32_t* idx,
                                                           int64_t idx_row, const float* val, int64_t val_row,
-                                                          const int32_t* rowptr, int32_t n_ranges,
-                                                          float* update, const float* w_in, float* w_out) {
+                                                          const int32_t* rowptr, int32_t n_ranges, FinishArgs f) {
     static_assert(kAggRange == kGroup * 8, "8 components per thread");
     __shared__ float acc[kAggRange];
+    __shared__ unsigned char hit[kAggRange];
     __shared__ int32_t st_idx[kAggStage];
     __shared__ float st_val[kAggStage];
     __shared__ int32_t src[kMaxWorkers];
@@ -1069,16 +1168,25 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
     const int r = blockIdx.x;
     const int64_t base = (int64_t)r * kAggRange;
     const int64_t n = (int64_t)d - base < kAggRange ? (int64_t)d - base : kAggRange;
-    const bool vec = n == kAggRange && (update == nullptr || aligned16(update)) &&
-                     (!kApply || (aligned16(w_in) && aligned16(w_out)));
+    const float s = f.s;
+    const bool vec = n == kAggRange && (f.update == nullptr || aligned16(f.update)) &&
+                     (!kApply || (aligned16(f.w_in) && aligned16(f.w_out) &&
+                                  (f.w_prev == nullptr || aligned16(f.w_prev))));
     // this thread's components: [base + 4t, +4) and [base + 1024 + 4t, +4)
     const int q0 = threadIdx.x * 4, q1 = kGroup * 4 + threadIdx.x * 4;
-    float4 w0 = make_float4(0.f, 0.f, 0.f, 0.f), w1 = w0;
+    float4 w0 = make_float4(0.f, 0.f, 0.f, 0.f), w1 = w0, p0 = w0, p1 = w0;
     if (kApply && vec) {
-        w0 = ld4(w_in + base + q0);
-        w1 = ld4(w_in + base + q1);
+        w0 = ld4(f.w_in + base + q0);
+        w1 = ld4(f.w_in + base + q1);
+        if (f.w_prev) {
+            p0 = ld4(f.w_prev + base + q0);
+            p1 = ld4(f.w_prev + base + q1);
+        }
     }
-    for (int q = threadIdx.x; q < kAggRange; q += kGroup) acc[q] = 0.0f;
+    for (int q = threadIdx.x; q < kAggRange; q += kGroup) {
+        acc[q] = 0.0f;
+        hit[q] = 0;
+    }
     if (threadIdx.x < K) {
         const int32_t* rp = rowptr + (size_t)threadIdx.x * (n_ranges + 1);
         const int32_t lo = rp[r], hi = rp[r + 1];
@@ -1105,7 +1213,10 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             if (pre[k + 1] > pre[k]) {
                 for (int32_t i = pre[k] + threadIdx.x; i < pre[k + 1]; i += kGroup) {
                     const int64_t j = (int64_t)st_idx[i] - base;
-                    if (j >= 0 && j < kAggRange) acc[j] = acc[j] + st_val[i];
+                    if (j >= 0 && j < kAggRange) {
+                        acc[j] = acc[j] + st_val[i];
+                        hit[j] = 1;
+                    }
                 }
                 __syncthreads();  // worker k's additions land before worker k+1's
             }
@@ -1115,7 +1226,10 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             for (int32_t i = threadIdx.x; i < pre[k + 1] - pre[k]; i += kGroup) {
                 const int64_t q = (int64_t)src[k] + i;
                 const int64_t j = (int64_t)idx[(size_t)k * idx_row + q] - base;
-                if (j >= 0 && j < kAggRange) acc[j] = acc[j] + val[(size_t)k * val_row + q];
+                if (j >= 0 && j < kAggRange) {
+                    acc[j] = acc[j] + val[(size_t)k * val_row + q];
+                    hit[j] = 1;
+                }
             }
             __syncthreads();
         }
@@ -1124,29 +1238,38 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
     if (vec) {
         const float4 d0 = make_float4(-(s * acc[q0]), -(s * acc[q0 + 1]), -(s * acc[q0 + 2]), -(s * acc[q0 + 3]));
         const float4 d1 = make_float4(-(s * acc[q1]), -(s * acc[q1 + 1]), -(s * acc[q1 + 2]), -(s * acc[q1 + 3]));
-        if (update) {
-            st4(update + base + q0, d0);
-            st4(update + base + q1, d1);
+        if (f.update) {
+            st4(f.update + base + q0, d0);
+            st4(f.update + base + q1, d1);
         }
         if (kApply) {
-            st4(w_out + base + q0, make_float4(w0.x + d0.x, w0.y + d0.y, w0.z + d0.z, w0.w + d0.w));
-            st4(w_out + base + q1, make_float4(w1.x + d1.x, w1.y + d1.y, w1.z + d1.z, w1.w + d1.w));
+            float4 n0 = make_float4(w0.x + d0.x, w0.y + d0.y, w0.z + d0.z, w0.w + d0.w);
+            float4 n1 = make_float4(w1.x + d1.x, w1.y + d1.y, w1.z + d1.z, w1.w + d1.w);
+            if (f.w_prev) {  // momentum on the server
+                const float b = f.b;
+                n0 = make_float4(n0.x + b * (w0.x - p0.x), n0.y + b * (w0.y - p0.y), n0.z + b * (w0.z - p0.z),
+                                 n0.w + b * (w0.w - p0.w));
+                n1 = make_float4(n1.x + b * (w1.x - p1.x), n1.y + b * (w1.y - p1.y), n1.z + b * (w1.z - p1.z),
+                                 n1.w + b * (w1.w - p1.w));
+            }
+            st4(f.w_out + base + q0, n0);
+            st4(f.w_out + base + q1, n1);
         }
     } else {
-        write_update<kApply>(acc, s, base, n, update, w_in, w_out);
+        write_update<kApply>(acc, base, n, f);
     }
+    if (kApply && f.detach) finish_detach(hit, base, n, K, f);
 }
 
-hipError_t launch_agg_topk(int32_t K, int32_t d, float s, const int32_t* idx, int64_t idx_row,
+hipError_t launch_agg_topk(int32_t K, int32_t d, const int32_t* idx, int64_t idx_row,
                            const float* val, int64_t val_row, const int32_t* rowptr,
-                           int32_t n_ranges, float* update, const float* w_in, float* w_out,
-                           hipStream_t st) {
-    if (w_out)
-        hipLaunchKernelGGL(agg_topk_kernel<true>, dim3(n_ranges), dim3(kGroup), 0, st, K, d, s, idx, idx_row, val,
-                           val_row, rowptr, n_ranges, update, w_in, w_out);
+                           int32_t n_ranges, const FinishArgs& f, hipStream_t st) {
+    if (f.w_out)
+        hipLaunchKernelGGL(agg_topk_kernel<true>, dim3(n_ranges), dim3(kGroup), 0, st, K, d, idx, idx_row, val,
+                           val_row, rowptr, n_ranges, f);
     else
-        hipLaunchKernelGGL(agg_topk_kernel<false>, dim3(n_ranges), dim3(kGroup), 0, st, K, d, s, idx, idx_row, val,
-                           val_row, rowptr, n_ranges, update, w_in, w_out);
+        hipLaunchKernelGGL(agg_topk_kernel<false>, dim3(n_ranges), dim3(kGroup), 0, st, K, d, idx, idx_row, val,
+                           val_row, rowptr, n_ranges, f);
     return hipGetLastError();
 }
 
@@ -1154,15 +1277,16 @@ hipError_t launch_agg_topk(int32_t K, int32_t d, float s, const int32_t* idx, in
 // a component of block blocks[q] sits at q*B + offset in each message.  One
 // workgroup per range of kAggRange components, like the top-s kernel.
 template <bool kApply>
-__global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, int32_t B, float s,
-                                                          const int32_t* blocks, int32_t n_sel,
-                                                          const float* val, int64_t val_row,
-                                                          float* update, const float* w_in, float* w_out) {
+__global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, int32_t B, const int32_t* blocks,
+                                                          int32_t n_sel, const float* val, int64_t val_row,
+                                                          FinishArgs f) {
     __shared__ float acc[kAggRange];
+    __shared__ unsigned char hit[kAggRange];
     const int64_t base = (int64_t)blockIdx.x * kAggRange;
     const int64_t n = (int64_t)d - base < kAggRange ? (int64_t)d - base : kAggRange;
     for (int q = threadIdx.x; q < kAggRange; q += kGroup) {
         float a = 0.0f;
+        unsigned char sent = 0;
         if (q < n) {
             const int64_t j = base + q;
             const int32_t b = (int32_t)(j / B);
@@ -1179,24 +1303,60 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
             if (slot >= 0) {
                 const int64_t vpos = (int64_t)slot * B + (j - (int64_t)b * B);
                 for (int k = 0; k < K; ++k) a = a + val[(size_t)k * val_row + vpos];
+                sent = 1;
             }
         }
         acc[q] = a;
+        hit[q] = sent;
     }
     __syncthreads();
-    write_update<kApply>(acc, s, base, n, update, w_in, w_out);
+    write_update<kApply>(acc, base, n, f);
+    if (kApply && f.detach) finish_detach(hit, base, n, K, f);
 }
 
-hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, float s, const int32_t* blocks,
-                           int32_t n_sel, const float* val, int64_t val_row, float* update,
-                           const float* w_in, float* w_out, hipStream_t st) {
+hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, const int32_t* blocks,
+                           int32_t n_sel, const float* val, int64_t val_row, const FinishArgs& f,
+                           hipStream_t st) {
     const int grid = (int)(((int64_t)d + kAggRange - 1) / kAggRange);
-    if (w_out)
-        hipLaunchKernelGGL(agg_rbgs_kernel<true>, dim3(grid), dim3(kGroup), 0, st, K, d, B, s, blocks, n_sel, val,
-                           val_row, update, w_in, w_out);
+    if (f.w_out)
+        hipLaunchKernelGGL(agg_rbgs_kernel<true>, dim3(grid), dim3(kGroup), 0, st, K, d, B, blocks, n_sel, val,
+                           val_row, f);
     else
-        hipLaunchKernelGGL(agg_rbgs_kernel<false>, dim3(grid), dim3(kGroup), 0, st, K, d, B, s, blocks, n_sel, val,
-                           val_row, update, w_in, w_out);
+        hipLaunchKernelGGL(agg_rbgs_kernel<false>, dim3(grid), dim3(kGroup), 0, st, K, d, B, blocks, n_sel, val,
+                           val_row, f);
+    return hipGetLastError();
+}
+
+// ============================================================================
+// GMC+ detached points, dense: y_k = w - q e_k (Algorithm 2, detach)
+// ============================================================================
+
+// One workgroup per (chunk of kChunk components, worker), like the fused
+// pass: w is read through the cache by the K workgroups of a chunk, e_k and
+// y_k are streamed.
+__global__ __launch_bounds__(kGroup) void detach_kernel(DetachArgs a, int32_t K) {
+    const int chunk = blockIdx.x / K, k = blockIdx.x % K;
+    const int64_t start = (int64_t)chunk * kChunk;
+    const int64_t len = (int64_t)a.d - start < kChunk ? (int64_t)a.d - start : kChunk;
+    const float* e = a.e[k];
+    float* y = a.y[k];
+    const float q = a.q;
+    if (len == kChunk && aligned16(a.w) && aligned16(e) && aligned16(y)) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int64_t j = start + i * (kGroup * 4) + threadIdx.x * 4;
+            const float4 w = ld4(a.w + j), ev = ld4_stream(e + j);
+            st4_stream(y + j, make_float4(detached(w.x, ev.x, q), detached(w.y, ev.y, q), detached(w.z, ev.z, q),
+                                          detached(w.w, ev.w, q)));
+        }
+        return;
+    }
+    for (int64_t o = threadIdx.x; o < len; o += kGroup) y[start + o] = detached(a.w[start + o], e[start + o], q);
+}
+
+hipError_t launch_detach(const DetachArgs& a, int32_t K, hipStream_t st) {
+    const int64_t chunks = ((int64_t)a.d + kChunk - 1) / kChunk;
+    hipLaunchKernelGGL(detach_kernel, dim3((unsigned)(chunks * K)), dim3(kGroup), 0, st, a, K);
     return hipGetLastError();
 }
 

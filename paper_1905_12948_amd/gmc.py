@@ -27,7 +27,10 @@ COMPRESSORS = {"topk": GMC_TOPK_GLOBAL, "topk_seg": GMC_TOPK_SEGMENTED, "rbgs": 
 EXPORTS = ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "gmc_message_len",
            "gmc_index_len", "gmc_step", "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step",
            "gmc_set_option", "gmc_stats", "gmc_profile_read", "gmc_last_error", "gmc_destroy",
-           "gmc_calib_copy", "gmc_aggregate_apply")
+           "gmc_calib_copy", "gmc_aggregate_apply", "gmc_set_rule", "gmc_set_eta", "gmc_set_lambda",
+           "gmc_step_detach", "gmc_finish", "gmc_detach")
+
+RULES = {"gmc": 0, "server_momentum": 1, "lr_in_residual": 2}
 
 
 class GmcError(RuntimeError):
@@ -72,9 +75,17 @@ def load() -> ctypes.CDLL:
     lib.gmc_destroy.restype = None
     lib.gmc_calib_copy.argtypes = [P, P, P, i64]
     lib.gmc_aggregate_apply.argtypes = [P, P, P, P, P, P, P]
+    lib.gmc_set_rule.argtypes = [P, i32]
+    lib.gmc_set_eta.argtypes = [P, dbl]
+    lib.gmc_set_lambda.argtypes = [P, dbl]
+    lib.gmc_step_detach.argtypes = [P, P, P, P, P, P, P, P, P]
+    lib.gmc_finish.argtypes = [P, P, P, P, P, P, P, P, P, P]
+    lib.gmc_detach.argtypes = [P, P, P, P]
     for name in ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "gmc_step",
                  "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step", "gmc_set_option",
-                 "gmc_stats", "gmc_profile_read", "gmc_calib_copy", "gmc_aggregate_apply"):
+                 "gmc_stats", "gmc_profile_read", "gmc_calib_copy", "gmc_aggregate_apply",
+                 "gmc_set_rule", "gmc_set_eta", "gmc_set_lambda", "gmc_step_detach", "gmc_finish",
+                 "gmc_detach"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -138,7 +149,8 @@ class Gmc:
 
     def __init__(self, d: int, K: int, compressor: str = "topk", ratio: float = 0.001,
                  beta: float = 0.9, eta: float = 0.1, seed: int = 0,
-                 segments: Optional[Sequence[int]] = None, block: Optional[int] = None):
+                 segments: Optional[Sequence[int]] = None, block: Optional[int] = None,
+                 rule: str = "gmc", lam: float = 0.0):
         self._lib = load()
         self.d, self.K, self.compressor = int(d), int(K), compressor
         if compressor not in COMPRESSORS:
@@ -154,6 +166,21 @@ class Gmc:
             self._call(self._lib.gmc_set_segments(self._ctx, len(segments) - 1, off))
         if block is not None:
             self._call(self._lib.gmc_set_block(self._ctx, int(block)))
+        if rule not in RULES:
+            raise ValueError("rule must be one of %s" % list(RULES))
+        self.rule = rule
+        if rule != "gmc":
+            self._call(self._lib.gmc_set_rule(self._ctx, RULES[rule]))
+        if lam:
+            self.set_lambda(lam)
+
+    def set_eta(self, eta: float):
+        """Learning rate of the following iterations (a schedule)."""
+        self._call(self._lib.gmc_set_eta(self._ctx, float(eta)))
+
+    def set_lambda(self, lam: float):
+        """GMC+'s detach coefficient (Algorithm 2)."""
+        self._call(self._lib.gmc_set_lambda(self._ctx, float(lam)))
 
     # -- plumbing -------------------------------------------------------
     def _call(self, st: int):
@@ -194,7 +221,10 @@ class Gmc:
                 torch.zeros((self.K,), dtype=torch.int64, device=device))
 
     # -- the three calls of one iteration ---------------------------------
-    def step(self, w_t, w_prev, grads, err, idx, val, msg_len):
+    def step(self, w_t, w_prev, grads, err, idx, val, msg_len, w_k=None):
+        """Worker pass; with ``w_k`` ([K, >=d] or K tensors) also GMC+'s
+        detached points where they are already final (gmc_step_detach;
+        ``finish`` with the same ``w_k`` completes them)."""
         torch = _torch()
         d, K = self.d, self.K
         pw = _check(w_t, torch.float32, d, "w_t")
@@ -205,7 +235,41 @@ class Gmc:
         pv = _check(val, torch.float32, K * self.message_len, "val")
         pl = _check(msg_len, torch.int64, K, "msg_len")
         self._stream(w_t.device)
-        self._call(self._lib.gmc_step(self._ctx, pw, pp, gp, ep, pi, pv, pl))
+        if w_k is None:
+            self._call(self._lib.gmc_step(self._ctx, pw, pp, gp, ep, pi, pv, pl))
+        else:
+            yp = (ctypes.c_void_p * K)(*_rows(w_k, d, K, "w_k"))
+            self._call(self._lib.gmc_step_detach(self._ctx, pw, pp, gp, ep, yp, pi, pv, pl))
+
+    def finish(self, idx, val, msg_len, w, w_out, w_prev=None, update=None, err=None, w_k=None):
+        """Server pass under the context's rule: w_out = w_{t+1} (w_prev is
+        needed by momentum on the server and may be w_out itself), optionally
+        the update and the completion of GMC+'s detached points ``w_k``."""
+        torch = _torch()
+        K, d = self.K, self.d
+        pi = _check(idx, torch.int32, K * self.index_len, "idx")
+        pv = _check(val, torch.float32, K * self.message_len, "val")
+        pl = _check(msg_len, torch.int64, K, "msg_len")
+        pw = _check(w, torch.float32, d, "w")
+        po = _check(w_out, torch.float32, d, "w_out")
+        pp = None if w_prev is None else _check(w_prev, torch.float32, d, "w_prev")
+        pu = None if update is None else _check(update, torch.float32, d, "update")
+        ep = yp = None
+        if w_k is not None:
+            ep = (ctypes.c_void_p * K)(*_rows(err, d, K, "err"))
+            yp = (ctypes.c_void_p * K)(*_rows(w_k, d, K, "w_k"))
+        self._stream(w.device)
+        self._call(self._lib.gmc_finish(self._ctx, pi, pv, pl, pw, pp, po, pu, ep, yp))
+
+    def detach(self, w, err, w_k):
+        """GMC+'s detached points in one dense pass: w_k = w - (lambda eta) err."""
+        torch = _torch()
+        K, d = self.K, self.d
+        pw = _check(w, torch.float32, d, "w")
+        ep = (ctypes.c_void_p * K)(*_rows(err, d, K, "err"))
+        yp = (ctypes.c_void_p * K)(*_rows(w_k, d, K, "w_k"))
+        self._stream(w.device)
+        self._call(self._lib.gmc_detach(self._ctx, pw, ep, yp))
 
     def aggregate(self, idx, val, msg_len, update):
         torch = _torch()

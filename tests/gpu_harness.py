@@ -45,7 +45,12 @@ class Case:
     grad_hook: Optional[Callable] = None   # (t, grads) -> grads, host side
     label: str = ""
     fused_apply: bool = False     # gmc_aggregate_apply out of place, buffers swapped
-    write_update: bool = True     # with fused_apply: also materialise the update
+    write_update: bool = True     # with fused_apply / finish: also materialise the update
+    rule: str = "gmc"             # update rule (gmc, server_momentum, lr_in_residual)
+    lam: float = 0.0              # GMC+ detach coefficient
+    detach: str = ""              # "fused": gmc_step_detach + gmc_finish; "dense": gmc_detach
+    eta_fn: Optional[Callable] = None      # t -> eta_t (a schedule)
+    finish: bool = False          # server pass through gmc_finish (implied by rule / detach)
 
 
 def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
@@ -57,16 +62,17 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
     comp = wl.compressor
     seg = wl.topk_segments() if comp == "topk_seg" else None
     if verbose:
-        print("lockstep %s: d=%d K=%d %s ratio=%g steps=%d opts=%s pad=%d"
-              % (case.label or wl.name, d, K, comp, wl.ratio, case.steps, case.options, case.row_pad),
-              flush=True)
+        print("lockstep %s: d=%d K=%d %s ratio=%g steps=%d opts=%s pad=%d rule=%s lam=%g detach=%s"
+              % (case.label or wl.name, d, K, comp, wl.ratio, case.steps, case.options, case.row_pad,
+                 case.rule, case.lam, case.detach or "-"), flush=True)
     g = Gmc(d, K, comp, wl.ratio, wl.beta, wl.eta, seed=wl.seed,
             segments=None if seg is None else seg.tolist(),
-            block=wl.block if comp == "rbgs" else None)
+            block=wl.block if comp == "rbgs" else None, rule=case.rule, lam=case.lam)
     for opt, val in case.options:
         g.set_option(opt, val)
     orc = oracle.GmcOracle(d, K, "rbgs" if comp == "rbgs" else "topk", wl.ratio, wl.beta, wl.eta,
-                           seed=wl.seed, seg_off=seg, block=wl.block)
+                           seed=wl.seed, seg_off=seg, block=wl.block, variant=case.rule, lam=case.lam)
+    use_finish = case.finish or case.rule != "gmc" or bool(case.detach)
     assert g.message_len == orc.message_len and g.index_len == orc.index_len
 
     dev = torch.device(device)
@@ -81,6 +87,10 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
     off = 1 if case.row_pad else 0       # odd start: 4-byte but not 16-byte aligned rows
     e_rows = [e_store[off + k * stride: off + k * stride + d] for k in range(K)]
     g_rows = [g_store[off + k * stride: off + k * stride + d] for k in range(K)]
+    wk_rows = None
+    if case.detach:
+        y_store = torch.full((K * stride + 1,), float("nan"), dtype=torch.float32, device=dev)
+        wk_rows = [y_store[off + k * stride: off + k * stride + d] for k in range(K)]
     idx, val, ln = g.alloc_messages(dev)
     upd = torch.empty(d, dtype=torch.float32, device=dev)
     for t in range(case.steps):
@@ -89,8 +99,19 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
             gr = case.grad_hook(t, gr)
         for k in range(K):
             g_rows[k].copy_(torch.from_numpy(gr[k]))
-        g.step(w, wp, g_rows, e_rows, idx, val, ln)
-        if case.fused_apply:
+        if case.eta_fn is not None:
+            eta_t = case.eta_fn(t)
+            g.set_eta(eta_t)
+            orc.set_eta(eta_t)
+        fused_detach = case.detach == "fused"
+        g.step(w, wp, g_rows, e_rows, idx, val, ln, w_k=wk_rows if fused_detach else None)
+        if use_finish:
+            g.finish(idx, val, ln, w, wp, w_prev=wp, update=upd if case.write_update else None,
+                     err=e_rows if fused_detach else None, w_k=wk_rows if fused_detach else None)
+            w, wp = wp, w
+            if case.detach == "dense":
+                g.detach(w, e_rows, wk_rows)
+        elif case.fused_apply:
             g.aggregate_apply(idx, val, ln, w, wp, update=upd if case.write_update else None)
             w, wp = wp, w
         else:
@@ -99,9 +120,9 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
 
         oi, ov, ol = orc.step(w_h, wp_h, gr, e_h)
         od = orc.aggregate(oi, ov, ol)
-        wn = w_h.copy()
-        orc.apply(wn, od)
+        wn = orc.next_params(w_h, wp_h, od)
         wp_h, w_h = w_h, wn
+        wk_h = orc.detach(w_h, e_h) if case.detach else None
         if (t + 1) % check_every and t != case.steps - 1:
             continue
         torch.cuda.synchronize()
@@ -117,10 +138,13 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
             m = int(ol[k])
             assert_same_f32(gv[k, :m], ov[k, :m], tag + ": values of worker %d" % k)
             assert_same_f32(e_rows[k].cpu().numpy(), e_h[k], tag + ": residual of worker %d" % k)
-        if case.write_update or not case.fused_apply:
+        if case.write_update or not (case.fused_apply or use_finish):
             assert_same_f32(upd.cpu().numpy(), od, tag + ": update")
         assert_same_f32(w.cpu().numpy(), w_h, tag + ": w")
         assert_same_f32(wp.cpu().numpy(), wp_h, tag + ": w_prev")
+        if case.detach:
+            for k in range(K):
+                assert_same_f32(wk_rows[k].cpu().numpy(), wk_h[k], tag + ": detached point of worker %d" % k)
         if verbose:
             print("  %s ok" % tag, flush=True)
     st = g.stats()

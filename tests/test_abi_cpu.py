@@ -68,6 +68,12 @@ def test_null_handles(lib):
     assert lib.gmc_set_segments(None, 1, None) == -1
     assert lib.gmc_set_block(None, 4) == -1
     assert lib.gmc_set_option(None, 1, 1) == -1
+    assert lib.gmc_set_rule(None, 0) == -1
+    assert lib.gmc_set_eta(None, 0.1) == -1
+    assert lib.gmc_set_lambda(None, 0.5) == -1
+    assert lib.gmc_step_detach(None, None, None, None, None, None, None, None, None) == -1
+    assert lib.gmc_finish(None, None, None, None, None, None, None, None, None, None) == -1
+    assert lib.gmc_detach(None, None, None, None) == -1
     assert isinstance(lib.gmc_last_error(None), bytes)
     lib.gmc_destroy(None)
 

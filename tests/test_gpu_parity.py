@@ -2,6 +2,8 @@
 inputs: every workload shape (shrunk so the oracle finishes in seconds while
 still spanning many chunks, items and ragged tails), both selection paths,
 misaligned rows and the degenerate cases of the method."""
+import math
+
 import numpy as np
 import pytest
 
@@ -128,3 +130,57 @@ def test_fused_aggregate_apply_swapping_buffers(name, shrink, steps):
 def test_fused_aggregate_apply_without_update():
     run_lockstep(Case(W("resnet18").shrunk(16, K=4), steps=3, fused_apply=True, write_update=False,
                       label="fused-no-update"))
+
+
+# ---------------------------------------------------------------------------
+# GMC+ detached points (Algorithm 2), the appendix's update rules, eta schedule
+# ---------------------------------------------------------------------------
+
+def _cosine(eta, T):
+    return lambda t: eta * 0.5 * (1 + math.cos(math.pi * t / T))
+
+
+@pytest.mark.parametrize("name,shrink,K", [("rbgs", 16, 8), ("resnet18", 16, 4), ("gpt2", 64, 3)])
+def test_gmcplus_fused_detach(name, shrink, K):
+    run_lockstep(Case(W(name).shrunk(shrink, K=K), steps=4, lam=0.5, detach="fused",
+                      label="gmc+ fused/" + name))
+
+
+def test_gmcplus_fused_detach_misaligned_rows():
+    run_lockstep(Case(W("resnet18").shrunk(32, K=3), steps=3, lam=0.3, detach="fused", row_pad=1,
+                      label="gmc+ fused misaligned"))
+
+
+def test_gmcplus_fused_detach_full_data_path():
+    run_lockstep(Case(W("resnet50").shrunk(64, K=4), steps=3, lam=1.0, detach="fused",
+                      options=((OPT_FULL, 1),), label="gmc+ fused full-data"))
+
+
+@pytest.mark.parametrize("rule", ["gmc", "server_momentum", "lr_in_residual"])
+def test_dense_detach(rule):
+    run_lockstep(Case(W("rbgs").shrunk(16, K=4), steps=3, lam=0.5, detach="dense", rule=rule,
+                      label="dense detach/" + rule))
+
+
+@pytest.mark.parametrize("name,shrink", [("resnet18", 16), ("rbgs", 16), ("gpt2", 64)])
+def test_server_momentum_rule(name, shrink):
+    run_lockstep(Case(W(name).shrunk(shrink, K=4), steps=4, rule="server_momentum",
+                      label="server momentum/" + name))
+
+
+@pytest.mark.parametrize("name,shrink", [("resnet50", 32), ("rbgs", 16)])
+def test_lr_in_residual_rule(name, shrink):
+    run_lockstep(Case(W(name).shrunk(shrink, K=6), steps=4, rule="lr_in_residual",
+                      label="lr in residual/" + name))
+
+
+def test_lr_in_residual_with_fused_detach():
+    run_lockstep(Case(W("resnet18").shrunk(16, K=4), steps=3, rule="lr_in_residual", lam=0.5,
+                      detach="fused", label="lr in residual + detach"))
+
+
+@pytest.mark.parametrize("name,shrink,rule", [("resnet18", 16, "gmc"), ("rbgs", 16, "gmc"),
+                                              ("resnet18", 16, "lr_in_residual")])
+def test_eta_schedule(name, shrink, rule):
+    wl = W(name).shrunk(shrink, K=4)
+    run_lockstep(Case(wl, steps=5, rule=rule, eta_fn=_cosine(wl.eta, 6), label="cosine eta/" + name))
