@@ -42,7 +42,8 @@ DESCRIPTIONS = {
                 "log-uniform scales in [1e-5,1e-1], beta=0.9, eta=0.1",
     "resnet18": "ResNet-18-sized GMC step: d=11,173,962 fp32 in 62 tensors, K=8, global top-k 1%, "
                 "non-IID Gaussian gradients",
-    "rbgs": "GMC+ RBGS step: d=25,557,032 fp32, K=8, 1% of 4096-element blocks per step",
+    "rbgs": "GMC+ RBGS step: d=25,557,032 fp32, K=8, 1% of 4096-element blocks per step, detached "
+            "points w_{t+1,k} = w_{t+1} - lambda eta e_{t+1,k} with lambda=0.5",
     "gpt2": "Transformer-sized GMC step: d=124,439,808 fp32 in 148 tensors, K=8, per-tensor top-k "
             "0.1%, Student-t(4) gradients",
     "tiny": "Tiny GMC step: d=2^20, K=4, global top-k 1%",
@@ -61,12 +62,13 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def algorithmic_bytes(wl, msg_len: int) -> dict:
+def algorithmic_bytes(wl, msg_len: int, detach: bool) -> dict:
     """Bytes one step must move (per step, whole job), and those of the fused
     worker pass alone.  top-s: read g, read e, write e (12 B per worker-
     element); read w_t, w_prev for the momentum term and read + write w in
     the apply (16 B per element); write (idx, val) and read them back in the
-    aggregation (16 B per message entry).  RBGS sends values only (8 B)."""
+    aggregation (16 B per message entry).  RBGS sends values only (8 B).
+    GMC+'s detached points add one write per worker-element (4 B)."""
     K, d = wl.K, wl.d
     if wl.compressor == "rbgs":
         step = 12 * K * d + 16 * d + 8 * K * msg_len
@@ -74,6 +76,9 @@ def algorithmic_bytes(wl, msg_len: int) -> dict:
     else:
         step = 12 * K * d + 16 * d + 16 * K * msg_len
         fused = 12 * K * d + 8 * d
+    if detach:
+        step += 4 * K * d
+        fused += 4 * K * d
     return {"step": step, "fused": fused}
 
 
@@ -99,10 +104,11 @@ def read_pmc_summary():
         return None
 
 
-def cpu_baseline(wl, workers: int, steps: int) -> dict:
+def cpu_baseline(wl, workers: int, steps: int, lam: float = 0.0) -> dict:
     """The CPU oracle (single-threaded C, as it stands) on a bounded sample
     of the workload: `workers` of the K workers at the full d for `steps`
-    iterations, with host-generated inputs of the same recipe."""
+    iterations, with host-generated inputs of the same recipe (and GMC+'s
+    detached points when lam > 0)."""
     import numpy as np
     import oracle
     import synth
@@ -110,7 +116,7 @@ def cpu_baseline(wl, workers: int, steps: int) -> dict:
     sub = dataclasses.replace(wl, K=workers)
     seg = sub.topk_segments() if sub.compressor == "topk_seg" else None
     orc = oracle.GmcOracle(sub.d, workers, "rbgs" if sub.compressor == "rbgs" else "topk",
-                           sub.ratio, sub.beta, sub.eta, seed=sub.seed, seg_off=seg, block=sub.block)
+                           sub.ratio, sub.beta, sub.eta, seed=sub.seed, seg_off=seg, block=sub.block, lam=lam)
     w = sub.w0()
     wp = w.copy()
     err = np.zeros((workers, sub.d), np.float32)
@@ -121,6 +127,8 @@ def cpu_baseline(wl, workers: int, steps: int) -> dict:
         delta = orc.aggregate(idx, val, ln)
         wn = w.copy()
         orc.apply(wn, delta)
+        if lam > 0.0:
+            orc.detach(wn, err)
         wp, w = w, wn
     dt = time.perf_counter() - t0
     return {"value": workers * sub.d * steps / dt / 1e9, "unit": UNIT, "cores": 1, "kind": "oracle",
@@ -138,6 +146,8 @@ def main():
     ap.add_argument("--grad-batches", type=int, default=4)
     ap.add_argument("--margin", type=int, default=None,
                     help="candidate margin (multiple of k) of the speculative selection")
+    ap.add_argument("--lam", type=float, default=None,
+                    help="GMC+ detach coefficient (default 0.5 for the rbgs workload, else 0: plain GMC)")
     ap.add_argument("--cpu-workers", type=int, default=2)
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -162,8 +172,10 @@ def main():
     wl = synth.workload(args.workload)
     d, K = wl.d, wl.K
     seg = wl.topk_segments().tolist() if wl.compressor == "topk_seg" else None
+    lam = args.lam if args.lam is not None else (0.5 if wl.compressor == "rbgs" else 0.0)
+    detach = lam > 0.0
     gm = Gmc(d, K, wl.compressor, wl.ratio, wl.beta, wl.eta, seed=wl.seed, segments=seg,
-             block=wl.block if wl.compressor == "rbgs" else None)
+             block=wl.block if wl.compressor == "rbgs" else None, lam=lam)
     if args.margin is not None:
         from paper_1905_12948_amd import GMC_OPT_CAND_MARGIN
         gm.set_option(GMC_OPT_CAND_MARGIN, args.margin)
@@ -175,6 +187,7 @@ def main():
     err = sdev.rows(K, d, dev, zero=True)
     G = [sdev.grads(wl, t, dev) for t in range(args.grad_batches)]
     idx, val, ln = gm.alloc_messages(dev)
+    wk = sdev.rows(K, d, dev) if detach else None   # GMC+ detached points w_{t+1,k}
     if args.calib:
         cal_src = torch.ones(1 << 28, dtype=torch.float32, device=dev)     # 1 GiB
         cal_dst = torch.empty_like(cal_src)
@@ -187,8 +200,12 @@ def main():
 
     def one_step():
         cur, prev = bufs[step_no[0] % 2], bufs[(step_no[0] + 1) % 2]
-        gm.step(cur, prev, G[step_no[0] % len(G)], err, idx, val, ln)
-        gm.aggregate_apply(idx, val, ln, cur, prev)
+        if detach:
+            gm.step(cur, prev, G[step_no[0] % len(G)], err, idx, val, ln, w_k=wk)
+            gm.finish(idx, val, ln, cur, prev, err=err, w_k=wk)
+        else:
+            gm.step(cur, prev, G[step_no[0] % len(G)], err, idx, val, ln)
+            gm.aggregate_apply(idx, val, ln, cur, prev)
         step_no[0] += 1
 
     log("warmup %d steps" % args.warmup)
@@ -215,11 +232,11 @@ def main():
 
     ms_step = elapsed * 1e3 / args.steps
     msg_len = int(ln[0].item())
-    ab = algorithmic_bytes(wl, msg_len)
+    ab = algorithmic_bytes(wl, msg_len, detach)
     fused_ms_total, fused_n = prof["fused_vec"]
     fused_ms = fused_ms_total / max(fused_n, 1)
     achieved = ab["fused"] / (fused_ms * 1e-3) / 1e9
-    traffic = read_pmc_summary()
+    traffic = read_pmc_summary() if (wl.name == "resnet50" and not detach) else None
     roofline = {"kernel": "topk_fused_vec_kernel" if wl.compressor != "rbgs" else "rbgs_fused_kernel",
                 "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
@@ -228,12 +245,13 @@ def main():
     value = K * d / (ms_step * 1e-3) / 1e9
     sel = {k: stats1[k] - stats0[k] for k in ("from_candidates", "full_data", "candidates")}
     out = {
-        "metric": METRIC, "value": round(value, 2), "unit": UNIT, "n_gpus": 1,
+        "metric": METRIC if wl.name == "resnet50" else METRIC.split(",")[0] + ", " + wl.name,
+        "value": round(value, 2), "unit": UNIT, "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": DESCRIPTIONS[wl.name], "d": d, "K": K, "compressor": wl.compressor,
-                   "ratio": wl.ratio, "message_len": msg_len, "grad_batches": len(G)},
+                   "ratio": wl.ratio, "lambda": lam, "message_len": msg_len, "grad_batches": len(G)},
         "hbm_peak_frac": round(ab["step"] / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "alg_bytes_per_step": ab["step"],
         "selection": sel,
@@ -243,7 +261,7 @@ def main():
         log("cpu baseline: oracle on %d workers x %d steps" % (args.cpu_workers, args.cpu_steps))
         del G
         torch.cuda.empty_cache()
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_workers, args.cpu_steps)
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_workers, args.cpu_steps, lam)
     gm.close()
     print(json.dumps(out), flush=True)
 

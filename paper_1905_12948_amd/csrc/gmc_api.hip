@@ -529,7 +529,14 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
                                            idx_dev, row_i, msg_len_dev, ctx->stream));
         GMC_TRY(prof_end(ctx, 2, ev));
         GMC_TRY(prof_begin(ctx, 0, &ev));
-        GMC_LAUNCH(ctx, launch_rbgs_fused(a, ctx->K, ctx->block, ctx->rbgs_slot, val_dev, row_v, ctx->stream));
+        uint64_t vec_mask = 0;
+        const bool shared_ok = ((uintptr_t)w_t_dev & 15u) == 0 && ((uintptr_t)w_prev_dev & 15u) == 0 &&
+                               ((uintptr_t)val_dev & 15u) == 0 && (row_v & 3) == 0 && (ctx->block & 3) == 0;
+        for (int k = 0; k < ctx->K && shared_ok; ++k)
+            if ((((uintptr_t)grads_dev[k] | (uintptr_t)err_dev[k] | (uintptr_t)a.wp.y[k]) & 15u) == 0)
+                vec_mask |= 1ull << k;
+        GMC_LAUNCH(ctx, launch_rbgs_fused(a, ctx->K, ctx->block, ctx->rbgs_slot, val_dev, row_v, vec_mask,
+                                          ctx->stream));
         GMC_TRY(prof_end(ctx, 0, ev));
     } else {
         // worker k takes the vector pass when its rows and w_t, w_prev are 16-byte aligned
@@ -605,7 +612,7 @@ gmc_status aggregate_impl(gmc_ctx* ctx, const int32_t* idx_dev, const float* val
     hipEvent_t ev;
     GMC_TRY(prof_begin(ctx, 4, &ev));
     if (ctx->comp == GMC_RBGS) {
-        GMC_LAUNCH(ctx, launch_agg_rbgs(ctx->K, (int32_t)ctx->d, ctx->block, idx_dev, ctx->n_sel, val_dev, row_v, f,
+        GMC_LAUNCH(ctx, launch_agg_rbgs(ctx->K, (int32_t)ctx->d, ctx->block, ctx->rbgs_slot, val_dev, row_v, f,
                                         ctx->stream));
     } else {
         GMC_LAUNCH(ctx, launch_agg_rowptr(ctx->K, (int32_t)ctx->d, idx_dev, row_i, msg_len_dev, ctx->rowptr,
@@ -668,10 +675,12 @@ gmc_status gmc_finish(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev
             return fail(ctx, GMC_EINVAL, "gmc_finish: detached points with momentum on the server: use gmc_detach");
         if (!err_dev) return fail(ctx, GMC_EINVAL, "gmc_finish: detached points need err");
         f.detach = 1;
+        f.rows16 = 1;
         for (int k = 0; k < ctx->K; ++k) {
             if (!err_dev[k] || !w_k_dev[k]) return fail(ctx, GMC_EINVAL, "gmc_finish: NULL worker pointer");
             f.e[k] = err_dev[k];
             f.y[k] = w_k_dev[k];
+            if ((((uintptr_t)err_dev[k] | (uintptr_t)w_k_dev[k]) & 15u) != 0) f.rows16 = 0;
         }
     }
     return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, f);

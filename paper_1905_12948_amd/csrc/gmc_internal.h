@@ -129,6 +129,7 @@ struct FinishArgs {
     float b;              // server momentum coefficient (beta) when w_prev is set
     float q;              // lambda*eta
     int32_t detach;       // 1: y_k = w_{t+1} - q e_k at the sent components
+    int32_t rows16;       // 1: every e[k] and y[k] is 16-byte aligned
     const float* e[kMaxWorkers];  // e_{t+1,k}
     float* y[kMaxWorkers];        // w_{t+1,k}
 };
@@ -165,8 +166,10 @@ hipError_t launch_rbgs_sample(uint64_t seed, uint64_t t, int32_t nb, int32_t n_s
                               int32_t B, int32_t K, uint32_t* bitmap, int32_t* blocks,
                               int32_t* block_slot, int32_t* idx, int64_t idx_row,
                               int64_t* msg_len, hipStream_t st);
+// vec_mask: workers whose rows (g, e, detached points) are 16-byte aligned,
+// with w_t, w_prev and the message rows aligned and B a multiple of 4 (else 0)
 hipError_t launch_rbgs_fused(const StepArgs& a, int32_t K, int32_t B, const int32_t* block_slot,
-                             float* val, int64_t val_row, hipStream_t st);
+                             float* val, int64_t val_row, uint64_t vec_mask, hipStream_t st);
 
 hipError_t launch_agg_rowptr(int32_t K, int32_t d, const int32_t* idx, int64_t idx_row,
                              const int64_t* msg_len, int32_t* rowptr, int32_t n_ranges,
@@ -176,9 +179,9 @@ hipError_t launch_agg_rowptr(int32_t K, int32_t d, const int32_t* idx, int64_t i
 hipError_t launch_agg_topk(int32_t K, int32_t d, const int32_t* idx, int64_t idx_row,
                            const float* val, int64_t val_row, const int32_t* rowptr,
                            int32_t n_ranges, const FinishArgs& f, hipStream_t st);
-hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, const int32_t* blocks,
-                           int32_t n_sel, const float* val, int64_t val_row, const FinishArgs& f,
-                           hipStream_t st);
+// block_slot: the last step's table from launch_rbgs_sample
+hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, const int32_t* block_slot,
+                           const float* val, int64_t val_row, const FinishArgs& f, hipStream_t st);
 hipError_t launch_detach(const DetachArgs& a, int32_t K, hipStream_t st);
 
 hipError_t launch_apply(int32_t d, float* w, float* w_prev_out, const float* update,

@@ -963,10 +963,13 @@ hipError_t launch_rbgs_sample(uint64_t seed, uint64_t t, int32_t nb, int32_t n_s
 // block but the last is full, so this is the concatenation in block order).
 __global__ __launch_bounds__(kGroup) void rbgs_fused_kernel(StepArgs a, int32_t K, int32_t B,
                                                             const int32_t* block_slot, float* val,
-                                                            int64_t val_row) {
+                                                            int64_t val_row, int64_t j_begin,
+                                                            uint64_t vec_mask, int64_t vec_end) {
     const int32_t d = a.d;
-    const int64_t j0 = ((int64_t)blockIdx.x * kGroup + threadIdx.x) * 4;
+    const int64_t j0 = j_begin + ((int64_t)blockIdx.x * kGroup + threadIdx.x) * 4;
     if (j0 >= d) return;
+    // workers in vec_mask had [0, vec_end) done by the vector kernel
+    const uint64_t skip = j0 < vec_end ? vec_mask : 0ull;
     const float c = a.c, h = a.h, qd = a.q;
     const int rule = a.rule;
     const bool full = j0 + 4 <= d;
@@ -979,6 +982,7 @@ __global__ __launch_bounds__(kGroup) void rbgs_fused_kernel(StepArgs a, int32_t 
         const float4 wt = ld4(a.w_t + j), wp = ld4(a.w_prev + j);
         const int64_t vpos = (int64_t)slot * B + (j - (int64_t)b * B);
         for (int k = 0; k < K; ++k) {
+            if ((skip >> k) & 1ull) continue;
             float* e = a.wp.e[k];
             const float* gr = a.wp.g[k];
             float* y = a.wp.y[k];
@@ -1023,7 +1027,9 @@ __global__ __launch_bounds__(kGroup) void rbgs_fused_kernel(StepArgs a, int32_t 
         const int32_t slot = block_slot[b];
         const float wtj = a.w_t[j], wpj = a.w_prev[j];
         const int64_t vpos = (int64_t)slot * B + (j - (int64_t)b * B);
+        const uint64_t skip_j = j < vec_end ? vec_mask : 0ull;
         for (int k = 0; k < K; ++k) {
+            if ((skip_j >> k) & 1ull) continue;
             float* e = a.wp.e[k];
             const float u = rule_u_rt(rule, e[j], a.wp.g[k][j], wtj, wpj, c, h);
             if (slot >= 0) {
@@ -1037,11 +1043,98 @@ __global__ __launch_bounds__(kGroup) void rbgs_fused_kernel(StepArgs a, int32_t 
     }
 }
 
+// Vector path of the RBGS worker pass: one workgroup per (chunk of kChunk
+// components, worker), 8 components per thread, like the top-s pass: w_t
+// and w_prev through the cache, g, e (and the detached points) streamed.  B
+// is a multiple of 4, so each float4 lies in one block; a selected block's
+// components go to the message, the rest stay in the residual.
+template <int kRule, bool kDetach>
+__global__ __launch_bounds__(kGroup) void rbgs_vec_kernel(StepArgs a, int32_t K, int32_t B,
+                                                          const int32_t* block_slot, float* val, int64_t val_row,
+                                                          uint64_t vec_mask) {
+    const int chunk = blockIdx.x / K, k = blockIdx.x % K;
+    if (!((vec_mask >> k) & 1ull)) return;  // the element-wise kernel's
+    const int o0 = threadIdx.x * 4;
+    const int64_t start = (int64_t)chunk * kChunk + o0;
+    float* ep = a.wp.e[k] + start;
+    const float* gp = a.wp.g[k] + start;
+    constexpr bool kNeedW = kRule != kRuleServerMomentum || kDetach;
+    const float c = a.c, h = a.h;
+    float4 u[2], gv[2], wt[2], wv[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        u[i] = ld4_stream(ep + i * (kGroup * 4));
+        gv[i] = ld4_stream(gp + i * (kGroup * 4));
+        if (kNeedW) {
+            wt[i] = ld4(a.w_t + start + i * (kGroup * 4));
+            wv[i] = ld4(a.w_prev + start + i * (kGroup * 4));
+        } else {
+            wt[i] = wv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int64_t j = start + i * (kGroup * 4);
+        const int32_t b = (int32_t)(j / B);
+        const int32_t slot = block_slot[b];
+        u[i].x = rule_u<kRule>(u[i].x, gv[i].x, wt[i].x, wv[i].x, c, h);
+        u[i].y = rule_u<kRule>(u[i].y, gv[i].y, wt[i].y, wv[i].y, c, h);
+        u[i].z = rule_u<kRule>(u[i].z, gv[i].z, wt[i].z, wv[i].z, c, h);
+        u[i].w = rule_u<kRule>(u[i].w, gv[i].w, wt[i].w, wv[i].w, c, h);
+        if (slot >= 0) {
+            st4(val + (size_t)k * val_row + (int64_t)slot * B + (j - (int64_t)b * B), u[i]);
+            st4_stream(ep + i * (kGroup * 4),
+                       make_float4(u[i].x - u[i].x, u[i].y - u[i].y, u[i].z - u[i].z, u[i].w - u[i].w));
+        } else {
+            st4_stream(ep + i * (kGroup * 4), u[i]);
+            // unsent: e_{t+1} = u and w_{t+1} = w_t here, so this is final
+            if (kDetach) {
+                const float q = a.q;
+                st4_stream(a.wp.y[k] + j, make_float4(detached(wt[i].x, u[i].x, q), detached(wt[i].y, u[i].y, q),
+                                                      detached(wt[i].z, u[i].z, q), detached(wt[i].w, u[i].w, q)));
+            }
+        }
+    }
+}
+
 hipError_t launch_rbgs_fused(const StepArgs& a, int32_t K, int32_t B, const int32_t* block_slot,
-                             float* val, int64_t val_row, hipStream_t st) {
-    const int64_t threads = ((int64_t)a.d + 3) / 4;
+                             float* val, int64_t val_row, uint64_t vec_mask, hipStream_t st) {
+    // vector kernel over the whole chunks for the workers in vec_mask (B a
+    // multiple of 4 and the message rows 16-byte aligned, checked by the
+    // caller), element-wise kernel for the rest
+    const int64_t n_full = vec_mask ? (int64_t)a.d / kChunk : 0;
+    const int64_t vec_end = n_full * kChunk;
+    if (n_full > 0) {
+        const dim3 grid((unsigned)(n_full * K));
+        if (a.rule == kRuleServerMomentum) {
+            if (a.detach) return hipErrorInvalidValue;
+            hipLaunchKernelGGL((rbgs_vec_kernel<kRuleServerMomentum, false>), grid, dim3(kGroup), 0, st, a, K, B,
+                               block_slot, val, val_row, vec_mask);
+        } else if (a.rule == kRuleLrInResidual) {
+            if (a.detach)
+                hipLaunchKernelGGL((rbgs_vec_kernel<kRuleLrInResidual, true>), grid, dim3(kGroup), 0, st, a, K, B,
+                                   block_slot, val, val_row, vec_mask);
+            else
+                hipLaunchKernelGGL((rbgs_vec_kernel<kRuleLrInResidual, false>), grid, dim3(kGroup), 0, st, a, K, B,
+                                   block_slot, val, val_row, vec_mask);
+        } else {
+            if (a.detach)
+                hipLaunchKernelGGL((rbgs_vec_kernel<kRuleGmc, true>), grid, dim3(kGroup), 0, st, a, K, B, block_slot,
+                                   val, val_row, vec_mask);
+            else
+                hipLaunchKernelGGL((rbgs_vec_kernel<kRuleGmc, false>), grid, dim3(kGroup), 0, st, a, K, B,
+                                   block_slot, val, val_row, vec_mask);
+        }
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const uint64_t all = K == 64 ? ~0ull : ((1ull << K) - 1ull);
+    const int64_t j_begin = vec_mask == all ? vec_end : 0;
+    const int64_t threads = ((int64_t)a.d - j_begin + 3) / 4;
+    if (threads <= 0) return hipSuccess;
     const int grid = (int)((threads + kGroup - 1) / kGroup);
-    hipLaunchKernelGGL(rbgs_fused_kernel, dim3(grid), dim3(kGroup), 0, st, a, K, B, block_slot, val, val_row);
+    hipLaunchKernelGGL(rbgs_fused_kernel, dim3(grid), dim3(kGroup), 0, st, a, K, B, block_slot, val, val_row,
+                       j_begin, vec_mask, vec_end);
     return hipGetLastError();
 }
 
@@ -1273,33 +1366,81 @@ hipError_t launch_agg_topk(int32_t K, int32_t d, const int32_t* idx, int64_t idx
     return hipGetLastError();
 }
 
-// RBGS: every worker sent the same blocks (ascending ids in blocks[0..n_sel));
-// a component of block blocks[q] sits at q*B + offset in each message.  One
-// workgroup per range of kAggRange components, like the top-s kernel.
+// RBGS: every worker sent the same blocks; block_slot[b] is the position q
+// of block b among the step's ascending block ids (-1: not drawn), and a
+// component of block b sits at q*B + offset in each message.  One workgroup
+// per range of kAggRange components, like the top-s kernel.
 template <bool kApply>
-__global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, int32_t B, const int32_t* blocks,
-                                                          int32_t n_sel, const float* val, int64_t val_row,
-                                                          FinishArgs f) {
+__global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, int32_t B, const int32_t* block_slot,
+                                                          const float* val, int64_t val_row, FinishArgs f) {
     __shared__ float acc[kAggRange];
     __shared__ unsigned char hit[kAggRange];
     const int64_t base = (int64_t)blockIdx.x * kAggRange;
     const int64_t n = (int64_t)d - base < kAggRange ? (int64_t)d - base : kAggRange;
+    const bool vec = n == kAggRange && (B & 3) == 0 && aligned16(val) && (val_row & 3) == 0 &&
+                     (f.update == nullptr || aligned16(f.update)) && (!f.detach || f.rows16) &&
+                     (!kApply || (aligned16(f.w_in) && aligned16(f.w_out) &&
+                                  (f.w_prev == nullptr || aligned16(f.w_prev))));
+    if (vec) {
+        // two float4 per thread; each lies in one block (B % 4 == 0), whose
+        // slot says where its values sit in every message
+        const float s = f.s;
+        float4 wv[2], pv[2];
+        int64_t js[2];
+        int32_t slots[2], bs[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            js[i] = base + i * (kGroup * 4) + threadIdx.x * 4;
+            bs[i] = (int32_t)(js[i] / B);
+            slots[i] = block_slot[bs[i]];
+            wv[i] = pv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (kApply) {
+                wv[i] = ld4(f.w_in + js[i]);
+                if (f.w_prev) pv[i] = ld4(f.w_prev + js[i]);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int64_t j = js[i];
+            float4 a4 = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (slots[i] >= 0) {
+                const float* v = val + (int64_t)slots[i] * B + (j - (int64_t)bs[i] * B);
+                for (int k = 0; k < K; ++k) {  // worker order
+                    const float4 x = ld4(v + (size_t)k * val_row);
+                    a4 = make_float4(a4.x + x.x, a4.y + x.y, a4.z + x.z, a4.w + x.w);
+                }
+            }
+            const float4 dl = make_float4(-(s * a4.x), -(s * a4.y), -(s * a4.z), -(s * a4.w));
+            if (f.update) st4(f.update + j, dl);
+            if (kApply) {
+                const float4 x = wv[i];
+                float4 nx = make_float4(x.x + dl.x, x.y + dl.y, x.z + dl.z, x.w + dl.w);
+                if (f.w_prev) {  // momentum on the server
+                    const float4 p = pv[i];
+                    const float b = f.b;
+                    nx = make_float4(nx.x + b * (x.x - p.x), nx.y + b * (x.y - p.y), nx.z + b * (x.z - p.z),
+                                     nx.w + b * (x.w - p.w));
+                }
+                st4(f.w_out + j, nx);
+                if (f.detach && slots[i] >= 0) {  // GMC+: the sent components' detached points
+                    const float q = f.q;
+                    for (int k = 0; k < K; ++k) {
+                        const float4 e = ld4(f.e[k] + j);
+                        st4(f.y[k] + j, make_float4(detached(nx.x, e.x, q), detached(nx.y, e.y, q),
+                                                    detached(nx.z, e.z, q), detached(nx.w, e.w, q)));
+                    }
+                }
+            }
+        }
+        return;
+    }
     for (int q = threadIdx.x; q < kAggRange; q += kGroup) {
         float a = 0.0f;
         unsigned char sent = 0;
         if (q < n) {
             const int64_t j = base + q;
             const int32_t b = (int32_t)(j / B);
-            int lo = 0, hi = n_sel - 1, slot = -1;
-            while (lo <= hi) {  // ascending block ids
-                const int mid = (lo + hi) >> 1;
-                const int32_t x = blocks[mid];
-                if (x == b) {
-                    slot = mid;
-                    break;
-                }
-                if (x < b) lo = mid + 1; else hi = mid - 1;
-            }
+            const int32_t slot = block_slot[b];
             if (slot >= 0) {
                 const int64_t vpos = (int64_t)slot * B + (j - (int64_t)b * B);
                 for (int k = 0; k < K; ++k) a = a + val[(size_t)k * val_row + vpos];
@@ -1314,15 +1455,14 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
     if (kApply && f.detach) finish_detach(hit, base, n, K, f);
 }
 
-hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, const int32_t* blocks,
-                           int32_t n_sel, const float* val, int64_t val_row, const FinishArgs& f,
-                           hipStream_t st) {
+hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, const int32_t* block_slot,
+                           const float* val, int64_t val_row, const FinishArgs& f, hipStream_t st) {
     const int grid = (int)(((int64_t)d + kAggRange - 1) / kAggRange);
     if (f.w_out)
-        hipLaunchKernelGGL(agg_rbgs_kernel<true>, dim3(grid), dim3(kGroup), 0, st, K, d, B, blocks, n_sel, val,
+        hipLaunchKernelGGL(agg_rbgs_kernel<true>, dim3(grid), dim3(kGroup), 0, st, K, d, B, block_slot, val,
                            val_row, f);
     else
-        hipLaunchKernelGGL(agg_rbgs_kernel<false>, dim3(grid), dim3(kGroup), 0, st, K, d, B, blocks, n_sel, val,
+        hipLaunchKernelGGL(agg_rbgs_kernel<false>, dim3(grid), dim3(kGroup), 0, st, K, d, B, block_slot, val,
                            val_row, f);
     return hipGetLastError();
 }

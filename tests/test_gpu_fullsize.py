@@ -12,7 +12,9 @@ For each step and two of the K workers (the first and the last):
     keys are the k largest with ties broken towards the lower index;
 the server update and the apply are compared with the oracle's aggregation
 of all K messages, for every component.  Step 0 takes the full-data
-selection path, later steps the candidate path."""
+selection path, later steps the candidate path.  With lambda > 0 (GMC+,
+gmc_step_detach then gmc_finish) the two workers' detached points are
+compared with the oracle's too."""
 import numpy as np
 import pytest
 
@@ -53,9 +55,10 @@ def check_topk_segment(u: np.ndarray, sel: np.ndarray, k: int, tag: str):
         assert tie_sel.max() < tie_rest.min(), tag + ": ties not broken towards the lower index"
 
 
-@pytest.mark.parametrize("name,steps", [("tiny", 3), ("resnet18", 3), ("resnet50", 3), ("rbgs", 3),
-                                        ("gpt2", 2)])
-def test_full_size_workload(name, steps):
+@pytest.mark.parametrize("name,steps,lam", [("tiny", 3, 0.0), ("resnet18", 3, 0.0), ("resnet50", 3, 0.0),
+                                            ("rbgs", 3, 0.0), ("gpt2", 2, 0.0), ("rbgs", 3, 0.5),
+                                            ("resnet50", 2, 0.5)])
+def test_full_size_workload(name, steps, lam):
     import torch
     import synth.device as sdev
     from paper_1905_12948_amd import Gmc
@@ -67,14 +70,15 @@ def test_full_size_workload(name, steps):
     seg = wl.topk_segments()
     g = Gmc(d, K, wl.compressor, wl.ratio, wl.beta, wl.eta, seed=wl.seed,
             segments=seg.tolist() if wl.compressor == "topk_seg" else None,
-            block=wl.block if rbgs else None)
+            block=wl.block if rbgs else None, lam=lam)
     orc = oracle.GmcOracle(d, K, "rbgs" if rbgs else "topk", wl.ratio, wl.beta, wl.eta, seed=wl.seed,
-                           seg_off=seg, block=wl.block)
-    print("full size %s: d=%d K=%d %s" % (name, d, K, wl.compressor), flush=True)
+                           seg_off=seg, block=wl.block, lam=lam)
+    print("full size %s: d=%d K=%d %s lambda=%g" % (name, d, K, wl.compressor, lam), flush=True)
     bufs = [sdev.w0(wl, dev), None]
     bufs[1] = bufs[0].clone()
     err = sdev.rows(K, d, dev, zero=True)
     idx, val, ln = g.alloc_messages(dev)
+    wk = sdev.rows(K, d, dev) if lam else None
     upd = torch.empty(d, dtype=torch.float32, device=dev)
     check = [0, K - 1]
     for t in range(steps):
@@ -82,8 +86,12 @@ def test_full_size_workload(name, steps):
         cur, prev = bufs[t % 2], bufs[(t + 1) % 2]
         w_h, wp_h = cur.cpu().numpy(), prev.cpu().numpy()
         e_before = {k: err[k].cpu().numpy() for k in check}
-        g.step(cur, prev, grads, err, idx, val, ln)
-        g.aggregate_apply(idx, val, ln, cur, prev, update=upd)
+        if lam:
+            g.step(cur, prev, grads, err, idx, val, ln, w_k=wk)
+            g.finish(idx, val, ln, cur, prev, update=upd, err=err, w_k=wk)
+        else:
+            g.step(cur, prev, grads, err, idx, val, ln)
+            g.aggregate_apply(idx, val, ln, cur, prev, update=upd)
         torch.cuda.synchronize()
         gi, gv, gl = idx.cpu().numpy(), val.cpu().numpy(), ln.cpu().numpy()
         if rbgs:
@@ -113,6 +121,10 @@ def test_full_size_workload(name, steps):
         w_next = w_h.copy()
         orc.apply(w_next, delta)
         assert_same_f32(prev.cpu().numpy(), w_next, "%s step %d: w_{t+1}" % (name, t))
+        if lam:
+            for k in check:
+                want = oracle.detach(orc.q, w_next, err[k].cpu().numpy())
+                assert_same_f32(wk[k].cpu().numpy(), want, "%s step %d: detached point of worker %d" % (name, t, k))
         print("  step %d ok (%s)" % (t, g.stats()), flush=True)
         del grads
     g.close()
