@@ -1,7 +1,8 @@
 """GMC oracle: a plain, slow, single-threaded CPU implementation of one GMC
 iteration (Algorithm 1), of GMC+'s RBGS compressor and detached point
-(Algorithm 2), and of the two alternative update rules of the appendix
-(momentum on the server; learning rate inside the residual).
+(Algorithm 2), of the two alternative update rules of the appendix
+(momentum on the server; learning rate inside the residual), and of the
+sampled-threshold top-s the experiments use (Section 5.1).
 
 TEST INFRASTRUCTURE.  Only the test suite, ``__graft_entry__.smoke()`` and the
 bench's ``cpu_baseline`` leg may import this package.  The device library does
@@ -77,6 +78,13 @@ def _bind(lib):
     lib.orc_precompress_lr.restype = None
     lib.orc_apply_server_momentum.argtypes = [c_i64, c_f, c_vp, c_vp, c_vp, c_vp]
     lib.orc_apply_server_momentum.restype = None
+    u64 = ctypes.c_uint64
+    lib.orc_sample_draw.argtypes = [u64, u64, u64, u64]
+    lib.orc_sample_draw.restype = u64
+    lib.orc_sample_positions.argtypes = [u64, u64, u64, c_i64, c_i64, c_vp]
+    lib.orc_sample_positions.restype = c_i64
+    lib.orc_compress_approx.argtypes = [c_vp, c_i64, u64, u64, u64, c_i64, ctypes.c_double, c_vp, c_vp]
+    lib.orc_compress_approx.restype = c_i64
     return lib
 
 
@@ -203,6 +211,25 @@ def detach(q, w_next, e_next, lib=None) -> np.ndarray:
     return out
 
 
+def sample_positions(seed: int, t: int, k: int, n: int, L: int, lib=None) -> np.ndarray:
+    """The approximate top-s sample: one position per stratum of L."""
+    out = np.empty(max(1, (n + L - 1) // L), dtype=np.int64)
+    m = (lib or load()).orc_sample_positions(seed, t, k, n, L, _ptr(out))
+    return out[:m]
+
+
+def compress_approx(u: np.ndarray, seed: int, t: int, k: int, L: int, ratio: float,
+                    lib=None) -> Tuple[np.ndarray, np.ndarray]:
+    """Approximate top-s of Section 5.1; ``u`` becomes the residual."""
+    assert u.dtype == np.float32 and u.flags.c_contiguous
+    idx = np.empty(max(1, u.size), dtype=np.int32)
+    val = np.empty(max(1, u.size), dtype=np.float32)
+    m = (lib or load()).orc_compress_approx(_ptr(u), u.size, seed, t, k, L, ratio, _ptr(idx), _ptr(val))
+    if m < 0:
+        raise MemoryError("oracle approximate top-s allocation failed")
+    return idx[:m], val[:m]
+
+
 VARIANTS = {"gmc": 0, "server_momentum": 1, "lr_in_residual": 2}
 
 
@@ -252,7 +279,7 @@ class GmcOracle:
 
     def __init__(self, d: int, K: int, compressor: str, ratio: float, beta: float, eta: float,
                  seed: int = 0, seg_off=None, block: int = 4096, lib=None, variant: str = "gmc",
-                 lam: float = 0.0):
+                 lam: float = 0.0, stratum: int = 100):
         self.lib = lib or load()
         self.d, self.K, self.compressor = d, K, compressor
         self.ratio = ratio
@@ -262,11 +289,14 @@ class GmcOracle:
         if seg_off is None:
             seg_off = [0, d]
         self.seg_off = np.ascontiguousarray(seg_off, dtype=np.int64)
+        self.stratum = stratum
         if compressor == "rbgs":
             self.nb = (d + block - 1) // block
             self.n_sel = count(self.nb, ratio, self.lib)
             self.index_len = self.n_sel
             self.message_len = self.n_sel * block
+        elif compressor == "approx":
+            self.index_len = self.message_len = d
         else:
             ks = [count(int(self.seg_off[i + 1] - self.seg_off[i]), ratio, self.lib)
                   for i in range(len(self.seg_off) - 1)]
@@ -301,6 +331,11 @@ class GmcOracle:
                 idx[k, :] = blocks
                 val[k, :v.size] = v
                 msg_len[k] = v.size
+            elif self.compressor == "approx":
+                i_k, v_k = compress_approx(u, self.seed, self.t, k, self.stratum, self.ratio, self.lib)
+                idx[k, :i_k.size] = i_k
+                val[k, :v_k.size] = v_k
+                msg_len[k] = v_k.size
             else:
                 i_k, v_k = compress_topk(u, self.seg_off, self.ratio, self.lib)
                 idx[k, :] = i_k

@@ -361,3 +361,80 @@ void orc_apply_server_momentum(int64_t d, float b, const float* w_t, const float
         w_next[j] = moved + push;
     }
 }
+
+/* ------------------------------------------------------------------------- */
+/* The experiments' approximate top-s (Section 5.1)                           */
+/* ------------------------------------------------------------------------- */
+
+/* Draw i of worker k's sample at step t: output i of a SplitMix64 generator
+ * whose state starts at seed XOR mix(t + 1) XOR mix((k + 1) * 2^32). */
+uint64_t orc_sample_draw(uint64_t seed, uint64_t t, uint64_t k, uint64_t i)
+{
+    const uint64_t gamma = 0x9e3779b97f4a7c15ULL;
+    uint64_t state = seed ^ orc_splitmix64_mix(t + 1) ^ orc_splitmix64_mix((k + 1) << 32);
+    return orc_splitmix64_mix(state + (i + 1) * gamma);
+}
+
+/*
+ * The random subset S of Section 5.1, one component per stratum: stratum i
+ * covers [i L, min((i + 1) L, n)) and contributes the component at offset
+ * ((x_i >> 32) * len_i) >> 32 with x_i = orc_sample_draw(seed, t, k, i).
+ * |S| = ceil(n / L) (L = 100: the paper's |S| = d/100).  Writes the
+ * positions in ascending order and returns |S|.
+ */
+int64_t orc_sample_positions(uint64_t seed, uint64_t t, uint64_t k, int64_t n, int64_t L, int64_t* pos)
+{
+    int64_t m = (n + L - 1) / L;
+    for (int64_t i = 0; i < m; ++i) {
+        int64_t lo = i * L;
+        int64_t len = n - lo < L ? n - lo : L;
+        uint64_t x = orc_sample_draw(seed, t, k, (uint64_t)i);
+        pos[i] = lo + (int64_t)(((x >> 32) * (uint64_t)len) >> 32);
+    }
+    return m;
+}
+
+static int cmp_key_desc(const void* a, const void* b)
+{
+    uint32_t x = *(const uint32_t*)a, y = *(const uint32_t*)b;
+    return (x < y) - (x > y);
+}
+
+/*
+ * Approximate top-s (Section 5.1): theta is the magnitude key ranked r-th
+ * from the top among the sample's components, r = orc_count(|S|, ratio)
+ * (ratio 1/1024 in the paper), and C(u) keeps every component of u whose key
+ * is >= theta, in ascending order; the message length varies around n ratio.
+ * u becomes the residual u - C(u).  idx and val hold up to n entries.
+ * Returns the number kept, or -1 if the scratch allocation fails.
+ */
+int64_t orc_compress_approx(float* u, int64_t n, uint64_t seed, uint64_t t, uint64_t k, int64_t L,
+                            double ratio, int32_t* idx, float* val)
+{
+    int64_t m = (n + L - 1) / L;
+    int64_t* pos = (int64_t*)malloc((size_t)(m > 0 ? m : 1) * sizeof(int64_t));
+    uint32_t* keys = (uint32_t*)malloc((size_t)(m > 0 ? m : 1) * sizeof(uint32_t));
+    if (!pos || !keys) {
+        free(pos);
+        free(keys);
+        return -1;
+    }
+    orc_sample_positions(seed, t, k, n, L, pos);
+    for (int64_t i = 0; i < m; ++i) keys[i] = key_of(u[pos[i]]);
+    qsort(keys, (size_t)m, sizeof(uint32_t), cmp_key_desc);
+    int64_t r = orc_count(m, ratio);
+    uint32_t theta = keys[r - 1];
+    int64_t cnt = 0;
+    for (int64_t j = 0; j < n; ++j) {
+        if (key_of(u[j]) >= theta) {
+            const float kept = u[j];
+            idx[cnt] = (int32_t)j;
+            val[cnt] = kept;
+            u[j] = kept - kept;
+            ++cnt;
+        }
+    }
+    free(pos);
+    free(keys);
+    return cnt;
+}

@@ -554,10 +554,85 @@ def pin_eta_schedule_eq8(lib):
     _eq8_check(_run_rule(lib, wl, wl.ratio, wl.steps, eta_fn=sched), wl)
 
 
+# ---------------------------------------------------------------------------
+# the experiments' approximate top-s (Section 5.1)
+# ---------------------------------------------------------------------------
+
+def pin_approx_sample(lib):
+    """One position per stratum of L (|S| = ceil(n/L)), inside its stratum,
+    reproducible, different across workers and steps, and uniform within a
+    stratum."""
+    for n, L in [(1000, 100), (1001, 100), (17, 5), (5, 100), (64, 1)]:
+        pos = oracle.sample_positions(3, 2, 1, n, L, lib)
+        m = (n + L - 1) // L
+        assert pos.size == m
+        lo = np.arange(m) * L
+        assert np.all(pos >= lo) and np.all(pos < np.minimum(lo + L, n))
+        assert np.array_equal(pos, oracle.sample_positions(3, 2, 1, n, L, lib))
+    a = oracle.sample_positions(3, 2, 0, 100000, 100, lib)
+    assert not np.array_equal(a, oracle.sample_positions(3, 2, 1, 100000, 100, lib))
+    assert not np.array_equal(a, oracle.sample_positions(3, 3, 0, 100000, 100, lib))
+    from scipy.stats import chisquare
+    off = oracle.sample_positions(11, 0, 5, 8 * 40000, 8, lib) % 8
+    assert chisquare(np.bincount(off, minlength=8)).pvalue > 1e-4
+
+
+def pin_approx_threshold_bruteforce(lib):
+    """C(u) keeps every component whose magnitude key reaches theta, the
+    r-th largest key of the sample (r = count(|S|, ratio)), ties included;
+    the residual is u - C(u)."""
+    rng = np.random.default_rng(31)
+    vecs = [rng.standard_normal(20000).astype(np.float32),
+            rng.choice(np.array([0, 1, -1, 2, -2, 3], np.float32), 5000),
+            (rng.standard_t(3, 30001) * 1e-3).astype(np.float32)]
+    for u0 in vecs:
+        for L, ratio in [(100, 1 / 1024), (10, 0.01), (3, 0.2)]:
+            n = u0.size
+            pos = oracle.sample_positions(7, 4, 2, n, L, lib)
+            keys = sorted(_keys(u0[pos]).tolist(), reverse=True)
+            theta = keys[oracle.count(len(keys), ratio, lib) - 1]
+            want = np.nonzero(_keys(u0) >= theta)[0]
+            u = u0.copy()
+            idx, val = oracle.compress_approx(u, 7, 4, 2, L, ratio, lib)
+            assert np.array_equal(idx.astype(np.int64), want)
+            assert np.array_equal(_bits(val), _bits(u0[want]))
+            rest = np.ones(n, bool)
+            rest[want] = False
+            assert np.array_equal(_bits(u[rest]), _bits(u0[rest]))
+            assert np.all(_bits(u[want]) == 0)
+
+
+def pin_approx_full_sample_is_topk(lib):
+    """With L = 1 the sample is all of u, so theta is the k-th largest key and
+    on tie-free data C(u) is exactly top-k."""
+    rng = np.random.default_rng(41)
+    for n, ratio in [(5000, 0.01), (777, 0.05), (64, 1 / 1024)]:
+        u0 = rng.standard_normal(n).astype(np.float32)
+        assert np.unique(_keys(u0)).size == n
+        idx, _ = oracle.compress_approx(u0.copy(), 1, 0, 0, 1, ratio, lib)
+        assert np.array_equal(idx.astype(np.int64), brute_topk(u0, oracle.count(n, ratio, lib)))
+
+
+def pin_approx_count_near_target(lib):
+    """Section 5.1: the number kept is approximately n/1024 (Gaussian u,
+    |S| = n/100): within a factor 1.5 on each seed and within 10 % on
+    average over seeds."""
+    rng = np.random.default_rng(51)
+    n = 1 << 20
+    counts = []
+    for seed in range(12):
+        u = rng.standard_normal(n).astype(np.float32)
+        idx, _ = oracle.compress_approx(u, seed, 0, 0, 100, 1 / 1024, lib)
+        counts.append(idx.size)
+        assert n / 1024 / 1.5 <= idx.size <= n / 1024 * 1.5, idx.size
+    assert abs(np.mean(counts) / (n / 1024) - 1) < 0.1, counts
+
+
 ALL_PINS = [pin_count_rule, pin_constants, pin_topk_bruteforce, pin_delta_approximation,
             pin_error_feedback_identity, pin_msgd_reduction, pin_update_rule_eq8, pin_lemma1,
             pin_aggregate_single_worker, pin_aggregate_sum, pin_splitmix64_vectors,
             pin_rbgs_blocks, pin_rbgs_step_and_cost, pin_toy_quadratic_closed_form,
             pin_toy_quadratic_sparse_converges, pin_detach_lambda_zero, pin_gmcplus_average_rule,
             pin_gmcplus_lemma, pin_server_momentum_rule, pin_lr_in_residual_equals_gmc,
-            pin_eta_schedule_eq8]
+            pin_eta_schedule_eq8, pin_approx_sample, pin_approx_threshold_bruteforce,
+            pin_approx_full_sample_is_topk, pin_approx_count_near_target]

@@ -47,6 +47,12 @@ MUTANTS = {
     "server_momentum_sign": ("w_next[j] = moved + push;", "w_next[j] = moved - push;"),
     "server_momentum_dropped": ("w_next[j] = moved + push;", "w_next[j] = moved;"),
     "server_coeff_over_eta": ("*c = b;", "*c = c_gmc;"),
+    "approx_rank_off_by_one": ("uint32_t theta = keys[r - 1];", "uint32_t theta = keys[r];"),
+    "approx_strict_threshold": ("if (key_of(u[j]) >= theta) {", "if (key_of(u[j]) > theta) {"),
+    "approx_residual_kept": ("u[j] = kept - kept;", "u[j] = kept;"),
+    "sample_stratum_overrun": ("pos[i] = lo + (int64_t)(((x >> 32) * (uint64_t)len) >> 32);",
+                               "pos[i] = lo + (int64_t)(((x >> 32) * (uint64_t)L) >> 32);"),
+    "sample_same_for_workers": ("^ orc_splitmix64_mix((k + 1) << 32);", ";"),
 }
 
 
