@@ -47,6 +47,9 @@ DESCRIPTIONS = {
     "gpt2": "Transformer-sized GMC step: d=124,439,808 fp32 in 148 tensors, K=8, per-tensor top-k "
             "0.1%, Student-t(4) gradients",
     "tiny": "Tiny GMC step: d=2^20, K=4, global top-k 1%",
+    "resnet50_approx": "ResNet-50-sized GMC step with the sampled-threshold top-s of the experiments: "
+                       "d=25,557,032, K=16, |S|=d/100 stratified sample, threshold at rank |S|/1024, "
+                       "every component at or above it kept",
 }
 
 
@@ -115,7 +118,7 @@ def cpu_baseline(wl, workers: int, steps: int, lam: float = 0.0) -> dict:
     import dataclasses
     sub = dataclasses.replace(wl, K=workers)
     seg = sub.topk_segments() if sub.compressor == "topk_seg" else None
-    orc = oracle.GmcOracle(sub.d, workers, "rbgs" if sub.compressor == "rbgs" else "topk",
+    orc = oracle.GmcOracle(sub.d, workers, sub.compressor if sub.compressor in ("rbgs", "approx") else "topk",
                            sub.ratio, sub.beta, sub.eta, seed=sub.seed, seg_off=seg, block=sub.block, lam=lam)
     w = sub.w0()
     wp = w.copy()
@@ -231,7 +234,7 @@ def main():
         torch.cuda.synchronize()
 
     ms_step = elapsed * 1e3 / args.steps
-    msg_len = int(ln[0].item())
+    msg_len = int(round(float(ln.double().mean().item())))  # varies per worker for the sampled threshold
     ab = algorithmic_bytes(wl, msg_len, detach)
     fused_ms_total, fused_n = prof["fused_vec"]
     fused_ms = fused_ms_total / max(fused_n, 1)

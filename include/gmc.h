@@ -62,8 +62,23 @@ typedef struct gmc_ctx gmc_ctx;
 typedef enum {
     GMC_TOPK_GLOBAL = 0,    /* top-s over the whole vector (one segment)          */
     GMC_TOPK_SEGMENTED = 1, /* top-s per segment (per tensor), see gmc_set_segments */
-    GMC_RBGS = 2            /* random blocks shared by all workers                */
+    GMC_RBGS = 2,           /* random blocks shared by all workers                */
+    GMC_TOPK_APPROX = 3     /* the experiments' sampled-threshold top-s, whole vector
+                               (Section 5.1): see below                            */
 } gmc_compressor;
+
+/*
+ * GMC_TOPK_APPROX: worker k's sample S at step t holds one component per
+ * stratum of L consecutive components (L = 100 by default, the paper's
+ * |S| = d/100; GMC_OPT_SAMPLE_STRATUM): stratum i = [iL, min((i+1)L, d))
+ * contributes the component at offset ((x >> 32) * len_i) >> 32, x the
+ * i-th output (i = 0, 1, ...) of a SplitMix64 stream started at
+ * seed XOR mix64(t + 1) XOR mix64((k + 1) << 32).  theta is the key ranked
+ * r = min(|S|, max(1, ceil(ratio |S|))) from the top among the sample's
+ * magnitude keys (ratio = 1/1024 in the paper), and the message keeps every
+ * component whose key is >= theta, in ascending order: about ratio * d of
+ * them, a number that varies (msg_len).  Message capacity: d per worker.
+ */
 
 typedef enum {
     GMC_OK = 0,
@@ -108,11 +123,12 @@ gmc_status gmc_set_block(gmc_ctx* ctx, int32_t block);
 gmc_status gmc_set_stream(gmc_ctx* ctx, void* hip_stream);
 
 /* Per-worker message capacity the caller must provide, in elements:
- * top-s: k_tot = sum over segments of k; RBGS: n_sel * B. */
+ * top-s: k_tot = sum over segments of k; RBGS: n_sel * B; sampled-threshold
+ * top-s: d. */
 int64_t gmc_message_len(const gmc_ctx* ctx);
 
 /* Per-worker index capacity: top-s: k_tot (element indices);
- * RBGS: n_sel (block ids). */
+ * RBGS: n_sel (block ids); sampled-threshold top-s: d. */
 int64_t gmc_index_len(const gmc_ctx* ctx);
 
 /*
@@ -128,7 +144,9 @@ int64_t gmc_index_len(const gmc_ctx* ctx);
  *                         ascending block ids, the same row for every worker
  *   val_dev               [K][gmc_message_len] fp32 out: u_k at the kept
  *                         components, in idx order (RBGS: block after block)
- *   msg_len_dev           [K] int64 out: values written per worker
+ *   msg_len_dev           [K] int64 out: values written per worker (k_tot,
+ *                         RBGS: n_sel blocks' worth, sampled-threshold
+ *                         top-s: the number kept)
  * Device buffers must not overlap each other.  Pointers that are not 16-byte
  * aligned are accepted (slower path).  w is never written.
  */
@@ -253,12 +271,15 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
  *   GMC_OPT_PROFILE            bit mask of the stages to time with HIP events
  *                              on the context's stream (0: off); see
  *                              gmc_profile_read for the stage numbers
+ *   GMC_OPT_SAMPLE_STRATUM     GMC_TOPK_APPROX: components per sample stratum
+ *                              L in [1, d] (default 100); before the first step
  */
 enum {
     GMC_OPT_FORCE_FULL_SELECT = 1,
     GMC_OPT_CAND_MARGIN = 2,
     GMC_OPT_CAND_CAP_MULT = 3,
-    GMC_OPT_PROFILE = 4
+    GMC_OPT_PROFILE = 4,
+    GMC_OPT_SAMPLE_STRATUM = 5
 };
 gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value);
 

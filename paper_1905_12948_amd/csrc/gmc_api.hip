@@ -46,6 +46,7 @@ struct gmc_ctx {
     int force_full = 0;
     int margin = 2;
     int cap_mult = 16;
+    int32_t stratum = 100;         // sampled-threshold top-s: components per sample stratum
 
     // derived
     std::vector<int32_t> seg_k;
@@ -230,6 +231,8 @@ gmc_status prepare(gmc_ctx* ctx) {
     ctx->n_ranges = (int32_t)((d + kAggRange - 1) / kAggRange);
 
     TopkTables T;
+    const bool approx = ctx->comp == GMC_TOPK_APPROX;
+    const int64_t samp_n = approx ? (ctx->d + ctx->stratum - 1) / ctx->stratum : 0;
     size_t bytes = 0;
     auto add = [&](size_t n, size_t sz) { bytes = ((bytes + 255) & ~(size_t)255) + n * sz; };
     add(8, sizeof(int64_t));  // stats
@@ -254,6 +257,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         add((size_t)T.cand_total, 4); add((size_t)T.cand_total, 4);
         for (int q = 0; q < 4; ++q) add((size_t)K * nsl, 4);
         add((size_t)K * (ctx->n_ranges + 1), 4);
+        if (approx) add((size_t)K * samp_n, 4);
     }
     bytes += 256;
     void* mem = nullptr;
@@ -286,6 +290,10 @@ gmc_status prepare(gmc_ctx* ctx) {
         g.n_chunks = (int32_t)nc;
         g.n_cgroups = (int32_t)ng;
         g.n_slices = (int32_t)nsl;
+        g.approx = approx ? 1 : 0;
+        g.stratum = ctx->stratum;
+        g.samp_n = (int32_t)samp_n;
+        g.samp_r = approx ? (int32_t)count_for(samp_n, ctx->ratio) : 0;
         GMC_TRY(put(T.seg_start, &g.seg_start));
         GMC_TRY(put(T.seg_out, &g.seg_out));
         GMC_TRY(put(T.chunk_start, &g.chunk_start));
@@ -331,6 +339,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         sc.sl_tiebase = cv.take<uint32_t>((size_t)K * nsl);
         sc.stats = ctx->stats;
         ctx->rowptr = cv.take<int32_t>((size_t)K * (ctx->n_ranges + 1));
+        sc.samp = approx ? cv.take<float>((size_t)K * samp_n) : nullptr;
     }
     if (cv.off > bytes) return fail(ctx, GMC_ENOMEM, "internal: scratch layout overflow");
     ctx->prepared = true;
@@ -404,7 +413,8 @@ gmc_status gmc_init(gmc_ctx** out, int64_t d, int32_t K, int32_t compressor, dou
     *out = nullptr;
     if (d < 1 || d > 0x7fffffffLL) return fail(nullptr, GMC_EINVAL, "gmc_init: d must be in [1, 2^31)");
     if (K < 1 || K > GMC_MAX_WORKERS) return fail(nullptr, GMC_EINVAL, "gmc_init: K must be in [1, 64]");
-    if (compressor != GMC_TOPK_GLOBAL && compressor != GMC_TOPK_SEGMENTED && compressor != GMC_RBGS)
+    if (compressor != GMC_TOPK_GLOBAL && compressor != GMC_TOPK_SEGMENTED && compressor != GMC_RBGS &&
+        compressor != GMC_TOPK_APPROX)
         return fail(nullptr, GMC_EINVAL, "gmc_init: unknown compressor");
     if (!(ratio > 0.0 && ratio <= 1.0)) return fail(nullptr, GMC_EINVAL, "gmc_init: ratio must be in (0, 1]");
     if (!(beta >= 0.0 && beta < 1.0)) return fail(nullptr, GMC_EINVAL, "gmc_init: beta must be in [0, 1)");
@@ -448,8 +458,8 @@ gmc_status gmc_set_segments(gmc_ctx* ctx, int32_t n_seg, const int64_t* seg_off)
     if (ctx->started) return fail(ctx, GMC_ESTATE, "gmc_set_segments: segments are fixed after the first step");
     if (ctx->comp == GMC_RBGS) return fail(ctx, GMC_EINVAL, "gmc_set_segments: not a top-s context");
     if (!seg_off || n_seg < 1 || n_seg > ctx->d) return fail(ctx, GMC_EINVAL, "gmc_set_segments: bad n_seg or NULL table");
-    if (ctx->comp == GMC_TOPK_GLOBAL && n_seg != 1)
-        return fail(ctx, GMC_EINVAL, "gmc_set_segments: GMC_TOPK_GLOBAL has exactly one segment");
+    if ((ctx->comp == GMC_TOPK_GLOBAL || ctx->comp == GMC_TOPK_APPROX) && n_seg != 1)
+        return fail(ctx, GMC_EINVAL, "gmc_set_segments: this compressor works on one segment");
     if (seg_off[0] != 0 || seg_off[n_seg] != ctx->d)
         return fail(ctx, GMC_EINVAL, "gmc_set_segments: offsets must start at 0 and end at d");
     for (int32_t i = 0; i < n_seg; ++i)
@@ -486,11 +496,13 @@ gmc_status gmc_set_stream(gmc_ctx* ctx, void* hip_stream) {
 
 int64_t gmc_message_len(const gmc_ctx* ctx) {
     if (!ctx) return -1;
+    if (ctx->comp == GMC_TOPK_APPROX) return ctx->d;  // the count varies, up to d
     return ctx->comp == GMC_RBGS ? (int64_t)ctx->n_sel * ctx->block : ctx->k_tot;
 }
 
 int64_t gmc_index_len(const gmc_ctx* ctx) {
     if (!ctx) return -1;
+    if (ctx->comp == GMC_TOPK_APPROX) return ctx->d;
     return ctx->comp == GMC_RBGS ? (int64_t)ctx->n_sel : ctx->k_tot;
 }
 
@@ -510,6 +522,8 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
     a.rule = ctx->rule;
     a.detach = y_dev ? 1 : 0;
     a.d = (int32_t)ctx->d;
+    a.seed = ctx->seed;
+    a.t = (uint64_t)ctx->t;
     for (int k = 0; k < ctx->K; ++k) {
         if (!grads_dev[k] || !err_dev[k] || (y_dev && !y_dev[k]))
             return fail(ctx, GMC_EINVAL, "gmc_step: NULL worker pointer");
@@ -770,6 +784,14 @@ gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value) {
             if (value < 1 || value > 1024) return fail(ctx, GMC_EINVAL, "gmc_set_option: cap multiple must be in [1, 1024]");
             if (ctx->started) return fail(ctx, GMC_ESTATE, "gmc_set_option: capacity is fixed after the first step");
             ctx->cap_mult = (int)value;
+            ctx->prepared = false;
+            return prepare(ctx);
+        case GMC_OPT_SAMPLE_STRATUM:
+            if (ctx->comp != GMC_TOPK_APPROX)
+                return fail(ctx, GMC_EINVAL, "gmc_set_option: the sample stratum belongs to GMC_TOPK_APPROX");
+            if (value < 1 || value > ctx->d) return fail(ctx, GMC_EINVAL, "gmc_set_option: stratum must be in [1, d]");
+            if (ctx->started) return fail(ctx, GMC_ESTATE, "gmc_set_option: the stratum is fixed after the first step");
+            ctx->stratum = (int32_t)value;
             ctx->prepared = false;
             return prepare(ctx);
         case GMC_OPT_PROFILE:

@@ -62,12 +62,17 @@ struct PairState {
     int32_t r;          // components with key == T to take (lowest index)
     uint32_t done;      // finished workgroups of the current kernel
     uint32_t cand_used; // candidates of this step (cand is reset for the next)
-    uint32_t pad[7];
+    uint32_t tau_used;  // the candidate threshold this step's fused pass used
+    uint32_t pad[6];
 };
 
 // Static geometry of the top-s selection (built on the host at init).
 struct TopkGeometry {
     int32_t K, n_seg, n_chunks, n_cgroups, n_slices;
+    // sampled-threshold top-s (one segment): each worker's sample holds one
+    // component per stratum of `stratum`; the threshold is its samp_r-th
+    // largest key
+    int32_t approx, stratum, samp_n, samp_r;
     const int32_t* seg_start;     // [n_seg+1] segment offsets
     const int32_t* seg_out;       // [n_seg] offset of the segment in a message row
     const int32_t* chunk_start;   // [n_chunks]
@@ -102,6 +107,7 @@ struct TopkScratch {
     uint32_t* sl_ties;            // [K*n_slices] at-threshold count
     uint32_t* sl_out;             // [K*n_slices] message offset of the slice's first kept component
     uint32_t* sl_tiebase;         // [K*n_slices] at-threshold components in earlier slices
+    float* samp;                  // [K][samp_n] the sample's values (sampled-threshold top-s)
     int64_t* stats;               // [8]
 };
 
@@ -115,6 +121,8 @@ struct StepArgs {
     int32_t rule;    // kRule*
     int32_t detach;  // 1: also write y_k = w_t - q u_k (completed by the server pass)
     int32_t d;
+    uint64_t seed;   // sample draws of the sampled-threshold top-s
+    uint64_t t;      // step
 };
 
 // The server pass after the sum over workers: update = -(s * sum), the

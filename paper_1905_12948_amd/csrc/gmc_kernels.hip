@@ -97,6 +97,37 @@ __device__ __forceinline__ float rule_u_rt(int rule, float e, float g, float wt,
     return rule_u<kRuleGmc>(e, g, wt, wp, c, h);
 }
 
+// The output mix of SplitMix64 (Steele, Lea and Flood, OOPSLA 2014).
+__device__ __forceinline__ uint64_t splitmix64_mix(uint64_t z) {
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    return z ^ (z >> 31);
+}
+
+// Sampled-threshold top-s (Section 5.1): worker k's sample at step t holds
+// one component per stratum of L consecutive components, at offset
+// ((x >> 32) * len) >> 32 of stratum i, x the i-th output of a SplitMix64
+// stream started at seed ^ mix(t + 1) ^ mix((k + 1) << 32).
+__device__ __forceinline__ uint64_t sample_state(uint64_t seed, uint64_t t, int k) {
+    return seed ^ splitmix64_mix(t + 1) ^ splitmix64_mix((uint64_t)(k + 1) << 32);
+}
+
+__device__ __forceinline__ int32_t sample_pos(uint64_t state, int32_t i, int32_t L, int32_t n) {
+    const uint64_t x = splitmix64_mix(state + (uint64_t)(i + 1) * 0x9e3779b97f4a7c15ull);
+    const int32_t lo = i * L;
+    const int32_t len = n - lo < L ? n - lo : L;
+    return lo + (int32_t)(((x >> 32) * (uint64_t)len) >> 32);
+}
+
+// Records the sample components among the four at [j, j + 4).
+__device__ __forceinline__ void sample_float4(float* samp, uint64_t state, int32_t j, float4 u, int32_t L,
+                                              int32_t n) {
+    for (int32_t i = j / L; (int64_t)i * L < (int64_t)j + 4 && (int64_t)i * L < n; ++i) {
+        const int32_t o = sample_pos(state, i, L, n) - j;
+        if (o >= 0 && o < 4) samp[i] = o == 0 ? u.x : o == 1 ? u.y : o == 2 ? u.z : u.w;
+    }
+}
+
 // GMC+'s detached point from w and the residual: w - q e (Algorithm 2).
 __device__ __forceinline__ float detached(float w, float e, float q) {
     const float r = q * e;
@@ -170,7 +201,7 @@ __device__ __forceinline__ void store_agent(uint32_t* p, uint32_t v) {
 // streaming pass takes no atomics; the compaction kernel packs the slots.
 // ---------------------------------------------------------------------------
 
-template <int kRule, bool kDetach>
+template <int kRule, bool kDetach, bool kApprox>
 __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                                 uint64_t vec_mask) {
     __shared__ uint32_t wtot[2][kWavesPerGroup];
@@ -223,6 +254,12 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
         flags |= (key_of(u[i].y) >= tau ? 1u : 0u) << (i * 4 + 1);
         flags |= (key_of(u[i].z) >= tau ? 1u : 0u) << (i * 4 + 2);
         flags |= (key_of(u[i].w) >= tau ? 1u : 0u) << (i * 4 + 3);
+    }
+    if (kApprox) {
+        const uint64_t sst = sample_state(a.seed, a.t, k);
+        float* sp = s.samp + (size_t)k * g.samp_n;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) sample_float4(sp, sst, start + o0 + i * (kGroup * 4), u[i], g.stratum, a.d);
     }
     const size_t run_slot = (size_t)k * g.n_chunks + chunk;
     if (__syncthreads_or(flags != 0u) == 0) {
@@ -387,6 +424,7 @@ __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, Topk
     float* e = a.wp.e[k];
     const float* gr = a.wp.g[k];
     uint32_t flags = 0;
+    const uint64_t sst = g.approx ? sample_state(a.seed, a.t, k) : 0ull;
 #pragma unroll 4
     for (int i = 0; i < kIt; ++i) {
         const int o = i * kWave + lane;
@@ -396,6 +434,10 @@ __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, Topk
             e[j] = u;
             if (a.detach) a.wp.y[k][j] = detached(a.w_t[j], u, a.q);
             flags |= (key_of(u) >= tau ? 1u : 0u) << i;
+            if (g.approx) {
+                const int32_t q = j / g.stratum;
+                if (sample_pos(sst, q, g.stratum, a.d) == j) s.samp[(size_t)k * g.samp_n + q] = u;
+            }
         }
     }
     // the chunk's slot, in index order (iteration-major, then lane)
@@ -415,29 +457,36 @@ __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, Topk
     if (lane == 0) s.run_cnt[run_slot] = base;
 }
 
-hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
-                                 uint64_t vec_mask, hipStream_t st) {
+template <bool kApprox>
+static hipError_t launch_fused_vec_rule(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
+                                       uint64_t vec_mask, hipStream_t st) {
     const int grid = g.n_chunks * g.K;
     if (a.rule == kRuleServerMomentum) {
         if (a.detach) return hipErrorInvalidValue;  // the detached points need w_{t+1} = w_t off the sent set
-        hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleServerMomentum, false>), dim3(grid), dim3(kGroup), 0, st, a,
-                           g, s, vec_mask);
+        hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleServerMomentum, false, kApprox>), dim3(grid), dim3(kGroup), 0,
+                           st, a, g, s, vec_mask);
     } else if (a.rule == kRuleLrInResidual) {
         if (a.detach)
-            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleLrInResidual, true>), dim3(grid), dim3(kGroup), 0, st, a,
-                               g, s, vec_mask);
+            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleLrInResidual, true, kApprox>), dim3(grid), dim3(kGroup),
+                               0, st, a, g, s, vec_mask);
         else
-            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleLrInResidual, false>), dim3(grid), dim3(kGroup), 0, st,
-                               a, g, s, vec_mask);
+            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleLrInResidual, false, kApprox>), dim3(grid), dim3(kGroup),
+                               0, st, a, g, s, vec_mask);
     } else {
         if (a.detach)
-            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleGmc, true>), dim3(grid), dim3(kGroup), 0, st, a, g, s,
-                               vec_mask);
+            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleGmc, true, kApprox>), dim3(grid), dim3(kGroup), 0, st, a,
+                               g, s, vec_mask);
         else
-            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleGmc, false>), dim3(grid), dim3(kGroup), 0, st, a, g, s,
-                               vec_mask);
+            hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleGmc, false, kApprox>), dim3(grid), dim3(kGroup), 0, st,
+                               a, g, s, vec_mask);
     }
     return hipGetLastError();
+}
+
+hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
+                                 uint64_t vec_mask, hipStream_t st) {
+    return g.approx ? launch_fused_vec_rule<true>(a, g, s, vec_mask, st)
+                    : launch_fused_vec_rule<false>(a, g, s, vec_mask, st);
 }
 
 hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
@@ -471,7 +520,8 @@ constexpr int kEmitStage = kGroup * kEmitLoads;  // elements staged in LDS per r
 // A workgroup's slice of a pair's selection input.
 struct Slice {
     int64_t lo, hi;          // positions in the input array
-    const float* val;        // mode 0: candidate values; mode 1: u of the segment (held in e)
+    const float* val;        // mode 0: candidate values; mode 1: u of the segment (held in e);
+                             // mode 2: the sample
     const int32_t* idx;      // mode 0: candidate indices; mode 1: NULL (index = seg_lo + position)
     int32_t seg_lo;
 };
@@ -480,12 +530,17 @@ __device__ __forceinline__ Slice open_slice(int mode, uint32_t cand, int k, int 
                                             const StepArgs& a, const TopkGeometry& g, const TopkScratch& s) {
     Slice v;
     v.seg_lo = g.seg_start[seg];
-    const int64_t total = mode == 0 ? (int64_t)cand : (int64_t)(g.seg_start[seg + 1] - v.seg_lo);
+    const int64_t total = mode == 0   ? (int64_t)cand
+                          : mode == 2 ? (int64_t)g.samp_n
+                                      : (int64_t)(g.seg_start[seg + 1] - v.seg_lo);
     v.lo = total * w / W;
     v.hi = total * (w + 1) / W;
     if (mode == 0) {
         v.val = s.cand_val + g.pair_cand[p];
         v.idx = s.cand_idx + g.pair_cand[p];
+    } else if (mode == 2) {  // the sample (sampled-threshold top-s; values only)
+        v.val = s.samp + (size_t)k * g.samp_n;
+        v.idx = nullptr;
     } else {
         v.val = a.wp.e[k] + v.seg_lo;
         v.idx = nullptr;
@@ -592,10 +647,13 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
 
     const SliceId id = slice_id(g);
     PairState* ps = &s.pair[id.p];
-    const int kp = g.pair_k[id.p];
+    // sampled-threshold top-s: the passes select over the sample, rank samp_r
+    const bool approx = g.approx != 0;
+    const int kp = approx ? g.samp_r : g.pair_k[id.p];
     const uint32_t cand = PASS == 1 ? ps->cand : ps->cand_used;
-    const int mode = PASS == 1 ? ((force_full || cand < (uint32_t)kp || cand > (uint32_t)g.pair_cap[id.p]) ? 1 : 0)
-                               : ps->mode;
+    const int mode = approx      ? 2
+                     : PASS == 1 ? ((force_full || cand < (uint32_t)kp || cand > (uint32_t)g.pair_cap[id.p]) ? 1 : 0)
+                                 : ps->mode;
     const uint32_t prefix = PASS == 1 ? 0u : ps->prefix;
 
     for (int b = threadIdx.x; b < nbins; b += kGroup) h[b] = 0u;
@@ -640,12 +698,15 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
         if (threadIdx.x == 0) {
             if (want64 > total && tb > 0) --tb;  // too few counted: widen by one bin
             if (tb < 0) tb = 0;
+            ps->tau_used = ps->tau;
             ps->tau = (uint32_t)tb << kShift1;
             ps->mode = mode;
             ps->cand_used = cand;
             ps->cand = 0u;  // every workgroup of the pair has read it
-            atomicAdd((unsigned long long*)&s.stats[mode == 0 ? 1 : 2], 1ull);
-            if (mode == 0) atomicAdd((unsigned long long*)&s.stats[3], (unsigned long long)cand);
+            if (!approx) {
+                atomicAdd((unsigned long long*)&s.stats[mode == 0 ? 1 : 2], 1ull);
+                if (mode == 0) atomicAdd((unsigned long long*)&s.stats[3], (unsigned long long)cand);
+            }
         }
     }
     if (threadIdx.x == 0) {
@@ -658,8 +719,20 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
             ps->prefix = (prefix << 11) | b;
             ps->need = (int32_t)(need - above);
         } else {
-            ps->T = (prefix << 9) | b;
+            const uint32_t T = (prefix << 9) | b;
+            ps->T = T;
             ps->r = (int32_t)(need - above);
+            if (approx) {
+                // keep every component at or above the sample's threshold;
+                // the candidates hold them all when T reaches the threshold
+                // the fused pass collected with and none were dropped
+                ps->r = 0x7fffffff;
+                const uint32_t cu = ps->cand_used;
+                const int m = (!force_full && T >= ps->tau_used && cu <= (uint32_t)g.pair_cap[id.p]) ? 0 : 1;
+                ps->mode = m;
+                atomicAdd((unsigned long long*)&s.stats[m == 0 ? 1 : 2], 1ull);
+                if (m == 0) atomicAdd((unsigned long long*)&s.stats[3], (unsigned long long)cu);
+            }
         }
         store_agent(&ps->done, 0u);
     }
@@ -754,8 +827,12 @@ __global__ __launch_bounds__(kGroup) void topk_count_kernel(StepArgs a, TopkGeom
         __syncthreads();
     }
     if (threadIdx.x == 0) {
-        if (carry[1] != (uint32_t)g.pair_k[id.p]) atomicAdd((unsigned long long*)&s.stats[4], 1ull);
-        if (id.seg == 0) msg_len[id.k] = msg_total;
+        if (g.approx) {
+            msg_len[id.k] = (int64_t)carry[1];  // one segment; the count varies
+        } else {
+            if (carry[1] != (uint32_t)g.pair_k[id.p]) atomicAdd((unsigned long long*)&s.stats[4], 1ull);
+            if (id.seg == 0) msg_len[id.k] = msg_total;
+        }
         store_agent(&ps->done, 0u);
     }
 }
@@ -797,7 +874,10 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
     const uint32_t out0 = s.sl_out[sl];
     int64_t quota = r - (int64_t)s.sl_tiebase[sl];  // ties this slice may still take, in index order
     if (quota < 0) quota = 0;
-    const uint32_t kseg = (uint32_t)g.pair_k[id.p];
+    // capacity of the segment's part of the row: k (top-s) or the whole
+    // segment (sampled threshold)
+    const uint32_t kseg = g.approx ? (uint32_t)(g.seg_start[id.seg + 1] - g.seg_start[id.seg])
+                                   : (uint32_t)g.pair_k[id.p];
     int32_t* irow = idx + (size_t)id.k * row_len + g.seg_out[id.seg];
     float* vrow = val + (size_t)id.k * row_len + g.seg_out[id.seg];
     float* e = a.wp.e[id.k];
@@ -869,12 +949,6 @@ hipError_t launch_topk_emit(const StepArgs& a, const TopkGeometry& g, const Topk
 // ============================================================================
 
 namespace {
-
-__device__ __forceinline__ uint64_t splitmix64_mix(uint64_t z) {
-    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
-    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
-    return z ^ (z >> 31);
-}
 
 constexpr int kLdsBitmapWords = 8192;  // 262144 blocks
 

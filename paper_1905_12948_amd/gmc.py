@@ -15,13 +15,15 @@ from typing import List, Optional, Sequence, Tuple, Union
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgmc.so")
 
-GMC_TOPK_GLOBAL, GMC_TOPK_SEGMENTED, GMC_RBGS = 0, 1, 2
+GMC_TOPK_GLOBAL, GMC_TOPK_SEGMENTED, GMC_RBGS, GMC_TOPK_APPROX = 0, 1, 2, 3
 GMC_OK, GMC_EINVAL, GMC_ENOMEM, GMC_EDEVICE, GMC_ESTATE = 0, -1, -2, -3, -4
 GMC_OPT_FORCE_FULL_SELECT, GMC_OPT_CAND_MARGIN, GMC_OPT_CAND_CAP_MULT, GMC_OPT_PROFILE = 1, 2, 3, 4
+GMC_OPT_SAMPLE_STRATUM = 5
 MAX_WORKERS = 64
 STAGES = ("fused_vec", "fused_gen", "select", "emit", "aggregate", "apply")
 
-COMPRESSORS = {"topk": GMC_TOPK_GLOBAL, "topk_seg": GMC_TOPK_SEGMENTED, "rbgs": GMC_RBGS}
+COMPRESSORS = {"topk": GMC_TOPK_GLOBAL, "topk_seg": GMC_TOPK_SEGMENTED, "rbgs": GMC_RBGS,
+               "approx": GMC_TOPK_APPROX}
 
 # every entry point include/gmc.h declares
 EXPORTS = ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "gmc_message_len",
@@ -143,14 +145,15 @@ class Gmc:
     """One GMC context: ``step`` (workers), ``aggregate`` (server), ``apply``.
 
     compressor: "topk" (global top-s), "topk_seg" (top-s per segment; pass
-    ``segments`` as the n_seg+1 offsets) or "rbgs" (``block`` elements per
-    block).  Calls run on torch's current stream of the tensors' device.
+    ``segments`` as the n_seg+1 offsets), "rbgs" (``block`` elements per
+    block) or "approx" (the sampled-threshold top-s, ``stratum`` components
+    per sample stratum).  Calls run on torch's current stream of the tensors' device.
     """
 
     def __init__(self, d: int, K: int, compressor: str = "topk", ratio: float = 0.001,
                  beta: float = 0.9, eta: float = 0.1, seed: int = 0,
                  segments: Optional[Sequence[int]] = None, block: Optional[int] = None,
-                 rule: str = "gmc", lam: float = 0.0):
+                 rule: str = "gmc", lam: float = 0.0, stratum: Optional[int] = None):
         self._lib = load()
         self.d, self.K, self.compressor = int(d), int(K), compressor
         if compressor not in COMPRESSORS:
@@ -166,6 +169,8 @@ class Gmc:
             self._call(self._lib.gmc_set_segments(self._ctx, len(segments) - 1, off))
         if block is not None:
             self._call(self._lib.gmc_set_block(self._ctx, int(block)))
+        if stratum is not None:
+            self.set_option(GMC_OPT_SAMPLE_STRATUM, int(stratum))
         if rule not in RULES:
             raise ValueError("rule must be one of %s" % list(RULES))
         self.rule = rule

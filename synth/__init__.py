@@ -17,6 +17,8 @@ Workloads (flat fp32 parameter vectors shaped like real models):
                 4096-element blocks, 1 % of blocks per step.
 * ``gpt2``      d = 124,439,808 in 148 tensors, K = 8, Student-t(4)
                 gradients, per-tensor top-k 0.1 %.
+* ``resnet50_approx``  the ``resnet50`` inputs with the sampled-threshold
+                top-s of the experiments (|S| = d/100, rank |S|/1024).
 
 Each workload can be shrunk (``shrink=f``) for oracle-sized parity tests: every
 tensor keeps its place in the layout and is divided by ``f`` (at least one
@@ -231,10 +233,15 @@ WORKLOADS = {
     "gpt2": Workload("gpt2", gpt2_small_sizes(), K=8, ratio=0.001, beta=0.9, eta=0.05,
                      steps=10, compressor="topk_seg", dist="student_t", nu=4,
                      scale_lo=1e-5, scale_hi=1e-2),
+    # the ResNet-50-sized step with the experiments' sampled-threshold top-s
+    # (|S| = d/100, threshold at rank |S|/1024)
+    "resnet50_approx": Workload("resnet50_approx", resnet50_sizes(), K=16, ratio=1 / 1024, beta=0.9,
+                                eta=0.1, steps=20, compressor="approx", dist="student_t", nu=3,
+                                scale_lo=1e-5, scale_hi=1e-1),
 }
 
 EXPECTED_D = {"tiny": 1048576, "resnet18": 11173962, "resnet50": 25557032,
-              "rbgs": 25557032, "gpt2": 124439808}
+              "rbgs": 25557032, "gpt2": 124439808, "resnet50_approx": 25557032}
 
 
 def workload(name: str) -> Workload:

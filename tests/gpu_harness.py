@@ -51,6 +51,7 @@ class Case:
     detach: str = ""              # "fused": gmc_step_detach + gmc_finish; "dense": gmc_detach
     eta_fn: Optional[Callable] = None      # t -> eta_t (a schedule)
     finish: bool = False          # server pass through gmc_finish (implied by rule / detach)
+    stratum: int = 100            # sampled-threshold top-s: components per sample stratum
 
 
 def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
@@ -67,11 +68,13 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
                  case.rule, case.lam, case.detach or "-"), flush=True)
     g = Gmc(d, K, comp, wl.ratio, wl.beta, wl.eta, seed=wl.seed,
             segments=None if seg is None else seg.tolist(),
-            block=wl.block if comp == "rbgs" else None, rule=case.rule, lam=case.lam)
+            block=wl.block if comp == "rbgs" else None, rule=case.rule, lam=case.lam,
+            stratum=case.stratum if comp == "approx" else None)
     for opt, val in case.options:
         g.set_option(opt, val)
-    orc = oracle.GmcOracle(d, K, "rbgs" if comp == "rbgs" else "topk", wl.ratio, wl.beta, wl.eta,
-                           seed=wl.seed, seg_off=seg, block=wl.block, variant=case.rule, lam=case.lam)
+    orc = oracle.GmcOracle(d, K, comp if comp in ("rbgs", "approx") else "topk", wl.ratio, wl.beta, wl.eta,
+                           seed=wl.seed, seg_off=seg, block=wl.block, variant=case.rule, lam=case.lam,
+                           stratum=case.stratum)
     use_finish = case.finish or case.rule != "gmc" or bool(case.detach)
     assert g.message_len == orc.message_len and g.index_len == orc.index_len
 
@@ -129,6 +132,9 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
         tag = "%s step %d" % (case.label or wl.name, t)
         assert np.array_equal(ln.cpu().numpy(), ol), tag + ": message lengths"
         gi = idx.cpu().numpy()
+        if comp == "approx":  # variable-length rows: compare the written part
+            gi = np.where(np.arange(gi.shape[1])[None, :] < ol[:, None], gi, 0)
+            oi = np.where(np.arange(oi.shape[1])[None, :] < ol[:, None], oi, 0)
         if not np.array_equal(gi, oi):
             bad = np.argwhere(gi != oi)
             raise AssertionError("%s: indices differ at %d places, first %s (got %d want %d)"

@@ -9,7 +9,8 @@ For each step and two of the K workers (the first and the last):
     the sent components bit for bit, the sent values bit for bit, and the
     residual there is u - u;
   * per segment the message holds exactly k components, ascending, whose
-    keys are the k largest with ties broken towards the lower index;
+    keys are the k largest with ties broken towards the lower index (the
+    sampled-threshold top-s: exactly the oracle's selection on the same u);
 the server update and the apply are compared with the oracle's aggregation
 of all K messages, for every component.  Step 0 takes the full-data
 selection path, later steps the candidate path.  With lambda > 0 (GMC+,
@@ -57,7 +58,7 @@ def check_topk_segment(u: np.ndarray, sel: np.ndarray, k: int, tag: str):
 
 @pytest.mark.parametrize("name,steps,lam", [("tiny", 3, 0.0), ("resnet18", 3, 0.0), ("resnet50", 3, 0.0),
                                             ("rbgs", 3, 0.0), ("gpt2", 2, 0.0), ("rbgs", 3, 0.5),
-                                            ("resnet50", 2, 0.5)])
+                                            ("resnet50", 2, 0.5), ("resnet50_approx", 3, 0.0)])
 def test_full_size_workload(name, steps, lam):
     import torch
     import synth.device as sdev
@@ -67,12 +68,13 @@ def test_full_size_workload(name, steps, lam):
     d, K = wl.d, wl.K
     dev = torch.device("cuda:0")
     rbgs = wl.compressor == "rbgs"
+    approx = wl.compressor == "approx"
     seg = wl.topk_segments()
     g = Gmc(d, K, wl.compressor, wl.ratio, wl.beta, wl.eta, seed=wl.seed,
             segments=seg.tolist() if wl.compressor == "topk_seg" else None,
             block=wl.block if rbgs else None, lam=lam)
-    orc = oracle.GmcOracle(d, K, "rbgs" if rbgs else "topk", wl.ratio, wl.beta, wl.eta, seed=wl.seed,
-                           seg_off=seg, block=wl.block, lam=lam)
+    orc = oracle.GmcOracle(d, K, wl.compressor if (rbgs or approx) else "topk", wl.ratio, wl.beta, wl.eta,
+                           seed=wl.seed, seg_off=seg, block=wl.block, lam=lam)
     print("full size %s: d=%d K=%d %s lambda=%g" % (name, d, K, wl.compressor, lam), flush=True)
     bufs = [sdev.w0(wl, dev), None]
     bufs[1] = bufs[0].clone()
@@ -99,7 +101,7 @@ def test_full_size_workload(name, steps, lam):
             assert all(np.array_equal(gi[k], blocks) for k in range(K)), "RBGS blocks"
             m = sum(min((b + 1) * wl.block, d) - b * wl.block for b in blocks)
             assert np.all(gl == m), "message lengths"
-        else:
+        elif not approx:
             assert np.all(gl == orc.message_len), "message lengths"
         for k in check:
             tag = "%s step %d worker %d" % (name, t, k)
@@ -111,7 +113,11 @@ def test_full_size_workload(name, steps, lam):
             rest = np.ones(d, bool)
             rest[sent] = False
             assert_same_f32(e_after[rest], u[rest], tag + ": residual elsewhere")
-            if not rbgs:
+            if approx:  # the sampled threshold: the oracle's selection on the same u
+                oi_k, ov_k = oracle.compress_approx(u.copy(), wl.seed, t, k, orc.stratum, wl.ratio)
+                assert np.array_equal(sent.astype(np.int64), oi_k.astype(np.int64)), tag + ": kept set"
+                assert_same_f32(gv[k, :int(gl[k])], ov_k, tag + ": kept values")
+            elif not rbgs:
                 for s_i in range(len(orc.seg_off) - 1):
                     a, b = int(orc.seg_off[s_i]), int(orc.seg_off[s_i + 1])
                     sel = sent[(sent >= a) & (sent < b)] - a

@@ -2,6 +2,7 @@
 inputs: every workload shape (shrunk so the oracle finishes in seconds while
 still spanning many chunks, items and ragged tails), both selection paths,
 misaligned rows and the degenerate cases of the method."""
+import dataclasses
 import math
 
 import numpy as np
@@ -184,3 +185,32 @@ def test_lr_in_residual_with_fused_detach():
 def test_eta_schedule(name, shrink, rule):
     wl = W(name).shrunk(shrink, K=4)
     run_lockstep(Case(wl, steps=5, rule=rule, eta_fn=_cosine(wl.eta, 6), label="cosine eta/" + name))
+
+
+# ---------------------------------------------------------------------------
+# the experiments' sampled-threshold top-s (Section 5.1)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shrink,K,stratum", [(16, 4, 100), (64, 6, 7), (256, 3, 1)])
+def test_sampled_threshold_topk(shrink, K, stratum):
+    st = run_lockstep(Case(W("resnet50_approx").shrunk(shrink, K=K), steps=5, stratum=stratum,
+                           label="approx/%d" % stratum))
+    assert st["from_candidates"] > 0, st
+
+
+def test_sampled_threshold_full_data_path():
+    run_lockstep(Case(W("resnet50_approx").shrunk(32, K=4), steps=3, options=((OPT_FULL, 1),),
+                      label="approx full-data"))
+
+
+def test_sampled_threshold_ties_and_zeros():
+    wl = dataclasses.replace(W("resnet50_approx").shrunk(64, K=3), ratio=0.01)
+    quantise = lambda t, g: (np.round(g * 4) / 4).astype(np.float32)
+    run_lockstep(Case(wl, steps=3, grad_hook=quantise, stratum=10, label="approx ties"))
+    run_lockstep(Case(wl, steps=2, grad_hook=lambda t, g: np.zeros_like(g), label="approx zeros"))
+
+
+def test_sampled_threshold_gmcplus_and_rules():
+    wl = W("resnet50_approx").shrunk(64, K=4)
+    run_lockstep(Case(wl, steps=3, lam=0.5, detach="fused", label="approx gmc+"))
+    run_lockstep(Case(wl, steps=3, rule="server_momentum", label="approx server momentum"))
