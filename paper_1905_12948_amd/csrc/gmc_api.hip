@@ -161,6 +161,8 @@ struct TopkTables {
     std::vector<int32_t> slice_seg, slice_rank, seg_slices, seg_slice_lo;
     std::vector<int32_t> pair_k, pair_cap;
     std::vector<int64_t> pair_cand;
+    std::vector<int2> tile_map;       // per worker: tile -> (segment, tile in the segment)
+    std::vector<int32_t> seg_tile_off;
     std::vector<int32_t> gen_list;  // partial chunks and chunks with an unaligned start
     int64_t cand_total = 0;
 };
@@ -208,6 +210,10 @@ TopkTables build_tables(const gmc_ctx* ctx) {
         }
         T.seg_out.push_back((int32_t)out);
         out += ctx->seg_k[sg];
+        // copy tiles: at most cap/kTile whole ones plus a partial one per group
+        const int64_t ntile = (cap + kTile - 1) / kTile + rank;
+        T.seg_tile_off.push_back((int32_t)T.tile_map.size());
+        for (int64_t i = 0; i < ntile; ++i) T.tile_map.push_back(make_int2(sg, (int)i));
     }
     for (int k = 0; k < ctx->K; ++k) {
         for (int sg = 0; sg < n_seg; ++sg) {
@@ -250,6 +256,8 @@ gmc_status prepare(gmc_ctx* ctx) {
         add(nsl, 4); add(nsl, 4); add(ns, 4); add(ns, 4);
         add(np, 4); add(np, 4); add(np, 8);
         add(T.gen_list.size() + 1, 4);
+        add(T.tile_map.size(), sizeof(int2)); add(ns, 4);
+        add((size_t)K * ng, 4); add((size_t)K * T.tile_map.size(), sizeof(int2));
         add(np, sizeof(PairState));
         add(np * kBins, 4);
         add((size_t)K * nc, 4); add((size_t)K * nc, 4); add((size_t)K * ng, 4);
@@ -318,6 +326,13 @@ gmc_status prepare(gmc_ctx* ctx) {
         GMC_TRY(put(T.gen_list, &gl));
         ctx->gen_list = const_cast<int32_t*>(gl);
         ctx->n_gen = (int32_t)T.gen_list.size();
+        int2* tm = cv.take<int2>(T.tile_map.size());
+        GMC_HIP(ctx, hipMemcpy(tm, T.tile_map.data(), T.tile_map.size() * sizeof(int2), hipMemcpyHostToDevice));
+        g.tile_map = tm;
+        g.tiles_per_worker = (int32_t)T.tile_map.size();
+        GMC_TRY(put(T.seg_tile_off, &g.seg_tile_off));
+        ctx->scr.grp_base = cv.take<uint32_t>((size_t)K * ng);
+        ctx->scr.tiles = cv.take<int2>((size_t)K * T.tile_map.size());
         TopkScratch& sc = ctx->scr;
         sc.pair = cv.take<PairState>(np);
         std::vector<PairState> init(np);
@@ -573,7 +588,7 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
             GMC_TRY(prof_end(ctx, 1, ev));
         }
         GMC_TRY(prof_begin(ctx, 2, &ev));
-        GMC_LAUNCH(ctx, launch_topk_compact(ctx->geo, ctx->scr, ctx->stream));
+        GMC_LAUNCH(ctx, launch_topk_compact(a, ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
         for (int pass = 1; pass <= 3; ++pass)
             GMC_LAUNCH(ctx, launch_topk_hist(pass, a, ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
         GMC_LAUNCH(ctx, launch_topk_count(a, ctx->geo, ctx->scr, msg_len_dev, ctx->k_tot, ctx->stream));

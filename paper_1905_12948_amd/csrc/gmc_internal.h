@@ -20,12 +20,12 @@ constexpr int kChunk = kWave * 4 * kVecIters;   // 2048 elements
 
 // Selection: the fused pass leaves each (worker, chunk)'s candidates in the
 // chunk's own staging slot; compaction groups of kCompactChunks chunks pack
-// them, in index order, into the pair's candidate list (each group's copy is
-// split over kCompactParts workgroups).  The histogram, count and emit passes
+// them, in index order, into the pair's candidate list, in tiles of kTile
+// candidates (one workgroup each).  The histogram, count and emit passes
 // read the list (or, on the full-data path, the segment's u) as "slices":
 // seg_slices even shares, one workgroup each.
 constexpr int kCompactChunks = 256;        // chunks per compaction group (one per thread)
-constexpr int kCompactParts = 8;
+constexpr int kTile = kGroup * 8;          // candidates one copy workgroup moves
 constexpr int64_t kSliceElems = 1 << 19;   // full-data elements per slice (at most)
 constexpr int64_t kSliceCands = 8192;      // candidate capacity per slice (at most)
 constexpr int kMaxSlices = 256;
@@ -63,7 +63,10 @@ struct PairState {
     uint32_t done;      // finished workgroups of the current kernel
     uint32_t cand_used; // candidates of this step (cand is reset for the next)
     uint32_t tau_used;  // the candidate threshold this step's fused pass used
-    uint32_t pad[6];
+    uint32_t n_tiles;   // copy tiles of this step's candidate list (0: not copied)
+    uint32_t fuse1;     // 1: the copy kernel also does the first histogram pass
+    uint32_t p1_done;   // 1: it has (the first histogram kernel skips the pair)
+    uint32_t pad[3];
 };
 
 // Static geometry of the top-s selection (built on the host at init).
@@ -91,6 +94,12 @@ struct TopkGeometry {
     const int32_t* pair_k;        // [K*n_seg]
     const int32_t* pair_cap;      // [K*n_seg]
     const int64_t* pair_cand;     // [K*n_seg] start of the pair's candidate list
+    // copy tiles: a worker's tile capacity is tiles_per_worker; tile tt of a
+    // worker belongs to segment tile_map[tt].x as its tile tile_map[tt].y;
+    // the segment's tiles start at seg_tile_off[seg]
+    int32_t tiles_per_worker;
+    const int2* tile_map;         // [tiles_per_worker]
+    const int32_t* seg_tile_off;  // [n_seg]
 };
 
 struct TopkScratch {
@@ -99,6 +108,8 @@ struct TopkScratch {
     uint32_t* run_cnt;            // [K*n_chunks] candidates of (worker, chunk)
     uint32_t* run_pre;            // [K*n_chunks] exclusive prefix of run_cnt within the group
     uint32_t* grp_total;          // [K*n_cgroups]
+    uint32_t* grp_base;           // [K*n_cgroups] the group's first position in the pair's list
+    int2* tiles;                  // [K*tiles_per_worker] (group rank in the segment, tile in the group)
     int2* slot;                   // [K*n_chunks][kChunk] candidates of (worker, chunk) in index
                                   // order: (index, bit pattern of u)
     int32_t* cand_idx;            // [sum cap] candidate lists, ascending index
@@ -162,7 +173,10 @@ hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const
 hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                                  uint64_t vec_mask, const int32_t* gen_list, int32_t n_gen,
                                  hipStream_t st);
-hipError_t launch_topk_compact(const TopkGeometry& g, const TopkScratch& s, hipStream_t st);  // count + copy
+// count + copy; the copy also does the first histogram pass of the pairs
+// that resolve from their candidates (exact top-s)
+hipError_t launch_topk_compact(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int force_full,
+                               int margin, hipStream_t st);
 hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
                             const TopkScratch& s, int force_full, int margin, hipStream_t st);
 hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,

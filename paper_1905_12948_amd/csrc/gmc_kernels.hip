@@ -306,99 +306,6 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
     for (uint32_t q = threadIdx.x; q < total; q += kGroup) sp[q] = stage[q];
 }
 
-// Compaction, first half: the exclusive prefix of the run counts of each
-// group of kCompactChunks chunks, and the group's total.
-__global__ __launch_bounds__(kGroup) void topk_compact_count_kernel(TopkGeometry g, TopkScratch s) {
-    static_assert(kCompactChunks == kGroup, "one chunk per thread");
-    __shared__ uint32_t wsum[kWavesPerGroup];
-    const int k = blockIdx.x / g.n_cgroups;
-    const int cg = blockIdx.x % g.n_cgroups;
-    const int clo = g.cgrp_lo[cg], nch = g.cgrp_hi[cg] - clo;
-    const size_t slot0 = (size_t)k * g.n_chunks + clo;
-    const uint32_t cnt = threadIdx.x < nch ? s.run_cnt[slot0 + threadIdx.x] : 0u;
-    uint32_t total;
-    const uint32_t pre = block_scan_excl(cnt, &total, wsum);
-    if (threadIdx.x < nch) s.run_pre[slot0 + threadIdx.x] = pre;
-    if (threadIdx.x == 0) s.grp_total[(size_t)k * g.n_cgroups + cg] = total;
-}
-
-// Compaction, second half: group cg of a segment starts at the sum of the
-// totals of the segment's earlier groups, so the pair's candidate list comes
-// out in ascending index order.  Each group's copy is split over
-// kCompactParts workgroups.  The first workgroup of a segment also publishes
-// the pair's candidate count.  A pair whose candidates exceed its capacity
-// is not copied (it takes the full-data path).
-__global__ __launch_bounds__(kGroup) void topk_compact_copy_kernel(TopkGeometry g, TopkScratch s) {
-    __shared__ uint32_t pre[kCompactChunks + 1];
-    __shared__ uint32_t wsum[kWavesPerGroup];
-    const int part = blockIdx.x % kCompactParts;
-    const int rest = blockIdx.x / kCompactParts;
-    const int k = rest / g.n_cgroups;
-    const int cg = rest % g.n_cgroups;
-    const int seg = g.cgrp_seg[cg];
-    const int p = k * g.n_seg + seg;
-    const int rank = g.cgrp_rank[cg];
-    const size_t grp0 = (size_t)k * g.n_cgroups + g.seg_cgrp_lo[seg];
-    uint32_t before = 0, all = 0;
-    for (int r0 = 0; r0 < g.seg_cgrps[seg]; r0 += kGroup) {
-        const int r = r0 + threadIdx.x;
-        const uint32_t t = r < g.seg_cgrps[seg] ? s.grp_total[grp0 + r] : 0u;
-        uint32_t tot;
-        const uint32_t ex = block_scan_excl(t, &tot, wsum);
-        if (r == rank) pre[kCompactChunks] = all + ex;  // temporarily: this group's base
-        all += tot;
-    }
-    __syncthreads();
-    before = pre[kCompactChunks];
-    if (rank == 0 && part == 0 && threadIdx.x == 0) s.pair[p].cand = all;
-    const uint32_t total = s.grp_total[grp0 + rank];
-    if (all > (uint32_t)g.pair_cap[p] || total == 0) return;
-    const uint32_t lo = (uint32_t)((uint64_t)total * part / kCompactParts);
-    const uint32_t hi = (uint32_t)((uint64_t)total * (part + 1) / kCompactParts);
-    if (lo == hi) return;
-    const int clo = g.cgrp_lo[cg], nch = g.cgrp_hi[cg] - clo;
-    const size_t slot0 = (size_t)k * g.n_chunks + clo;
-    __syncthreads();
-    if (threadIdx.x < nch) pre[threadIdx.x] = s.run_pre[slot0 + threadIdx.x];
-    __syncthreads();
-    int32_t* ci = s.cand_idx + g.pair_cand[p] + before;
-    float* cv = s.cand_val + g.pair_cand[p] + before;
-    for (uint32_t q0 = lo; q0 < hi; q0 += kGroup * 8) {
-        int32_t jv[8];
-        float xv[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const uint32_t q = q0 + i * kGroup + threadIdx.x;
-            if (q < hi) {
-                int a = 0, b = nch - 1;  // chunk c with pre[c] <= q < pre[c+1]
-                while (a < b) {
-                    const int mid = (a + b + 1) >> 1;
-                    if (pre[mid] <= q) a = mid; else b = mid - 1;
-                }
-                const int2 c = s.slot[(slot0 + a) * kChunk + (q - pre[a])];
-                jv[i] = c.x;
-                xv[i] = __int_as_float(c.y);
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const uint32_t q = q0 + i * kGroup + threadIdx.x;
-            if (q < hi) {
-                ci[q] = jv[i];
-                cv[q] = xv[i];
-            }
-        }
-    }
-}
-
-hipError_t launch_topk_compact(const TopkGeometry& g, const TopkScratch& s, hipStream_t st) {
-    hipLaunchKernelGGL(topk_compact_count_kernel, dim3(g.K * g.n_cgroups), dim3(kGroup), 0, st, g, s);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(topk_compact_copy_kernel, dim3(g.K * g.n_cgroups * kCompactParts), dim3(kGroup), 0, st, g,
-                       s);
-    return hipGetLastError();
-}
 
 // Element-wise path for the (chunk, worker) pairs the vector kernel skips:
 // partial chunks (a segment's last), chunks with an unaligned start, and
@@ -636,45 +543,14 @@ __device__ __forceinline__ bool finish_slice(uint32_t* done, int W, int* sh_flag
 // histogram passes: 11 + 11 + 9 bits of the 31-bit magnitude key
 // ----------------------------------------------------------------------------
 
+// The last workgroup of a pair after a histogram pass: reads and clears the
+// pair's global histogram, picks the digit and updates the pair's state; pass
+// 1 also sets the next step's candidate threshold.  h: [kBins] in LDS.
 template <int PASS>
-__global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
-                                                           int force_full, int margin) {
+__device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, int kp, int mode, uint32_t cand,
+                             uint32_t prefix, int margin, int force_full, bool approx, const TopkGeometry& g,
+                             const TopkScratch& s, uint32_t* sh_wsum, int* sh_res) {
     constexpr int nbins = PASS == 3 ? 512 : kBins;
-    __shared__ uint32_t h[kBins];
-    __shared__ uint32_t sh_wsum[kWavesPerGroup];
-    __shared__ int sh_res[2];
-    __shared__ int sh_last;
-
-    const SliceId id = slice_id(g);
-    PairState* ps = &s.pair[id.p];
-    // sampled-threshold top-s: the passes select over the sample, rank samp_r
-    const bool approx = g.approx != 0;
-    const int kp = approx ? g.samp_r : g.pair_k[id.p];
-    const uint32_t cand = PASS == 1 ? ps->cand : ps->cand_used;
-    const int mode = approx      ? 2
-                     : PASS == 1 ? ((force_full || cand < (uint32_t)kp || cand > (uint32_t)g.pair_cap[id.p]) ? 1 : 0)
-                                 : ps->mode;
-    const uint32_t prefix = PASS == 1 ? 0u : ps->prefix;
-
-    for (int b = threadIdx.x; b < nbins; b += kGroup) h[b] = 0u;
-    __syncthreads();
-    const Slice v = open_slice(mode, cand, id.k, id.seg, id.p, id.w, id.W, a, g, s);
-    for_slice<false>(v, [&](uint32_t key, int32_t) {
-        if (PASS == 1) {
-            atomicAdd(&h[key >> kShift1], 1u);
-        } else if (PASS == 2) {
-            if ((key >> kShift1) == prefix) atomicAdd(&h[(key >> kShift2) & (kBins - 1)], 1u);
-        } else {
-            if ((key >> kShift2) == prefix) atomicAdd(&h[key & 511u], 1u);
-        }
-    });
-    __syncthreads();
-    uint32_t* gh = s.hist + (size_t)id.p * kBins;
-    for (int b = threadIdx.x; b < nbins; b += kGroup)
-        if (h[b]) atomicAdd(&gh[b], h[b]);
-    if (!finish_slice(&ps->done, id.W, &sh_last)) return;
-
-    // last workgroup of the pair: read and clear the histogram, pick the digit
     for (int b = threadIdx.x; b < nbins; b += kGroup) {
         h[b] = load_agent(&gh[b]);
         store_agent(&gh[b], 0u);
@@ -728,7 +604,7 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
                 // the fused pass collected with and none were dropped
                 ps->r = 0x7fffffff;
                 const uint32_t cu = ps->cand_used;
-                const int m = (!force_full && T >= ps->tau_used && cu <= (uint32_t)g.pair_cap[id.p]) ? 0 : 1;
+                const int m = (!force_full && T >= ps->tau_used && cu <= (uint32_t)g.pair_cap[p]) ? 0 : 1;
                 ps->mode = m;
                 atomicAdd((unsigned long long*)&s.stats[m == 0 ? 1 : 2], 1ull);
                 if (m == 0) atomicAdd((unsigned long long*)&s.stats[3], (unsigned long long)cu);
@@ -736,6 +612,48 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
         }
         store_agent(&ps->done, 0u);
     }
+}
+
+template <int PASS>
+__global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
+                                                           int force_full, int margin) {
+    constexpr int nbins = PASS == 3 ? 512 : kBins;
+    __shared__ uint32_t h[kBins];
+    __shared__ uint32_t sh_wsum[kWavesPerGroup];
+    __shared__ int sh_res[2];
+    __shared__ int sh_last;
+
+    const SliceId id = slice_id(g);
+    PairState* ps = &s.pair[id.p];
+    if (PASS == 1 && ps->p1_done) return;  // the compaction took this pass
+    // sampled-threshold top-s: the passes select over the sample, rank samp_r
+    const bool approx = g.approx != 0;
+    const int kp = approx ? g.samp_r : g.pair_k[id.p];
+    const uint32_t cand = PASS == 1 ? ps->cand : ps->cand_used;
+    const int mode = approx      ? 2
+                     : PASS == 1 ? ((force_full || cand < (uint32_t)kp || cand > (uint32_t)g.pair_cap[id.p]) ? 1 : 0)
+                                 : ps->mode;
+    const uint32_t prefix = PASS == 1 ? 0u : ps->prefix;
+
+    for (int b = threadIdx.x; b < nbins; b += kGroup) h[b] = 0u;
+    __syncthreads();
+    const Slice v = open_slice(mode, cand, id.k, id.seg, id.p, id.w, id.W, a, g, s);
+    for_slice<false>(v, [&](uint32_t key, int32_t) {
+        if (PASS == 1) {
+            atomicAdd(&h[key >> kShift1], 1u);
+        } else if (PASS == 2) {
+            if ((key >> kShift1) == prefix) atomicAdd(&h[(key >> kShift2) & (kBins - 1)], 1u);
+        } else {
+            if ((key >> kShift2) == prefix) atomicAdd(&h[key & 511u], 1u);
+        }
+    });
+    __syncthreads();
+    uint32_t* gh = s.hist + (size_t)id.p * kBins;
+    for (int b = threadIdx.x; b < nbins; b += kGroup)
+        if (h[b]) atomicAdd(&gh[b], h[b]);
+    if (!finish_slice(&ps->done, id.W, &sh_last)) return;
+
+    finish_digit<PASS>(ps, id.p, h, gh, kp, mode, cand, prefix, margin, force_full, approx, g, s, sh_wsum, sh_res);
 }
 
 hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
@@ -747,6 +665,159 @@ hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
         hipLaunchKernelGGL(topk_hist_kernel<2>, dim3(grid), dim3(kGroup), 0, st, a, g, s, force_full, margin);
     else
         hipLaunchKernelGGL(topk_hist_kernel<3>, dim3(grid), dim3(kGroup), 0, st, a, g, s, force_full, margin);
+    return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
+// compaction of the candidates
+// ----------------------------------------------------------------------------
+
+// First half, one workgroup per (worker, compaction group): the exclusive
+// prefix of the group's run counts and the group's total.  The last
+// workgroup of each (worker, segment) then scans the segment's group totals
+// (each group's base in the pair's list, the pair's count), decides whether
+// the list is copied (at most the capacity) and whether the copy also takes
+// the first histogram pass (exact top-s resolving from its candidates), and
+// lays out the copy tiles.
+__global__ __launch_bounds__(kGroup) void topk_compact_count_kernel(TopkGeometry g, TopkScratch s, int force_full) {
+    static_assert(kCompactChunks == kGroup, "one chunk per thread");
+    __shared__ uint32_t wsum[kWavesPerGroup];
+    __shared__ uint32_t carry[2];
+    __shared__ int sh_last;
+    const int k = blockIdx.x / g.n_cgroups;
+    const int cg = blockIdx.x % g.n_cgroups;
+    const int clo = g.cgrp_lo[cg], nch = g.cgrp_hi[cg] - clo;
+    const size_t slot0 = (size_t)k * g.n_chunks + clo;
+    const uint32_t cnt = threadIdx.x < nch ? s.run_cnt[slot0 + threadIdx.x] : 0u;
+    uint32_t total;
+    const uint32_t pre = block_scan_excl(cnt, &total, wsum);
+    if (threadIdx.x < nch) s.run_pre[slot0 + threadIdx.x] = pre;
+    if (threadIdx.x == 0) store_agent(&s.grp_total[(size_t)k * g.n_cgroups + cg], total);
+    const int seg = g.cgrp_seg[cg];
+    const int p = k * g.n_seg + seg;
+    PairState* ps = &s.pair[p];
+    const int ng = g.seg_cgrps[seg];
+    if (!finish_slice(&ps->done, ng, &sh_last)) return;
+
+    // last workgroup of the pair
+    const size_t grp0 = (size_t)k * g.n_cgroups + g.seg_cgrp_lo[seg];
+    if (threadIdx.x == 0) carry[0] = 0u;
+    __syncthreads();
+    for (int r0 = 0; r0 < ng; r0 += kGroup) {
+        const int r = r0 + threadIdx.x;
+        const uint32_t t = r < ng ? load_agent(&s.grp_total[grp0 + r]) : 0u;
+        uint32_t tot;
+        const uint32_t ex = block_scan_excl(t, &tot, wsum);
+        if (r < ng) s.grp_base[grp0 + r] = carry[0] + ex;
+        __syncthreads();
+        if (threadIdx.x == 0) carry[0] += tot;
+        __syncthreads();
+    }
+    const uint32_t all = carry[0];
+    const bool copy = all <= (uint32_t)g.pair_cap[p];
+    const bool fuse = !g.approx && !force_full && copy && all >= (uint32_t)g.pair_k[p];
+    int2* tl = s.tiles + (size_t)k * g.tiles_per_worker + g.seg_tile_off[seg];
+    if (threadIdx.x == 0) carry[1] = 0u;
+    __syncthreads();
+    for (int r0 = 0; r0 < ng; r0 += kGroup) {
+        const int r = r0 + threadIdx.x;
+        const uint32_t t = r < ng && copy ? load_agent(&s.grp_total[grp0 + r]) : 0u;
+        const uint32_t nt = (t + kTile - 1) / kTile;
+        uint32_t tot;
+        const uint32_t ex = carry[1] + block_scan_excl(nt, &tot, wsum);
+        for (uint32_t i = 0; i < nt; ++i) tl[ex + i] = make_int2(r, (int)i);
+        __syncthreads();
+        if (threadIdx.x == 0) carry[1] += tot;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        ps->cand = all;
+        ps->n_tiles = carry[1];
+        ps->fuse1 = fuse ? 1u : 0u;
+        ps->p1_done = 0u;
+        store_agent(&ps->done, 0u);
+    }
+}
+
+// Second half, one workgroup per (worker, tile): the tile's kTile candidates
+// of one group go to the pair's list at the group's base, so the list comes
+// out in ascending index order.  For the pairs of exact top-s that resolve
+// from their candidates the copy also histograms the first digit, and its
+// last workgroup picks it (the first histogram kernel then skips the pair).
+__global__ __launch_bounds__(kGroup) void topk_compact_copy_kernel(TopkGeometry g, TopkScratch s, int margin) {
+    __shared__ uint32_t pre[kCompactChunks];
+    __shared__ uint32_t h[kBins];
+    __shared__ uint32_t sh_wsum[kWavesPerGroup];
+    __shared__ int sh_res[2];
+    __shared__ int sh_last;
+    const int k = blockIdx.x / g.tiles_per_worker;
+    const int2 tm = g.tile_map[blockIdx.x % g.tiles_per_worker];
+    const int seg = tm.x;
+    const int p = k * g.n_seg + seg;
+    PairState* ps = &s.pair[p];
+    const uint32_t n_tiles = ps->n_tiles;
+    if ((uint32_t)tm.y >= n_tiles) return;
+    const bool fuse = ps->fuse1 != 0u;
+    const int2 te = s.tiles[(size_t)k * g.tiles_per_worker + g.seg_tile_off[seg] + tm.y];
+    const int cg = g.seg_cgrp_lo[seg] + te.x;
+    const int clo = g.cgrp_lo[cg], nch = g.cgrp_hi[cg] - clo;
+    const size_t gi = (size_t)k * g.n_cgroups + cg;
+    const uint32_t total = s.grp_total[gi], base = s.grp_base[gi];
+    const uint32_t lo = (uint32_t)te.y * kTile;
+    const uint32_t hi = lo + kTile < total ? lo + kTile : total;
+    const size_t slot0 = (size_t)k * g.n_chunks + clo;
+    if (threadIdx.x < nch) pre[threadIdx.x] = s.run_pre[slot0 + threadIdx.x];
+    if (fuse)
+        for (int b = threadIdx.x; b < kBins; b += kGroup) h[b] = 0u;
+    __syncthreads();
+    int32_t* ci = s.cand_idx + g.pair_cand[p] + base;
+    float* cv = s.cand_val + g.pair_cand[p] + base;
+    int32_t jv[8];
+    float xv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const uint32_t q = lo + i * kGroup + threadIdx.x;
+        jv[i] = 0;
+        xv[i] = 0.0f;
+        if (q < hi) {
+            int a0 = 0, a1 = nch - 1;  // chunk c with pre[c] <= q < pre[c+1]
+            while (a0 < a1) {
+                const int mid = (a0 + a1 + 1) >> 1;
+                if (pre[mid] <= q) a0 = mid; else a1 = mid - 1;
+            }
+            const int2 c = s.slot[(slot0 + a0) * kChunk + (q - pre[a0])];
+            jv[i] = c.x;
+            xv[i] = __int_as_float(c.y);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const uint32_t q = lo + i * kGroup + threadIdx.x;
+        if (q < hi) {
+            ci[q] = jv[i];
+            cv[q] = xv[i];
+            if (fuse) atomicAdd(&h[key_of(xv[i]) >> kShift1], 1u);
+        }
+    }
+    if (!fuse) return;
+    __syncthreads();
+    uint32_t* gh = s.hist + (size_t)p * kBins;
+    for (int b = threadIdx.x; b < kBins; b += kGroup)
+        if (h[b]) atomicAdd(&gh[b], h[b]);
+    if (!finish_slice(&ps->done, (int)n_tiles, &sh_last)) return;
+    const uint32_t cand = ps->cand;
+    finish_digit<1>(ps, p, h, gh, g.pair_k[p], 0, cand, 0u, margin, 0, false, g, s, sh_wsum, sh_res);
+    if (threadIdx.x == 0) ps->p1_done = 1u;
+}
+
+hipError_t launch_topk_compact(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int force_full,
+                               int margin, hipStream_t st) {
+    (void)a;
+    hipLaunchKernelGGL(topk_compact_count_kernel, dim3(g.K * g.n_cgroups), dim3(kGroup), 0, st, g, s, force_full);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(topk_compact_copy_kernel, dim3((unsigned)((int64_t)g.K * g.tiles_per_worker)), dim3(kGroup),
+                       0, st, g, s, margin);
     return hipGetLastError();
 }
 
