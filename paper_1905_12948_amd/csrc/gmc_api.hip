@@ -61,8 +61,6 @@ struct gmc_ctx {
     TopkScratch scr{};
     int32_t* rowptr = nullptr;
     int32_t n_ranges = 0;
-    int32_t* gen_list = nullptr;   // chunks the vector pass cannot take
-    int32_t n_gen = 0;
     uint32_t* rbgs_bitmap = nullptr;
     int32_t* rbgs_blocks = nullptr;
     int32_t* rbgs_slot = nullptr;
@@ -163,7 +161,6 @@ struct TopkTables {
     std::vector<int64_t> pair_cand;
     std::vector<int2> tile_map;       // per worker: tile -> (segment, tile in the segment)
     std::vector<int32_t> seg_tile_off;
-    std::vector<int32_t> gen_list;  // partial chunks and chunks with an unaligned start
     int64_t cand_total = 0;
 };
 
@@ -182,7 +179,6 @@ TopkTables build_tables(const gmc_ctx* ctx) {
         const int32_t first_chunk = (int32_t)T.chunk_start.size();
         for (int64_t a = lo; a < hi; a += kChunk) {
             const int32_t len = (int32_t)std::min<int64_t>(kChunk, hi - a);
-            if ((a & 3) != 0 || len != kChunk) T.gen_list.push_back((int32_t)T.chunk_start.size());
             T.chunk_start.push_back((int32_t)a);
             T.chunk_len.push_back(len);
             T.chunk_seg.push_back(sg);
@@ -255,7 +251,6 @@ gmc_status prepare(gmc_ctx* ctx) {
         add(ng, 4); add(ng, 4); add(ng, 4); add(ng, 4); add(ns, 4); add(ns, 4);
         add(nsl, 4); add(nsl, 4); add(ns, 4); add(ns, 4);
         add(np, 4); add(np, 4); add(np, 8);
-        add(T.gen_list.size() + 1, 4);
         add(T.tile_map.size(), sizeof(int2)); add(ns, 4);
         add((size_t)K * ng, 4); add((size_t)K * T.tile_map.size(), sizeof(int2));
         add(np, sizeof(PairState));
@@ -322,10 +317,6 @@ gmc_status prepare(gmc_ctx* ctx) {
         int64_t* pcd = cv.take<int64_t>(np);
         GMC_HIP(ctx, hipMemcpy(pcd, T.pair_cand.data(), np * 8, hipMemcpyHostToDevice));
         g.pair_cand = pcd;
-        const int32_t* gl = nullptr;
-        GMC_TRY(put(T.gen_list, &gl));
-        ctx->gen_list = const_cast<int32_t*>(gl);
-        ctx->n_gen = (int32_t)T.gen_list.size();
         int2* tm = cv.take<int2>(T.tile_map.size());
         GMC_HIP(ctx, hipMemcpy(tm, T.tile_map.data(), T.tile_map.size() * sizeof(int2), hipMemcpyHostToDevice));
         g.tile_map = tm;
@@ -574,9 +565,12 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
         for (int k = 0; k < ctx->K && w_ok; ++k)
             if ((((uintptr_t)grads_dev[k] | (uintptr_t)err_dev[k] | (uintptr_t)a.wp.y[k]) & 15u) == 0)
                 vec_mask |= 1ull << k;
+        // the vector kernel takes every chunk of the workers in vec_mask
+        // (partial and unaligned ones element-wise); the element-wise kernel
+        // every chunk of the others
         const uint64_t all = ctx->K == 64 ? ~0ull : ((1ull << ctx->K) - 1ull);
-        const int32_t* gl = vec_mask == all ? ctx->gen_list : nullptr;
-        const int32_t ng = vec_mask == all ? ctx->n_gen : ctx->geo.n_chunks;
+        const int32_t* gl = nullptr;
+        const int32_t ng = vec_mask == all ? 0 : ctx->geo.n_chunks;
         if (vec_mask) {
             GMC_TRY(prof_begin(ctx, 0, &ev));
             GMC_LAUNCH(ctx, launch_topk_fused_vec(a, ctx->geo, ctx->scr, vec_mask, ctx->stream));

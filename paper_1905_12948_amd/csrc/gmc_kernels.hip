@@ -201,6 +201,9 @@ __device__ __forceinline__ void store_agent(uint32_t* p, uint32_t v) {
 // streaming pass takes no atomics; the compaction kernel packs the slots.
 // ---------------------------------------------------------------------------
 
+__device__ void fused_chunk_wave(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int chunk,
+                                 int k);
+
 template <int kRule, bool kDetach, bool kApprox>
 __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                                 uint64_t vec_mask) {
@@ -212,7 +215,10 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
     const bool one = g.n_seg == 1;
     const int start = one ? chunk * kChunk : g.chunk_start[chunk];
     const int len = one ? min(kChunk, a.d - start) : g.chunk_len[chunk];
-    if ((start & 3) != 0 || len != kChunk) return;  // the element-wise kernel's
+    if ((start & 3) != 0 || len != kChunk) {  // partial or unaligned chunk: element-wise, one wavefront
+        if (threadIdx.x < kWave) fused_chunk_wave(a, g, s, chunk, k);
+        return;
+    }
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
     const int seg = one ? 0 : g.chunk_seg[chunk];
     const int p = k * g.n_seg + seg;
@@ -307,22 +313,14 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
 }
 
 
-// Element-wise path for the (chunk, worker) pairs the vector kernel skips:
-// partial chunks (a segment's last), chunks with an unaligned start, and
-// workers (or w) whose rows are not 16-byte aligned.  One wavefront per (chunk, worker);
-// `list` holds the chunk ids to visit (NULL: every chunk).
-__global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
-                                                                uint64_t vec_mask, const int32_t* list,
-                                                                int32_t n_list) {
+// Element-wise pass of one wavefront over one (chunk, worker): the chunks the
+// vector path cannot take (a segment's partial last chunk, chunks with an
+// unaligned start) and the workers whose rows are not 16-byte aligned.
+__device__ void fused_chunk_wave(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int chunk,
+                                 int k) {
     const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x >> 6;
-    const int64_t wid = (int64_t)blockIdx.x * kWavesPerGroup + wave;
-    if (wid >= (int64_t)n_list * g.K) return;  // wave-uniform; no workgroup barrier below
-    const int li = (int)(wid / g.K), k = (int)(wid % g.K);
-    const int chunk = list ? list[li] : li;
     const int start = g.chunk_start[chunk];
     const int len = g.chunk_len[chunk];
-    if ((start & 3) == 0 && len == kChunk && ((vec_mask >> k) & 1ull)) return;  // the vector kernel's
     const int seg = g.chunk_seg[chunk];
     const float c = a.c;
     constexpr int kIt = kChunk / kWave;  // 32
@@ -362,6 +360,21 @@ __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, Topk
         base += popc64(b);
     }
     if (lane == 0) s.run_cnt[run_slot] = base;
+}
+
+// The element-wise kernel: one wavefront per (chunk, worker) for the workers
+// outside vec_mask (the vector kernel takes every chunk of the others,
+// partial ones included); `list` holds the chunk ids to visit (NULL: every
+// chunk).
+__global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
+                                                                uint64_t vec_mask, const int32_t* list,
+                                                                int32_t n_list) {
+    const int wave = threadIdx.x >> 6;
+    const int64_t wid = (int64_t)blockIdx.x * kWavesPerGroup + wave;
+    if (wid >= (int64_t)n_list * g.K) return;  // wave-uniform; no workgroup barrier below
+    const int li = (int)(wid / g.K), k = (int)(wid % g.K);
+    if ((vec_mask >> k) & 1ull) return;  // the vector kernel's
+    fused_chunk_wave(a, g, s, list ? list[li] : li, k);
 }
 
 template <bool kApprox>
@@ -421,7 +434,7 @@ hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const
 namespace {
 
 constexpr int kSliceLoads = 16;      // independent loads in flight per thread
-constexpr int kEmitLoads = 4;        // staged elements per thread in the emit pass
+constexpr int kEmitLoads = 12;       // staged elements per thread in the emit pass
 constexpr int kEmitStage = kGroup * kEmitLoads;  // elements staged in LDS per round
 
 // A workgroup's slice of a pair's selection input.
@@ -551,9 +564,15 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
                              uint32_t prefix, int margin, int force_full, bool approx, const TopkGeometry& g,
                              const TopkScratch& s, uint32_t* sh_wsum, int* sh_res) {
     constexpr int nbins = PASS == 3 ? 512 : kBins;
-    for (int b = threadIdx.x; b < nbins; b += kGroup) {
-        h[b] = load_agent(&gh[b]);
-        store_agent(&gh[b], 0u);
+    constexpr int per = nbins / kGroup;
+    // all of this thread's loads in flight at once, then the clears
+    uint32_t v[per];
+#pragma unroll
+    for (int i = 0; i < per; ++i) v[i] = load_agent(&gh[threadIdx.x + i * kGroup]);
+#pragma unroll
+    for (int i = 0; i < per; ++i) {
+        h[threadIdx.x + i * kGroup] = v[i];
+        store_agent(&gh[threadIdx.x + i * kGroup], 0u);
     }
     __syncthreads();
     const uint32_t need = PASS == 1 ? (uint32_t)kp : (uint32_t)ps->need;
@@ -922,15 +941,17 @@ hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const Top
 // of kEmitStage (coalesced loads, all in flight together); in a round each
 // thread owns kEmitLoads consecutive elements, one block-wide scan of its
 // (above, tie) counts places them, and the thread writes its kept ones in
-// order.  LDS rows are padded by one word per kEmitLoads entries so that the
-// threads' strided reads hit distinct banks.
+// order.  LDS rows are padded by one word per 4 entries, so consecutive
+// threads' rows start an odd number of words apart and their strided reads
+// hit distinct banks.
 // ----------------------------------------------------------------------------
 
 __device__ __forceinline__ int stage_slot(int q) { return q + (q >> 2); }
 
 __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                            int32_t* idx, float* val, int64_t row_len) {
-    static_assert(kEmitLoads == 4, "stage_slot pads every 4 entries");
+    static_assert(kEmitLoads % 4 == 0 && (kEmitLoads + kEmitLoads / 4) % 2 == 1,
+                  "one pad word per 4 entries; each thread's row then starts an odd number of words on");
     constexpr int kStageSlots = kEmitStage + kEmitStage / 4;
     __shared__ int32_t st_idx[kStageSlots];
     __shared__ float st_val[kStageSlots];
