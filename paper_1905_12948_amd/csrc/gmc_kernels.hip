@@ -1240,9 +1240,27 @@ __global__ __launch_bounds__(kGroup) void rbgs_vec_kernel(StepArgs a, int32_t K,
                                                           uint64_t vec_mask) {
     int chunk, k;
     run_order(blockIdx.x, K, &chunk, &k);
-    if ((int64_t)chunk >= (int64_t)a.d / kChunk || !((vec_mask >> k) & 1ull)) return;  // padding, or the element-wise kernel's
+    const int64_t chunk0 = (int64_t)chunk * kChunk;
+    if (chunk0 >= a.d || !((vec_mask >> k) & 1ull)) return;  // padding, or the element-wise kernel's
+    if (chunk0 + kChunk > a.d) {  // the partial last chunk, element by element
+        const float wq = a.q;
+        for (int64_t j = chunk0 + threadIdx.x; j < a.d; j += kGroup) {
+            const int32_t b = (int32_t)(j / B);
+            const int32_t slot = block_slot[b];
+            const float wtj = a.w_t[j], wpj = a.w_prev[j];
+            const float u = rule_u<kRule>(a.wp.e[k][j], a.wp.g[k][j], wtj, wpj, a.c, a.h);
+            if (slot >= 0) {
+                val[(size_t)k * val_row + (int64_t)slot * B + (j - (int64_t)b * B)] = u;
+                a.wp.e[k][j] = u - u;
+            } else {
+                a.wp.e[k][j] = u;
+                if (kDetach) a.wp.y[k][j] = detached(wtj, u, wq);
+            }
+        }
+        return;
+    }
     const int o0 = threadIdx.x * 4;
-    const int64_t start = (int64_t)chunk * kChunk + o0;
+    const int64_t start = chunk0 + o0;
     float* ep = a.wp.e[k] + start;
     const float* gp = a.wp.g[k] + start;
     constexpr bool kNeedW = kRule != kRuleServerMomentum || kDetach;
@@ -1286,13 +1304,14 @@ __global__ __launch_bounds__(kGroup) void rbgs_vec_kernel(StepArgs a, int32_t K,
 
 hipError_t launch_rbgs_fused(const StepArgs& a, int32_t K, int32_t B, const int32_t* block_slot,
                              float* val, int64_t val_row, uint64_t vec_mask, hipStream_t st) {
-    // vector kernel over the whole chunks for the workers in vec_mask (B a
-    // multiple of 4 and the message rows 16-byte aligned, checked by the
-    // caller), element-wise kernel for the rest
-    const int64_t n_full = vec_mask ? (int64_t)a.d / kChunk : 0;
-    const int64_t vec_end = n_full * kChunk;
-    if (n_full > 0) {
-        const dim3 grid((unsigned)run_order_grid(n_full, K));
+    // vector kernel over all chunks (the partial last one element by
+    // element) for the workers in vec_mask (B a multiple of 4 and the message
+    // rows 16-byte aligned, checked by the caller), element-wise kernel for
+    // the rest
+    const int64_t n_chunks = vec_mask ? ((int64_t)a.d + kChunk - 1) / kChunk : 0;
+    const int64_t vec_end = vec_mask ? (int64_t)a.d : 0;
+    if (n_chunks > 0) {
+        const dim3 grid((unsigned)run_order_grid(n_chunks, K));
         if (a.rule == kRuleServerMomentum) {
             if (a.detach) return hipErrorInvalidValue;
             hipLaunchKernelGGL((rbgs_vec_kernel<kRuleServerMomentum, false>), grid, dim3(kGroup), 0, st, a, K, B,
@@ -1316,9 +1335,9 @@ hipError_t launch_rbgs_fused(const StepArgs& a, int32_t K, int32_t B, const int3
         if (e != hipSuccess) return e;
     }
     const uint64_t all = K == 64 ? ~0ull : ((1ull << K) - 1ull);
-    const int64_t j_begin = vec_mask == all ? vec_end : 0;
+    if (vec_mask == all) return hipSuccess;
+    const int64_t j_begin = 0;
     const int64_t threads = ((int64_t)a.d - j_begin + 3) / 4;
-    if (threads <= 0) return hipSuccess;
     const int grid = (int)((threads + kGroup - 1) / kGroup);
     hipLaunchKernelGGL(rbgs_fused_kernel, dim3(grid), dim3(kGroup), 0, st, a, K, B, block_slot, val, val_row,
                        j_begin, vec_mask, vec_end);
