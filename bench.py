@@ -65,30 +65,36 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def algorithmic_bytes(wl, msg_len: int, detach: bool) -> dict:
+def algorithmic_bytes(wl, msg_len: int, detach: bool, sparse_w: bool = False) -> dict:
     """Bytes one step must move (per step, whole job), and those of the fused
     worker pass alone.  top-s: read g, read e, write e (12 B per worker-
     element); read w_t, w_prev for the momentum term and read + write w in
     the apply (16 B per element); write (idx, val) and read them back in the
     aggregation (16 B per message entry).  RBGS sends values only (8 B).
-    GMC+'s detached points add one write per worker-element (4 B)."""
+    GMC+'s detached points add one write per worker-element (4 B).
+
+    With the sparse momentum term (w_t - w_prev is +0 off the components the
+    last server pass changed) the worker pass reads, instead of w_t and
+    w_prev, the server pass's bitmap (d/8 B, written once and read once) and
+    w_t, w_prev at the changed components: at most the K message entries
+    (8 B each).  GMC+'s detached points still read w_t (4 B per element)."""
     K, d = wl.K, wl.d
-    if wl.compressor == "rbgs":
-        step = 12 * K * d + 16 * d + 8 * K * msg_len
-        fused = 12 * K * d + 8 * d + 4 * K * msg_len
-    else:
-        step = 12 * K * d + 16 * d + 16 * K * msg_len
-        fused = 12 * K * d + 8 * d
+    per_msg = 8 if wl.compressor == "rbgs" else 16
+    w_momentum = 8 * d
+    if sparse_w:
+        w_momentum = d // 8 + 8 * K * msg_len + (4 * d if detach else 0)
+    step = 12 * K * d + w_momentum + 8 * d + per_msg * K * msg_len + (d // 8 if sparse_w else 0)
+    fused = 12 * K * d + w_momentum + (4 * K * msg_len if wl.compressor == "rbgs" else 0)
     if detach:
         step += 4 * K * d
         fused += 4 * K * d
     return {"step": step, "fused": fused}
 
 
-def read_pmc_summary():
+def read_pmc_summary(sparse_w: bool = True):
     """Per-dispatch HBM traffic of the fused kernel from the committed
     rocprofv3 counter summary, scaled by the copy-kernel calibration; None if
-    absent or taken on different kernel sources."""
+    absent, taken on different kernel sources or in the other momentum mode."""
     if not os.path.exists(PMC_SUMMARY):
         return None
     kv = {}
@@ -99,6 +105,8 @@ def read_pmc_summary():
                 kv[k.strip()] = v.strip()
     try:
         if kv.get("kernel_source_sha256") != kernel_source_hash():
+            return None
+        if kv.get("sparse_momentum", "0") != ("1" if sparse_w else "0"):
             return None
         fs = float(kv["copy_bytes"]) / (float(kv["copy_fetch_kib"]) * 1024.0)
         ws = float(kv["copy_bytes"]) / (float(kv["copy_write_kib"]) * 1024.0)
@@ -151,6 +159,8 @@ def main():
                     help="candidate margin (multiple of k) of the speculative selection")
     ap.add_argument("--lam", type=float, default=None,
                     help="GMC+ detach coefficient (default 0.5 for the rbgs workload, else 0: plain GMC)")
+    ap.add_argument("--dense-momentum", action="store_true",
+                    help="read w_t and w_prev everywhere (no GMC_OPT_SPARSE_MOMENTUM)")
     ap.add_argument("--cpu-workers", type=int, default=2)
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -182,6 +192,12 @@ def main():
     if args.margin is not None:
         from paper_1905_12948_amd import GMC_OPT_CAND_MARGIN
         gm.set_option(GMC_OPT_CAND_MARGIN, args.margin)
+    # the bench keeps w untouched between the server pass and the next worker
+    # pass and swaps the two buffers, as the sparse momentum term requires
+    sparse_w = not args.dense_momentum
+    if sparse_w:
+        from paper_1905_12948_amd import GMC_OPT_SPARSE_MOMENTUM
+        gm.set_option(GMC_OPT_SPARSE_MOMENTUM, 1)
     log("workload %s: d=%d K=%d %s ratio=%g; generating %d gradient batches on the GPU"
         % (wl.name, d, K, wl.compressor, wl.ratio, args.grad_batches))
     w = sdev.w0(wl, dev)
@@ -235,18 +251,19 @@ def main():
 
     ms_step = elapsed * 1e3 / args.steps
     msg_len = int(round(float(ln.double().mean().item())))  # varies per worker for the sampled threshold
-    ab = algorithmic_bytes(wl, msg_len, detach)
+    ab = algorithmic_bytes(wl, msg_len, detach, sparse_w)
     fused_ms_total, fused_n = prof["fused_vec"]
     fused_ms = fused_ms_total / max(fused_n, 1)
     achieved = ab["fused"] / (fused_ms * 1e-3) / 1e9
-    traffic = read_pmc_summary() if (wl.name == "resnet50" and not detach) else None
+    traffic = read_pmc_summary(sparse_w) if (wl.name == "resnet50" and not detach) else None
     roofline = {"kernel": "topk_fused_vec_kernel" if wl.compressor != "rbgs" else "rbgs_fused_kernel",
                 "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": None if traffic is None else int(traffic),
                 "alg_bytes_per_launch": ab["fused"], "avg_ms": round(fused_ms, 4)}
     value = K * d / (ms_step * 1e-3) / 1e9
-    sel = {k: stats1[k] - stats0[k] for k in ("from_candidates", "full_data", "candidates")}
+    sel = {k: stats1[k] - stats0[k] for k in ("from_candidates", "full_data", "candidates",
+                                              "sparse_momentum_steps")}
     out = {
         "metric": METRIC if wl.name == "resnet50" else METRIC.split(",")[0] + ", " + wl.name,
         "value": round(value, 2), "unit": UNIT, "n_gpus": 1,
@@ -254,7 +271,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": DESCRIPTIONS[wl.name], "d": d, "K": K, "compressor": wl.compressor,
-                   "ratio": wl.ratio, "lambda": lam, "message_len": msg_len, "grad_batches": len(G)},
+                   "ratio": wl.ratio, "lambda": lam, "message_len": msg_len, "grad_batches": len(G),
+                   "sparse_momentum": sparse_w},
         "hbm_peak_frac": round(ab["step"] / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "alg_bytes_per_step": ab["step"],
         "selection": sel,

@@ -273,13 +273,28 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
  *                              gmc_profile_read for the stage numbers
  *   GMC_OPT_SAMPLE_STRATUM     GMC_TOPK_APPROX: components per sample stratum
  *                              L in [1, d] (default 100); before the first step
+ *   GMC_OPT_SPARSE_MOMENTUM    1: the caller promises not to change w between
+ *                              a server pass and the next gmc_step (default
+ *                              0).  Then a server pass out of place
+ *                              (gmc_aggregate_apply, gmc_finish; not with
+ *                              momentum on the server) records which
+ *                              components it changed, and when the next
+ *                              gmc_step gets that pass's output as w_t and its
+ *                              input as w_prev, the worker pass reads w_t and
+ *                              w_prev only there: everywhere else
+ *                              w_t - w_prev is exactly +0, as in Algorithm 1,
+ *                              where the workers receive the server's sparse
+ *                              w_{t+1} - w_t.  Results are bit for bit those
+ *                              of the dense path; other calls, or other
+ *                              buffers, fall back to it.
  */
 enum {
     GMC_OPT_FORCE_FULL_SELECT = 1,
     GMC_OPT_CAND_MARGIN = 2,
     GMC_OPT_CAND_CAP_MULT = 3,
     GMC_OPT_PROFILE = 4,
-    GMC_OPT_SAMPLE_STRATUM = 5
+    GMC_OPT_SAMPLE_STRATUM = 5,
+    GMC_OPT_SPARSE_MOMENTUM = 6
 };
 gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value);
 
@@ -288,6 +303,8 @@ gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value);
  *   [0] steps taken  [1] top-s segment selections resolved from candidates
  *   [2] selections that took the full-data path  [3] candidates collected
  *   [4] selections whose count check failed (must stay 0)
+ *   [5] worker passes that read w only at the last server pass's changed
+ *       components (GMC_OPT_SPARSE_MOMENTUM)
  */
 gmc_status gmc_stats(gmc_ctx* ctx, int64_t* out, int32_t n);
 

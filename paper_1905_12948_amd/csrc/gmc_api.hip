@@ -47,6 +47,15 @@ struct gmc_ctx {
     int margin = 2;
     int cap_mult = 16;
     int32_t stratum = 100;         // sampled-threshold top-s: components per sample stratum
+    int sparse_w = 0;              // GMC_OPT_SPARSE_MOMENTUM
+
+    // the last server pass's bitmap of changed components (sparse_w)
+    uint32_t* wbits = nullptr;
+    bool wbits_valid = false;
+    const float* wbits_in = nullptr;   // that pass's w_t ...
+    const float* wbits_out = nullptr;  // ... and w_{t+1}
+    int64_t wbits_t = -1;              // the step the bitmap serves
+    int64_t sparse_steps = 0;          // worker passes that used it
 
     // derived
     std::vector<int32_t> seg_k;
@@ -238,6 +247,7 @@ gmc_status prepare(gmc_ctx* ctx) {
     size_t bytes = 0;
     auto add = [&](size_t n, size_t sz) { bytes = ((bytes + 255) & ~(size_t)255) + n * sz; };
     add(8, sizeof(int64_t));  // stats
+    add((size_t)(ctx->d + 31) / 32, 4);  // bitmap of the components the last server pass changed
     if (ctx->comp == GMC_RBGS) {
         add((size_t)(ctx->nb + 31) / 32, 4);
         add((size_t)ctx->n_sel, 4);
@@ -274,6 +284,8 @@ gmc_status prepare(gmc_ctx* ctx) {
     GMC_HIP(ctx, hipMemset(mem, 0, bytes));
     Carver cv{reinterpret_cast<char*>(mem)};
     ctx->stats = cv.take<int64_t>(8);
+    ctx->wbits = cv.take<uint32_t>((size_t)(ctx->d + 31) / 32);
+    ctx->wbits_valid = false;
     if (ctx->comp == GMC_RBGS) {
         ctx->rbgs_bitmap = cv.take<uint32_t>((ctx->nb + 31) / 32);
         ctx->rbgs_blocks = cv.take<int32_t>(ctx->n_sel);
@@ -530,6 +542,14 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
     a.d = (int32_t)ctx->d;
     a.seed = ctx->seed;
     a.t = (uint64_t)ctx->t;
+    // w_t - w_prev is +0 outside the bitmap when w_t, w_prev are the last
+    // server pass's output and input and no step ran since
+    a.wbits = (ctx->sparse_w && ctx->wbits_valid && ctx->wbits_t == ctx->t && w_t_dev == ctx->wbits_out &&
+               w_prev_dev == ctx->wbits_in)
+                  ? ctx->wbits
+                  : nullptr;
+    ctx->wbits_valid = false;
+    if (a.wbits) ++ctx->sparse_steps;
     for (int k = 0; k < ctx->K; ++k) {
         if (!grads_dev[k] || !err_dev[k] || (y_dev && !y_dev[k]))
             return fail(ctx, GMC_EINVAL, "gmc_step: NULL worker pointer");
@@ -569,20 +589,18 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
         // (partial and unaligned ones element-wise); the element-wise kernel
         // every chunk of the others
         const uint64_t all = ctx->K == 64 ? ~0ull : ((1ull << ctx->K) - 1ull);
-        const int32_t* gl = nullptr;
-        const int32_t ng = vec_mask == all ? 0 : ctx->geo.n_chunks;
         if (vec_mask) {
             GMC_TRY(prof_begin(ctx, 0, &ev));
             GMC_LAUNCH(ctx, launch_topk_fused_vec(a, ctx->geo, ctx->scr, vec_mask, ctx->stream));
             GMC_TRY(prof_end(ctx, 0, ev));
         }
-        if (ng > 0) {
+        if (vec_mask != all) {
             GMC_TRY(prof_begin(ctx, 1, &ev));
-            GMC_LAUNCH(ctx, launch_topk_fused_gen(a, ctx->geo, ctx->scr, vec_mask, gl, ng, ctx->stream));
+            GMC_LAUNCH(ctx, launch_topk_fused_gen(a, ctx->geo, ctx->scr, vec_mask, ctx->stream));
             GMC_TRY(prof_end(ctx, 1, ev));
         }
         GMC_TRY(prof_begin(ctx, 2, &ev));
-        GMC_LAUNCH(ctx, launch_topk_compact(a, ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
+        GMC_LAUNCH(ctx, launch_topk_compact(ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
         for (int pass = 1; pass <= 3; ++pass)
             GMC_LAUNCH(ctx, launch_topk_hist(pass, a, ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
         GMC_LAUNCH(ctx, launch_topk_count(a, ctx->geo, ctx->scr, msg_len_dev, ctx->k_tot, ctx->stream));
@@ -631,6 +649,14 @@ gmc_status aggregate_impl(gmc_ctx* ctx, const int32_t* idx_dev, const float* val
     f.s = ctx->s;
     f.b = ctx->b;
     f.q = ctx->q;
+    // the bitmap for the next worker pass: out of place, and not with momentum
+    // on the server (w_{t+1} differs from w_t everywhere there)
+    const bool mark = ctx->sparse_w && f.w_in && f.w_out && f.w_in != f.w_out && ctx->rule != kRuleServerMomentum;
+    f.wbits = mark ? ctx->wbits : nullptr;
+    ctx->wbits_valid = mark;
+    ctx->wbits_in = f.w_in;
+    ctx->wbits_out = f.w_out;
+    ctx->wbits_t = ctx->t;
     const int64_t row_i = gmc_index_len(ctx), row_v = gmc_message_len(ctx);
     hipEvent_t ev;
     GMC_TRY(prof_begin(ctx, 4, &ev));
@@ -732,6 +758,7 @@ gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const fl
     if (w_prev_out_dev == w_dev) return fail(ctx, GMC_EINVAL, "gmc_apply: w_prev_out may not alias w");
     if (ctx->rule == kRuleServerMomentum)
         return fail(ctx, GMC_EINVAL, "gmc_apply: momentum on the server needs w_{t-1}; use gmc_finish");
+    ctx->wbits_valid = false;
     GMC_HIP(ctx, hipSetDevice(ctx->device));
     hipEvent_t ev;
     GMC_TRY(prof_begin(ctx, 5, &ev));
@@ -803,6 +830,10 @@ gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value) {
             ctx->stratum = (int32_t)value;
             ctx->prepared = false;
             return prepare(ctx);
+        case GMC_OPT_SPARSE_MOMENTUM:
+            ctx->sparse_w = value ? 1 : 0;
+            ctx->wbits_valid = false;
+            return GMC_OK;
         case GMC_OPT_PROFILE:
             if (ctx->profile) GMC_HIP(ctx, hipStreamSynchronize(ctx->stream));
             prof_clear(ctx);
@@ -820,6 +851,7 @@ gmc_status gmc_stats(gmc_ctx* ctx, int64_t* out, int32_t n) {
     int64_t host[8] = {0};
     if (ctx->stats) GMC_HIP(ctx, hipMemcpy(host, ctx->stats, sizeof host, hipMemcpyDeviceToHost));
     host[0] = ctx->t;
+    host[5] = ctx->sparse_steps;
     for (int32_t i = 0; i < n && i < 8; ++i) out[i] = host[i];
     return GMC_OK;
 }

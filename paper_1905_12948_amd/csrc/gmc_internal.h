@@ -134,6 +134,11 @@ struct StepArgs {
     int32_t d;
     uint64_t seed;   // sample draws of the sampled-threshold top-s
     uint64_t t;      // step
+    // nullable: the previous server pass's bitmap (FinishArgs::wbits) when
+    // w_t and w_prev are that pass's output and input; the vector passes then
+    // read w_t, w_prev only at the marked components, since elsewhere
+    // w_t - w_prev is exactly +0
+    const uint32_t* wbits;
 };
 
 // The server pass after the sum over workers: update = -(s * sum), the
@@ -149,6 +154,9 @@ struct FinishArgs {
     float q;              // lambda*eta
     int32_t detach;       // 1: y_k = w_{t+1} - q e_k at the sent components
     int32_t rows16;       // 1: every e[k] and y[k] is 16-byte aligned
+    // nullable, [ceil(d/32)]: bit j set where some worker sent j or w_{t+1}[j]
+    // is not finite; everywhere else w_{t+1}[j] equals w_t[j] bit for bit
+    uint32_t* wbits;
     const float* e[kMaxWorkers];  // e_{t+1,k}
     float* y[kMaxWorkers];        // w_{t+1,k}
 };
@@ -166,17 +174,16 @@ struct DetachArgs {
 // launchers (gmc_kernels.hip); each returns the launch status
 // ----------------------------------------------------------------------------
 // vec_mask: bit k set when worker k's rows (and w_t, w_prev) are 16-byte
-// aligned.  gen_list/n_gen: chunks the element-wise kernel visits (NULL list:
-// chunks 0..n_gen-1).
+// aligned.  The vector kernel takes every chunk of those workers, the
+// element-wise kernel every chunk of the others.
 hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                                  uint64_t vec_mask, hipStream_t st);
 hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
-                                 uint64_t vec_mask, const int32_t* gen_list, int32_t n_gen,
-                                 hipStream_t st);
+                                 uint64_t vec_mask, hipStream_t st);
 // count + copy; the copy also does the first histogram pass of the pairs
 // that resolve from their candidates (exact top-s)
-hipError_t launch_topk_compact(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int force_full,
-                               int margin, hipStream_t st);
+hipError_t launch_topk_compact(const TopkGeometry& g, const TopkScratch& s, int force_full, int margin,
+                               hipStream_t st);
 hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
                             const TopkScratch& s, int force_full, int margin, hipStream_t st);
 hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,

@@ -147,6 +147,30 @@ __host__ __device__ inline int64_t run_order_grid(int64_t n_chunks, int K) {
     return (n_chunks + kRunChunks - 1) / kRunChunks * kRunChunks * K;
 }
 
+// w_t and w_prev of the four components at j for the worker passes.  With the
+// previous server pass's bitmap (a.wbits), unmarked components have
+// w_t == w_prev, finite: w_t - w_prev is exactly +0 there, so the loads are
+// skipped (w_t is still read when the detached points need it) and the
+// momentum term comes out +0, bit for bit what the dense loads give.
+template <bool kDetach>
+__device__ __forceinline__ void load_w4(const StepArgs& a, int64_t j, float4* wt, float4* wv) {
+    if (a.wbits) {
+        const uint32_t marked = (a.wbits[j >> 5] >> (j & 31)) & 0xfu;
+        if (marked) {
+            *wt = ld4(a.w_t + j);
+            *wv = ld4(a.w_prev + j);
+        } else if (kDetach) {
+            *wt = ld4(a.w_t + j);
+            *wv = *wt;
+        } else {
+            *wt = *wv = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        return;
+    }
+    *wt = ld4(a.w_t + j);
+    *wv = ld4(a.w_prev + j);
+}
+
 // GMC+'s detached point from w and the residual: w - q e (Algorithm 2).
 __device__ __forceinline__ float detached(float w, float e, float q) {
     const float r = q * e;
@@ -247,20 +271,16 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
     const int o0 = threadIdx.x * 4;               // components o0..o0+3 and 1024+o0..1024+o0+3
     float* ep = a.wp.e[k] + start + o0;
     const float* gp = a.wp.g[k] + start + o0;
-    const float* wt_p = a.w_t + start + o0;
-    const float* wp_p = a.w_prev + start + o0;
     constexpr bool kNeedW = kRule != kRuleServerMomentum || kDetach;
     float4 u[2], gv[2], wt[2], wv[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         u[i] = ld4_stream(ep + i * (kGroup * 4));
         gv[i] = ld4_stream(gp + i * (kGroup * 4));
-        if (kNeedW) {
-            wt[i] = ld4(wt_p + i * (kGroup * 4));
-            wv[i] = ld4(wp_p + i * (kGroup * 4));
-        } else {
+        if (kNeedW)
+            load_w4<kDetach>(a, (int64_t)start + o0 + i * (kGroup * 4), &wt[i], &wv[i]);
+        else
             wt[i] = wv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-        }
     }
     uint32_t flags = 0;
 #pragma unroll
@@ -384,17 +404,15 @@ __device__ void fused_chunk_wave(const StepArgs& a, const TopkGeometry& g, const
 
 // The element-wise kernel: one wavefront per (chunk, worker) for the workers
 // outside vec_mask (the vector kernel takes every chunk of the others,
-// partial ones included); `list` holds the chunk ids to visit (NULL: every
-// chunk).
+// partial ones included).
 __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
-                                                                uint64_t vec_mask, const int32_t* list,
-                                                                int32_t n_list) {
+                                                                uint64_t vec_mask) {
     const int wave = threadIdx.x >> 6;
     const int64_t wid = (int64_t)blockIdx.x * kWavesPerGroup + wave;
-    if (wid >= (int64_t)n_list * g.K) return;  // wave-uniform; no workgroup barrier below
-    const int li = (int)(wid / g.K), k = (int)(wid % g.K);
+    if (wid >= (int64_t)g.n_chunks * g.K) return;  // wave-uniform; no workgroup barrier below
+    const int chunk = (int)(wid / g.K), k = (int)(wid % g.K);
     if ((vec_mask >> k) & 1ull) return;  // the vector kernel's
-    fused_chunk_wave(a, g, s, list ? list[li] : li, k);
+    fused_chunk_wave(a, g, s, chunk, k);
 }
 
 template <bool kApprox>
@@ -430,11 +448,10 @@ hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const
 }
 
 hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
-                                 uint64_t vec_mask, const int32_t* gen_list, int32_t n_gen, hipStream_t st) {
-    const int64_t waves = (int64_t)n_gen * g.K;
+                                 uint64_t vec_mask, hipStream_t st) {
+    const int64_t waves = (int64_t)g.n_chunks * g.K;
     const int grid = (int)((waves + kWavesPerGroup - 1) / kWavesPerGroup);
-    hipLaunchKernelGGL(topk_fused_gen_kernel, dim3(grid), dim3(kGroup), 0, st, a, g, s, vec_mask, gen_list,
-                       n_gen);
+    hipLaunchKernelGGL(topk_fused_gen_kernel, dim3(grid), dim3(kGroup), 0, st, a, g, s, vec_mask);
     return hipGetLastError();
 }
 
@@ -849,9 +866,8 @@ __global__ __launch_bounds__(kGroup) void topk_compact_copy_kernel(TopkGeometry 
     if (threadIdx.x == 0) ps->p1_done = 1u;
 }
 
-hipError_t launch_topk_compact(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int force_full,
-                               int margin, hipStream_t st) {
-    (void)a;
+hipError_t launch_topk_compact(const TopkGeometry& g, const TopkScratch& s, int force_full, int margin,
+                               hipStream_t st) {
     hipLaunchKernelGGL(topk_compact_count_kernel, dim3(g.K * g.n_cgroups), dim3(kGroup), 0, st, g, s, force_full);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -1270,12 +1286,10 @@ __global__ __launch_bounds__(kGroup) void rbgs_vec_kernel(StepArgs a, int32_t K,
     for (int i = 0; i < 2; ++i) {
         u[i] = ld4_stream(ep + i * (kGroup * 4));
         gv[i] = ld4_stream(gp + i * (kGroup * 4));
-        if (kNeedW) {
-            wt[i] = ld4(a.w_t + start + i * (kGroup * 4));
-            wv[i] = ld4(a.w_prev + start + i * (kGroup * 4));
-        } else {
+        if (kNeedW)
+            load_w4<kDetach>(a, start + i * (kGroup * 4), &wt[i], &wv[i]);
+        else
             wt[i] = wv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-        }
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -1358,10 +1372,31 @@ __device__ __forceinline__ float next_w(float x, float dl, const float* w_prev, 
     return moved + push;
 }
 
+__device__ __forceinline__ uint32_t not_finite(float x) {
+    return (__float_as_uint(x) & 0x7f800000u) == 0x7f800000u ? 1u : 0u;
+}
+
+// Bits of the four components at q of a range for the next worker pass:
+// some worker sent the component (hit) or w_{t+1} there is not finite.
+__device__ __forceinline__ uint32_t mark4(const unsigned char* hit, int q, float4 wn) {
+    return (hit[q] || not_finite(wn.x) ? 1u : 0u) | (hit[q + 1] || not_finite(wn.y) ? 2u : 0u) |
+           (hit[q + 2] || not_finite(wn.z) ? 4u : 0u) | (hit[q + 3] || not_finite(wn.w) ? 8u : 0u);
+}
+
+// Stores the range's bitmap words (wb in LDS, one bit per component) once
+// every thread has marked its components.
+__device__ __forceinline__ void flush_marks(const uint32_t* wb, int64_t base, int64_t n, uint32_t* wbits) {
+    __syncthreads();
+    const int words = (int)((n + 31) / 32);
+    if ((int)threadIdx.x < words) wbits[(base >> 5) + threadIdx.x] = wb[threadIdx.x];
+}
+
 // Writes update = -(s * acc) for the n components of a range starting at base
-// (when f.update is not NULL) and, with kApply, w_out = next_w(w_in, update).
+// (when f.update is not NULL) and, with kApply, w_out = next_w(w_in, update);
+// with f.wbits also marks the components for the next worker pass in wb.
 template <bool kApply>
-__device__ __forceinline__ void write_update(const float* acc, int64_t base, int64_t n, const FinishArgs& f) {
+__device__ __forceinline__ void write_update(const float* acc, const unsigned char* hit, uint32_t* wb, int64_t base,
+                                             int64_t n, const FinishArgs& f) {
     const float s = f.s;
     const bool vec = n == kAggRange && (base & 3) == 0 && (f.update == nullptr || aligned16(f.update)) &&
                      (!kApply || (aligned16(f.w_in) && aligned16(f.w_out) &&
@@ -1381,6 +1416,7 @@ __device__ __forceinline__ void write_update(const float* acc, int64_t base, int
                                      nx.w + b * (x.w - p.w));
                 }
                 st4(f.w_out + j, nx);
+                if (f.wbits) atomicOr(&wb[q >> 5], mark4(hit, q, nx) << (q & 31));
             }
         }
         return;
@@ -1389,7 +1425,11 @@ __device__ __forceinline__ void write_update(const float* acc, int64_t base, int
         const int64_t j = base + q;
         const float dl = -(s * acc[q]);
         if (f.update) f.update[j] = dl;
-        if (kApply) f.w_out[j] = next_w(f.w_in[j], dl, f.w_prev, j, f.b);
+        if (kApply) {
+            const float wn = next_w(f.w_in[j], dl, f.w_prev, j, f.b);
+            f.w_out[j] = wn;
+            if (f.wbits && (hit[q] || not_finite(wn))) atomicOr(&wb[q >> 5], 1u << (q & 31));
+        }
     }
 }
 
@@ -1460,6 +1500,7 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
     static_assert(kAggRange == kGroup * 8, "8 components per thread");
     __shared__ float acc[kAggRange];
     __shared__ unsigned char hit[kAggRange];
+    __shared__ uint32_t wb[kAggRange / 32];
     __shared__ int32_t st_idx[kAggStage];
     __shared__ float st_val[kAggStage];
     __shared__ int32_t src[kMaxWorkers];
@@ -1486,6 +1527,7 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
         acc[q] = 0.0f;
         hit[q] = 0;
     }
+    if (threadIdx.x < kAggRange / 32) wb[threadIdx.x] = 0u;
     if (threadIdx.x < K) {
         const int32_t* rp = rowptr + (size_t)threadIdx.x * (n_ranges + 1);
         const int32_t lo = rp[r], hi = rp[r + 1];
@@ -1553,10 +1595,15 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             }
             st4(f.w_out + base + q0, n0);
             st4(f.w_out + base + q1, n1);
+            if (f.wbits) {
+                atomicOr(&wb[q0 >> 5], mark4(hit, q0, n0) << (q0 & 31));
+                atomicOr(&wb[q1 >> 5], mark4(hit, q1, n1) << (q1 & 31));
+            }
         }
     } else {
-        write_update<kApply>(acc, base, n, f);
+        write_update<kApply>(acc, hit, wb, base, n, f);
     }
+    if (kApply && f.wbits) flush_marks(wb, base, n, f.wbits);
     if (kApply && f.detach) finish_detach(hit, base, n, K, f);
 }
 
@@ -1581,8 +1628,11 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
                                                           const float* val, int64_t val_row, FinishArgs f) {
     __shared__ float acc[kAggRange];
     __shared__ unsigned char hit[kAggRange];
+    __shared__ uint32_t wb[kAggRange / 32];
     const int64_t base = (int64_t)blockIdx.x * kAggRange;
     const int64_t n = (int64_t)d - base < kAggRange ? (int64_t)d - base : kAggRange;
+    if (threadIdx.x < kAggRange / 32) wb[threadIdx.x] = 0u;
+    if (f.wbits) __syncthreads();  // wb cleared before any mark
     const bool vec = n == kAggRange && (B & 3) == 0 && aligned16(val) && (val_row & 3) == 0 &&
                      (f.update == nullptr || aligned16(f.update)) && (!f.detach || f.rows16) &&
                      (!kApply || (aligned16(f.w_in) && aligned16(f.w_out) &&
@@ -1628,6 +1678,12 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
                                      nx.w + b * (x.w - p.w));
                 }
                 st4(f.w_out + j, nx);
+                if (f.wbits) {
+                    const int q = (int)(j - base);
+                    const uint32_t m = (slots[i] >= 0 ? 0xfu : 0u) | not_finite(nx.x) | (not_finite(nx.y) << 1) |
+                                       (not_finite(nx.z) << 2) | (not_finite(nx.w) << 3);
+                    atomicOr(&wb[q >> 5], m << (q & 31));
+                }
                 if (f.detach && slots[i] >= 0) {  // GMC+: the sent components' detached points
                     const float q = f.q;
                     for (int k = 0; k < K; ++k) {
@@ -1638,6 +1694,7 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
                 }
             }
         }
+        if (kApply && f.wbits) flush_marks(wb, base, n, f.wbits);
         return;
     }
     for (int q = threadIdx.x; q < kAggRange; q += kGroup) {
@@ -1657,7 +1714,8 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
         hit[q] = sent;
     }
     __syncthreads();
-    write_update<kApply>(acc, base, n, f);
+    write_update<kApply>(acc, hit, wb, base, n, f);
+    if (kApply && f.wbits) flush_marks(wb, base, n, f.wbits);
     if (kApply && f.detach) finish_detach(hit, base, n, K, f);
 }
 

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libgmc.so")
 GMC_TOPK_GLOBAL, GMC_TOPK_SEGMENTED, GMC_RBGS, GMC_TOPK_APPROX = 0, 1, 2, 3
 GMC_OK, GMC_EINVAL, GMC_ENOMEM, GMC_EDEVICE, GMC_ESTATE = 0, -1, -2, -3, -4
 GMC_OPT_FORCE_FULL_SELECT, GMC_OPT_CAND_MARGIN, GMC_OPT_CAND_CAP_MULT, GMC_OPT_PROFILE = 1, 2, 3, 4
-GMC_OPT_SAMPLE_STRATUM = 5
+GMC_OPT_SAMPLE_STRATUM, GMC_OPT_SPARSE_MOMENTUM = 5, 6
 MAX_WORKERS = 64
 STAGES = ("fused_vec", "fused_gen", "select", "emit", "aggregate", "apply")
 
@@ -323,7 +323,7 @@ class Gmc:
     def stats(self) -> dict:
         out = (ctypes.c_int64 * 8)()
         self._call(self._lib.gmc_stats(self._ctx, out, 8))
-        keys = ("steps", "from_candidates", "full_data", "candidates", "count_errors")
+        keys = ("steps", "from_candidates", "full_data", "candidates", "count_errors", "sparse_momentum_steps")
         return {k: int(out[i]) for i, k in enumerate(keys)}
 
     def profile(self, stages=None):

@@ -52,6 +52,8 @@ class Case:
     eta_fn: Optional[Callable] = None      # t -> eta_t (a schedule)
     finish: bool = False          # server pass through gmc_finish (implied by rule / detach)
     stratum: int = 100            # sampled-threshold top-s: components per sample stratum
+    sparse_w: bool = False        # GMC_OPT_SPARSE_MOMENTUM
+    w0_hook: Optional[Callable] = None     # w0 -> w0, host side
 
 
 def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
@@ -72,6 +74,9 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
             stratum=case.stratum if comp == "approx" else None)
     for opt, val in case.options:
         g.set_option(opt, val)
+    if case.sparse_w:
+        from paper_1905_12948_amd import GMC_OPT_SPARSE_MOMENTUM
+        g.set_option(GMC_OPT_SPARSE_MOMENTUM, 1)
     orc = oracle.GmcOracle(d, K, comp if comp in ("rbgs", "approx") else "topk", wl.ratio, wl.beta, wl.eta,
                            seed=wl.seed, seg_off=seg, block=wl.block, variant=case.rule, lam=case.lam,
                            stratum=case.stratum)
@@ -80,6 +85,8 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
 
     dev = torch.device(device)
     w0 = wl.w0()
+    if case.w0_hook is not None:
+        w0 = case.w0_hook(w0)
     w_h, wp_h = w0.copy(), w0.copy()
     e_h = np.zeros((K, d), np.float32)
     stride = d + case.row_pad

@@ -32,6 +32,10 @@ def test_algorithmic_bytes_of_the_workloads():
     ab = bench.algorithmic_bytes(rb, m, detach=True)
     assert ab["step"] == 12 * 8 * d + 16 * d + 8 * 8 * m + 4 * 8 * d
     assert ab["fused"] == 12 * 8 * d + 8 * d + 4 * 8 * m + 4 * 8 * d
+    # sparse momentum term: the bitmap and the changed components instead of w_t, w_prev
+    ab = bench.algorithmic_bytes(wl, 25558, detach=False, sparse_w=True)
+    assert ab["fused"] == 12 * K * d + d // 8 + 8 * K * 25558
+    assert ab["step"] == 12 * K * d + d // 8 + 8 * K * 25558 + 8 * d + 16 * K * 25558 + d // 8
 
 
 def test_pmc_summary_matches_the_sources_or_is_ignored(tmp_path, monkeypatch):
@@ -45,7 +49,7 @@ def test_pmc_summary_matches_the_sources_or_is_ignored(tmp_path, monkeypatch):
             if "=" in line and not line.lstrip().startswith("#"):
                 k, v = line.split("=", 1)
                 kv[k.strip()] = v.strip()
-    if kv["kernel_source_sha256"] == bench.kernel_source_hash():
+    if kv["kernel_source_sha256"] == bench.kernel_source_hash() and kv.get("sparse_momentum", "0") == "1":
         fs = float(kv["copy_bytes"]) / (float(kv["copy_fetch_kib"]) * 1024)
         ws = float(kv["copy_bytes"]) / (float(kv["copy_write_kib"]) * 1024)
         want = float(kv["fused_fetch_kib"]) * 1024 * fs + float(kv["fused_write_kib"]) * 1024 * ws

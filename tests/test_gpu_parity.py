@@ -251,3 +251,35 @@ def test_rule_and_compressor_errors():
         a.set_option(GMC_OPT_SAMPLE_STRATUM, 0)
     assert a.message_len == d and a.index_len == d
     a.close()
+
+
+
+# ---------------------------------------------------------------------------
+# GMC_OPT_SPARSE_MOMENTUM: w read only where the last server pass changed it
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name,shrink,K,extra", [
+    ("resnet18", 16, 4, {}), ("resnet50", 32, 16, {}), ("rbgs", 16, 8, {}), ("gpt2", 64, 3, {}),
+    ("resnet50_approx", 64, 4, {}), ("rbgs", 16, 4, {"lam": 0.5, "detach": "fused"}),
+    ("resnet18", 16, 4, {"lam": 0.5, "detach": "fused"}), ("resnet18", 16, 4, {"rule": "lr_in_residual"}),
+    ("resnet18", 32, 3, {"row_pad": 1}), ("resnet18", 16, 4, {"rule": "server_momentum"})])
+def test_sparse_momentum_is_bitwise_the_dense_path(name, shrink, K, extra):
+    st = run_lockstep(Case(W(name).shrunk(shrink, K=K), steps=5, fused_apply=True, sparse_w=True,
+                           label="sparse momentum/" + name, **extra))
+    if extra.get("rule") != "server_momentum":
+        assert st["sparse_momentum_steps"] == 4, st   # every step after the first
+
+
+def test_sparse_momentum_with_non_finite_parameters():
+    def poison(w0):
+        w0 = w0.copy()
+        w0[[5, 777, 4096, 9000]] = [np.inf, -np.inf, np.nan, np.inf]
+        return w0
+    st = run_lockstep(Case(W("resnet18").shrunk(32, K=3), steps=4, fused_apply=True, sparse_w=True,
+                           w0_hook=poison, label="sparse momentum, non-finite w"))
+    assert st["sparse_momentum_steps"] == 3, st
+
+
+def test_sparse_momentum_falls_back_when_the_buffers_change():
+    st = run_lockstep(Case(W("resnet18").shrunk(32, K=3), steps=4, sparse_w=True, label="sparse momentum, apply"))
+    assert st["sparse_momentum_steps"] == 0, st   # gmc_aggregate + gmc_apply: no bitmap
