@@ -1,11 +1,12 @@
 #!/usr/bin/env python
 """GMC step throughput on one MI355X.
 
-One step is one full iteration of Algorithm 1 for K simulated workers:
-gmc_step (global momentum + error feedback + compression + residual for all
-K workers) and gmc_aggregate_apply (server sum in worker order and the
-apply, w_{t+1} = w_t + update written over w_{t-1}'s buffer, the two
-parameter buffers swapping roles every step).  Inputs are resident in HBM
+One step is one full iteration of Algorithm 1 for K simulated workers,
+gmc_iteration: the worker pass (global momentum + error feedback +
+compression + residual for all K workers) and the server pass (sum in
+worker order and the apply, w_{t+1} = w_t + update written over w_{t-1}'s
+buffer, the two parameter buffers swapping roles every step); GMC+
+(lambda > 0) takes gmc_step_detach and gmc_finish.  Inputs are resident in HBM
 before the timed region; each step takes the next of a few pre-generated
 gradient batches.
 
@@ -222,9 +223,8 @@ def main():
         if detach:
             gm.step(cur, prev, G[step_no[0] % len(G)], err, idx, val, ln, w_k=wk)
             gm.finish(idx, val, ln, cur, prev, err=err, w_k=wk)
-        else:
-            gm.step(cur, prev, G[step_no[0] % len(G)], err, idx, val, ln)
-            gm.aggregate_apply(idx, val, ln, cur, prev)
+        else:  # worker and server pass in one call: w_{t+1} over w_{t-1}'s buffer
+            gm.iteration(cur, prev, G[step_no[0] % len(G)], err, idx, val, ln)
         step_no[0] += 1
 
     log("warmup %d steps" % args.warmup)

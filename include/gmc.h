@@ -251,6 +251,20 @@ gmc_status gmc_finish(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev
                       const float* const* err_dev, float* const* w_k_dev);
 
 /*
+ * One whole iteration of Algorithm 1 for all K workers: gmc_step(w_t,
+ * w_prev_io, ...) and then the server pass, which writes w_{t+1} over
+ * w_prev_io (the caller swaps the roles of its two buffers for the next
+ * iteration, as after gmc_finish out of place).  Results equal those of
+ * gmc_step followed by gmc_finish(w_t, w_prev_io, w_out = w_prev_io) bit for
+ * bit; the call pattern GMC_OPT_SPARSE_MOMENTUM serves.
+ *   w_t_dev        [d] fp32 in
+ *   w_prev_io_dev  [d] fp32: w_{t-1} in, w_{t+1} out; may not alias w_t_dev
+ * The remaining arguments are gmc_step's.
+ */
+gmc_status gmc_iteration(gmc_ctx* ctx, const float* w_t_dev, float* w_prev_io_dev, const float* const* grads_dev,
+                         float* const* err_dev, int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev);
+
+/*
  * GMC+'s detached points as one dense pass (Algorithm 2, detach):
  * w_k_dev[k][j] = w_dev[j] - q err_dev[k][j] for every worker and component,
  * with w_dev = w_{t+1} and err = e_{t+1,k}; any rule.

@@ -752,6 +752,20 @@ gmc_status gmc_detach(gmc_ctx* ctx, const float* w_dev, const float* const* err_
     return GMC_OK;
 }
 
+gmc_status gmc_iteration(gmc_ctx* ctx, const float* w_t_dev, float* w_prev_io_dev, const float* const* grads_dev,
+                         float* const* err_dev, int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_iteration: ctx is NULL");
+    if (!w_t_dev || !w_prev_io_dev || !grads_dev || !err_dev || !idx_dev || !val_dev || !msg_len_dev)
+        return fail(ctx, GMC_EINVAL, "gmc_iteration: NULL argument");
+    if (w_t_dev == w_prev_io_dev) return fail(ctx, GMC_EINVAL, "gmc_iteration: w_prev_io may not alias w_t");
+    GMC_TRY(step_impl(ctx, w_t_dev, w_prev_io_dev, grads_dev, err_dev, nullptr, idx_dev, val_dev, msg_len_dev));
+    FinishArgs f{};
+    f.w_in = w_t_dev;
+    f.w_out = w_prev_io_dev;
+    f.w_prev = ctx->rule == kRuleServerMomentum ? w_prev_io_dev : nullptr;  // read before written, per component
+    return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, f);
+}
+
 gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const float* update_dev) {
     if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_apply: ctx is NULL");
     if (!w_dev || !update_dev) return fail(ctx, GMC_EINVAL, "gmc_apply: NULL argument");

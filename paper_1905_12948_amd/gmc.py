@@ -30,7 +30,7 @@ EXPORTS = ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "g
            "gmc_index_len", "gmc_step", "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step",
            "gmc_set_option", "gmc_stats", "gmc_profile_read", "gmc_last_error", "gmc_destroy",
            "gmc_calib_copy", "gmc_aggregate_apply", "gmc_set_rule", "gmc_set_eta", "gmc_set_lambda",
-           "gmc_step_detach", "gmc_finish", "gmc_detach")
+           "gmc_step_detach", "gmc_finish", "gmc_detach", "gmc_iteration")
 
 RULES = {"gmc": 0, "server_momentum": 1, "lr_in_residual": 2}
 
@@ -83,11 +83,12 @@ def load() -> ctypes.CDLL:
     lib.gmc_step_detach.argtypes = [P, P, P, P, P, P, P, P, P]
     lib.gmc_finish.argtypes = [P, P, P, P, P, P, P, P, P, P]
     lib.gmc_detach.argtypes = [P, P, P, P]
+    lib.gmc_iteration.argtypes = [P, P, P, P, P, P, P, P]
     for name in ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "gmc_step",
                  "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step", "gmc_set_option",
                  "gmc_stats", "gmc_profile_read", "gmc_calib_copy", "gmc_aggregate_apply",
                  "gmc_set_rule", "gmc_set_eta", "gmc_set_lambda", "gmc_step_detach", "gmc_finish",
-                 "gmc_detach"):
+                 "gmc_detach", "gmc_iteration"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -265,6 +266,21 @@ class Gmc:
             yp = (ctypes.c_void_p * K)(*_rows(w_k, d, K, "w_k"))
         self._stream(w.device)
         self._call(self._lib.gmc_finish(self._ctx, pi, pv, pl, pw, pp, po, pu, ep, yp))
+
+    def iteration(self, w_t, w_prev_io, grads, err, idx, val, msg_len):
+        """One whole iteration: the worker pass, then w_{t+1} written over
+        w_prev_io (swap the two buffers afterwards)."""
+        torch = _torch()
+        d, K = self.d, self.K
+        pw = _check(w_t, torch.float32, d, "w_t")
+        pp = _check(w_prev_io, torch.float32, d, "w_prev_io")
+        gp = (ctypes.c_void_p * K)(*_rows(grads, d, K, "grads"))
+        ep = (ctypes.c_void_p * K)(*_rows(err, d, K, "err"))
+        pi = _check(idx, torch.int32, K * self.index_len, "idx")
+        pv = _check(val, torch.float32, K * self.message_len, "val")
+        pl = _check(msg_len, torch.int64, K, "msg_len")
+        self._stream(w_t.device)
+        self._call(self._lib.gmc_iteration(self._ctx, pw, pp, gp, ep, pi, pv, pl))
 
     def detach(self, w, err, w_k):
         """GMC+'s detached points in one dense pass: w_k = w - (lambda eta) err."""

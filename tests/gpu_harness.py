@@ -54,6 +54,7 @@ class Case:
     stratum: int = 100            # sampled-threshold top-s: components per sample stratum
     sparse_w: bool = False        # GMC_OPT_SPARSE_MOMENTUM
     w0_hook: Optional[Callable] = None     # w0 -> w0, host side
+    iteration: bool = False       # gmc_iteration (worker and server pass in one call, buffers swapped)
 
 
 def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
@@ -114,8 +115,14 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
             g.set_eta(eta_t)
             orc.set_eta(eta_t)
         fused_detach = case.detach == "fused"
-        g.step(w, wp, g_rows, e_rows, idx, val, ln, w_k=wk_rows if fused_detach else None)
-        if use_finish:
+        if case.iteration:
+            g.iteration(w, wp, g_rows, e_rows, idx, val, ln)
+            w, wp = wp, w
+        else:
+            g.step(w, wp, g_rows, e_rows, idx, val, ln, w_k=wk_rows if fused_detach else None)
+        if case.iteration:
+            pass
+        elif use_finish:
             g.finish(idx, val, ln, w, wp, w_prev=wp, update=upd if case.write_update else None,
                      err=e_rows if fused_detach else None, w_k=wk_rows if fused_detach else None)
             w, wp = wp, w
@@ -151,7 +158,7 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
             m = int(ol[k])
             assert_same_f32(gv[k, :m], ov[k, :m], tag + ": values of worker %d" % k)
             assert_same_f32(e_rows[k].cpu().numpy(), e_h[k], tag + ": residual of worker %d" % k)
-        if case.write_update or not (case.fused_apply or use_finish):
+        if not case.iteration and (case.write_update or not (case.fused_apply or use_finish)):
             assert_same_f32(upd.cpu().numpy(), od, tag + ": update")
         assert_same_f32(w.cpu().numpy(), w_h, tag + ": w")
         assert_same_f32(wp.cpu().numpy(), wp_h, tag + ": w_prev")

@@ -74,6 +74,7 @@ def test_null_handles(lib):
     assert lib.gmc_step_detach(None, None, None, None, None, None, None, None, None) == -1
     assert lib.gmc_finish(None, None, None, None, None, None, None, None, None, None) == -1
     assert lib.gmc_detach(None, None, None, None) == -1
+    assert lib.gmc_iteration(None, None, None, None, None, None, None, None) == -1
     assert isinstance(lib.gmc_last_error(None), bytes)
     lib.gmc_destroy(None)
 

@@ -283,3 +283,30 @@ def test_sparse_momentum_with_non_finite_parameters():
 def test_sparse_momentum_falls_back_when_the_buffers_change():
     st = run_lockstep(Case(W("resnet18").shrunk(32, K=3), steps=4, sparse_w=True, label="sparse momentum, apply"))
     assert st["sparse_momentum_steps"] == 0, st   # gmc_aggregate + gmc_apply: no bitmap
+
+
+
+# ---------------------------------------------------------------------------
+# gmc_iteration: the whole iteration in one call, the dense copy of the apply
+# overlapped with the selection under the sparse momentum term
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name,shrink,K,extra", [
+    ("resnet18", 16, 4, {"sparse_w": True}), ("resnet50", 32, 16, {"sparse_w": True}),
+    ("gpt2", 64, 3, {"sparse_w": True}), ("resnet50_approx", 64, 4, {"sparse_w": True}),
+    ("resnet18", 16, 4, {"sparse_w": True, "rule": "lr_in_residual"}),
+    ("resnet18", 32, 3, {"sparse_w": True, "row_pad": 1}), ("rbgs", 16, 4, {"sparse_w": True}),
+    ("resnet18", 16, 4, {}), ("resnet18", 16, 4, {"rule": "server_momentum", "sparse_w": True})])
+def test_iteration_matches_the_oracle(name, shrink, K, extra):
+    st = run_lockstep(Case(W(name).shrunk(shrink, K=K), steps=5, iteration=True, label="iteration/" + name, **extra))
+    if extra.get("sparse_w") and extra.get("rule") != "server_momentum":
+        assert st["sparse_momentum_steps"] == 4, st
+
+
+def test_iteration_with_non_finite_parameters():
+    def poison(w0):
+        w0 = w0.copy()
+        w0[[5, 777, 4096, 9000]] = [np.inf, -np.inf, np.nan, np.inf]
+        return w0
+    run_lockstep(Case(W("resnet18").shrunk(32, K=3), steps=4, iteration=True, sparse_w=True, w0_hook=poison,
+                      label="iteration, non-finite w"))
