@@ -323,6 +323,17 @@ gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value);
 gmc_status gmc_stats(gmc_ctx* ctx, int64_t* out, int32_t n);
 
 /*
+ * Per-(worker, segment) selection diagnostics of the last gmc_step (top-s
+ * compressors), synchronising the context's stream first.  Pair p = k *
+ * n_seg + segment; for p < min(n, K * n_seg): mode[p] = 0 when the pair's
+ * top-s was resolved from its speculative candidates, 1 when it took the
+ * full-data path (too few or too many candidates), and cand[p] = the
+ * candidates the worker pass collected for it.  *n_pairs = K * n_seg.
+ * GMC_EINVAL for RBGS, GMC_ESTATE before the first step.
+ */
+gmc_status gmc_pair_stats(gmc_ctx* ctx, int32_t* mode, int64_t* cand, int32_t n, int32_t* n_pairs);
+
+/*
  * Stage timings of the stages GMC_OPT_PROFILE selects: for each stage i < n,
  * total milliseconds and timed launches since the option was last set.
  * Stages: 0 fused worker pass (vector kernel; RBGS: its fused gather pass),
@@ -337,6 +348,19 @@ gmc_status gmc_profile_read(gmc_ctx* ctx, double* ms, int64_t* launches, int32_t
  * traffic against which memory counters are scaled.  Buffers must not overlap.
  */
 gmc_status gmc_calib_copy(void* hip_stream, float* dst_dev, const float* src_dev, int64_t n);
+
+/*
+ * Measurement support, not part of the method: a plain stream with the
+ * access pattern of the fused worker pass of gmc_step (two streamed reads
+ * and one streamed write per worker-element, one workgroup per (chunk of
+ * 2048 components, worker), the K workers of a chunk consecutive):
+ * e_dev[k*row_pitch + j] += g_dev[k*row_pitch + j] for k < K, j < d, on
+ * hip_stream.  Its rate is the ceiling the memory system gives that pattern.
+ *   row_pitch >= d; 1 <= d < 2^31; K >= 1; the two K-row regions must not
+ *   overlap.  Rows that are not 16-byte aligned take an element-wise path.
+ */
+gmc_status gmc_calib_stream(void* hip_stream, float* e_dev, const float* g_dev, int64_t row_pitch, int32_t K,
+                            int64_t d);
 
 /* Message for the last non-OK status of this context (or of gmc_init when
  * ctx is NULL); never NULL. */

@@ -45,7 +45,7 @@ struct gmc_ctx {
     int32_t block = 4096;          // RBGS block length
     int force_full = 0;
     int margin = 2;
-    int cap_mult = 16;
+    int cap_mult = 64;
     int32_t stratum = 100;         // sampled-threshold top-s: components per sample stratum
     int sparse_w = 0;              // GMC_OPT_SPARSE_MOMENTUM
 
@@ -168,13 +168,22 @@ struct TopkTables {
     std::vector<int32_t> slice_seg, slice_rank, seg_slices, seg_slice_lo;
     std::vector<int32_t> pair_k, pair_cap;
     std::vector<int64_t> pair_cand;
-    std::vector<int2> tile_map;       // per worker: tile -> (segment, tile in the segment)
-    std::vector<int32_t> seg_tile_off;
+    std::vector<int2> tile_map;       // per worker: launched tile -> (segment, first tile in the segment)
+    std::vector<int32_t> seg_tile_stride, seg_tile_cap_off;
+    int32_t tiles_cap = 0;            // tile-list entries per worker
     int64_t cand_total = 0;
 };
 
 int64_t pair_capacity(const gmc_ctx* ctx, int64_t n, int64_t k) {
     return std::min<int64_t>(n, (int64_t)ctx->cap_mult * k + 2048);
+}
+
+// Candidates the selection launches are sized for: the speculative threshold
+// aims at a few k (the margin, then the growth of the residual from one step
+// to the next); longer lists, up to the capacity, are walked in strides.
+constexpr int64_t kLaunchMult = 8;
+int64_t pair_launch(const gmc_ctx* ctx, int64_t n, int64_t k) {
+    return std::min<int64_t>(pair_capacity(ctx, n, k), kLaunchMult * k + 2048);
 }
 
 TopkTables build_tables(const gmc_ctx* ctx) {
@@ -205,7 +214,8 @@ TopkTables build_tables(const gmc_ctx* ctx) {
         T.seg_cgrps.push_back(rank);
         // slices of the selection passes
         const int64_t cap = pair_capacity(ctx, n, ctx->seg_k[sg]);
-        int64_t w = std::max((n + kSliceElems - 1) / kSliceElems, (cap + kSliceCands - 1) / kSliceCands);
+        const int64_t lc = pair_launch(ctx, n, ctx->seg_k[sg]);
+        int64_t w = std::max((n + kSliceElems - 1) / kSliceElems, (lc + kSliceCands - 1) / kSliceCands);
         w = std::max<int64_t>(1, std::min<int64_t>(w, kMaxSlices));
         T.seg_slice_lo.push_back((int32_t)T.slice_seg.size());
         T.seg_slices.push_back((int32_t)w);
@@ -215,10 +225,13 @@ TopkTables build_tables(const gmc_ctx* ctx) {
         }
         T.seg_out.push_back((int32_t)out);
         out += ctx->seg_k[sg];
-        // copy tiles: at most cap/kTile whole ones plus a partial one per group
-        const int64_t ntile = (cap + kTile - 1) / kTile + rank;
-        T.seg_tile_off.push_back((int32_t)T.tile_map.size());
-        for (int64_t i = 0; i < ntile; ++i) T.tile_map.push_back(make_int2(sg, (int)i));
+        // copy tiles: a list of c candidates takes at most c/kTile whole
+        // tiles plus a partial one per group
+        T.seg_tile_cap_off.push_back(T.tiles_cap);
+        T.tiles_cap += (int32_t)((cap + kTile - 1) / kTile + rank);
+        const int64_t nlaunch = (lc + kTile - 1) / kTile + rank;
+        T.seg_tile_stride.push_back((int32_t)nlaunch);
+        for (int64_t i = 0; i < nlaunch; ++i) T.tile_map.push_back(make_int2(sg, (int)i));
     }
     for (int k = 0; k < ctx->K; ++k) {
         for (int sg = 0; sg < n_seg; ++sg) {
@@ -261,8 +274,8 @@ gmc_status prepare(gmc_ctx* ctx) {
         add(ng, 4); add(ng, 4); add(ng, 4); add(ng, 4); add(ns, 4); add(ns, 4);
         add(nsl, 4); add(nsl, 4); add(ns, 4); add(ns, 4);
         add(np, 4); add(np, 4); add(np, 8);
-        add(T.tile_map.size(), sizeof(int2)); add(ns, 4);
-        add((size_t)K * ng, 4); add((size_t)K * T.tile_map.size(), sizeof(int2));
+        add(T.tile_map.size(), sizeof(int2)); add(ns, 4); add(ns, 4);
+        add((size_t)K * ng, 4); add((size_t)K * T.tiles_cap, sizeof(int2));
         add(np, sizeof(PairState));
         add(np * kBins, 4);
         add((size_t)K * nc, 4); add((size_t)K * nc, 4); add((size_t)K * ng, 4);
@@ -333,9 +346,11 @@ gmc_status prepare(gmc_ctx* ctx) {
         GMC_HIP(ctx, hipMemcpy(tm, T.tile_map.data(), T.tile_map.size() * sizeof(int2), hipMemcpyHostToDevice));
         g.tile_map = tm;
         g.tiles_per_worker = (int32_t)T.tile_map.size();
-        GMC_TRY(put(T.seg_tile_off, &g.seg_tile_off));
+        GMC_TRY(put(T.seg_tile_stride, &g.seg_tile_stride));
+        g.tiles_cap_per_worker = T.tiles_cap;
+        GMC_TRY(put(T.seg_tile_cap_off, &g.seg_tile_cap_off));
         ctx->scr.grp_base = cv.take<uint32_t>((size_t)K * ng);
-        ctx->scr.tiles = cv.take<int2>((size_t)K * T.tile_map.size());
+        ctx->scr.tiles = cv.take<int2>((size_t)K * T.tiles_cap);
         TopkScratch& sc = ctx->scr;
         sc.pair = cv.take<PairState>(np);
         std::vector<PairState> init(np);
@@ -870,6 +885,24 @@ gmc_status gmc_stats(gmc_ctx* ctx, int64_t* out, int32_t n) {
     return GMC_OK;
 }
 
+gmc_status gmc_pair_stats(gmc_ctx* ctx, int32_t* mode, int64_t* cand, int32_t n, int32_t* n_pairs) {
+    if (!ctx || !n_pairs || n < 0 || (n > 0 && (!mode || !cand)))
+        return fail(ctx, GMC_EINVAL, "gmc_pair_stats: bad argument");
+    if (ctx->comp == GMC_RBGS) return fail(ctx, GMC_EINVAL, "gmc_pair_stats: RBGS selects no (worker, segment) pairs");
+    if (!ctx->started) return fail(ctx, GMC_ESTATE, "gmc_pair_stats: no step taken yet");
+    const int32_t np = ctx->K * ctx->geo.n_seg;
+    *n_pairs = np;
+    GMC_HIP(ctx, hipSetDevice(ctx->device));
+    GMC_HIP(ctx, hipStreamSynchronize(ctx->stream));
+    std::vector<PairState> host((size_t)np);
+    GMC_HIP(ctx, hipMemcpy(host.data(), ctx->scr.pair, sizeof(PairState) * (size_t)np, hipMemcpyDeviceToHost));
+    for (int32_t i = 0; i < n && i < np; ++i) {
+        mode[i] = host[(size_t)i].mode;
+        cand[i] = (int64_t)host[(size_t)i].cand_used;
+    }
+    return GMC_OK;
+}
+
 gmc_status gmc_profile_read(gmc_ctx* ctx, double* ms, int64_t* launches, int32_t n) {
     if (!ctx || !ms || !launches || n < 0) return fail(ctx, GMC_EINVAL, "gmc_profile_read: bad argument");
     GMC_HIP(ctx, hipSetDevice(ctx->device));
@@ -897,6 +930,19 @@ gmc_status gmc_calib_copy(void* hip_stream, float* dst_dev, const float* src_dev
     if (n == 0) return GMC_OK;
     hipError_t e = launch_calib_copy(dst_dev, src_dev, n, reinterpret_cast<hipStream_t>(hip_stream));
     if (e != hipSuccess) return hip_fail(nullptr, e, "gmc_calib_copy");
+    return GMC_OK;
+}
+
+gmc_status gmc_calib_stream(void* hip_stream, float* e_dev, const float* g_dev, int64_t row_pitch, int32_t K,
+                            int64_t d) {
+    if (!e_dev || !g_dev) return fail(nullptr, GMC_EINVAL, "gmc_calib_stream: NULL argument");
+    if (d < 1 || d >= (int64_t(1) << 31) || K < 1 || row_pitch < d)
+        return fail(nullptr, GMC_EINVAL, "gmc_calib_stream: need 1 <= d < 2^31, K >= 1, row_pitch >= d");
+    const int64_t span = (int64_t)(K - 1) * row_pitch + d;  // elements each buffer covers
+    if ((e_dev < g_dev + span) && (g_dev < e_dev + span))
+        return fail(nullptr, GMC_EINVAL, "gmc_calib_stream: e and g overlap");
+    hipError_t e = launch_calib_stream(e_dev, g_dev, row_pitch, K, (int32_t)d, reinterpret_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return hip_fail(nullptr, e, "gmc_calib_stream");
     return GMC_OK;
 }
 

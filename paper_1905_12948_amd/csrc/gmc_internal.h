@@ -27,7 +27,7 @@ constexpr int kChunk = kWave * 4 * kVecIters;   // 2048 elements
 constexpr int kCompactChunks = 256;        // chunks per compaction group (one per thread)
 constexpr int kTile = kGroup * 8;          // candidates one copy workgroup moves
 constexpr int64_t kSliceElems = 1 << 19;   // full-data elements per slice (at most)
-constexpr int64_t kSliceCands = 8192;      // candidate capacity per slice (at most)
+constexpr int64_t kSliceCands = 8192;      // usual candidates per slice (more when a list runs long)
 constexpr int kMaxSlices = 256;
 
 // Radix select over the 31-bit magnitude key in three digits: 11 + 11 + 9.
@@ -94,12 +94,17 @@ struct TopkGeometry {
     const int32_t* pair_k;        // [K*n_seg]
     const int32_t* pair_cap;      // [K*n_seg]
     const int64_t* pair_cand;     // [K*n_seg] start of the pair's candidate list
-    // copy tiles: a worker's tile capacity is tiles_per_worker; tile tt of a
-    // worker belongs to segment tile_map[tt].x as its tile tile_map[tt].y;
-    // the segment's tiles start at seg_tile_off[seg]
+    // copy tiles.  Layout: a worker's tile list (s.tiles) has room for
+    // tiles_cap_per_worker entries, segment seg's from seg_tile_cap_off[seg]
+    // (enough for a full candidate list).  Launch: tiles_per_worker
+    // workgroups per worker; workgroup tt takes segment tile_map[tt].x's
+    // tiles tile_map[tt].y, + seg_tile_stride[seg], ... (the launch is sized
+    // for the usual candidate count, the stride covers longer lists)
     int32_t tiles_per_worker;
-    const int2* tile_map;         // [tiles_per_worker]
-    const int32_t* seg_tile_off;  // [n_seg]
+    const int2* tile_map;             // [tiles_per_worker]
+    const int32_t* seg_tile_stride;   // [n_seg] workgroups launched per (worker, segment)
+    int32_t tiles_cap_per_worker;
+    const int32_t* seg_tile_cap_off;  // [n_seg]
 };
 
 struct TopkScratch {
@@ -109,7 +114,7 @@ struct TopkScratch {
     uint32_t* run_pre;            // [K*n_chunks] exclusive prefix of run_cnt within the group
     uint32_t* grp_total;          // [K*n_cgroups]
     uint32_t* grp_base;           // [K*n_cgroups] the group's first position in the pair's list
-    int2* tiles;                  // [K*tiles_per_worker] (group rank in the segment, tile in the group)
+    int2* tiles;                  // [K*tiles_cap_per_worker] (group rank in the segment, tile in the group)
     int2* slot;                   // [K*n_chunks][kChunk] candidates of (worker, chunk) in index
                                   // order: (index, bit pattern of u)
     int32_t* cand_idx;            // [sum cap] candidate lists, ascending index
@@ -218,5 +223,7 @@ hipError_t launch_apply(int32_t d, float* w, float* w_prev_out, const float* upd
 
 // plain copy of n floats (memory-counter calibration)
 hipError_t launch_calib_copy(float* dst, const float* src, int64_t n, hipStream_t st);
+// e[k][j] += g[k][j] in the fused worker pass's launch shape (stream ceiling)
+hipError_t launch_calib_stream(float* e, const float* g, int64_t pitch, int32_t K, int32_t d, hipStream_t st);
 
 }  // namespace gmc

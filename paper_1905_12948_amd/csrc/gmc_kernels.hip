@@ -774,7 +774,7 @@ __global__ __launch_bounds__(kGroup) void topk_compact_count_kernel(TopkGeometry
     const uint32_t all = carry[0];
     const bool copy = all <= (uint32_t)g.pair_cap[p];
     const bool fuse = !g.approx && !force_full && copy && all >= (uint32_t)g.pair_k[p];
-    int2* tl = s.tiles + (size_t)k * g.tiles_per_worker + g.seg_tile_off[seg];
+    int2* tl = s.tiles + (size_t)k * g.tiles_cap_per_worker + g.seg_tile_cap_off[seg];
     if (threadIdx.x == 0) carry[1] = 0u;
     __syncthreads();
     for (int r0 = 0; r0 < ng; r0 += kGroup) {
@@ -797,11 +797,14 @@ __global__ __launch_bounds__(kGroup) void topk_compact_count_kernel(TopkGeometry
     }
 }
 
-// Second half, one workgroup per (worker, tile): the tile's kTile candidates
-// of one group go to the pair's list at the group's base, so the list comes
-// out in ascending index order.  For the pairs of exact top-s that resolve
-// from their candidates the copy also histograms the first digit, and its
-// last workgroup picks it (the first histogram kernel then skips the pair).
+// Second half: the pair's candidates go, tile by tile (kTile candidates of
+// one group each), to the pair's list at their group's base, so the list
+// comes out in ascending index order.  Workgroup (worker, tile_map entry
+// (seg, i)) takes the pair's tiles i, i + stride, ... (stride = the
+// workgroups launched for the pair, sized for the usual count).  For the
+// pairs of exact top-s that resolve from their candidates the copy also
+// histograms the first digit, and the last of the pair's workgroups picks it
+// (the first histogram kernel then skips the pair).
 __global__ __launch_bounds__(kGroup) void topk_compact_copy_kernel(TopkGeometry g, TopkScratch s, int margin) {
     __shared__ uint32_t pre[kCompactChunks];
     __shared__ uint32_t h[kBins];
@@ -815,46 +818,54 @@ __global__ __launch_bounds__(kGroup) void topk_compact_copy_kernel(TopkGeometry 
     PairState* ps = &s.pair[p];
     const uint32_t n_tiles = ps->n_tiles;
     if ((uint32_t)tm.y >= n_tiles) return;
+    const uint32_t stride = (uint32_t)g.seg_tile_stride[seg];
+    const uint32_t n_wg = n_tiles < stride ? n_tiles : stride;  // workgroups of the pair with tiles
     const bool fuse = ps->fuse1 != 0u;
-    const int2 te = s.tiles[(size_t)k * g.tiles_per_worker + g.seg_tile_off[seg] + tm.y];
-    const int cg = g.seg_cgrp_lo[seg] + te.x;
-    const int clo = g.cgrp_lo[cg], nch = g.cgrp_hi[cg] - clo;
-    const size_t gi = (size_t)k * g.n_cgroups + cg;
-    const uint32_t total = s.grp_total[gi], base = s.grp_base[gi];
-    const uint32_t lo = (uint32_t)te.y * kTile;
-    const uint32_t hi = lo + kTile < total ? lo + kTile : total;
-    const size_t slot0 = (size_t)k * g.n_chunks + clo;
-    if (threadIdx.x < nch) pre[threadIdx.x] = s.run_pre[slot0 + threadIdx.x];
     if (fuse)
         for (int b = threadIdx.x; b < kBins; b += kGroup) h[b] = 0u;
-    __syncthreads();
-    int32_t* ci = s.cand_idx + g.pair_cand[p] + base;
-    float* cv = s.cand_val + g.pair_cand[p] + base;
-    int32_t jv[8];
-    float xv[8];
+    const int2* tl = s.tiles + (size_t)k * g.tiles_cap_per_worker + g.seg_tile_cap_off[seg];
+    int32_t* ci0 = s.cand_idx + g.pair_cand[p];
+    float* cv0 = s.cand_val + g.pair_cand[p];
+    for (uint32_t tt = (uint32_t)tm.y; tt < n_tiles; tt += stride) {
+        const int2 te = tl[tt];
+        const int cg = g.seg_cgrp_lo[seg] + te.x;
+        const int clo = g.cgrp_lo[cg], nch = g.cgrp_hi[cg] - clo;
+        const size_t gi = (size_t)k * g.n_cgroups + cg;
+        const uint32_t total = s.grp_total[gi], base = s.grp_base[gi];
+        const uint32_t lo = (uint32_t)te.y * kTile;
+        const uint32_t hi = lo + kTile < total ? lo + kTile : total;
+        const size_t slot0 = (size_t)k * g.n_chunks + clo;
+        __syncthreads();  // the previous tile's searches are done with pre
+        if (threadIdx.x < nch) pre[threadIdx.x] = s.run_pre[slot0 + threadIdx.x];
+        __syncthreads();
+        int32_t* ci = ci0 + base;
+        float* cv = cv0 + base;
+        int32_t jv[8];
+        float xv[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const uint32_t q = lo + i * kGroup + threadIdx.x;
-        jv[i] = 0;
-        xv[i] = 0.0f;
-        if (q < hi) {
-            int a0 = 0, a1 = nch - 1;  // chunk c with pre[c] <= q < pre[c+1]
-            while (a0 < a1) {
-                const int mid = (a0 + a1 + 1) >> 1;
-                if (pre[mid] <= q) a0 = mid; else a1 = mid - 1;
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t q = lo + i * kGroup + threadIdx.x;
+            jv[i] = 0;
+            xv[i] = 0.0f;
+            if (q < hi) {
+                int a0 = 0, a1 = nch - 1;  // chunk c with pre[c] <= q < pre[c+1]
+                while (a0 < a1) {
+                    const int mid = (a0 + a1 + 1) >> 1;
+                    if (pre[mid] <= q) a0 = mid; else a1 = mid - 1;
+                }
+                const int2 c = s.slot[(slot0 + a0) * kChunk + (q - pre[a0])];
+                jv[i] = c.x;
+                xv[i] = __int_as_float(c.y);
             }
-            const int2 c = s.slot[(slot0 + a0) * kChunk + (q - pre[a0])];
-            jv[i] = c.x;
-            xv[i] = __int_as_float(c.y);
         }
-    }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const uint32_t q = lo + i * kGroup + threadIdx.x;
-        if (q < hi) {
-            ci[q] = jv[i];
-            cv[q] = xv[i];
-            if (fuse) atomicAdd(&h[key_of(xv[i]) >> kShift1], 1u);
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t q = lo + i * kGroup + threadIdx.x;
+            if (q < hi) {
+                ci[q] = jv[i];
+                cv[q] = xv[i];
+                if (fuse) atomicAdd(&h[key_of(xv[i]) >> kShift1], 1u);
+            }
         }
     }
     if (!fuse) return;
@@ -862,7 +873,7 @@ __global__ __launch_bounds__(kGroup) void topk_compact_copy_kernel(TopkGeometry 
     uint32_t* gh = s.hist + (size_t)p * kBins;
     for (int b = threadIdx.x; b < kBins; b += kGroup)
         if (h[b]) atomicAdd(&gh[b], h[b]);
-    if (!finish_slice(&ps->done, (int)n_tiles, &sh_last)) return;
+    if (!finish_slice(&ps->done, (int)n_wg, &sh_last)) return;
     const uint32_t cand = ps->cand;
     finish_digit<1>(ps, p, h, gh, g.pair_k[p], 0, cand, 0u, margin, 0, false, g, s, sh_wsum, sh_res);
     if (threadIdx.x == 0) ps->p1_done = 1u;
@@ -1816,6 +1827,52 @@ hipError_t launch_calib_copy(float* dst, const float* src, int64_t n, hipStream_
     const int64_t threads = (n + 3) / 4;
     const int grid = (int)((threads + kGroup - 1) / kGroup);
     hipLaunchKernelGGL(calib_copy_kernel, dim3(grid), dim3(kGroup), 0, st, dst, src, n);
+    return hipGetLastError();
+}
+
+}  // namespace gmc
+
+namespace gmc {
+
+// ============================================================================
+// a plain stream in the fused worker pass's shape, the reference for how
+// close that pass comes to what the memory system gives its access pattern
+// ============================================================================
+
+// e[k][j] = e[k][j] + g[k][j] for K rows of d components (row pitch `pitch`):
+// two streamed reads and one streamed write per worker-element, one
+// workgroup per (chunk of kChunk components, worker) in the fused pass's
+// chunk-major order, 2 float4 per thread per row.
+__global__ __launch_bounds__(kGroup) void calib_stream_kernel(float* e, const float* g, int64_t pitch, int32_t K,
+                                                              int32_t d) {
+    int chunk, k;
+    run_order(blockIdx.x, K, 1, &chunk, &k);
+    const int64_t start = (int64_t)chunk * kChunk;
+    if (start >= d) return;
+    const int64_t len = (int64_t)d - start < kChunk ? (int64_t)d - start : kChunk;
+    float* ep = e + (int64_t)k * pitch + start;
+    const float* gp = g + (int64_t)k * pitch + start;
+    if (len == kChunk && aligned16(ep) && aligned16(gp)) {
+        const int o0 = threadIdx.x * 4;
+        float4 a[2], b[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            a[i] = ld4_stream(ep + o0 + i * (kGroup * 4));
+            b[i] = ld4_stream(gp + o0 + i * (kGroup * 4));
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+            st4_stream(ep + o0 + i * (kGroup * 4),
+                       make_float4(a[i].x + b[i].x, a[i].y + b[i].y, a[i].z + b[i].z, a[i].w + b[i].w));
+        return;
+    }
+    for (int64_t o = threadIdx.x; o < len; o += kGroup) ep[o] = ep[o] + gp[o];
+}
+
+hipError_t launch_calib_stream(float* e, const float* g, int64_t pitch, int32_t K, int32_t d, hipStream_t st) {
+    const int64_t chunks = ((int64_t)d + kChunk - 1) / kChunk;
+    hipLaunchKernelGGL(calib_stream_kernel, dim3((unsigned)run_order_grid(chunks, K, 1)), dim3(kGroup), 0, st, e, g,
+                       pitch, K, d);
     return hipGetLastError();
 }
 

@@ -30,7 +30,7 @@ EXPORTS = ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "g
            "gmc_index_len", "gmc_step", "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step",
            "gmc_set_option", "gmc_stats", "gmc_profile_read", "gmc_last_error", "gmc_destroy",
            "gmc_calib_copy", "gmc_aggregate_apply", "gmc_set_rule", "gmc_set_eta", "gmc_set_lambda",
-           "gmc_step_detach", "gmc_finish", "gmc_detach", "gmc_iteration")
+           "gmc_step_detach", "gmc_finish", "gmc_detach", "gmc_iteration", "gmc_calib_stream", "gmc_pair_stats")
 
 RULES = {"gmc": 0, "server_momentum": 1, "lr_in_residual": 2}
 
@@ -84,11 +84,13 @@ def load() -> ctypes.CDLL:
     lib.gmc_finish.argtypes = [P, P, P, P, P, P, P, P, P, P]
     lib.gmc_detach.argtypes = [P, P, P, P]
     lib.gmc_iteration.argtypes = [P, P, P, P, P, P, P, P]
+    lib.gmc_calib_stream.argtypes = [P, P, P, i64, i32, i64]
+    lib.gmc_pair_stats.argtypes = [P, P, P, i32, ctypes.POINTER(i32)]
     for name in ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "gmc_step",
                  "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step", "gmc_set_option",
                  "gmc_stats", "gmc_profile_read", "gmc_calib_copy", "gmc_aggregate_apply",
                  "gmc_set_rule", "gmc_set_eta", "gmc_set_lambda", "gmc_step_detach", "gmc_finish",
-                 "gmc_detach", "gmc_iteration"):
+                 "gmc_detach", "gmc_iteration", "gmc_calib_stream", "gmc_pair_stats"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -138,6 +140,25 @@ def calib_copy(dst, src):
     ps = _check(src, torch.float32, n, "src")
     lib = load()
     st = lib.gmc_calib_copy(ctypes.c_void_p(torch.cuda.current_stream(src.device).cuda_stream), pd, ps, n)
+    if st != GMC_OK:
+        raise GmcError(st, lib.gmc_last_error(None).decode())
+
+
+def calib_stream(e, g):
+    """e[k, :] += g[k, :] for two [K, d] fp32 views with the same row stride,
+    in the fused worker pass's access pattern: the stream ceiling that pass
+    is measured against."""
+    torch = _torch()
+    for name, t in (("e", e), ("g", g)):
+        if not isinstance(t, torch.Tensor) or t.dim() != 2 or t.dtype != torch.float32 \
+                or t.device.type != "cuda" or t.stride(1) != 1:
+            raise ValueError("%s must be a [K, d] float32 GPU tensor with unit inner stride" % name)
+    if e.shape != g.shape or e.stride(0) != g.stride(0):
+        raise ValueError("e and g must have the same shape and row stride")
+    K, d = e.shape
+    lib = load()
+    st = lib.gmc_calib_stream(ctypes.c_void_p(torch.cuda.current_stream(e.device).cuda_stream),
+                              e.data_ptr(), g.data_ptr(), e.stride(0), K, d)
     if st != GMC_OK:
         raise GmcError(st, lib.gmc_last_error(None).decode())
 
@@ -341,6 +362,19 @@ class Gmc:
         self._call(self._lib.gmc_stats(self._ctx, out, 8))
         keys = ("steps", "from_candidates", "full_data", "candidates", "count_errors", "sparse_momentum_steps")
         return {k: int(out[i]) for i, k in enumerate(keys)}
+
+    def pair_stats(self):
+        """(mode, cand) per (worker, segment) pair of the last step, as [K, n_seg]
+        int arrays: mode 0 = resolved from the speculative candidates, 1 =
+        full-data path; cand = candidates the worker pass collected."""
+        import numpy as np
+        np_ = ctypes.c_int32(0)
+        self._call(self._lib.gmc_pair_stats(self._ctx, None, None, 0, ctypes.byref(np_)))
+        n = np_.value
+        mode = np.zeros(n, np.int32)
+        cand = np.zeros(n, np.int64)
+        self._call(self._lib.gmc_pair_stats(self._ctx, mode.ctypes.data, cand.ctypes.data, n, ctypes.byref(np_)))
+        return mode.reshape(self.K, -1), cand.reshape(self.K, -1)
 
     def profile(self, stages=None):
         """Time the given stage names (None: all; []: off) with HIP events."""

@@ -61,6 +61,17 @@ def test_candidate_overflow_takes_full_data_path():
     assert st["full_data"] > 0
 
 
+def test_long_candidate_lists_stride_the_copy_launch():
+    # margin 16: the candidate lists run to several times the 8 k + 2048 the
+    # copy and selection launches are sized for (within the 64 k capacity),
+    # so the copy workgroups stride over the extra tiles and the slices run long
+    wl = W("resnet18").shrunk(16, K=4)
+    k = math.ceil(wl.ratio * wl.d)
+    st = run_lockstep(Case(wl, steps=4, options=((OPT_MARGIN, 16),), label="long lists"))
+    assert st["from_candidates"] >= 2 * wl.K
+    assert st["candidates"] / st["from_candidates"] > 8 * k + 2048
+
+
 def test_misaligned_rows():
     wl = synth.Workload("odd", [5000, 3, 77777, 2048 * 3 + 1], K=3, ratio=0.01, beta=0.9, eta=0.1,
                         steps=3, compressor="topk_seg", dist="normal")
