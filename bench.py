@@ -69,26 +69,30 @@ def kernel_source_hash() -> str:
 def algorithmic_bytes(wl, msg_len: int, detach: bool, sparse_w: bool = False) -> dict:
     """Bytes one step must move (per step, whole job), and those of the fused
     worker pass alone.  top-s: read g, read e, write e (12 B per worker-
-    element); read w_t, w_prev for the momentum term and read + write w in
-    the apply (16 B per element); write (idx, val) and read them back in the
-    aggregation (16 B per message entry).  RBGS sends values only (8 B).
-    GMC+'s detached points add one write per worker-element (4 B).
+    element); read w_t, w_prev for the momentum term and read w_t, write
+    w_{t+1} in the apply (8 B per element each); write (idx, val) and read
+    them back in the aggregation (16 B per message entry).  RBGS sends values
+    only (8 B).  GMC+'s detached points add one write per worker-element.
 
-    With the sparse momentum term (w_t - w_prev is +0 off the components the
-    last server pass changed) the worker pass reads, instead of w_t and
-    w_prev, the server pass's bitmap (d/8 B, written once and read once) and
-    w_t, w_prev at the changed components: at most the K message entries
-    (8 B each).  GMC+'s detached points still read w_t (4 B per element)."""
+    With the sparse momentum term the parameters move only where they change:
+    w_t - w_prev is +0 off the components the last server pass changed, so
+    the worker pass reads that pass's bitmap (d/8 B) and w_t, w_prev at most
+    at the K message entries (8 B each); the server pass reads the old
+    bitmap, writes the new one and reads w_t, writes w_{t+1} at most at the
+    old and the new entries (2 x 8 B each).  GMC+'s detached points still
+    read w_t whole (4 B per element)."""
     K, d = wl.K, wl.d
-    per_msg = 8 if wl.compressor == "rbgs" else 16
-    w_momentum = 8 * d
+    rbgs = wl.compressor == "rbgs"
+    per_msg = 8 if rbgs else 16
+    sent = K * msg_len
     if sparse_w:
-        w_momentum = d // 8 + 8 * K * msg_len + (4 * d if detach else 0)
-    step = 12 * K * d + w_momentum + 8 * d + per_msg * K * msg_len + (d // 8 if sparse_w else 0)
-    fused = 12 * K * d + w_momentum + (4 * K * msg_len if wl.compressor == "rbgs" else 0)
-    if detach:
-        step += 4 * K * d
-        fused += 4 * K * d
+        w_worker = d // 8 + 8 * sent + (4 * d if detach else 0)
+        w_server = 2 * (d // 8) + 16 * sent
+    else:
+        w_worker, w_server = 8 * d, 8 * d
+    points = 4 * K * d if detach else 0
+    step = 12 * K * d + w_worker + w_server + per_msg * sent + points
+    fused = 12 * K * d + w_worker + (4 * sent if rbgs else 0) + points
     return {"step": step, "fused": fused}
 
 
@@ -157,7 +161,7 @@ def main():
     ap.add_argument("--workload", default="resnet50", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--grad-batches", type=int, default=4)
     ap.add_argument("--margin", type=int, default=None,
-                    help="candidate margin (multiple of k) of the speculative selection")
+                    help="rank of the speculative threshold in quarters of k (default 6)")
     ap.add_argument("--lam", type=float, default=None,
                     help="GMC+ detach coefficient (default 0.5 for the rbgs workload, else 0: plain GMC)")
     ap.add_argument("--dense-momentum", action="store_true",
@@ -284,7 +288,7 @@ def main():
         roofline["stream_ceiling"] = stream
     value = K * d / (ms_step * 1e-3) / 1e9
     sel = {k: stats1[k] - stats0[k] for k in ("from_candidates", "full_data", "candidates",
-                                              "sparse_momentum_steps")}
+                                              "sparse_momentum_steps", "sparse_applies")}
     out = {
         "metric": METRIC if wl.name == "resnet50" else METRIC.split(",")[0] + ", " + wl.name,
         "value": round(value, 2), "unit": UNIT, "n_gpus": 1,

@@ -279,7 +279,12 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
  * Tuning and test options (value semantics per option):
  *   GMC_OPT_FORCE_FULL_SELECT  1: every top-s selection takes the full-data
  *                              path (no speculative candidates)
- *   GMC_OPT_CAND_MARGIN        candidate target as a multiple of k (>= 1)
+ *   GMC_OPT_CAND_MARGIN        rank of the next step's speculative threshold,
+ *                              in quarters of k (4..4096; default 6: the
+ *                              threshold sits at the floor of the 22-bit key
+ *                              bin holding this step's key of rank 1.5 k, and
+ *                              the residual's growth brings about 2.5-3.5 k
+ *                              candidates the next step)
  *   GMC_OPT_CAND_CAP_MULT      candidate capacity as a multiple of k (>= 1);
  *                              reallocates scratch; before the first step
  *   GMC_OPT_PROFILE            bit mask of the stages to time with HIP events
@@ -287,20 +292,24 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
  *                              gmc_profile_read for the stage numbers
  *   GMC_OPT_SAMPLE_STRATUM     GMC_TOPK_APPROX: components per sample stratum
  *                              L in [1, d] (default 100); before the first step
- *   GMC_OPT_SPARSE_MOMENTUM    1: the caller promises not to change w between
- *                              a server pass and the next gmc_step (default
- *                              0).  Then a server pass out of place
- *                              (gmc_aggregate_apply, gmc_finish; not with
- *                              momentum on the server) records which
- *                              components it changed, and when the next
- *                              gmc_step gets that pass's output as w_t and its
- *                              input as w_prev, the worker pass reads w_t and
- *                              w_prev only there: everywhere else
- *                              w_t - w_prev is exactly +0, as in Algorithm 1,
- *                              where the workers receive the server's sparse
- *                              w_{t+1} - w_t.  Results are bit for bit those
- *                              of the dense path; other calls, or other
- *                              buffers, fall back to it.
+ *   GMC_OPT_SPARSE_MOMENTUM    1: the caller promises not to change either
+ *                              parameter buffer between a server pass and the
+ *                              next server pass (default 0).  Then a server
+ *                              pass out of place (gmc_aggregate_apply,
+ *                              gmc_finish, gmc_iteration; not with momentum on
+ *                              the server) records which components it
+ *                              changed, and when the next gmc_step gets that
+ *                              pass's output as w_t and its input as w_prev,
+ *                              the worker pass reads w_t and w_prev only there:
+ *                              everywhere else w_t - w_prev is exactly +0, as
+ *                              in Algorithm 1, where the workers receive the
+ *                              server's sparse w_{t+1} - w_t.  The server pass
+ *                              that follows, writing over w_prev's buffer,
+ *                              writes w_{t+1} only in the 32-component words
+ *                              where it differs from w_{t-1} (the recorded
+ *                              components and the ones sent now).  Results
+ *                              are bit for bit those of the dense path; other
+ *                              calls, or other buffers, fall back to it.
  */
 enum {
     GMC_OPT_FORCE_FULL_SELECT = 1,
@@ -319,6 +328,8 @@ gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value);
  *   [4] selections whose count check failed (must stay 0)
  *   [5] worker passes that read w only at the last server pass's changed
  *       components (GMC_OPT_SPARSE_MOMENTUM)
+ *   [6] server passes that wrote w_{t+1} only where their output buffer
+ *       did not hold it yet (GMC_OPT_SPARSE_MOMENTUM)
  */
 gmc_status gmc_stats(gmc_ctx* ctx, int64_t* out, int32_t n);
 

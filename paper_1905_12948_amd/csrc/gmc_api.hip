@@ -44,7 +44,7 @@ struct gmc_ctx {
     std::vector<int64_t> seg_off;  // top-s segments (host)
     int32_t block = 4096;          // RBGS block length
     int force_full = 0;
-    int margin = 2;
+    int margin = 6;                // speculative threshold rank, quarters of k (1.5 k)
     int cap_mult = 64;
     int32_t stratum = 100;         // sampled-threshold top-s: components per sample stratum
     int sparse_w = 0;              // GMC_OPT_SPARSE_MOMENTUM
@@ -56,6 +56,14 @@ struct gmc_ctx {
     const float* wbits_out = nullptr;  // ... and w_{t+1}
     int64_t wbits_t = -1;              // the step the bitmap serves
     int64_t sparse_steps = 0;          // worker passes that used it
+    // the bitmap still describes its pass's two buffers (cleared by calls
+    // that write w or drop the marks), and the step at which a worker pass
+    // last read w through it (-1: the last worker pass did not): together
+    // they let the next server pass, writing over that pass's input buffer,
+    // skip the components where the buffer already holds w_{t+1}
+    bool wbits_pair = false;
+    int64_t wbits_used_t = -1;
+    int64_t sparse_applies = 0;        // server passes that wrote w only where it changes
 
     // derived
     std::vector<int32_t> seg_k;
@@ -278,6 +286,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         add((size_t)K * ng, 4); add((size_t)K * T.tiles_cap, sizeof(int2));
         add(np, sizeof(PairState));
         add(np * kBins, 4);
+        add(np * kBins, 4);
         add((size_t)K * nc, 4); add((size_t)K * nc, 4); add((size_t)K * ng, 4);
         add((size_t)K * nc * kChunk, sizeof(int2));
         add((size_t)T.cand_total, 4); add((size_t)T.cand_total, 4);
@@ -299,6 +308,8 @@ gmc_status prepare(gmc_ctx* ctx) {
     ctx->stats = cv.take<int64_t>(8);
     ctx->wbits = cv.take<uint32_t>((size_t)(ctx->d + 31) / 32);
     ctx->wbits_valid = false;
+    ctx->wbits_pair = false;
+    ctx->wbits_used_t = -1;
     if (ctx->comp == GMC_RBGS) {
         ctx->rbgs_bitmap = cv.take<uint32_t>((ctx->nb + 31) / 32);
         ctx->rbgs_blocks = cv.take<int32_t>(ctx->n_sel);
@@ -360,6 +371,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         }
         GMC_HIP(ctx, hipMemcpy(sc.pair, init.data(), np * sizeof(PairState), hipMemcpyHostToDevice));
         sc.hist = cv.take<uint32_t>(np * kBins);
+        sc.hist2 = cv.take<uint32_t>(np * kBins);
         sc.run_cnt = cv.take<uint32_t>((size_t)K * nc);
         sc.run_pre = cv.take<uint32_t>((size_t)K * nc);
         sc.grp_total = cv.take<uint32_t>((size_t)K * ng);
@@ -564,6 +576,7 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
                   ? ctx->wbits
                   : nullptr;
     ctx->wbits_valid = false;
+    ctx->wbits_used_t = a.wbits ? ctx->t : -1;
     if (a.wbits) ++ctx->sparse_steps;
     for (int k = 0; k < ctx->K; ++k) {
         if (!grads_dev[k] || !err_dev[k] || (y_dev && !y_dev[k]))
@@ -668,6 +681,17 @@ gmc_status aggregate_impl(gmc_ctx* ctx, const int32_t* idx_dev, const float* val
     // on the server (w_{t+1} differs from w_t everywhere there)
     const bool mark = ctx->sparse_w && f.w_in && f.w_out && f.w_in != f.w_out && ctx->rule != kRuleServerMomentum;
     f.wbits = mark ? ctx->wbits : nullptr;
+    // w_out is the last pass's input buffer and w_in its output, and the
+    // worker pass in between read them through that pass's bitmap: w_out
+    // still holds w_{t-1}, which equals w_t off the marks, and w_{t+1}
+    // equals w_t off the marks and this pass's sent components
+    f.sparse_apply = (mark && ctx->wbits_pair && ctx->wbits_used_t == ctx->t - 1 && ctx->wbits_in == f.w_out &&
+                      ctx->wbits_out == f.w_in)
+                         ? 1
+                         : 0;
+    if (f.sparse_apply) ++ctx->sparse_applies;
+    ctx->wbits_used_t = -1;
+    ctx->wbits_pair = mark;
     ctx->wbits_valid = mark;
     ctx->wbits_in = f.w_in;
     ctx->wbits_out = f.w_out;
@@ -788,6 +812,7 @@ gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const fl
     if (ctx->rule == kRuleServerMomentum)
         return fail(ctx, GMC_EINVAL, "gmc_apply: momentum on the server needs w_{t-1}; use gmc_finish");
     ctx->wbits_valid = false;
+    ctx->wbits_pair = false;
     GMC_HIP(ctx, hipSetDevice(ctx->device));
     hipEvent_t ev;
     GMC_TRY(prof_begin(ctx, 5, &ev));
@@ -832,6 +857,9 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t) {
     if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_set_step: ctx is NULL");
     if (t < 0) return fail(ctx, GMC_EINVAL, "gmc_set_step: t must be >= 0");
     ctx->t = t;
+    ctx->wbits_valid = false;  // a resume may bring other parameters
+    ctx->wbits_pair = false;
+    ctx->wbits_used_t = -1;
     return GMC_OK;
 }
 
@@ -842,7 +870,8 @@ gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value) {
             ctx->force_full = value ? 1 : 0;
             return GMC_OK;
         case GMC_OPT_CAND_MARGIN:
-            if (value < 1 || value > 1024) return fail(ctx, GMC_EINVAL, "gmc_set_option: margin must be in [1, 1024]");
+            if (value < 4 || value > 4096)
+                return fail(ctx, GMC_EINVAL, "gmc_set_option: margin (quarters of k) must be in [4, 4096]");
             ctx->margin = (int)value;
             return GMC_OK;
         case GMC_OPT_CAND_CAP_MULT:
@@ -862,6 +891,8 @@ gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value) {
         case GMC_OPT_SPARSE_MOMENTUM:
             ctx->sparse_w = value ? 1 : 0;
             ctx->wbits_valid = false;
+            ctx->wbits_pair = false;
+            ctx->wbits_used_t = -1;
             return GMC_OK;
         case GMC_OPT_PROFILE:
             if (ctx->profile) GMC_HIP(ctx, hipStreamSynchronize(ctx->stream));
@@ -881,6 +912,7 @@ gmc_status gmc_stats(gmc_ctx* ctx, int64_t* out, int32_t n) {
     if (ctx->stats) GMC_HIP(ctx, hipMemcpy(host, ctx->stats, sizeof host, hipMemcpyDeviceToHost));
     host[0] = ctx->t;
     host[5] = ctx->sparse_steps;
+    host[6] = ctx->sparse_applies;
     for (int32_t i = 0; i < n && i < 8; ++i) out[i] = host[i];
     return GMC_OK;
 }

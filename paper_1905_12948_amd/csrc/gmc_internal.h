@@ -28,6 +28,7 @@ constexpr int kCompactChunks = 256;        // chunks per compaction group (one p
 constexpr int kTile = kGroup * 8;          // candidates one copy workgroup moves
 constexpr int64_t kSliceElems = 1 << 19;   // full-data elements per slice (at most)
 constexpr int64_t kSliceCands = 8192;      // usual candidates per slice (more when a list runs long)
+constexpr int64_t kHistSliceCands = 8192;  // candidates per histogram-pass workgroup (fewer workgroups)
 constexpr int kMaxSlices = 256;
 
 // Radix select over the 31-bit magnitude key in three digits: 11 + 11 + 9.
@@ -66,7 +67,13 @@ struct PairState {
     uint32_t n_tiles;   // copy tiles of this step's candidate list (0: not copied)
     uint32_t fuse1;     // 1: the copy kernel also does the first histogram pass
     uint32_t p1_done;   // 1: it has (the first histogram kernel skips the pair)
-    uint32_t pad[3];
+    // exact top-s: the first pass puts the next step's threshold at the floor
+    // of the 11-bit bin tau_bin holding the key of rank margin*k; with
+    // tau_fine the second pass narrows it to the floor of the 22-bit bin
+    // holding that key, the tau_need-th of bin tau_bin from the top
+    uint32_t tau_bin;
+    uint32_t tau_need;
+    uint32_t tau_fine;
 };
 
 // Static geometry of the top-s selection (built on the host at init).
@@ -110,6 +117,7 @@ struct TopkGeometry {
 struct TopkScratch {
     PairState* pair;              // [K*n_seg]
     uint32_t* hist;               // [K*n_seg][kBins]
+    uint32_t* hist2;              // [K*n_seg][kBins] second-digit histogram of the threshold's bin
     uint32_t* run_cnt;            // [K*n_chunks] candidates of (worker, chunk)
     uint32_t* run_pre;            // [K*n_chunks] exclusive prefix of run_cnt within the group
     uint32_t* grp_total;          // [K*n_cgroups]
@@ -162,6 +170,11 @@ struct FinishArgs {
     // nullable, [ceil(d/32)]: bit j set where some worker sent j or w_{t+1}[j]
     // is not finite; everywhere else w_{t+1}[j] equals w_t[j] bit for bit
     uint32_t* wbits;
+    // 1 (with wbits): wbits holds, on entry, the previous pass's marks, and
+    // w_out holds that pass's input w_{t-1}, which equals w_in = w_t off
+    // those marks: w_out is written only in the 32-component words where
+    // the old marks or this pass's sent components fall
+    int32_t sparse_apply;
     const float* e[kMaxWorkers];  // e_{t+1,k}
     float* y[kMaxWorkers];        // w_{t+1,k}
 };

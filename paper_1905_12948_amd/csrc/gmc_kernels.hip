@@ -598,13 +598,11 @@ __device__ __forceinline__ bool finish_slice(uint32_t* done, int W, int* sh_flag
 // The last workgroup of a pair after a histogram pass: reads and clears the
 // pair's global histogram, picks the digit and updates the pair's state; pass
 // 1 also sets the next step's candidate threshold.  h: [kBins] in LDS.
-template <int PASS>
-__device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, int kp, int mode, uint32_t cand,
-                             uint32_t prefix, int margin, int force_full, bool approx, const TopkGeometry& g,
-                             const TopkScratch& s, uint32_t* sh_wsum, int* sh_res) {
-    constexpr int nbins = PASS == 3 ? 512 : kBins;
+// The pair's global histogram gh into LDS h (nbins, a multiple of kGroup),
+// clearing gh for the next step; all of a thread's loads in flight at once.
+template <int nbins>
+__device__ __forceinline__ void take_hist(uint32_t* h, uint32_t* gh) {
     constexpr int per = nbins / kGroup;
-    // all of this thread's loads in flight at once, then the clears
     uint32_t v[per];
 #pragma unroll
     for (int i = 0; i < per; ++i) v[i] = load_agent(&gh[threadIdx.x + i * kGroup]);
@@ -614,26 +612,66 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
         store_agent(&gh[threadIdx.x + i * kGroup], 0u);
     }
     __syncthreads();
+}
+
+// take_hist for two histograms at once.
+template <int nbins>
+__device__ __forceinline__ void take_hist2(uint32_t* h, uint32_t* gh, uint32_t* h2, uint32_t* gh2) {
+    constexpr int per = nbins / kGroup;
+    uint32_t v[per], v2[per];
+#pragma unroll
+    for (int i = 0; i < per; ++i) {
+        v[i] = load_agent(&gh[threadIdx.x + i * kGroup]);
+        v2[i] = load_agent(&gh2[threadIdx.x + i * kGroup]);
+    }
+#pragma unroll
+    for (int i = 0; i < per; ++i) {
+        h[threadIdx.x + i * kGroup] = v[i];
+        h2[threadIdx.x + i * kGroup] = v2[i];
+        store_agent(&gh[threadIdx.x + i * kGroup], 0u);
+        store_agent(&gh2[threadIdx.x + i * kGroup], 0u);
+    }
+    __syncthreads();
+}
+
+// margin: the speculative threshold's rank, in quarters of k.  h2/gh2: the
+// second pass's histogram of the threshold's bin (PASS 2 only; gh2 holds it
+// unless that bin is the one h covers).
+template <int PASS>
+__device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, int kp, int mode, uint32_t cand,
+                             uint32_t prefix, int margin, int force_full, bool approx, const TopkGeometry& g,
+                             const TopkScratch& s, uint32_t* sh_wsum, int* sh_res, uint32_t* h2 = nullptr,
+                             uint32_t* gh2 = nullptr) {
+    constexpr int nbins = PASS == 3 ? 512 : kBins;
+    // second pass: the threshold's bin histogram comes in with T's
+    const bool fine2 = PASS == 2 && ps->tau_fine != 0u && ps->tau_bin != prefix;
+    if (fine2) take_hist2<kBins>(h, gh, h2, gh2);
+    else take_hist<nbins>(h, gh);
     const uint32_t need = PASS == 1 ? (uint32_t)kp : (uint32_t)ps->need;
     uint32_t above = 0;
     const int bin = find_bin(h, nbins, need, &above, sh_wsum, sh_res);
 
     if (PASS == 1) {
-        // speculative threshold of the next step: the lowest bin down to
-        // which at least margin*k components were counted this step
+        // speculative threshold of the next step: the floor of the bin that
+        // holds the key of rank margin*k/4 this step (the second pass of
+        // exact top-s narrows it to 22 bits)
         uint32_t mine = 0;
         for (int b = threadIdx.x; b < nbins; b += kGroup) mine += h[b];
         uint32_t total;
         block_scan_excl(mine, &total, sh_wsum);
-        const uint64_t want64 = (uint64_t)margin * (uint64_t)kp;
+        const uint64_t want64 = ((uint64_t)margin * (uint64_t)kp + 3) / 4;
         const uint32_t want = (uint32_t)(want64 < total ? want64 : total);
         uint32_t ab2 = 0;
         int tb = find_bin(h, nbins, want, &ab2, sh_wsum, sh_res);
         if (threadIdx.x == 0) {
-            if (want64 > total && tb > 0) --tb;  // too few counted: widen by one bin
+            const bool widen = want64 > total;
+            if (widen && tb > 0) --tb;  // too few counted: widen by one bin
             if (tb < 0) tb = 0;
             ps->tau_used = ps->tau;
             ps->tau = (uint32_t)tb << kShift1;
+            ps->tau_fine = (!approx && !widen) ? 1u : 0u;
+            ps->tau_bin = (uint32_t)tb;
+            ps->tau_need = want - ab2;
             ps->mode = mode;
             ps->cand_used = cand;
             ps->cand = 0u;  // every workgroup of the pair has read it
@@ -668,7 +706,18 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
                 if (m == 0) atomicAdd((unsigned long long*)&s.stats[3], (unsigned long long)cu);
             }
         }
-        store_agent(&ps->done, 0u);
+        if (PASS != 2) store_agent(&ps->done, 0u);
+    }
+    if (PASS == 2) {
+        // the speculative threshold at the floor of the 22-bit bin holding
+        // the key of rank margin*k/4: the tau_need-th key of bin tau_bin
+        if (ps->tau_fine) {
+            const uint32_t tb = ps->tau_bin;
+            uint32_t ab = 0;
+            const int sb = find_bin(fine2 ? h2 : h, kBins, ps->tau_need, &ab, sh_wsum, sh_res);
+            if (threadIdx.x == 0 && sb >= 0) ps->tau = (tb << kShift1) | ((uint32_t)sb << kShift2);
+        }
+        if (threadIdx.x == 0) store_agent(&ps->done, 0u);
     }
 }
 
@@ -677,6 +726,7 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
                                                            int force_full, int margin) {
     constexpr int nbins = PASS == 3 ? 512 : kBins;
     __shared__ uint32_t h[kBins];
+    __shared__ uint32_t h2[PASS == 2 ? kBins : 1];
     __shared__ uint32_t sh_wsum[kWavesPerGroup];
     __shared__ int sh_res[2];
     __shared__ int sh_last;
@@ -692,26 +742,45 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
                      : PASS == 1 ? ((force_full || cand < (uint32_t)kp || cand > (uint32_t)g.pair_cap[id.p]) ? 1 : 0)
                                  : ps->mode;
     const uint32_t prefix = PASS == 1 ? 0u : ps->prefix;
+    // a candidate list is histogrammed in slices of about kHistSliceCands
+    // (each workgroup merges its slice's histogram into the pair's with one
+    // global atomic per nonzero bin, so fewer, fuller slices cost less); the
+    // other workgroups of the pair leave at once
+    const int W = mode == 0 ? max(1, min(id.W, (int)((cand + kHistSliceCands - 1) / kHistSliceCands))) : id.W;
+    if (id.w >= W) return;
+    // second pass: also the second digit of the speculative threshold's bin
+    // when it is not T's
+    const uint32_t tbin = ps->tau_bin;
+    const bool fine2 = PASS == 2 && ps->tau_fine != 0u && tbin != prefix;
 
-    for (int b = threadIdx.x; b < nbins; b += kGroup) h[b] = 0u;
+    for (int b = threadIdx.x; b < nbins; b += kGroup) {
+        h[b] = 0u;
+        if (PASS == 2) h2[b] = 0u;
+    }
     __syncthreads();
-    const Slice v = open_slice(mode, cand, id.k, id.seg, id.p, id.w, id.W, a, g, s);
+    const Slice v = open_slice(mode, cand, id.k, id.seg, id.p, id.w, W, a, g, s);
     for_slice<false>(v, [&](uint32_t key, int32_t) {
         if (PASS == 1) {
             atomicAdd(&h[key >> kShift1], 1u);
         } else if (PASS == 2) {
-            if ((key >> kShift1) == prefix) atomicAdd(&h[(key >> kShift2) & (kBins - 1)], 1u);
+            const uint32_t d1 = key >> kShift1;
+            if (d1 == prefix) atomicAdd(&h[(key >> kShift2) & (kBins - 1)], 1u);
+            else if (fine2 && d1 == tbin) atomicAdd(&h2[(key >> kShift2) & (kBins - 1)], 1u);
         } else {
             if ((key >> kShift2) == prefix) atomicAdd(&h[key & 511u], 1u);
         }
     });
     __syncthreads();
     uint32_t* gh = s.hist + (size_t)id.p * kBins;
-    for (int b = threadIdx.x; b < nbins; b += kGroup)
+    uint32_t* gh2 = s.hist2 + (size_t)id.p * kBins;
+    for (int b = threadIdx.x; b < nbins; b += kGroup) {
         if (h[b]) atomicAdd(&gh[b], h[b]);
-    if (!finish_slice(&ps->done, id.W, &sh_last)) return;
+        if (fine2 && h2[b]) atomicAdd(&gh2[b], h2[b]);
+    }
+    if (!finish_slice(&ps->done, W, &sh_last)) return;
 
-    finish_digit<PASS>(ps, id.p, h, gh, kp, mode, cand, prefix, margin, force_full, approx, g, s, sh_wsum, sh_res);
+    finish_digit<PASS>(ps, id.p, h, gh, kp, mode, cand, prefix, margin, force_full, approx, g, s, sh_wsum, sh_res,
+                       PASS == 2 ? h2 : nullptr, gh2);
 }
 
 hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
@@ -1404,12 +1473,30 @@ __device__ __forceinline__ void flush_marks(const uint32_t* wb, int64_t base, in
     if ((int)threadIdx.x < words) wbits[(base >> 5) + threadIdx.x] = wb[threadIdx.x];
 }
 
+// Sparse apply (f.sparse_apply): the range's words of the previous pass's
+// marks (read before this pass overwrites them), or-ed with the components
+// some worker sent now.  Where a word is zero, w_out already holds w_{t+1}:
+// w_{t-1} = w_t there (unmarked), and w_{t+1} = w_t + (-0) = w_t (finite,
+// nothing sent).
+__device__ __forceinline__ void visit_words(uint32_t* wv, const unsigned char* hit, int64_t base, int64_t n,
+                                            const uint32_t* wbits) {
+    const int words = (int)((n + 31) / 32);
+    for (int w = threadIdx.x; w < words; w += kGroup) {
+        uint32_t m = wbits[(base >> 5) + w];
+        const int lim = n - w * 32 < 32 ? (int)(n - w * 32) : 32;
+        for (int b = 0; b < lim; ++b) m |= hit[w * 32 + b] ? (1u << b) : 0u;
+        wv[w] = m;
+    }
+    __syncthreads();
+}
+
 // Writes update = -(s * acc) for the n components of a range starting at base
-// (when f.update is not NULL) and, with kApply, w_out = next_w(w_in, update);
-// with f.wbits also marks the components for the next worker pass in wb.
+// (when f.update is not NULL) and, with kApply, w_out = next_w(w_in, update),
+// only in the words wv marks when wv is not NULL (sparse apply); with f.wbits
+// also marks the components for the next worker pass in wb.
 template <bool kApply>
 __device__ __forceinline__ void write_update(const float* acc, const unsigned char* hit, uint32_t* wb, int64_t base,
-                                             int64_t n, const FinishArgs& f) {
+                                             int64_t n, const FinishArgs& f, const uint32_t* wv) {
     const float s = f.s;
     const bool vec = n == kAggRange && (base & 3) == 0 && (f.update == nullptr || aligned16(f.update)) &&
                      (!kApply || (aligned16(f.w_in) && aligned16(f.w_out) &&
@@ -1419,7 +1506,7 @@ __device__ __forceinline__ void write_update(const float* acc, const unsigned ch
             const int64_t j = base + q;
             const float4 dl = make_float4(-(s * acc[q]), -(s * acc[q + 1]), -(s * acc[q + 2]), -(s * acc[q + 3]));
             if (f.update) st4(f.update + j, dl);
-            if (kApply) {
+            if (kApply && (!wv || wv[q >> 5])) {
                 const float4 x = ld4(f.w_in + j);
                 float4 nx = make_float4(x.x + dl.x, x.y + dl.y, x.z + dl.z, x.w + dl.w);
                 if (f.w_prev) {  // momentum on the server
@@ -1438,7 +1525,7 @@ __device__ __forceinline__ void write_update(const float* acc, const unsigned ch
         const int64_t j = base + q;
         const float dl = -(s * acc[q]);
         if (f.update) f.update[j] = dl;
-        if (kApply) {
+        if (kApply && (!wv || wv[q >> 5])) {
             const float wn = next_w(f.w_in[j], dl, f.w_prev, j, f.b);
             f.w_out[j] = wn;
             if (f.wbits && (hit[q] || not_finite(wn))) atomicOr(&wb[q >> 5], 1u << (q & 31));
@@ -1514,6 +1601,7 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
     __shared__ float acc[kAggRange];
     __shared__ unsigned char hit[kAggRange];
     __shared__ uint32_t wb[kAggRange / 32];
+    __shared__ uint32_t wv[kAggRange / 32];
     __shared__ int32_t st_idx[kAggStage];
     __shared__ float st_val[kAggStage];
     __shared__ int32_t src[kMaxWorkers];
@@ -1527,7 +1615,12 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
                                   (f.w_prev == nullptr || aligned16(f.w_prev))));
     // this thread's components: [base + 4t, +4) and [base + 1024 + 4t, +4)
     const int q0 = threadIdx.x * 4, q1 = kGroup * 4 + threadIdx.x * 4;
+    const bool sparse = kApply && f.sparse_apply;
     float4 w0 = make_float4(0.f, 0.f, 0.f, 0.f), w1 = w0, p0 = w0, p1 = w0;
+    // w_t is fetched up front, while the messages are staged and summed,
+    // also for the sparse apply, which then writes only some words: the
+    // fetch is off the kernel's critical path, a fetch that waited for the
+    // marks would be on it
     if (kApply && vec) {
         w0 = ld4(f.w_in + base + q0);
         w1 = ld4(f.w_in + base + q1);
@@ -1540,7 +1633,12 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
         acc[q] = 0.0f;
         hit[q] = 0;
     }
-    if (threadIdx.x < kAggRange / 32) wb[threadIdx.x] = 0u;
+    if (threadIdx.x < kAggRange / 32) {
+        wb[threadIdx.x] = 0u;
+        // sparse apply: the previous pass's marks of the range; the sent
+        // components are or-ed in as the messages are read
+        if (sparse) wv[threadIdx.x] = threadIdx.x < (n + 31) / 32 ? f.wbits[(base >> 5) + threadIdx.x] : 0u;
+    }
     if (threadIdx.x < K) {
         const int32_t* rp = rowptr + (size_t)threadIdx.x * (n_ranges + 1);
         const int32_t lo = rp[r], hi = rp[r + 1];
@@ -1559,8 +1657,11 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             int k = 0;
             while (i >= pre[k + 1]) ++k;
             const int64_t q = (int64_t)src[k] + (i - pre[k]);
-            st_idx[i] = idx[(size_t)k * idx_row + q];
+            const int32_t jj = idx[(size_t)k * idx_row + q];
+            st_idx[i] = jj;
             st_val[i] = val[(size_t)k * val_row + q];
+            const int64_t j = (int64_t)jj - base;
+            if (sparse && j >= 0 && j < kAggRange) atomicOr(&wv[j >> 5], 1u << (j & 31));
         }
         __syncthreads();
         for (int k = 0; k < K; ++k) {
@@ -1583,6 +1684,7 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
                 if (j >= 0 && j < kAggRange) {
                     acc[j] = acc[j] + val[(size_t)k * val_row + q];
                     hit[j] = 1;
+                    if (sparse) atomicOr(&wv[j >> 5], 1u << (j & 31));
                 }
             }
             __syncthreads();
@@ -1596,7 +1698,18 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             st4(f.update + base + q0, d0);
             st4(f.update + base + q1, d1);
         }
-        if (kApply) {
+        if (kApply && sparse) {  // only the words where w_out does not hold w_{t+1} yet
+            if (wv[q0 >> 5]) {
+                const float4 n0 = make_float4(w0.x + d0.x, w0.y + d0.y, w0.z + d0.z, w0.w + d0.w);
+                st4(f.w_out + base + q0, n0);
+                atomicOr(&wb[q0 >> 5], mark4(hit, q0, n0) << (q0 & 31));
+            }
+            if (wv[q1 >> 5]) {
+                const float4 n1 = make_float4(w1.x + d1.x, w1.y + d1.y, w1.z + d1.z, w1.w + d1.w);
+                st4(f.w_out + base + q1, n1);
+                atomicOr(&wb[q1 >> 5], mark4(hit, q1, n1) << (q1 & 31));
+            }
+        } else if (kApply) {
             float4 n0 = make_float4(w0.x + d0.x, w0.y + d0.y, w0.z + d0.z, w0.w + d0.w);
             float4 n1 = make_float4(w1.x + d1.x, w1.y + d1.y, w1.z + d1.z, w1.w + d1.w);
             if (f.w_prev) {  // momentum on the server
@@ -1614,7 +1727,7 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             }
         }
     } else {
-        write_update<kApply>(acc, hit, wb, base, n, f);
+        write_update<kApply>(acc, hit, wb, base, n, f, sparse ? wv : nullptr);
     }
     if (kApply && f.wbits) flush_marks(wb, base, n, f.wbits);
     if (kApply && f.detach) finish_detach(hit, base, n, K, f);
@@ -1642,8 +1755,10 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
     __shared__ float acc[kAggRange];
     __shared__ unsigned char hit[kAggRange];
     __shared__ uint32_t wb[kAggRange / 32];
+    __shared__ uint32_t wv[kAggRange / 32];
     const int64_t base = (int64_t)blockIdx.x * kAggRange;
     const int64_t n = (int64_t)d - base < kAggRange ? (int64_t)d - base : kAggRange;
+    const bool sparse = kApply && f.sparse_apply;
     if (threadIdx.x < kAggRange / 32) wb[threadIdx.x] = 0u;
     if (f.wbits) __syncthreads();  // wb cleared before any mark
     const bool vec = n == kAggRange && (B & 3) == 0 && aligned16(val) && (val_row & 3) == 0 &&
@@ -1654,17 +1769,23 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
         // two float4 per thread; each lies in one block (B % 4 == 0), whose
         // slot says where its values sit in every message
         const float s = f.s;
-        float4 wv[2], pv[2];
+        float4 wx[2], pv[2];
         int64_t js[2];
         int32_t slots[2], bs[2];
+        bool visit[2];
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             js[i] = base + i * (kGroup * 4) + threadIdx.x * 4;
             bs[i] = (int32_t)(js[i] / B);
             slots[i] = block_slot[bs[i]];
-            wv[i] = pv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (kApply) {
-                wv[i] = ld4(f.w_in + js[i]);
+            // sparse apply: the four components need writing where the
+            // previous marks fall or the block was sent (j is a multiple of
+            // 4, so its four bits sit in one word; flush_marks rewrites the
+            // words only after a barrier)
+            visit[i] = !sparse || slots[i] >= 0 || ((f.wbits[js[i] >> 5] >> (js[i] & 31)) & 0xfu) != 0u;
+            wx[i] = pv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (kApply && visit[i]) {
+                wx[i] = ld4(f.w_in + js[i]);
                 if (f.w_prev) pv[i] = ld4(f.w_prev + js[i]);
             }
         }
@@ -1681,8 +1802,8 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
             }
             const float4 dl = make_float4(-(s * a4.x), -(s * a4.y), -(s * a4.z), -(s * a4.w));
             if (f.update) st4(f.update + j, dl);
-            if (kApply) {
-                const float4 x = wv[i];
+            if (kApply && visit[i]) {
+                const float4 x = wx[i];
                 float4 nx = make_float4(x.x + dl.x, x.y + dl.y, x.z + dl.z, x.w + dl.w);
                 if (f.w_prev) {  // momentum on the server
                     const float4 p = pv[i];
@@ -1727,7 +1848,8 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
         hit[q] = sent;
     }
     __syncthreads();
-    write_update<kApply>(acc, hit, wb, base, n, f);
+    if (sparse) visit_words(wv, hit, base, n, f.wbits);
+    write_update<kApply>(acc, hit, wb, base, n, f, sparse ? wv : nullptr);
     if (kApply && f.wbits) flush_marks(wb, base, n, f.wbits);
     if (kApply && f.detach) finish_detach(hit, base, n, K, f);
 }

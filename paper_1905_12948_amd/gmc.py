@@ -360,7 +360,8 @@ class Gmc:
     def stats(self) -> dict:
         out = (ctypes.c_int64 * 8)()
         self._call(self._lib.gmc_stats(self._ctx, out, 8))
-        keys = ("steps", "from_candidates", "full_data", "candidates", "count_errors", "sparse_momentum_steps")
+        keys = ("steps", "from_candidates", "full_data", "candidates", "count_errors", "sparse_momentum_steps",
+                "sparse_applies")
         return {k: int(out[i]) for i, k in enumerate(keys)}
 
     def pair_stats(self):

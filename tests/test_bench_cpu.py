@@ -32,10 +32,13 @@ def test_algorithmic_bytes_of_the_workloads():
     ab = bench.algorithmic_bytes(rb, m, detach=True)
     assert ab["step"] == 12 * 8 * d + 16 * d + 8 * 8 * m + 4 * 8 * d
     assert ab["fused"] == 12 * 8 * d + 8 * d + 4 * 8 * m + 4 * 8 * d
-    # sparse momentum term: the bitmap and the changed components instead of w_t, w_prev
+    # sparse momentum term: the bitmap and the changed components instead of w_t, w_prev;
+    # the server pass reads the old bitmap, writes the new one, and moves w only at the
+    # old and the new entries
     ab = bench.algorithmic_bytes(wl, 25558, detach=False, sparse_w=True)
     assert ab["fused"] == 12 * K * d + d // 8 + 8 * K * 25558
-    assert ab["step"] == 12 * K * d + d // 8 + 8 * K * 25558 + 8 * d + 16 * K * 25558 + d // 8
+    assert ab["step"] == (12 * K * d + d // 8 + 8 * K * 25558 + 2 * (d // 8) + 16 * K * 25558
+                          + 16 * K * 25558)
 
 
 def test_pmc_summary_matches_the_sources_or_is_ignored(tmp_path, monkeypatch):

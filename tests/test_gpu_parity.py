@@ -57,17 +57,17 @@ def test_forced_full_data_path():
 
 def test_candidate_overflow_takes_full_data_path():
     st = run_lockstep(Case(W("resnet18").shrunk(16, K=4), steps=4,
-                           options=((OPT_CAP, 1), (OPT_MARGIN, 64)), label="overflow"))
+                           options=((OPT_CAP, 1), (OPT_MARGIN, 256)), label="overflow"))
     assert st["full_data"] > 0
 
 
 def test_long_candidate_lists_stride_the_copy_launch():
-    # margin 16: the candidate lists run to several times the 8 k + 2048 the
+    # margin 16 k: the candidate lists run to several times the 8 k + 2048 the
     # copy and selection launches are sized for (within the 64 k capacity),
     # so the copy workgroups stride over the extra tiles and the slices run long
     wl = W("resnet18").shrunk(16, K=4)
     k = math.ceil(wl.ratio * wl.d)
-    st = run_lockstep(Case(wl, steps=4, options=((OPT_MARGIN, 16),), label="long lists"))
+    st = run_lockstep(Case(wl, steps=4, options=((OPT_MARGIN, 64),), label="long lists"))
     assert st["from_candidates"] >= 2 * wl.K
     assert st["candidates"] / st["from_candidates"] > 8 * k + 2048
 
@@ -131,7 +131,7 @@ def test_many_workers_overflow_the_staging():
     # K = 64 leaves 64 staging entries per worker and workgroup; a generous
     # candidate margin pushes wavefronts onto the direct global append
     wl = W("resnet50").shrunk(256, K=64)
-    run_lockstep(Case(wl, steps=3, options=((OPT_MARGIN, 200),), label="K=64"))
+    run_lockstep(Case(wl, steps=3, options=((OPT_MARGIN, 800),), label="K=64"))
 
 
 @pytest.mark.parametrize("name,shrink,steps", [("resnet50", 32, 4), ("rbgs", 16, 4), ("gpt2", 64, 3)])
@@ -279,6 +279,7 @@ def test_sparse_momentum_is_bitwise_the_dense_path(name, shrink, K, extra):
                            label="sparse momentum/" + name, **extra))
     if extra.get("rule") != "server_momentum":
         assert st["sparse_momentum_steps"] == 4, st   # every step after the first
+        assert st["sparse_applies"] == 4, st          # and its server pass
 
 
 def test_sparse_momentum_with_non_finite_parameters():
@@ -289,11 +290,13 @@ def test_sparse_momentum_with_non_finite_parameters():
     st = run_lockstep(Case(W("resnet18").shrunk(32, K=3), steps=4, fused_apply=True, sparse_w=True,
                            w0_hook=poison, label="sparse momentum, non-finite w"))
     assert st["sparse_momentum_steps"] == 3, st
+    assert st["sparse_applies"] == 3, st
 
 
 def test_sparse_momentum_falls_back_when_the_buffers_change():
     st = run_lockstep(Case(W("resnet18").shrunk(32, K=3), steps=4, sparse_w=True, label="sparse momentum, apply"))
     assert st["sparse_momentum_steps"] == 0, st   # gmc_aggregate + gmc_apply: no bitmap
+    assert st["sparse_applies"] == 0, st
 
 
 
@@ -312,6 +315,7 @@ def test_iteration_matches_the_oracle(name, shrink, K, extra):
     st = run_lockstep(Case(W(name).shrunk(shrink, K=K), steps=5, iteration=True, label="iteration/" + name, **extra))
     if extra.get("sparse_w") and extra.get("rule") != "server_momentum":
         assert st["sparse_momentum_steps"] == 4, st
+        assert st["sparse_applies"] == 4, st
 
 
 def test_iteration_with_non_finite_parameters():
@@ -319,5 +323,6 @@ def test_iteration_with_non_finite_parameters():
         w0 = w0.copy()
         w0[[5, 777, 4096, 9000]] = [np.inf, -np.inf, np.nan, np.inf]
         return w0
-    run_lockstep(Case(W("resnet18").shrunk(32, K=3), steps=4, iteration=True, sparse_w=True, w0_hook=poison,
-                      label="iteration, non-finite w"))
+    st = run_lockstep(Case(W("resnet18").shrunk(32, K=3), steps=4, iteration=True, sparse_w=True, w0_hook=poison,
+                           label="iteration, non-finite w"))
+    assert st["sparse_applies"] == 3, st
