@@ -260,7 +260,7 @@ gmc_status prepare(gmc_ctx* ctx) {
     GMC_HIP(ctx, hipSetDevice(ctx->device));
     const int32_t K = ctx->K;
     const int64_t d = ctx->d;
-    ctx->n_ranges = (int32_t)((d + kAggRange - 1) / kAggRange);
+    ctx->n_ranges = (int32_t)((d + kAggTopkRange - 1) / kAggTopkRange);
 
     TopkTables T;
     const bool approx = ctx->comp == GMC_TOPK_APPROX;

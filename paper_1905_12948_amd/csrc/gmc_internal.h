@@ -35,8 +35,11 @@ constexpr int kMaxSlices = 256;
 constexpr int kBins = 2048;
 constexpr int kShift1 = 20, kShift2 = 9;
 
-// Aggregation range per workgroup.
+// Aggregation range per workgroup (RBGS), and for top-s with the number of
+// message entries one workgroup stages in LDS.
 constexpr int kAggRange = 2048;
+constexpr int kAggTopkRange = 4096;
+constexpr int kAggTopkStage = 512;
 
 constexpr uint32_t kNoThreshold = 0xffffffffu;  // no speculative candidates
 

@@ -1550,7 +1550,8 @@ __device__ __forceinline__ void finish_detach(const unsigned char* hit, int64_t 
 }
 
 // rowptr[k][r] = first message position of worker k whose index is >= r*R
-// (a lower bound by binary search over the worker's ascending row);
+// with R = kAggTopkRange (a lower bound by binary search over the worker's
+// ascending row);
 // rowptr[k][n_ranges] = the row's length.  Any row content keeps every entry
 // within [0, length].
 __global__ __launch_bounds__(kGroup) void agg_rowptr_kernel(int32_t K, int32_t d, const int32_t* idx,
@@ -1567,7 +1568,7 @@ __global__ __launch_bounds__(kGroup) void agg_rowptr_kernel(int32_t K, int32_t d
         rp[r] = (int32_t)L;
         return;
     }
-    const int64_t target = (int64_t)r * kAggRange;
+    const int64_t target = (int64_t)r * kAggTopkRange;
     const int32_t* row = idx + (size_t)k * idx_row;
     int64_t lo = 0, hi = L;
     while (lo < hi) {
@@ -1586,151 +1587,189 @@ hipError_t launch_agg_rowptr(int32_t K, int32_t d, const int32_t* idx, int64_t i
     return hipGetLastError();
 }
 
-// One workgroup per range of kAggRange components.  The workgroup first
-// issues its loads of w (fused apply), then fetches the K workers' entries of
-// the range into LDS together (one round of loads) and adds them to the
-// range's accumulator one worker after the other; a range with more entries
-// than the staging holds reads them worker by worker instead.
-constexpr int kAggStage = 1024;
-
+// One workgroup per range of kAggTopkRange components (16 per thread).  The
+// workgroup first issues its loads of w_t (fused apply) and of the
+// previous pass's marks, then fetches the K workers' entries of the range
+// into LDS together (one round of loads) and adds them to the range's
+// accumulator one worker after the other; a range with more entries than the
+// staging holds reads them worker by worker instead.  Sent components are
+// kept as a bitmap (hb), so a workgroup needs about 21 KB of LDS and seven
+// fit on a CU: the kernel is bound by its chain of dependent loads, and
+// twice the components per chain halves the chains.
 template <bool kApply>
 __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, const int32_t* idx,
                                                           int64_t idx_row, const float* val, int64_t val_row,
                                                           const int32_t* rowptr, int32_t n_ranges, FinishArgs f) {
-    static_assert(kAggRange == kGroup * 8, "8 components per thread");
-    __shared__ float acc[kAggRange];
-    __shared__ unsigned char hit[kAggRange];
-    __shared__ uint32_t wb[kAggRange / 32];
-    __shared__ uint32_t wv[kAggRange / 32];
-    __shared__ int32_t st_idx[kAggStage];
-    __shared__ float st_val[kAggStage];
+    constexpr int R = kAggTopkRange, NW = R / 32, V = R / (kGroup * 4);
+    static_assert(V * kGroup * 4 == R && NW <= kGroup, "whole float4 per thread, one word per thread");
+    __shared__ float acc[R];
+    __shared__ uint32_t hb[NW];  // components some worker sent
+    __shared__ uint32_t wb[NW];  // marks for the next worker pass
+    __shared__ uint32_t wv[NW];  // sparse apply: the words to write (old marks | sent)
+    __shared__ int32_t st_idx[kAggTopkStage];
+    __shared__ float st_val[kAggTopkStage];
     __shared__ int32_t src[kMaxWorkers];
     __shared__ int32_t pre[kMaxWorkers + 1];
     const int r = blockIdx.x;
-    const int64_t base = (int64_t)r * kAggRange;
-    const int64_t n = (int64_t)d - base < kAggRange ? (int64_t)d - base : kAggRange;
+    const int t = threadIdx.x;
+    const int64_t base = (int64_t)r * R;
+    const int64_t n = (int64_t)d - base < R ? (int64_t)d - base : R;
+    const int words = (int)((n + 31) / 32);
     const float s = f.s;
-    const bool vec = n == kAggRange && (f.update == nullptr || aligned16(f.update)) &&
+    const bool vec = n == R && (f.update == nullptr || aligned16(f.update)) &&
                      (!kApply || (aligned16(f.w_in) && aligned16(f.w_out) &&
                                   (f.w_prev == nullptr || aligned16(f.w_prev))));
-    // this thread's components: [base + 4t, +4) and [base + 1024 + 4t, +4)
-    const int q0 = threadIdx.x * 4, q1 = kGroup * 4 + threadIdx.x * 4;
     const bool sparse = kApply && f.sparse_apply;
-    float4 w0 = make_float4(0.f, 0.f, 0.f, 0.f), w1 = w0, p0 = w0, p1 = w0;
-    // w_t is fetched up front, while the messages are staged and summed,
-    // also for the sparse apply, which then writes only some words: the
-    // fetch is off the kernel's critical path, a fetch that waited for the
-    // marks would be on it
-    if (kApply && vec) {
-        w0 = ld4(f.w_in + base + q0);
-        w1 = ld4(f.w_in + base + q1);
-        if (f.w_prev) {
-            p0 = ld4(f.w_prev + base + q0);
-            p1 = ld4(f.w_prev + base + q1);
+    // this thread's components: [base + 1024 i + 4 t, +4), i < V
+    float4 wx[V], px[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) {
+        wx[i] = px[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (kApply && vec && !sparse) {
+            wx[i] = ld4(f.w_in + base + i * (kGroup * 4) + t * 4);
+            if (f.w_prev) px[i] = ld4(f.w_prev + base + i * (kGroup * 4) + t * 4);
         }
     }
-    for (int q = threadIdx.x; q < kAggRange; q += kGroup) {
-        acc[q] = 0.0f;
-        hit[q] = 0;
+    for (int q = t; q < R; q += kGroup) acc[q] = 0.0f;
+    if (t < NW) {
+        hb[t] = 0u;
+        wb[t] = 0u;
+        wv[t] = (sparse && t < words) ? f.wbits[(base >> 5) + t] : 0u;
     }
-    if (threadIdx.x < kAggRange / 32) {
-        wb[threadIdx.x] = 0u;
-        // sparse apply: the previous pass's marks of the range; the sent
-        // components are or-ed in as the messages are read
-        if (sparse) wv[threadIdx.x] = threadIdx.x < (n + 31) / 32 ? f.wbits[(base >> 5) + threadIdx.x] : 0u;
-    }
-    if (threadIdx.x < K) {
-        const int32_t* rp = rowptr + (size_t)threadIdx.x * (n_ranges + 1);
+    if (t < K) {
+        const int32_t* rp = rowptr + (size_t)t * (n_ranges + 1);
         const int32_t lo = rp[r], hi = rp[r + 1];
-        src[threadIdx.x] = lo;
-        pre[threadIdx.x + 1] = hi > lo ? hi - lo : 0;
+        src[t] = lo;
+        pre[t + 1] = hi > lo ? hi - lo : 0;
     }
-    __syncthreads();
-    if (threadIdx.x == 0) {
+    // sparse apply: a range the previous pass marked anywhere fetches all
+    // of its w_t while the messages are staged (sent components recur from
+    // step to step, so such a range usually has more to write and no late
+    // fetch); an unmarked range fetches only the words this pass's sent
+    // components mark, after the sum, and most such ranges write nothing
+    const bool marked = __syncthreads_or(sparse && t < NW && wv[t] != 0u) != 0;
+    bool got = false;
+    if (sparse && vec && marked) {
+#pragma unroll
+        for (int i = 0; i < V; ++i) wx[i] = ld4(f.w_in + base + i * (kGroup * 4) + t * 4);
+        got = true;
+    }
+    if (t == 0) {
         pre[0] = 0;
         for (int k = 0; k < K; ++k) pre[k + 1] += pre[k];
     }
     __syncthreads();
     const int32_t total = pre[K];
-    if (total <= kAggStage) {
-        for (int32_t i = threadIdx.x; i < total; i += kGroup) {
+    if (total <= kAggTopkStage) {
+        for (int32_t i = t; i < total; i += kGroup) {
             int k = 0;
             while (i >= pre[k + 1]) ++k;
             const int64_t q = (int64_t)src[k] + (i - pre[k]);
-            const int32_t jj = idx[(size_t)k * idx_row + q];
-            st_idx[i] = jj;
+            st_idx[i] = idx[(size_t)k * idx_row + q];
             st_val[i] = val[(size_t)k * val_row + q];
-            const int64_t j = (int64_t)jj - base;
-            if (sparse && j >= 0 && j < kAggRange) atomicOr(&wv[j >> 5], 1u << (j & 31));
         }
         __syncthreads();
         for (int k = 0; k < K; ++k) {
             if (pre[k + 1] > pre[k]) {
-                for (int32_t i = pre[k] + threadIdx.x; i < pre[k + 1]; i += kGroup) {
+                for (int32_t i = pre[k] + t; i < pre[k + 1]; i += kGroup) {
                     const int64_t j = (int64_t)st_idx[i] - base;
-                    if (j >= 0 && j < kAggRange) {
+                    if (j >= 0 && j < R) {
                         acc[j] = acc[j] + st_val[i];
-                        hit[j] = 1;
+                        atomicOr(&hb[j >> 5], 1u << (j & 31));
                     }
                 }
                 __syncthreads();  // worker k's additions land before worker k+1's
             }
         }
     } else {
+        // a dense range (up to K entries per component): worker after
+        // worker straight from the messages, kDirect loads in flight per thread
+        constexpr int kDirect = 4;
         for (int k = 0; k < K; ++k) {
-            for (int32_t i = threadIdx.x; i < pre[k + 1] - pre[k]; i += kGroup) {
-                const int64_t q = (int64_t)src[k] + i;
-                const int64_t j = (int64_t)idx[(size_t)k * idx_row + q] - base;
-                if (j >= 0 && j < kAggRange) {
-                    acc[j] = acc[j] + val[(size_t)k * val_row + q];
-                    hit[j] = 1;
-                    if (sparse) atomicOr(&wv[j >> 5], 1u << (j & 31));
+            const int32_t cnt = pre[k + 1] - pre[k];
+            const int32_t* ip = idx + (size_t)k * idx_row + src[k];
+            const float* vp = val + (size_t)k * val_row + src[k];
+            for (int32_t i0 = 0; i0 < cnt; i0 += kDirect * kGroup) {
+                int32_t jj[kDirect];
+                float vv[kDirect];
+#pragma unroll
+                for (int u = 0; u < kDirect; ++u) {
+                    const int32_t i = i0 + u * kGroup + t;
+                    jj[u] = -1;
+                    vv[u] = 0.0f;
+                    if (i < cnt) {
+                        jj[u] = ip[i];
+                        vv[u] = vp[i];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kDirect; ++u) {
+                    const int64_t j = (int64_t)jj[u] - base;
+                    if (i0 + u * kGroup + t < cnt && j >= 0 && j < R) {
+                        acc[j] = acc[j] + vv[u];
+                        atomicOr(&hb[j >> 5], 1u << (j & 31));
+                    }
                 }
             }
-            __syncthreads();
+            __syncthreads();  // worker k's additions land before worker k+1's
         }
     }
     __syncthreads();
+    if (sparse) {
+        if (t < NW) wv[t] |= hb[t];
+        __syncthreads();
+    }
     if (vec) {
-        const float4 d0 = make_float4(-(s * acc[q0]), -(s * acc[q0 + 1]), -(s * acc[q0 + 2]), -(s * acc[q0 + 3]));
-        const float4 d1 = make_float4(-(s * acc[q1]), -(s * acc[q1 + 1]), -(s * acc[q1 + 2]), -(s * acc[q1 + 3]));
-        if (f.update) {
-            st4(f.update + base + q0, d0);
-            st4(f.update + base + q1, d1);
-        }
-        if (kApply && sparse) {  // only the words where w_out does not hold w_{t+1} yet
-            if (wv[q0 >> 5]) {
-                const float4 n0 = make_float4(w0.x + d0.x, w0.y + d0.y, w0.z + d0.z, w0.w + d0.w);
-                st4(f.w_out + base + q0, n0);
-                atomicOr(&wb[q0 >> 5], mark4(hit, q0, n0) << (q0 & 31));
-            }
-            if (wv[q1 >> 5]) {
-                const float4 n1 = make_float4(w1.x + d1.x, w1.y + d1.y, w1.z + d1.z, w1.w + d1.w);
-                st4(f.w_out + base + q1, n1);
-                atomicOr(&wb[q1 >> 5], mark4(hit, q1, n1) << (q1 & 31));
-            }
-        } else if (kApply) {
-            float4 n0 = make_float4(w0.x + d0.x, w0.y + d0.y, w0.z + d0.z, w0.w + d0.w);
-            float4 n1 = make_float4(w1.x + d1.x, w1.y + d1.y, w1.z + d1.z, w1.w + d1.w);
-            if (f.w_prev) {  // momentum on the server
-                const float b = f.b;
-                n0 = make_float4(n0.x + b * (w0.x - p0.x), n0.y + b * (w0.y - p0.y), n0.z + b * (w0.z - p0.z),
-                                 n0.w + b * (w0.w - p0.w));
-                n1 = make_float4(n1.x + b * (w1.x - p1.x), n1.y + b * (w1.y - p1.y), n1.z + b * (w1.z - p1.z),
-                                 n1.w + b * (w1.w - p1.w));
-            }
-            st4(f.w_out + base + q0, n0);
-            st4(f.w_out + base + q1, n1);
-            if (f.wbits) {
-                atomicOr(&wb[q0 >> 5], mark4(hit, q0, n0) << (q0 & 31));
-                atomicOr(&wb[q1 >> 5], mark4(hit, q1, n1) << (q1 & 31));
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+            const int q = i * (kGroup * 4) + t * 4;
+            const float4 dl = make_float4(-(s * acc[q]), -(s * acc[q + 1]), -(s * acc[q + 2]), -(s * acc[q + 3]));
+            if (f.update) st4(f.update + base + q, dl);
+            if (kApply && (!sparse || wv[q >> 5])) {
+                const float4 x = (sparse && !got) ? ld4(f.w_in + base + q) : wx[i];
+                float4 nx = make_float4(x.x + dl.x, x.y + dl.y, x.z + dl.z, x.w + dl.w);
+                if (f.w_prev) {  // momentum on the server
+                    const float4 pp = px[i];
+                    const float b = f.b;
+                    nx = make_float4(nx.x + b * (x.x - pp.x), nx.y + b * (x.y - pp.y), nx.z + b * (x.z - pp.z),
+                                     nx.w + b * (x.w - pp.w));
+                }
+                st4(f.w_out + base + q, nx);
+                if (f.wbits) {
+                    const uint32_t m = ((hb[q >> 5] >> (q & 31)) & 0xfu) | not_finite(nx.x) | (not_finite(nx.y) << 1) |
+                                       (not_finite(nx.z) << 2) | (not_finite(nx.w) << 3);
+                    atomicOr(&wb[q >> 5], m << (q & 31));
+                }
             }
         }
     } else {
-        write_update<kApply>(acc, hit, wb, base, n, f, sparse ? wv : nullptr);
+        for (int q = t; q < n; q += kGroup) {
+            const int64_t j = base + q;
+            const float dl = -(s * acc[q]);
+            if (f.update) f.update[j] = dl;
+            if (kApply && (!sparse || wv[q >> 5])) {
+                const float wn = next_w(f.w_in[j], dl, f.w_prev, j, f.b);
+                f.w_out[j] = wn;
+                if (f.wbits && (((hb[q >> 5] >> (q & 31)) & 1u) || not_finite(wn)))
+                    atomicOr(&wb[q >> 5], 1u << (q & 31));
+            }
+        }
     }
-    if (kApply && f.wbits) flush_marks(wb, base, n, f.wbits);
-    if (kApply && f.detach) finish_detach(hit, base, n, K, f);
+    if (kApply && f.wbits) {
+        __syncthreads();
+        if (t < words) f.wbits[(base >> 5) + t] = wb[t];
+    }
+    if (kApply && f.detach) {
+        // GMC+: the detached points at the sent components, from w_{t+1}
+        // as this workgroup wrote it
+        __syncthreads();
+        for (int q = t; q < n; q += kGroup) {
+            if (!((hb[q >> 5] >> (q & 31)) & 1u)) continue;
+            const int64_t j = base + q;
+            const float wn = f.w_out[j];
+            for (int k = 0; k < K; ++k) f.y[k][j] = detached(wn, f.e[k][j], f.q);
+        }
+    }
 }
 
 hipError_t launch_agg_topk(int32_t K, int32_t d, const int32_t* idx, int64_t idx_row,
