@@ -1,8 +1,11 @@
 """The workloads at their full sizes, in the launch configuration the bench
-times (gmc_step, then gmc_aggregate_apply out of place with the parameter
-buffers swapping roles), checked against the oracle's per-element functions
-and the defining property of exact top-k (a full CPU sort of every worker's
-vector would take minutes).
+times (gmc_iteration with the sparse momentum term: the worker pass, then the
+server pass writing w_{t+1} over w_{t-1}'s buffer, the two parameter buffers
+swapping roles; GMC+ takes gmc_step_detach then gmc_finish), checked against
+the oracle's per-element functions and the defining property of exact top-k
+(a full CPU sort of every worker's vector would take minutes).  One case
+keeps the dense path (gmc_step, then gmc_aggregate_apply writing the update
+vector too).
 
 For each step and two of the K workers (the first and the last):
   * u (recomputed by the oracle from the step's inputs) equals e_{t+1} off
@@ -11,11 +14,12 @@ For each step and two of the K workers (the first and the last):
   * per segment the message holds exactly k components, ascending, whose
     keys are the k largest with ties broken towards the lower index (the
     sampled-threshold top-s: exactly the oracle's selection on the same u);
-the server update and the apply are compared with the oracle's aggregation
-of all K messages, for every component.  Step 0 takes the full-data
-selection path, later steps the candidate path.  With lambda > 0 (GMC+,
-gmc_step_detach then gmc_finish) the two workers' detached points are
-compared with the oracle's too."""
+w_{t+1} (and the update vector, where written) is compared with the oracle's
+aggregation of all K messages and its apply, for every component.  Step 0
+takes the full-data selection path and the dense parameter path, later steps
+the candidate path and, with the sparse momentum term, read and write the
+parameters only where they change.  With lambda > 0 the two workers'
+detached points are compared with the oracle's too."""
 import numpy as np
 import pytest
 
@@ -56,13 +60,14 @@ def check_topk_segment(u: np.ndarray, sel: np.ndarray, k: int, tag: str):
         assert tie_sel.max() < tie_rest.min(), tag + ": ties not broken towards the lower index"
 
 
-@pytest.mark.parametrize("name,steps,lam", [("tiny", 3, 0.0), ("resnet18", 3, 0.0), ("resnet50", 3, 0.0),
-                                            ("rbgs", 3, 0.0), ("gpt2", 2, 0.0), ("rbgs", 3, 0.5),
-                                            ("resnet50", 2, 0.5), ("resnet50_approx", 3, 0.0)])
-def test_full_size_workload(name, steps, lam):
+@pytest.mark.parametrize("name,steps,lam,dense", [
+    ("tiny", 3, 0.0, False), ("resnet18", 3, 0.0, False), ("resnet50", 3, 0.0, False), ("rbgs", 3, 0.0, False),
+    ("gpt2", 3, 0.0, False), ("rbgs", 3, 0.5, False), ("resnet50", 2, 0.5, False),
+    ("resnet50_approx", 3, 0.0, False), ("resnet50", 2, 0.0, True)])
+def test_full_size_workload(name, steps, lam, dense):
     import torch
     import synth.device as sdev
-    from paper_1905_12948_amd import Gmc
+    from paper_1905_12948_amd import Gmc, GMC_OPT_SPARSE_MOMENTUM
 
     wl = synth.workload(name)
     d, K = wl.d, wl.K
@@ -75,7 +80,10 @@ def test_full_size_workload(name, steps, lam):
             block=wl.block if rbgs else None, lam=lam)
     orc = oracle.GmcOracle(d, K, wl.compressor if (rbgs or approx) else "topk", wl.ratio, wl.beta, wl.eta,
                            seed=wl.seed, seg_off=seg, block=wl.block, lam=lam)
-    print("full size %s: d=%d K=%d %s lambda=%g" % (name, d, K, wl.compressor, lam), flush=True)
+    if not dense:
+        g.set_option(GMC_OPT_SPARSE_MOMENTUM, 1)
+    print("full size %s: d=%d K=%d %s lambda=%g %s" % (name, d, K, wl.compressor, lam,
+                                                    "dense" if dense else "sparse momentum"), flush=True)
     bufs = [sdev.w0(wl, dev), None]
     bufs[1] = bufs[0].clone()
     err = sdev.rows(K, d, dev, zero=True)
@@ -90,10 +98,12 @@ def test_full_size_workload(name, steps, lam):
         e_before = {k: err[k].cpu().numpy() for k in check}
         if lam:
             g.step(cur, prev, grads, err, idx, val, ln, w_k=wk)
-            g.finish(idx, val, ln, cur, prev, update=upd, err=err, w_k=wk)
-        else:
+            g.finish(idx, val, ln, cur, prev, err=err, w_k=wk)
+        elif dense:
             g.step(cur, prev, grads, err, idx, val, ln)
             g.aggregate_apply(idx, val, ln, cur, prev, update=upd)
+        else:
+            g.iteration(cur, prev, grads, err, idx, val, ln)
         torch.cuda.synchronize()
         gi, gv, gl = idx.cpu().numpy(), val.cpu().numpy(), ln.cpu().numpy()
         if rbgs:
@@ -123,7 +133,8 @@ def test_full_size_workload(name, steps, lam):
                     sel = sent[(sent >= a) & (sent < b)] - a
                     check_topk_segment(u[a:b], sel, int(orc.seg_k[s_i]), tag + " segment %d" % s_i)
         delta = orc.aggregate(gi, gv, gl)
-        assert_same_f32(upd.cpu().numpy(), delta, "%s step %d: update" % (name, t))
+        if dense:
+            assert_same_f32(upd.cpu().numpy(), delta, "%s step %d: update" % (name, t))
         w_next = w_h.copy()
         orc.apply(w_next, delta)
         assert_same_f32(prev.cpu().numpy(), w_next, "%s step %d: w_{t+1}" % (name, t))
@@ -133,4 +144,7 @@ def test_full_size_workload(name, steps, lam):
                 assert_same_f32(wk[k].cpu().numpy(), want, "%s step %d: detached point of worker %d" % (name, t, k))
         print("  step %d ok (%s)" % (t, g.stats()), flush=True)
         del grads
+    st = g.stats()
     g.close()
+    if not dense:  # every step after the first moved the parameters only where they change
+        assert st["sparse_momentum_steps"] == steps - 1 and st["sparse_applies"] == steps - 1, st
