@@ -58,11 +58,15 @@ def log(msg: str):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash():
+    """sha256 over the kernel sources, or None where they are not present."""
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
+    try:
+        for p in KERNEL_SOURCES:
+            with open(p, "rb") as f:
+                h.update(f.read())
+    except OSError:
+        return None
     return h.hexdigest()
 
 
@@ -109,7 +113,8 @@ def read_pmc_summary(sparse_w: bool = True):
                 k, v = line.split("=", 1)
                 kv[k.strip()] = v.strip()
     try:
-        if kv.get("kernel_source_sha256") != kernel_source_hash():
+        src = kernel_source_hash()
+        if src is None or kv.get("kernel_source_sha256") != src:
             return None
         if kv.get("sparse_momentum", "0") != ("1" if sparse_w else "0"):
             return None

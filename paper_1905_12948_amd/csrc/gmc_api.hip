@@ -577,6 +577,13 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
                   : nullptr;
     ctx->wbits_valid = false;
     ctx->wbits_used_t = a.wbits ? ctx->t : -1;
+    // workgroup order: w read everywhere (dense momentum term or GMC+'s
+    // detached points) in runs of 2 chunks; at the changed components only,
+    // runs of 1, or each chunk's workers on one XCD when the components the
+    // last server pass changed (at most K times a top-s message) reach 5% of d
+    const int64_t per_worker = ctx->comp == GMC_TOPK_APPROX ? count_for(ctx->d, ctx->ratio) : ctx->k_tot;
+    const bool dense_marks = ctx->comp != GMC_RBGS && (int64_t)ctx->K * per_worker * 20 >= ctx->d;
+    a.run = (!a.wbits || y_dev) ? 2 : (dense_marks ? 0 : 1);
     if (a.wbits) ++ctx->sparse_steps;
     for (int k = 0; k < ctx->K; ++k) {
         if (!grads_dev[k] || !err_dev[k] || (y_dev && !y_dev[k]))

@@ -155,6 +155,10 @@ struct StepArgs {
     // read w_t, w_prev only at the marked components, since elsewhere
     // w_t - w_prev is exactly +0
     const uint32_t* wbits;
+    // workgroup order of the vector worker passes: runs of `run` chunks of
+    // one worker (2: w read everywhere; 1: w read at sparse changes), or 0:
+    // each chunk's K workers on one XCD (w read at dense changes)
+    int32_t run;
 };
 
 // The server pass after the sum over workers: update = -(s * sum), the

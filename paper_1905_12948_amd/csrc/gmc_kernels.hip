@@ -128,24 +128,36 @@ __device__ __forceinline__ void sample_float4(float* samp, uint64_t state, int32
     }
 }
 
-// Workgroup order of the streaming passes over (chunk, worker): runs of
-// `run` consecutive chunks of one worker, the K workers of a run one after
-// the other.  Workgroups are dispatched round-robin over the 8 XCDs, so with
-// runs of 2 each chunk's w_t, w_prev are pulled into 4 XCD caches instead of
-// 8.  Measured with w read everywhere, on the ResNet-50-sized step (K = 16)
-// and the RBGS step (K = 8): runs of 1, 2, 4, 8 chunks took 893/888/904/926
-// us and 671/629/628/630 us.  When w is read only at the changed components
-// (the sparse momentum term) runs of 1 stream best: on a stream of the same
-// shape without w, 804 us against 824 us for runs of 2.
-__host__ __device__ inline int run_chunks(bool w_everywhere) { return w_everywhere ? 2 : 1; }
+// Workgroup order of the streaming passes over (chunk, worker) (StepArgs::run,
+// chosen on the host): runs of `run` consecutive chunks of one worker, the K
+// workers of a run one after the other; or, with run == 0, chunk c on XCD
+// c mod 8 with its K workers consecutive there.  Workgroups are dispatched
+// round-robin over the 8 XCDs (workgroup b on XCD b mod 8), so with runs of
+// 1 every XCD's cache pulls the w_t, w_prev lines a chunk reads, with runs of
+// 2 four of them, with run 0 one.  Measured with w read everywhere, on the
+// ResNet-50-sized step (K = 16) and the RBGS step (K = 8): runs of 1, 2, 4, 8
+// chunks took 893/888/904/926 us and 671/629/628/630 us.  When w is read only
+// at the changed components (the sparse momentum term) runs of 1 stream best
+// (on a stream of the same shape without w, 804 us against 824 us for runs of
+// 2; run 0 slows the ResNet-50-sized pass by 10%), unless the changed
+// components are dense: at the ResNet-18-sized workload (8 workers sending
+// 1% each) run 0 takes 186 us against 200 us.
+constexpr int kXcds = 8;
 
 __device__ __forceinline__ void run_order(int b, int K, int run, int* chunk, int* k) {
+    if (run == 0) {
+        const int x = b % kXcds, sl = b / kXcds;
+        *k = sl % K;
+        *chunk = (sl / K) * kXcds + x;
+        return;
+    }
     const int grp = b / (run * K), r = b % (run * K);
     *k = r / run;
     *chunk = grp * run + r % run;
 }
 
 __host__ __device__ inline int64_t run_order_grid(int64_t n_chunks, int K, int run) {
+    if (run == 0) return (n_chunks + kXcds - 1) / kXcds * kXcds * K;
     return (n_chunks + run - 1) / run * run * K;
 }
 
@@ -255,7 +267,7 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
     __shared__ uint32_t wtot[2][kWavesPerGroup];
     __shared__ int2 stage[kChunk];
     int chunk, k;
-    run_order(blockIdx.x, g.K, run_chunks(kDetach || !a.wbits), &chunk, &k);
+    run_order(blockIdx.x, g.K, a.run, &chunk, &k);
     if (chunk >= g.n_chunks || !((vec_mask >> k) & 1ull)) return;  // padding, or the element-wise kernel's
     // one segment (global top-s): the chunk's place is arithmetic, no table lookup
     const bool one = g.n_seg == 1;
@@ -420,7 +432,7 @@ __global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, Topk
 template <bool kApprox>
 static hipError_t launch_fused_vec_rule(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                                        uint64_t vec_mask, hipStream_t st) {
-    const int grid = (int)run_order_grid(g.n_chunks, g.K, run_chunks(a.detach || !a.wbits));
+    const int grid = (int)run_order_grid(g.n_chunks, g.K, a.run);
     if (a.rule == kRuleServerMomentum) {
         if (a.detach) return hipErrorInvalidValue;  // the detached points need w_{t+1} = w_t off the sent set
         hipLaunchKernelGGL((topk_fused_vec_kernel<kRuleServerMomentum, false, kApprox>), dim3(grid), dim3(kGroup), 0,
@@ -1337,7 +1349,7 @@ __global__ __launch_bounds__(kGroup) void rbgs_vec_kernel(StepArgs a, int32_t K,
                                                           const int32_t* block_slot, float* val, int64_t val_row,
                                                           uint64_t vec_mask) {
     int chunk, k;
-    run_order(blockIdx.x, K, run_chunks(kDetach || !a.wbits), &chunk, &k);
+    run_order(blockIdx.x, K, a.run, &chunk, &k);
     const int64_t chunk0 = (int64_t)chunk * kChunk;
     if (chunk0 >= a.d || !((vec_mask >> k) & 1ull)) return;  // padding, or the element-wise kernel's
     if (chunk0 + kChunk > a.d) {  // the partial last chunk, element by element
@@ -1407,7 +1419,7 @@ hipError_t launch_rbgs_fused(const StepArgs& a, int32_t K, int32_t B, const int3
     const int64_t n_chunks = vec_mask ? ((int64_t)a.d + kChunk - 1) / kChunk : 0;
     const int64_t vec_end = vec_mask ? (int64_t)a.d : 0;
     if (n_chunks > 0) {
-        const dim3 grid((unsigned)run_order_grid(n_chunks, K, run_chunks(a.detach || !a.wbits)));
+        const dim3 grid((unsigned)run_order_grid(n_chunks, K, a.run));
         if (a.rule == kRuleServerMomentum) {
             if (a.detach) return hipErrorInvalidValue;
             hipLaunchKernelGGL((rbgs_vec_kernel<kRuleServerMomentum, false>), grid, dim3(kGroup), 0, st, a, K, B,
@@ -1914,7 +1926,7 @@ hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, const int32_t* block
 // y_k are streamed.
 __global__ __launch_bounds__(kGroup) void detach_kernel(DetachArgs a, int32_t K) {
     int chunk, k;
-    run_order(blockIdx.x, K, run_chunks(true), &chunk, &k);
+    run_order(blockIdx.x, K, 2, &chunk, &k);
     const int64_t start = (int64_t)chunk * kChunk;
     if (start >= a.d) return;  // padding of the run order
     const int64_t len = (int64_t)a.d - start < kChunk ? (int64_t)a.d - start : kChunk;
@@ -1936,7 +1948,7 @@ __global__ __launch_bounds__(kGroup) void detach_kernel(DetachArgs a, int32_t K)
 
 hipError_t launch_detach(const DetachArgs& a, int32_t K, hipStream_t st) {
     const int64_t chunks = ((int64_t)a.d + kChunk - 1) / kChunk;
-    hipLaunchKernelGGL(detach_kernel, dim3((unsigned)run_order_grid(chunks, K, run_chunks(true))), dim3(kGroup), 0,
+    hipLaunchKernelGGL(detach_kernel, dim3((unsigned)run_order_grid(chunks, K, 2)), dim3(kGroup), 0,
                        st, a, K);
     return hipGetLastError();
 }

@@ -273,7 +273,10 @@ def test_rule_and_compressor_errors():
     ("resnet18", 16, 4, {}), ("resnet50", 32, 16, {}), ("rbgs", 16, 8, {}), ("gpt2", 64, 3, {}),
     ("resnet50_approx", 64, 4, {}), ("rbgs", 16, 4, {"lam": 0.5, "detach": "fused"}),
     ("resnet18", 16, 4, {"lam": 0.5, "detach": "fused"}), ("resnet18", 16, 4, {"rule": "lr_in_residual"}),
-    ("resnet18", 32, 3, {"row_pad": 1}), ("resnet18", 16, 4, {"rule": "server_momentum"})])
+    ("resnet18", 32, 3, {"row_pad": 1}), ("resnet18", 16, 4, {"rule": "server_momentum"}),
+    # 8 workers sending 1% each: the changed components are dense enough that
+    # the worker pass puts each chunk's workers on one XCD
+    ("resnet18", 16, 8, {}), ("tiny", 4, 8, {"rule": "lr_in_residual"})])
 def test_sparse_momentum_is_bitwise_the_dense_path(name, shrink, K, extra):
     st = run_lockstep(Case(W(name).shrunk(shrink, K=K), steps=5, fused_apply=True, sparse_w=True,
                            label="sparse momentum/" + name, **extra))
@@ -310,7 +313,8 @@ def test_sparse_momentum_falls_back_when_the_buffers_change():
     ("gpt2", 64, 3, {"sparse_w": True}), ("resnet50_approx", 64, 4, {"sparse_w": True}),
     ("resnet18", 16, 4, {"sparse_w": True, "rule": "lr_in_residual"}),
     ("resnet18", 32, 3, {"sparse_w": True, "row_pad": 1}), ("rbgs", 16, 4, {"sparse_w": True}),
-    ("resnet18", 16, 4, {}), ("resnet18", 16, 4, {"rule": "server_momentum", "sparse_w": True})])
+    ("resnet18", 16, 4, {}), ("resnet18", 16, 4, {"rule": "server_momentum", "sparse_w": True}),
+    ("resnet18", 16, 8, {"sparse_w": True})])
 def test_iteration_matches_the_oracle(name, shrink, K, extra):
     st = run_lockstep(Case(W(name).shrunk(shrink, K=K), steps=5, iteration=True, label="iteration/" + name, **extra))
     if extra.get("sparse_w") and extra.get("rule") != "server_momentum":
