@@ -291,6 +291,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         add((size_t)K * nc * kChunk, sizeof(int2));
         add((size_t)T.cand_total, 4); add((size_t)T.cand_total, 4);
         for (int q = 0; q < 4; ++q) add((size_t)K * nsl, 4);
+        add((size_t)K * nsl * kSlHist, 4);
         add((size_t)K * (ctx->n_ranges + 1), 4);
         if (approx) add((size_t)K * samp_n, 4);
     }
@@ -382,6 +383,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         sc.sl_ties = cv.take<uint32_t>((size_t)K * nsl);
         sc.sl_out = cv.take<uint32_t>((size_t)K * nsl);
         sc.sl_tiebase = cv.take<uint32_t>((size_t)K * nsl);
+        sc.sl_hist = cv.take<uint32_t>((size_t)K * nsl * kSlHist);
         sc.stats = ctx->stats;
         ctx->rowptr = cv.take<int32_t>((size_t)K * (ctx->n_ranges + 1));
         sc.samp = approx ? cv.take<float>((size_t)K * samp_n) : nullptr;
@@ -637,8 +639,10 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
         GMC_TRY(prof_begin(ctx, 2, &ev));
         GMC_LAUNCH(ctx, launch_topk_compact(ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
         for (int pass = 1; pass <= 3; ++pass)
-            GMC_LAUNCH(ctx, launch_topk_hist(pass, a, ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
-        GMC_LAUNCH(ctx, launch_topk_count(a, ctx->geo, ctx->scr, msg_len_dev, ctx->k_tot, ctx->stream));
+            GMC_LAUNCH(ctx, launch_topk_hist(pass, a, ctx->geo, ctx->scr, ctx->force_full, ctx->margin, msg_len_dev,
+                                             ctx->k_tot, ctx->stream));
+        if (ctx->comp == GMC_TOPK_APPROX)  // exact top-s counts in the third pass
+            GMC_LAUNCH(ctx, launch_topk_count(a, ctx->geo, ctx->scr, msg_len_dev, ctx->k_tot, ctx->stream));
         GMC_TRY(prof_end(ctx, 2, ev));
         GMC_TRY(prof_begin(ctx, 3, &ev));
         GMC_LAUNCH(ctx, launch_topk_emit(a, ctx->geo, ctx->scr, idx_dev, val_dev, row_v, ctx->stream));

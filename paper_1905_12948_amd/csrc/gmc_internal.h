@@ -30,6 +30,7 @@ constexpr int64_t kSliceElems = 1 << 19;   // full-data elements per slice (at m
 constexpr int64_t kSliceCands = 8192;      // usual candidates per slice (more when a list runs long)
 constexpr int64_t kHistSliceCands = 8192;  // candidates per histogram-pass workgroup (fewer workgroups)
 constexpr int kMaxSlices = 256;
+constexpr int kSlHist = 513;               // per slice: suffix sums of a 512-bin histogram + a count above
 
 // Radix select over the 31-bit magnitude key in three digits: 11 + 11 + 9.
 constexpr int kBins = 2048;
@@ -71,7 +72,7 @@ struct PairState {
     uint32_t fuse1;     // 1: the copy kernel also does the first histogram pass
     uint32_t p1_done;   // 1: it has (the first histogram kernel skips the pair)
     // exact top-s: the first pass puts the next step's threshold at the floor
-    // of the 11-bit bin tau_bin holding the key of rank margin*k; with
+    // of the 11-bit bin tau_bin holding the key of rank margin*k/4; with
     // tau_fine the second pass narrows it to the floor of the 22-bit bin
     // holding that key, the tau_need-th of bin tau_bin from the top
     uint32_t tau_bin;
@@ -134,6 +135,7 @@ struct TopkScratch {
     uint32_t* sl_ties;            // [K*n_slices] at-threshold count
     uint32_t* sl_out;             // [K*n_slices] message offset of the slice's first kept component
     uint32_t* sl_tiebase;         // [K*n_slices] at-threshold components in earlier slices
+    uint32_t* sl_hist;            // [K*n_slices][kSlHist] third-pass counts per slice (exact top-s)
     float* samp;                  // [K][samp_n] the sample's values (sampled-threshold top-s)
     int64_t* stats;               // [8]
 };
@@ -209,8 +211,10 @@ hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const
 // that resolve from their candidates (exact top-s)
 hipError_t launch_topk_compact(const TopkGeometry& g, const TopkScratch& s, int force_full, int margin,
                                hipStream_t st);
-hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
-                            const TopkScratch& s, int force_full, int margin, hipStream_t st);
+// pass 3 of exact top-s also lays out the message (per-slice offsets and
+// msg_len); the sampled-threshold top-s takes launch_topk_count for that
+hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
+                            int force_full, int margin, int64_t* msg_len, int64_t msg_total, hipStream_t st);
 hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                              int64_t* msg_len, int64_t msg_total, hipStream_t st);
 hipError_t launch_topk_emit(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,

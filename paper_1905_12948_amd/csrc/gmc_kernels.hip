@@ -601,6 +601,54 @@ __device__ __forceinline__ bool finish_slice(uint32_t* done, int W, int* sh_flag
     return true;
 }
 
+// The last workgroup of a pair, once T and r are known: from each slice's
+// counts of kept components above T and at T (get(slice, &A, &Ti), the
+// segment's slices in index order) the message offset of each slice's first
+// kept component and the at-T components in earlier slices (the r ties kept
+// go to the lowest indices); then the message length.  carry: 2 words of LDS.
+template <class Get>
+__device__ void scan_slices(const SliceId& id, int W, int32_t r, Get get, const TopkGeometry& g,
+                            const TopkScratch& s, int64_t* msg_len, int64_t msg_total, uint32_t* sh_wsum,
+                            uint32_t* carry) {
+    const size_t base = (size_t)id.k * g.n_slices + g.seg_slice_lo[id.seg];
+    if (threadIdx.x == 0) {
+        carry[0] = 0;  // ties before
+        carry[1] = 0;  // kept before
+    }
+    __syncthreads();
+    for (int c0 = 0; c0 < W; c0 += kGroup) {
+        const int i = c0 + threadIdx.x;
+        uint32_t A = 0, Ti = 0;
+        if (i < W) get(base + i, &A, &Ti);
+        uint32_t tot_t;
+        const uint32_t tie_pre = carry[0] + block_scan_excl(Ti, &tot_t, sh_wsum);
+        int64_t take = (int64_t)r - (int64_t)tie_pre;
+        if (take < 0) take = 0;
+        if (take > (int64_t)Ti) take = Ti;
+        const uint32_t sel = A + (uint32_t)take;
+        uint32_t tot_s;
+        const uint32_t sel_pre = carry[1] + block_scan_excl(sel, &tot_s, sh_wsum);
+        if (i < W) {
+            s.sl_tiebase[base + i] = tie_pre;
+            s.sl_out[base + i] = sel_pre;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            carry[0] += tot_t;
+            carry[1] += tot_s;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        if (g.approx) {
+            msg_len[id.k] = (int64_t)carry[1];  // one segment; the count varies
+        } else {
+            if (carry[1] != (uint32_t)g.pair_k[id.p]) atomicAdd((unsigned long long*)&s.stats[4], 1ull);
+            if (id.seg == 0) msg_len[id.k] = msg_total;
+        }
+    }
+}
+
 }  // namespace
 
 // ----------------------------------------------------------------------------
@@ -653,7 +701,7 @@ template <int PASS>
 __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, int kp, int mode, uint32_t cand,
                              uint32_t prefix, int margin, int force_full, bool approx, const TopkGeometry& g,
                              const TopkScratch& s, uint32_t* sh_wsum, int* sh_res, uint32_t* h2 = nullptr,
-                             uint32_t* gh2 = nullptr) {
+                             uint32_t* gh2 = nullptr, uint32_t* T_out = nullptr, int32_t* r_out = nullptr) {
     constexpr int nbins = PASS == 3 ? 512 : kBins;
     // second pass: the threshold's bin histogram comes in with T's
     const bool fine2 = PASS == 2 && ps->tau_fine != 0u && ps->tau_bin != prefix;
@@ -662,6 +710,10 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
     const uint32_t need = PASS == 1 ? (uint32_t)kp : (uint32_t)ps->need;
     uint32_t above = 0;
     const int bin = find_bin(h, nbins, need, &above, sh_wsum, sh_res);
+    if (PASS == 3 && T_out) {  // every thread: the threshold and the ties to take
+        *T_out = (prefix << 9) | (uint32_t)(bin < 0 ? 0 : bin);
+        *r_out = (int32_t)(need - above);
+    }
 
     if (PASS == 1) {
         // speculative threshold of the next step: the floor of the bin that
@@ -733,15 +785,22 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
     }
 }
 
+// The third pass of exact top-s also takes the count of the kept components
+// per slice: each workgroup stores its slice's count above T's 22-bit bin and
+// the suffix sums of its 512-bin histogram of that bin (sl_hist, kSlHist
+// words per slice), from which the last workgroup reads, once it has T, each
+// slice's counts above and at T and lays out the message.
 template <int PASS>
 __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
-                                                           int force_full, int margin) {
+                                                           int force_full, int margin, int64_t* msg_len,
+                                                           int64_t msg_total) {
     constexpr int nbins = PASS == 3 ? 512 : kBins;
     __shared__ uint32_t h[kBins];
     __shared__ uint32_t h2[PASS == 2 ? kBins : 1];
     __shared__ uint32_t sh_wsum[kWavesPerGroup];
     __shared__ int sh_res[2];
     __shared__ int sh_last;
+    __shared__ uint32_t carry[2];
 
     const SliceId id = slice_id(g);
     PairState* ps = &s.pair[id.p];
@@ -758,7 +817,11 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
     // (each workgroup merges its slice's histogram into the pair's with one
     // global atomic per nonzero bin, so fewer, fuller slices cost less); the
     // other workgroups of the pair leave at once
-    const int W = mode == 0 ? max(1, min(id.W, (int)((cand + kHistSliceCands - 1) / kHistSliceCands))) : id.W;
+    // the third pass of exact top-s counts per slice for the emit kernel, so
+    // it keeps the emit's slices
+    const bool count = PASS == 3 && !approx;
+    const int W = (mode == 0 && !count) ? max(1, min(id.W, (int)((cand + kHistSliceCands - 1) / kHistSliceCands)))
+                                        : id.W;
     if (id.w >= W) return;
     // second pass: also the second digit of the speculative threshold's bin
     // when it is not T's
@@ -771,6 +834,7 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
     }
     __syncthreads();
     const Slice v = open_slice(mode, cand, id.k, id.seg, id.p, id.w, W, a, g, s);
+    uint32_t above = 0;  // third pass: keys above T's 22-bit bin
     for_slice<false>(v, [&](uint32_t key, int32_t) {
         if (PASS == 1) {
             atomicAdd(&h[key >> kShift1], 1u);
@@ -779,7 +843,9 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
             if (d1 == prefix) atomicAdd(&h[(key >> kShift2) & (kBins - 1)], 1u);
             else if (fine2 && d1 == tbin) atomicAdd(&h2[(key >> kShift2) & (kBins - 1)], 1u);
         } else {
-            if ((key >> kShift2) == prefix) atomicAdd(&h[key & 511u], 1u);
+            const uint32_t d12 = key >> kShift2;
+            if (d12 == prefix) atomicAdd(&h[key & 511u], 1u);
+            else if (count && d12 > prefix) ++above;
         }
     });
     __syncthreads();
@@ -789,21 +855,51 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
         if (h[b]) atomicAdd(&gh[b], h[b]);
         if (fine2 && h2[b]) atomicAdd(&gh2[b], h2[b]);
     }
+    uint32_t* sh = nullptr;
+    if (count) {
+        // this slice's count above the bin and, for b < 512, S[b] = its keys
+        // in the bin with low bits >= b (thread t owns bins 511-2t, 510-2t)
+        sh = s.sl_hist + ((size_t)id.k * g.n_slices + g.seg_slice_lo[id.seg] + id.w) * kSlHist;
+        uint32_t tot;
+        block_scan_excl(above, &tot, sh_wsum);
+        if (threadIdx.x == 0) store_agent(&sh[512], tot);
+        const int b_hi = 511 - 2 * (int)threadIdx.x;
+        const uint32_t hh = h[b_hi], hl = h[b_hi - 1];
+        const uint32_t ex = block_scan_excl(hh + hl, &tot, sh_wsum);
+        store_agent(&sh[b_hi], ex + hh);
+        store_agent(&sh[b_hi - 1], ex + hh + hl);
+    }
     if (!finish_slice(&ps->done, W, &sh_last)) return;
 
+    uint32_t T = 0;
+    int32_t r = 0;
     finish_digit<PASS>(ps, id.p, h, gh, kp, mode, cand, prefix, margin, force_full, approx, g, s, sh_wsum, sh_res,
-                       PASS == 2 ? h2 : nullptr, gh2);
+                       PASS == 2 ? h2 : nullptr, gh2, &T, &r);
+    if (count) {
+        // each slice's counts above T and at T: above the bin, plus S[b+1];
+        // at T, S[b] - S[b+1] (b = T's low 9 bits)
+        const uint32_t b = T & 511u;
+        scan_slices(id, W, r, [&](size_t sl, uint32_t* A, uint32_t* Ti) {
+            const uint32_t* S = s.sl_hist + sl * kSlHist;
+            const uint32_t sb = load_agent(&S[b]), sb1 = b < 511u ? load_agent(&S[b + 1]) : 0u;
+            *A = load_agent(&S[512]) + sb1;
+            *Ti = sb - sb1;
+        }, g, s, msg_len, msg_total, sh_wsum, carry);
+    }
 }
 
-hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g,
-                            const TopkScratch& s, int force_full, int margin, hipStream_t st) {
+hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
+                            int force_full, int margin, int64_t* msg_len, int64_t msg_total, hipStream_t st) {
     const int grid = g.K * g.n_slices;
     if (pass == 1)
-        hipLaunchKernelGGL(topk_hist_kernel<1>, dim3(grid), dim3(kGroup), 0, st, a, g, s, force_full, margin);
+        hipLaunchKernelGGL(topk_hist_kernel<1>, dim3(grid), dim3(kGroup), 0, st, a, g, s, force_full, margin, msg_len,
+                           msg_total);
     else if (pass == 2)
-        hipLaunchKernelGGL(topk_hist_kernel<2>, dim3(grid), dim3(kGroup), 0, st, a, g, s, force_full, margin);
+        hipLaunchKernelGGL(topk_hist_kernel<2>, dim3(grid), dim3(kGroup), 0, st, a, g, s, force_full, margin, msg_len,
+                           msg_total);
     else
-        hipLaunchKernelGGL(topk_hist_kernel<3>, dim3(grid), dim3(kGroup), 0, st, a, g, s, force_full, margin);
+        hipLaunchKernelGGL(topk_hist_kernel<3>, dim3(grid), dim3(kGroup), 0, st, a, g, s, force_full, margin, msg_len,
+                           msg_total);
     return hipGetLastError();
 }
 
@@ -1014,47 +1110,11 @@ __global__ __launch_bounds__(kGroup) void topk_count_kernel(StepArgs a, TopkGeom
     if (!finish_slice(&ps->done, id.W, &sh_last)) return;
 
     // last workgroup of the pair: scan the segment's slices in index order
-    const int32_t r = ps->r;
-    if (threadIdx.x == 0) {
-        carry[0] = 0;  // ties before
-        carry[1] = 0;  // kept before
-    }
-    __syncthreads();
-    for (int c0 = 0; c0 < id.W; c0 += kGroup) {
-        const int i = c0 + threadIdx.x;
-        uint32_t A = 0, Ti = 0;
-        if (i < id.W) {
-            A = load_agent(&s.sl_above[base + i]);
-            Ti = load_agent(&s.sl_ties[base + i]);
-        }
-        uint32_t tot_t;
-        const uint32_t tie_pre = carry[0] + block_scan_excl(Ti, &tot_t, sh_wsum);
-        int64_t take = (int64_t)r - (int64_t)tie_pre;
-        if (take < 0) take = 0;
-        if (take > (int64_t)Ti) take = Ti;
-        const uint32_t sel = A + (uint32_t)take;
-        uint32_t tot_s;
-        const uint32_t sel_pre = carry[1] + block_scan_excl(sel, &tot_s, sh_wsum);
-        if (i < id.W) {
-            s.sl_tiebase[base + i] = tie_pre;
-            s.sl_out[base + i] = sel_pre;
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            carry[0] += tot_t;
-            carry[1] += tot_s;
-        }
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) {
-        if (g.approx) {
-            msg_len[id.k] = (int64_t)carry[1];  // one segment; the count varies
-        } else {
-            if (carry[1] != (uint32_t)g.pair_k[id.p]) atomicAdd((unsigned long long*)&s.stats[4], 1ull);
-            if (id.seg == 0) msg_len[id.k] = msg_total;
-        }
-        store_agent(&ps->done, 0u);
-    }
+    scan_slices(id, id.W, ps->r, [&](size_t sl, uint32_t* A, uint32_t* Ti) {
+        *A = load_agent(&s.sl_above[sl]);
+        *Ti = load_agent(&s.sl_ties[sl]);
+    }, g, s, msg_len, msg_total, sh_wsum, carry);
+    if (threadIdx.x == 0) store_agent(&ps->done, 0u);
 }
 
 hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
@@ -1799,7 +1859,7 @@ hipError_t launch_agg_topk(int32_t K, int32_t d, const int32_t* idx, int64_t idx
 // RBGS: every worker sent the same blocks; block_slot[b] is the position q
 // of block b among the step's ascending block ids (-1: not drawn), and a
 // component of block b sits at q*B + offset in each message.  One workgroup
-// per range of kAggRange components, like the top-s kernel.
+// per range of kAggRange components.
 template <bool kApply>
 __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, int32_t B, const int32_t* block_slot,
                                                           const float* val, int64_t val_row, FinishArgs f) {

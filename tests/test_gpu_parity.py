@@ -127,9 +127,10 @@ def test_rbgs_partial_last_block_and_small_blocks():
     run_lockstep(Case(wl, steps=3, label="rbgs-block7"))
 
 
-def test_many_workers_overflow_the_staging():
-    # K = 64 leaves 64 staging entries per worker and workgroup; a generous
-    # candidate margin pushes wavefronts onto the direct global append
+def test_many_workers_and_a_margin_beyond_the_capacity():
+    # K = 64, the most workers a context takes; a margin of 200 k puts the
+    # speculative threshold so low that the candidates overflow the 64 k
+    # capacity and the pairs take the full-data path
     wl = W("resnet50").shrunk(256, K=64)
     run_lockstep(Case(wl, steps=3, options=((OPT_MARGIN, 800),), label="K=64"))
 
