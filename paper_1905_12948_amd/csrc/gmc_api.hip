@@ -637,8 +637,8 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
             GMC_TRY(prof_end(ctx, 1, ev));
         }
         GMC_TRY(prof_begin(ctx, 2, &ev));
-        GMC_LAUNCH(ctx, launch_topk_compact(ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
-        for (int pass = 1; pass <= 3; ++pass)
+        GMC_LAUNCH(ctx, launch_topk_compact(a, ctx->geo, ctx->scr, ctx->force_full, ctx->margin, ctx->stream));
+        for (int pass = 2; pass <= 3; ++pass)
             GMC_LAUNCH(ctx, launch_topk_hist(pass, a, ctx->geo, ctx->scr, ctx->force_full, ctx->margin, msg_len_dev,
                                              ctx->k_tot, ctx->stream));
         if (ctx->comp == GMC_TOPK_APPROX)  // exact top-s counts in the third pass

@@ -69,8 +69,7 @@ struct PairState {
     uint32_t cand_used; // candidates of this step (cand is reset for the next)
     uint32_t tau_used;  // the candidate threshold this step's fused pass used
     uint32_t n_tiles;   // copy tiles of this step's candidate list (0: not copied)
-    uint32_t fuse1;     // 1: the copy kernel also does the first histogram pass
-    uint32_t p1_done;   // 1: it has (the first histogram kernel skips the pair)
+    uint32_t fuse1;     // 1: the copy also does the first histogram pass (else its own workgroups)
     // exact top-s: the first pass puts the next step's threshold at the floor
     // of the 11-bit bin tau_bin holding the key of rank margin*k/4; with
     // tau_fine the second pass narrows it to the floor of the 22-bit bin
@@ -78,6 +77,7 @@ struct PairState {
     uint32_t tau_bin;
     uint32_t tau_need;
     uint32_t tau_fine;
+    uint32_t pad;
 };
 
 // Static geometry of the top-s selection (built on the host at init).
@@ -207,12 +207,13 @@ hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const
                                  uint64_t vec_mask, hipStream_t st);
 hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                                  uint64_t vec_mask, hipStream_t st);
-// count + copy; the copy also does the first histogram pass of the pairs
-// that resolve from their candidates (exact top-s)
-hipError_t launch_topk_compact(const TopkGeometry& g, const TopkScratch& s, int force_full, int margin,
-                               hipStream_t st);
-// pass 3 of exact top-s also lays out the message (per-slice offsets and
-// msg_len); the sampled-threshold top-s takes launch_topk_count for that
+// count, then copy and the first histogram pass (the copy itself takes it
+// for the pairs of exact top-s that resolve from their candidates)
+hipError_t launch_topk_compact(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int force_full,
+                               int margin, hipStream_t st);
+// passes 2 and 3 (pass 1 runs in launch_topk_compact's second kernel); pass 3
+// of exact top-s also lays out the message (per-slice offsets and msg_len),
+// the sampled-threshold top-s takes launch_topk_count for that
 hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                             int force_full, int margin, int64_t* msg_len, int64_t msg_total, hipStream_t st);
 hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,

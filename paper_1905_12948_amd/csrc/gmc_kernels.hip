@@ -578,10 +578,10 @@ struct SliceId {
     int k, seg, p, w, W;
 };
 
-__device__ __forceinline__ SliceId slice_id(const TopkGeometry& g) {
+__device__ __forceinline__ SliceId slice_id(const TopkGeometry& g, int blk) {
     SliceId id;
-    id.k = blockIdx.x / g.n_slices;
-    const int r = blockIdx.x % g.n_slices;
+    id.k = blk / g.n_slices;
+    const int r = blk % g.n_slices;
     id.seg = g.slice_seg[r];
     id.w = g.slice_rank[r];
     id.W = g.seg_slices[id.seg];
@@ -791,9 +791,8 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
 // words per slice), from which the last workgroup reads, once it has T, each
 // slice's counts above and at T and lays out the message.
 template <int PASS>
-__global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
-                                                           int force_full, int margin, int64_t* msg_len,
-                                                           int64_t msg_total) {
+__device__ void hist_pass(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int force_full,
+                          int margin, int64_t* msg_len, int64_t msg_total, int blk) {
     constexpr int nbins = PASS == 3 ? 512 : kBins;
     __shared__ uint32_t h[kBins];
     __shared__ uint32_t h2[PASS == 2 ? kBins : 1];
@@ -802,9 +801,9 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
     __shared__ int sh_last;
     __shared__ uint32_t carry[2];
 
-    const SliceId id = slice_id(g);
+    const SliceId id = slice_id(g, blk);
     PairState* ps = &s.pair[id.p];
-    if (PASS == 1 && ps->p1_done) return;  // the compaction took this pass
+    if (PASS == 1 && ps->fuse1) return;  // the compaction copy takes this pass
     // sampled-threshold top-s: the passes select over the sample, rank samp_r
     const bool approx = g.approx != 0;
     const int kp = approx ? g.samp_r : g.pair_k[id.p];
@@ -888,6 +887,13 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
     }
 }
 
+template <int PASS>
+__global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
+                                                           int force_full, int margin, int64_t* msg_len,
+                                                           int64_t msg_total) {
+    hist_pass<PASS>(a, g, s, force_full, margin, msg_len, msg_total, blockIdx.x);
+}
+
 hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                             int force_full, int margin, int64_t* msg_len, int64_t msg_total, hipStream_t st) {
     const int grid = g.K * g.n_slices;
@@ -969,7 +975,6 @@ __global__ __launch_bounds__(kGroup) void topk_compact_count_kernel(TopkGeometry
         ps->cand = all;
         ps->n_tiles = carry[1];
         ps->fuse1 = fuse ? 1u : 0u;
-        ps->p1_done = 0u;
         store_agent(&ps->done, 0u);
     }
 }
@@ -982,14 +987,14 @@ __global__ __launch_bounds__(kGroup) void topk_compact_count_kernel(TopkGeometry
 // pairs of exact top-s that resolve from their candidates the copy also
 // histograms the first digit, and the last of the pair's workgroups picks it
 // (the first histogram kernel then skips the pair).
-__global__ __launch_bounds__(kGroup) void topk_compact_copy_kernel(TopkGeometry g, TopkScratch s, int margin) {
+__device__ void compact_copy(const TopkGeometry& g, const TopkScratch& s, int margin, int blk) {
     __shared__ uint32_t pre[kCompactChunks];
     __shared__ uint32_t h[kBins];
     __shared__ uint32_t sh_wsum[kWavesPerGroup];
     __shared__ int sh_res[2];
     __shared__ int sh_last;
-    const int k = blockIdx.x / g.tiles_per_worker;
-    const int2 tm = g.tile_map[blockIdx.x % g.tiles_per_worker];
+    const int k = blk / g.tiles_per_worker;
+    const int2 tm = g.tile_map[blk % g.tiles_per_worker];
     const int seg = tm.x;
     const int p = k * g.n_seg + seg;
     PairState* ps = &s.pair[p];
@@ -1053,16 +1058,29 @@ __global__ __launch_bounds__(kGroup) void topk_compact_copy_kernel(TopkGeometry 
     if (!finish_slice(&ps->done, (int)n_wg, &sh_last)) return;
     const uint32_t cand = ps->cand;
     finish_digit<1>(ps, p, h, gh, g.pair_k[p], 0, cand, 0u, margin, 0, false, g, s, sh_wsum, sh_res);
-    if (threadIdx.x == 0) ps->p1_done = 1u;
 }
 
-hipError_t launch_topk_compact(const TopkGeometry& g, const TopkScratch& s, int force_full, int margin,
-                               hipStream_t st) {
+// The copy and the first histogram pass in one launch: the first
+// K * tiles_per_worker workgroups copy (with the first pass of the pairs that
+// resolve from their candidates), the K * n_slices after them take the first
+// pass of the others (full data, or the sample of the sampled-threshold
+// top-s); which pairs those are the count kernel decided (PairState::fuse1).
+__global__ __launch_bounds__(kGroup) void topk_copy_pass1_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
+                                                                 int force_full, int margin) {
+    const int n_copy = g.K * g.tiles_per_worker;
+    if ((int)blockIdx.x < n_copy)
+        compact_copy(g, s, margin, blockIdx.x);
+    else
+        hist_pass<1>(a, g, s, force_full, margin, nullptr, 0, (int)blockIdx.x - n_copy);
+}
+
+hipError_t launch_topk_compact(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int force_full,
+                               int margin, hipStream_t st) {
     hipLaunchKernelGGL(topk_compact_count_kernel, dim3(g.K * g.n_cgroups), dim3(kGroup), 0, st, g, s, force_full);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(topk_compact_copy_kernel, dim3((unsigned)((int64_t)g.K * g.tiles_per_worker)), dim3(kGroup),
-                       0, st, g, s, margin);
+    const int64_t grid = (int64_t)g.K * g.tiles_per_worker + (int64_t)g.K * g.n_slices;
+    hipLaunchKernelGGL(topk_copy_pass1_kernel, dim3((unsigned)grid), dim3(kGroup), 0, st, a, g, s, force_full, margin);
     return hipGetLastError();
 }
 
@@ -1077,7 +1095,7 @@ __global__ __launch_bounds__(kGroup) void topk_count_kernel(StepArgs a, TopkGeom
     __shared__ int sh_last;
     __shared__ uint32_t carry[2];
 
-    const SliceId id = slice_id(g);
+    const SliceId id = slice_id(g, blockIdx.x);
     PairState* ps = &s.pair[id.p];
     const int mode = ps->mode;
     const uint32_t T = ps->T;
@@ -1147,7 +1165,7 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
     __shared__ float st_val[kStageSlots];
     __shared__ uint32_t sh_wsum[kWavesPerGroup];
 
-    const SliceId id = slice_id(g);
+    const SliceId id = slice_id(g, blockIdx.x);
     const PairState* ps = &s.pair[id.p];
     const int mode = ps->mode;
     const uint32_t T = ps->T;
