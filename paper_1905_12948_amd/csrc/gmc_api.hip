@@ -386,6 +386,8 @@ gmc_status prepare(gmc_ctx* ctx) {
         sc.sl_hist = cv.take<uint32_t>((size_t)K * nsl * kSlHist);
         sc.stats = ctx->stats;
         ctx->rowptr = cv.take<int32_t>((size_t)K * (ctx->n_ranges + 1));
+        sc.rowptr = ctx->rowptr;  // the emit kernel writes them for gmc_iteration's server pass
+        sc.n_ranges = ctx->n_ranges;
         sc.samp = approx ? cv.take<float>((size_t)K * samp_n) : nullptr;
     }
     if (cv.off > bytes) return fail(ctx, GMC_ENOMEM, "internal: scratch layout overflow");
@@ -681,8 +683,10 @@ gmc_status gmc_step_detach(gmc_ctx* ctx, const float* w_t_dev, const float* w_pr
 
 namespace {
 
+// rowptr_ready: the messages are the ones the context's last gmc_step just
+// emitted (gmc_iteration), whose emit kernel also wrote the row pointers
 gmc_status aggregate_impl(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev, const int64_t* msg_len_dev,
-                          FinishArgs& f) {
+                          FinishArgs& f, bool rowptr_ready = false) {
     GMC_TRY(prepare(ctx));
     GMC_HIP(ctx, hipSetDevice(ctx->device));
     f.s = ctx->s;
@@ -714,8 +718,9 @@ gmc_status aggregate_impl(gmc_ctx* ctx, const int32_t* idx_dev, const float* val
         GMC_LAUNCH(ctx, launch_agg_rbgs(ctx->K, (int32_t)ctx->d, ctx->block, ctx->rbgs_slot, val_dev, row_v, f,
                                         ctx->stream));
     } else {
-        GMC_LAUNCH(ctx, launch_agg_rowptr(ctx->K, (int32_t)ctx->d, idx_dev, row_i, msg_len_dev, ctx->rowptr,
-                                          ctx->n_ranges, ctx->stream));
+        if (!rowptr_ready)
+            GMC_LAUNCH(ctx, launch_agg_rowptr(ctx->K, (int32_t)ctx->d, idx_dev, row_i, msg_len_dev, ctx->rowptr,
+                                              ctx->n_ranges, ctx->stream));
         GMC_LAUNCH(ctx, launch_agg_topk(ctx->K, (int32_t)ctx->d, idx_dev, row_i, val_dev, row_v, ctx->rowptr,
                                         ctx->n_ranges, f, ctx->stream));
     }
@@ -813,7 +818,7 @@ gmc_status gmc_iteration(gmc_ctx* ctx, const float* w_t_dev, float* w_prev_io_de
     f.w_in = w_t_dev;
     f.w_out = w_prev_io_dev;
     f.w_prev = ctx->rule == kRuleServerMomentum ? w_prev_io_dev : nullptr;  // read before written, per component
-    return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, f);
+    return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, f, true);
 }
 
 gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const float* update_dev) {

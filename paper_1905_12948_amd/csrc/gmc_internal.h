@@ -137,6 +137,8 @@ struct TopkScratch {
     uint32_t* sl_tiebase;         // [K*n_slices] at-threshold components in earlier slices
     uint32_t* sl_hist;            // [K*n_slices][kSlHist] third-pass counts per slice (exact top-s)
     float* samp;                  // [K][samp_n] the sample's values (sampled-threshold top-s)
+    int32_t* rowptr;              // [K][n_ranges+1] server-pass row pointers, also written by the emit
+    int32_t n_ranges;             // ranges of kAggTopkRange components
     int64_t* stats;               // [8]
 };
 

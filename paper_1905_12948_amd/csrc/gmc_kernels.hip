@@ -1183,6 +1183,23 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
     float* e = a.wp.e[id.k];
 
     const Slice v = open_slice(mode, ps->cand_used, id.k, id.seg, id.p, id.w, id.W, a, g, s);
+    // The server pass's row pointers: the slices' index spans [B(w), B(w+1))
+    // tile the segment (B(0) its start, B(W) its end, B(w) the index of the
+    // slice's first element), so each range start r*R of the segment lies in
+    // one span, and there it is the row position of the first kept component
+    // at or after it: this slice's first position plus its kept components
+    // with a lower index.
+    const int64_t seg_lo = g.seg_start[id.seg], seg_hi = g.seg_start[id.seg + 1];
+    const int64_t in_total = mode == 0 ? (int64_t)ps->cand_used : seg_hi - seg_lo;
+    auto index_at = [&](int64_t pos) -> int64_t {
+        return pos < in_total ? (v.idx ? (int64_t)v.idx[pos] : seg_lo + pos) : seg_hi;
+    };
+    const int64_t span_lo = id.w == 0 ? seg_lo : index_at(v.lo);
+    const int64_t span_hi = id.w == id.W - 1 ? seg_hi : index_at(v.hi);
+    const int32_t row0 = g.seg_out[id.seg] + (int32_t)out0;  // this slice's first row position
+    int32_t* rp = s.rowptr + (size_t)id.k * (s.n_ranges + 1);
+    constexpr int64_t R = kAggTopkRange;
+    int64_t prev_last = span_lo - 1;  // the index before the round's first element
     uint32_t run_above = 0, run_ties = 0;  // over the earlier rounds
     for (int64_t s0 = v.lo; s0 < v.hi; s0 += kEmitStage) {
         const int32_t ns = (int32_t)(v.hi - s0 < kEmitStage ? v.hi - s0 : kEmitStage);
@@ -1208,11 +1225,14 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
         uint32_t tot;
         const uint32_t pre = block_scan_excl((na << 16) | nt, &tot, sh_wsum);  // counts < 2^16
         uint32_t a_before = run_above + (pre >> 16), t_before = run_ties + (pre & 0xffffu);
+        int32_t kbv[kEmitLoads];  // kept components of the slice before each element
 #pragma unroll
         for (int i = 0; i < kEmitLoads; ++i) {
-            if (q0 + i >= ns) break;
+            kbv[i] = 0;
+            if (q0 + i >= ns) continue;
             const float x = st_val[stage_slot(q0 + i)];
             const uint32_t key = key_of(x);
+            kbv[i] = (int32_t)(a_before + (uint32_t)((int64_t)t_before < quota ? (int64_t)t_before : quota));
             bool take = false;
             uint32_t o = 0;
             if (key > T) {
@@ -1233,8 +1253,33 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
         }
         run_above += tot >> 16;
         run_ties += tot & 0xffffu;
+        // row pointers of the range starts in (prev_last, the round's last
+        // index]: the row position of the round's first element at or after
+        // each (binary search over the staged indices, ascending), all
+        // threads sharing the range starts
+        __syncthreads();  // the round's values are read; the stage now holds the counts
+        int32_t* st_kb = reinterpret_cast<int32_t*>(st_val);
+#pragma unroll
+        for (int i = 0; i < kEmitLoads; ++i)
+            if (q0 + i < ns) st_kb[stage_slot(q0 + i)] = kbv[i];
         __syncthreads();
+        const int64_t j_end = st_idx[stage_slot(ns - 1)];
+        for (int64_t rr = (prev_last + R) / R + threadIdx.x; rr * R <= j_end; rr += kGroup) {
+            const int64_t start = rr * R;
+            int32_t lo = 0, hi = ns - 1;  // the first element whose index is >= start (the last one is)
+            while (lo < hi) {
+                const int32_t mid = (lo + hi) >> 1;
+                if ((int64_t)st_idx[stage_slot(mid)] < start) lo = mid + 1; else hi = mid;
+            }
+            rp[rr] = row0 + st_kb[stage_slot(lo)];
+        }
+        prev_last = j_end;
+        __syncthreads();  // the stage is read before the next round overwrites it
     }
+    // range starts after the slice's last element, up to the span's end
+    const int32_t kept = (int32_t)(run_above + (uint32_t)((int64_t)run_ties < quota ? (int64_t)run_ties : quota));
+    for (int64_t rr = (prev_last + R) / R + threadIdx.x; rr * R < span_hi; rr += kGroup) rp[rr] = row0 + kept;
+    if (threadIdx.x == 0 && id.seg == g.n_seg - 1 && id.w == id.W - 1) rp[s.n_ranges] = row0 + kept;  // the row's length
 }
 
 hipError_t launch_topk_emit(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
