@@ -9,13 +9,17 @@
 //   topk_hist    three radix-select passes (11 + 11 + 9 bits of the key) over
 //                the candidates, or over all of u when the candidates cannot
 //                prove they hold the top k; the last workgroup of each
-//                (worker, segment) picks the digit
-//   topk_count   per-slice counts above / at the threshold, then a scan over
-//                the segment's slices (last workgroup)
+//                (worker, segment) picks the digit.  The first pass runs
+//                with the compaction copy; the third also counts, per slice,
+//                the components above and at the threshold and lays out the
+//                message (the sampled-threshold top-s, whose passes run over
+//                its sample, counts in topk_count)
 //   topk_emit    ordered compaction of the kept components into the message,
-//                residual u - u at the kept components
+//                residual u - u at the kept components, and the server
+//                pass's row pointers
 //   rbgs_*       shared block draw and the fused pass that gathers whole blocks
-//   agg_*        the server sum over workers in worker order, dense update
+//   agg_*        the server sum over workers in worker order, the update and
+//                w_{t+1} = w_t + update
 //   apply        w_prev <- w (optional), w <- w + update
 //
 // Arithmetic is binary32 with one rounding per operation; the library is
@@ -487,6 +491,7 @@ namespace {
 constexpr int kSliceLoads = 16;      // independent loads in flight per thread
 constexpr int kEmitLoads = 12;       // staged elements per thread in the emit pass
 constexpr int kEmitStage = kGroup * kEmitLoads;  // elements staged in LDS per round
+constexpr int kFullRound = kGroup * 16;          // full-data elements per round of the emit
 
 // A workgroup's slice of a pair's selection input.
 struct Slice {
@@ -897,10 +902,8 @@ __global__ __launch_bounds__(kGroup) void topk_hist_kernel(StepArgs a, TopkGeome
 hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                             int force_full, int margin, int64_t* msg_len, int64_t msg_total, hipStream_t st) {
     const int grid = g.K * g.n_slices;
-    if (pass == 1)
-        hipLaunchKernelGGL(topk_hist_kernel<1>, dim3(grid), dim3(kGroup), 0, st, a, g, s, force_full, margin, msg_len,
-                           msg_total);
-    else if (pass == 2)
+    if (pass != 2 && pass != 3) return hipErrorInvalidValue;  // pass 1 runs with the compaction copy
+    if (pass == 2)
         hipLaunchKernelGGL(topk_hist_kernel<2>, dim3(grid), dim3(kGroup), 0, st, a, g, s, force_full, margin, msg_len,
                            msg_total);
     else
@@ -1201,7 +1204,76 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
     constexpr int64_t R = kAggTopkRange;
     int64_t prev_last = span_lo - 1;  // the index before the round's first element
     uint32_t run_above = 0, run_ties = 0;  // over the earlier rounds
-    for (int64_t s0 = v.lo; s0 < v.hi; s0 += kEmitStage) {
+    if (mode == 1) {
+        // Full data: the slice is a run of consecutive components of which
+        // few are kept, so it is streamed in rounds of kFullRound (coalesced
+        // loads, 16 per thread in flight) and only the kept components are
+        // placed: element (i, wave, lane) of a round has index order
+        // i-major, then wave, then lane, and its rank among the round's kept
+        // components comes from ballots and one scan of the 64 (i, wave)
+        // counts.  A range start at element j (j a multiple of R) gets the
+        // row position of the first kept component at or after it.
+        constexpr int kIt = kFullRound / kGroup;  // 16
+        static_assert(kIt * kWavesPerGroup == kWave, "one (i, wave) count per lane of the scanning wave");
+        const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+        const uint64_t lt = lanemask_lt();
+        uint32_t* cnt = reinterpret_cast<uint32_t*>(st_idx);  // [kIt][kWavesPerGroup]: above << 16 | ties
+        for (int64_t s0 = v.lo; s0 < v.hi; s0 += kFullRound) {
+            float x[kIt];
+            uint64_t ba[kIt], bt[kIt];
+#pragma unroll
+            for (int i = 0; i < kIt; ++i) {
+                const int64_t q = s0 + i * kGroup + threadIdx.x;
+                x[i] = q < v.hi ? v.val[q] : 0.0f;
+            }
+#pragma unroll
+            for (int i = 0; i < kIt; ++i) {
+                const bool in = s0 + i * kGroup + threadIdx.x < v.hi;
+                const uint32_t key = key_of(x[i]);
+                ba[i] = ballot(in && key > T);
+                bt[i] = ballot(in && key == T);
+                if (lane == 0) cnt[i * kWavesPerGroup + wave] = (popc64(ba[i]) << 16) | popc64(bt[i]);
+            }
+            __syncthreads();
+            if (wave == 0) {  // exclusive scan of the 64 counts in index order, and the round's total
+                const uint32_t c = cnt[lane];
+                uint32_t incl = c;
+#pragma unroll
+                for (int o = 1; o < kWave; o <<= 1) {
+                    const uint32_t y = __shfl_up(incl, o, kWave);
+                    if (lane >= o) incl += y;
+                }
+                cnt[kWave + lane] = incl - c;
+                if (lane == kWave - 1) cnt[2 * kWave] = incl;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < kIt; ++i) {
+                const int64_t q = s0 + i * kGroup + threadIdx.x;
+                const uint32_t pre = cnt[kWave + i * kWavesPerGroup + wave];
+                const uint32_t a_before = run_above + (pre >> 16) + popc64(ba[i] & lt);
+                const uint32_t t_before = run_ties + (pre & 0xffffu) + popc64(bt[i] & lt);
+                const int64_t j = seg_lo + q;
+                const int64_t tk = (int64_t)t_before < quota ? (int64_t)t_before : quota;
+                if (q < v.hi && (j & (R - 1)) == 0) rp[j / R] = row0 + (int32_t)(a_before + (uint32_t)tk);
+                const bool above = (ba[i] >> lane) & 1ull, tie = (bt[i] >> lane) & 1ull;
+                if (above || (tie && (int64_t)t_before < quota)) {
+                    const uint32_t o = out0 + a_before + (uint32_t)tk;
+                    if (o < kseg) {  // always, when the counts are consistent
+                        irow[o] = (int32_t)j;
+                        vrow[o] = x[i];
+                        e[j] = x[i] - x[i];  // residual u - C(u) at a kept component
+                    }
+                }
+            }
+            const uint32_t tot = cnt[2 * kWave];
+            run_above += tot >> 16;
+            run_ties += tot & 0xffffu;
+            __syncthreads();  // the counts are read before the next round writes them
+        }
+        if (v.hi > v.lo) prev_last = seg_lo + v.hi - 1;
+    }
+    for (int64_t s0 = v.lo; mode != 1 && s0 < v.hi; s0 += kEmitStage) {
         const int32_t ns = (int32_t)(v.hi - s0 < kEmitStage ? v.hi - s0 : kEmitStage);
 #pragma unroll
         for (int i = 0; i < kEmitLoads; ++i) {
