@@ -706,12 +706,17 @@ template <int PASS>
 __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, int kp, int mode, uint32_t cand,
                              uint32_t prefix, int margin, int force_full, bool approx, const TopkGeometry& g,
                              const TopkScratch& s, uint32_t* sh_wsum, int* sh_res, uint32_t* h2 = nullptr,
-                             uint32_t* gh2 = nullptr, uint32_t* T_out = nullptr, int32_t* r_out = nullptr) {
+                             uint32_t* gh2 = nullptr, uint32_t* T_out = nullptr, int32_t* r_out = nullptr,
+                             bool solo = false) {
     constexpr int nbins = PASS == 3 ? 512 : kBins;
-    // second pass: the threshold's bin histogram comes in with T's
+    // second pass: the threshold's bin histogram comes in with T's.  A pair
+    // that one workgroup covered (solo) has its whole histogram in LDS
+    // already and never wrote the global one.
     const bool fine2 = PASS == 2 && ps->tau_fine != 0u && ps->tau_bin != prefix;
-    if (fine2) take_hist2<kBins>(h, gh, h2, gh2);
-    else take_hist<nbins>(h, gh);
+    if (!solo) {
+        if (fine2) take_hist2<kBins>(h, gh, h2, gh2);
+        else take_hist<nbins>(h, gh);
+    }
     const uint32_t need = PASS == 1 ? (uint32_t)kp : (uint32_t)ps->need;
     uint32_t above = 0;
     const int bin = find_bin(h, nbins, need, &above, sh_wsum, sh_res);
@@ -855,7 +860,8 @@ __device__ void hist_pass(const StepArgs& a, const TopkGeometry& g, const TopkSc
     __syncthreads();
     uint32_t* gh = s.hist + (size_t)id.p * kBins;
     uint32_t* gh2 = s.hist2 + (size_t)id.p * kBins;
-    for (int b = threadIdx.x; b < nbins; b += kGroup) {
+    const bool solo = W == 1;  // the pair's whole histogram is this workgroup's
+    for (int b = threadIdx.x; !solo && b < nbins; b += kGroup) {
         if (h[b]) atomicAdd(&gh[b], h[b]);
         if (fine2 && h2[b]) atomicAdd(&gh2[b], h2[b]);
     }
@@ -878,7 +884,7 @@ __device__ void hist_pass(const StepArgs& a, const TopkGeometry& g, const TopkSc
     uint32_t T = 0;
     int32_t r = 0;
     finish_digit<PASS>(ps, id.p, h, gh, kp, mode, cand, prefix, margin, force_full, approx, g, s, sh_wsum, sh_res,
-                       PASS == 2 ? h2 : nullptr, gh2, &T, &r);
+                       PASS == 2 ? h2 : nullptr, gh2, &T, &r, solo);
     if (count) {
         // each slice's counts above T and at T: above the bin, plus S[b+1];
         // at T, S[b] - S[b+1] (b = T's low 9 bits)
@@ -1056,11 +1062,13 @@ __device__ void compact_copy(const TopkGeometry& g, const TopkScratch& s, int ma
     if (!fuse) return;
     __syncthreads();
     uint32_t* gh = s.hist + (size_t)p * kBins;
-    for (int b = threadIdx.x; b < kBins; b += kGroup)
+    const bool solo = n_wg == 1;  // the pair's whole histogram is this workgroup's
+    for (int b = threadIdx.x; !solo && b < kBins; b += kGroup)
         if (h[b]) atomicAdd(&gh[b], h[b]);
     if (!finish_slice(&ps->done, (int)n_wg, &sh_last)) return;
     const uint32_t cand = ps->cand;
-    finish_digit<1>(ps, p, h, gh, g.pair_k[p], 0, cand, 0u, margin, 0, false, g, s, sh_wsum, sh_res);
+    finish_digit<1>(ps, p, h, gh, g.pair_k[p], 0, cand, 0u, margin, 0, false, g, s, sh_wsum, sh_res, nullptr,
+                    nullptr, nullptr, nullptr, solo);
 }
 
 // The copy and the first histogram pass in one launch: the first
