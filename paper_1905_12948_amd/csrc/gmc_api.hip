@@ -81,6 +81,10 @@ struct gmc_ctx {
     uint32_t* rbgs_bitmap = nullptr;
     int32_t* rbgs_blocks = nullptr;
     int32_t* rbgs_slot = nullptr;
+    int32_t* rbgs_prev = nullptr;    // the previous step's blocks
+    int32_t* rbgs_visit = nullptr;   // the sparse server pass's ranges
+    uint32_t* rbgs_rbits = nullptr;  // zeroed bitmap of ranges (large d)
+    int32_t* rbgs_meta = nullptr;    // [0] ranges in rbgs_visit (-1: all), [1] non-finite flag
     int64_t* stats = nullptr;
 
     // profiling
@@ -273,6 +277,11 @@ gmc_status prepare(gmc_ctx* ctx) {
         add((size_t)(ctx->nb + 31) / 32, 4);
         add((size_t)ctx->n_sel, 4);
         add((size_t)ctx->nb, 4);
+        const size_t rr = (size_t)((ctx->d + kAggRange - 1) / kAggRange);
+        add((size_t)ctx->n_sel, 4);
+        add(rr, 4);
+        add((rr + 31) / 32, 4);
+        add(2, 4);
     } else {
         T = build_tables(ctx);
         const size_t nc = T.chunk_start.size(), ng = T.cgrp_lo.size(), nsl = T.slice_seg.size();
@@ -315,6 +324,11 @@ gmc_status prepare(gmc_ctx* ctx) {
         ctx->rbgs_bitmap = cv.take<uint32_t>((ctx->nb + 31) / 32);
         ctx->rbgs_blocks = cv.take<int32_t>(ctx->n_sel);
         ctx->rbgs_slot = cv.take<int32_t>(ctx->nb);
+        const size_t rr = (size_t)((ctx->d + kAggRange - 1) / kAggRange);
+        ctx->rbgs_prev = cv.take<int32_t>(ctx->n_sel);
+        ctx->rbgs_visit = cv.take<int32_t>(rr);
+        ctx->rbgs_rbits = cv.take<uint32_t>((rr + 31) / 32);
+        ctx->rbgs_meta = cv.take<int32_t>(2);
     } else {
         const size_t nc = T.chunk_start.size(), ng = T.cgrp_lo.size(), nsl = T.slice_seg.size();
         const size_t ns = T.seg_out.size(), np = (size_t)K * ns;
@@ -605,7 +619,8 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
         GMC_TRY(prof_begin(ctx, 2, &ev));
         GMC_LAUNCH(ctx, launch_rbgs_sample(ctx->seed, (uint64_t)ctx->t, ctx->nb, ctx->n_sel, (int32_t)ctx->d,
                                            ctx->block, ctx->K, ctx->rbgs_bitmap, ctx->rbgs_blocks, ctx->rbgs_slot,
-                                           idx_dev, row_i, msg_len_dev, ctx->stream));
+                                           idx_dev, row_i, msg_len_dev, ctx->rbgs_prev, ctx->rbgs_visit,
+                                           ctx->rbgs_rbits, ctx->rbgs_meta, ctx->stream));
         GMC_TRY(prof_end(ctx, 2, ev));
         GMC_TRY(prof_begin(ctx, 0, &ev));
         uint64_t vec_mask = 0;
@@ -715,7 +730,8 @@ gmc_status aggregate_impl(gmc_ctx* ctx, const int32_t* idx_dev, const float* val
     hipEvent_t ev;
     GMC_TRY(prof_begin(ctx, 4, &ev));
     if (ctx->comp == GMC_RBGS) {
-        GMC_LAUNCH(ctx, launch_agg_rbgs(ctx->K, (int32_t)ctx->d, ctx->block, ctx->rbgs_slot, val_dev, row_v, f,
+        GMC_LAUNCH(ctx, launch_agg_rbgs(ctx->K, (int32_t)ctx->d, ctx->block, ctx->n_sel, ctx->rbgs_slot, val_dev,
+                                        row_v, f, ctx->rbgs_visit, ctx->rbgs_meta,
                                         ctx->stream));
     } else {
         if (!rowptr_ready)

@@ -223,10 +223,15 @@ hipError_t launch_topk_count(const StepArgs& a, const TopkGeometry& g, const Top
 hipError_t launch_topk_emit(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                             int32_t* idx, float* val, int64_t row_len, hipStream_t st);
 
+// also keeps the previous step's blocks (prev, [n_sel]) and lays out the
+// sparse server pass's ranges (visit, [ceil(d/kAggRange)]; meta[0] their
+// count, -1: all; meta[1] the non-finite flag the server pass raises; rbits
+// a zeroed bitmap of ceil(d/kAggRange) bits for large d)
 hipError_t launch_rbgs_sample(uint64_t seed, uint64_t t, int32_t nb, int32_t n_sel, int32_t d,
                               int32_t B, int32_t K, uint32_t* bitmap, int32_t* blocks,
                               int32_t* block_slot, int32_t* idx, int64_t idx_row,
-                              int64_t* msg_len, hipStream_t st);
+                              int64_t* msg_len, int32_t* prev, int32_t* visit, uint32_t* rbits, int32_t* meta,
+                              hipStream_t st);
 // vec_mask: workers whose rows (g, e, detached points) are 16-byte aligned,
 // with w_t, w_prev and the message rows aligned and B a multiple of 4 (else 0)
 hipError_t launch_rbgs_fused(const StepArgs& a, int32_t K, int32_t B, const int32_t* block_slot,
@@ -240,9 +245,11 @@ hipError_t launch_agg_rowptr(int32_t K, int32_t d, const int32_t* idx, int64_t i
 hipError_t launch_agg_topk(int32_t K, int32_t d, const int32_t* idx, int64_t idx_row,
                            const float* val, int64_t val_row, const int32_t* rowptr,
                            int32_t n_ranges, const FinishArgs& f, hipStream_t st);
-// block_slot: the last step's table from launch_rbgs_sample
-hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, const int32_t* block_slot,
-                           const float* val, int64_t val_row, const FinishArgs& f, hipStream_t st);
+// block_slot: the last step's table from launch_rbgs_sample; visit, meta:
+// its range list for a sparse apply (meta[1]: the non-finite flag it raises)
+hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, int32_t n_sel, const int32_t* block_slot,
+                           const float* val, int64_t val_row, const FinishArgs& f, const int32_t* visit,
+                           int32_t* meta, hipStream_t st);
 hipError_t launch_detach(const DetachArgs& a, int32_t K, hipStream_t st);
 
 hipError_t launch_apply(int32_t d, float* w, float* w_prev_out, const float* update,

@@ -1382,15 +1382,25 @@ constexpr int kLdsBitmapWords = 8192;  // 262144 blocks
 // One workgroup.  Floyd's algorithm (one lane; the draws are sequential by
 // definition) marks n_sel of nb blocks in a bitmap; the workgroup then
 // compacts the bitmap into the ascending block list and the block -> slot map.
+// It also keeps the previous step's block list (prev) and lays out the ranges
+// of kAggRange components a sparse server pass must visit (visit, meta[0]):
+// those of this step's blocks and the previous step's, ascending, or every
+// range (meta[0] = -1) when the last server pass raised meta[1] (a non-finite
+// w outside the sent blocks, which stays marked).
 __global__ __launch_bounds__(kGroup) void rbgs_sample_kernel(uint64_t seed, uint64_t t, int32_t nb,
                                                              int32_t n_sel, int32_t d, int32_t B,
                                                              int32_t K, uint32_t* gbitmap,
                                                              int32_t* blocks, int32_t* block_slot,
                                                              int32_t* idx, int64_t idx_row,
-                                                             int64_t* msg_len) {
+                                                             int64_t* msg_len, int32_t* prev, int32_t* visit,
+                                                             uint32_t* grbits, int32_t* meta) {
     __shared__ uint32_t lbits[kLdsBitmapWords];
     __shared__ uint32_t wsum[kWavesPerGroup];
     __shared__ uint32_t carry;
+    __shared__ int32_t sh_nf;
+    for (int i = threadIdx.x; i < n_sel; i += kGroup) prev[i] = blocks[i];
+    if (threadIdx.x == 0) sh_nf = meta[1];
+    __syncthreads();  // the old list is read before it is rewritten
     const int nwords = (nb + 31) / 32;
     uint32_t* bits = nwords <= kLdsBitmapWords ? lbits : gbitmap;
     for (int w = threadIdx.x; w < nwords; w += kGroup) bits[w] = 0u;
@@ -1446,14 +1456,54 @@ __global__ __launch_bounds__(kGroup) void rbgs_sample_kernel(uint64_t seed, uint
     for (int kk = threadIdx.x; kk < K; kk += kGroup) msg_len[kk] = m;
     if (bits == gbitmap)
         for (int w = threadIdx.x; w < nwords; w += kGroup) gbitmap[w] = 0u;
+
+    // the sparse server pass's ranges
+    const int32_t n_ranges = (int32_t)(((int64_t)d + kAggRange - 1) / kAggRange);
+    if (sh_nf) {
+        if (threadIdx.x == 0) {
+            meta[0] = -1;
+            meta[1] = 0;
+        }
+        return;
+    }
+    const int rwords = (n_ranges + 31) / 32;
+    const bool in_lds = rwords <= kLdsBitmapWords;
+    uint32_t* rb = in_lds ? lbits : grbits;
+    __syncthreads();  // every thread is done with the block bitmap
+    if (in_lds)
+        for (int w = threadIdx.x; w < rwords; w += kGroup) lbits[w] = 0u;
+    __syncthreads();
+    for (int i = threadIdx.x; i < 2 * n_sel; i += kGroup) {
+        const int64_t b = i < n_sel ? blocks[i] : prev[i - n_sel];
+        const int64_t lo = b * B, hi = (b + 1) * B < d ? (b + 1) * B : d;
+        for (int64_t r = lo / kAggRange; r <= (hi - 1) / kAggRange; ++r) atomicOr(&rb[r >> 5], 1u << (r & 31));
+    }
+    if (!in_lds) __threadfence();  // the global bitmap's atomics are visible to the loads below
+    __syncthreads();
+    if (threadIdx.x == 0) carry = 0;
+    __syncthreads();
+    for (int w0 = 0; w0 < rwords; w0 += kGroup) {
+        const int w = w0 + threadIdx.x;
+        const uint32_t word = w < rwords ? (in_lds ? rb[w] : load_agent(&rb[w])) : 0u;
+        uint32_t tot;
+        uint32_t pos = carry + block_scan_excl((uint32_t)__popc(word), &tot, wsum);
+        for (int bb = 0; bb < 32; ++bb)
+            if ((word >> bb) & 1u) visit[pos++] = w * 32 + bb;
+        if (!in_lds && w < rwords) store_agent(&rb[w], 0u);  // clear for the next step
+        __syncthreads();
+        if (threadIdx.x == 0) carry += tot;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) meta[0] = (int32_t)carry;
 }
 
 hipError_t launch_rbgs_sample(uint64_t seed, uint64_t t, int32_t nb, int32_t n_sel, int32_t d,
                               int32_t B, int32_t K, uint32_t* bitmap, int32_t* blocks,
                               int32_t* block_slot, int32_t* idx, int64_t idx_row,
-                              int64_t* msg_len, hipStream_t st) {
+                              int64_t* msg_len, int32_t* prev, int32_t* visit, uint32_t* rbits, int32_t* meta,
+                              hipStream_t st) {
     hipLaunchKernelGGL(rbgs_sample_kernel, dim3(1), dim3(kGroup), 0, st, seed, t, nb, n_sel, d, B, K,
-                       bitmap, blocks, block_slot, idx, idx_row, msg_len);
+                       bitmap, blocks, block_slot, idx, idx_row, msg_len, prev, visit, rbits, meta);
     return hipGetLastError();
 }
 
@@ -1711,7 +1761,8 @@ __device__ __forceinline__ void visit_words(uint32_t* wv, const unsigned char* h
 // also marks the components for the next worker pass in wb.
 template <bool kApply>
 __device__ __forceinline__ void write_update(const float* acc, const unsigned char* hit, uint32_t* wb, int64_t base,
-                                             int64_t n, const FinishArgs& f, const uint32_t* wv) {
+                                             int64_t n, const FinishArgs& f, const uint32_t* wv,
+                                             int32_t* nf_flag = nullptr) {
     const float s = f.s;
     const bool vec = n == kAggRange && (base & 3) == 0 && (f.update == nullptr || aligned16(f.update)) &&
                      (!kApply || (aligned16(f.w_in) && aligned16(f.w_out) &&
@@ -1744,6 +1795,7 @@ __device__ __forceinline__ void write_update(const float* acc, const unsigned ch
             const float wn = next_w(f.w_in[j], dl, f.w_prev, j, f.b);
             f.w_out[j] = wn;
             if (f.wbits && (hit[q] || not_finite(wn))) atomicOr(&wb[q >> 5], 1u << (q & 31));
+            if (nf_flag && !hit[q] && not_finite(wn)) atomicOr(nf_flag, 1);
         }
     }
 }
@@ -2001,16 +2053,25 @@ hipError_t launch_agg_topk(int32_t K, int32_t d, const int32_t* idx, int64_t idx
 
 // RBGS: every worker sent the same blocks; block_slot[b] is the position q
 // of block b among the step's ascending block ids (-1: not drawn), and a
-// component of block b sits at q*B + offset in each message.  One workgroup
-// per range of kAggRange components.
+// component of block b sits at q*B + offset in each message.  The range of
+// kAggRange components starting at base.  nf_flag (nullable) is raised when a
+// component no worker sent gets a non-finite w_{t+1} (it stays marked, so the
+// next sparse server pass visits every range).
+struct RbgsLds {
+    float acc[kAggRange];
+    unsigned char hit[kAggRange];
+    uint32_t wb[kAggRange / 32];
+    uint32_t wv[kAggRange / 32];
+};
+
 template <bool kApply>
-__global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, int32_t B, const int32_t* block_slot,
-                                                          const float* val, int64_t val_row, FinishArgs f) {
-    __shared__ float acc[kAggRange];
-    __shared__ unsigned char hit[kAggRange];
-    __shared__ uint32_t wb[kAggRange / 32];
-    __shared__ uint32_t wv[kAggRange / 32];
-    const int64_t base = (int64_t)blockIdx.x * kAggRange;
+__device__ void agg_rbgs_range(int64_t base, int32_t K, int32_t d, int32_t B, const int32_t* block_slot,
+                               const float* val, int64_t val_row, const FinishArgs& f, int32_t* nf_flag,
+                               RbgsLds& L) {
+    float* acc = L.acc;
+    unsigned char* hit = L.hit;
+    uint32_t* wb = L.wb;
+    uint32_t* wv = L.wv;
     const int64_t n = (int64_t)d - base < kAggRange ? (int64_t)d - base : kAggRange;
     const bool sparse = kApply && f.sparse_apply;
     if (threadIdx.x < kAggRange / 32) wb[threadIdx.x] = 0u;
@@ -2068,16 +2129,23 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
                 st4(f.w_out + j, nx);
                 if (f.wbits) {
                     const int q = (int)(j - base);
-                    const uint32_t m = (slots[i] >= 0 ? 0xfu : 0u) | not_finite(nx.x) | (not_finite(nx.y) << 1) |
-                                       (not_finite(nx.z) << 2) | (not_finite(nx.w) << 3);
-                    atomicOr(&wb[q >> 5], m << (q & 31));
+                    const uint32_t nf = not_finite(nx.x) | (not_finite(nx.y) << 1) | (not_finite(nx.z) << 2) |
+                                        (not_finite(nx.w) << 3);
+                    atomicOr(&wb[q >> 5], ((slots[i] >= 0 ? 0xfu : 0u) | nf) << (q & 31));
+                    if (nf_flag && nf && slots[i] < 0) atomicOr(nf_flag, 1);
                 }
                 if (f.detach && slots[i] >= 0) {  // GMC+: the sent components' detached points
                     const float q = f.q;
-                    for (int k = 0; k < K; ++k) {
-                        const float4 e = ld4(f.e[k] + j);
-                        st4(f.y[k] + j, make_float4(detached(nx.x, e.x, q), detached(nx.y, e.y, q),
-                                                    detached(nx.z, e.z, q), detached(nx.w, e.w, q)));
+                    for (int k0 = 0; k0 < K; k0 += 4) {  // four workers' loads in flight
+                        float4 e[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u)
+                            if (k0 + u < K) e[u] = ld4(f.e[k0 + u] + j);
+#pragma unroll
+                        for (int u = 0; u < 4; ++u)
+                            if (k0 + u < K)
+                                st4(f.y[k0 + u] + j, make_float4(detached(nx.x, e[u].x, q), detached(nx.y, e[u].y, q),
+                                                                 detached(nx.z, e[u].z, q), detached(nx.w, e[u].w, q)));
                     }
                 }
             }
@@ -2103,20 +2171,57 @@ __global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, 
     }
     __syncthreads();
     if (sparse) visit_words(wv, hit, base, n, f.wbits);
-    write_update<kApply>(acc, hit, wb, base, n, f, sparse ? wv : nullptr);
+    write_update<kApply>(acc, hit, wb, base, n, f, sparse ? wv : nullptr, f.wbits ? nf_flag : nullptr);
     if (kApply && f.wbits) flush_marks(wb, base, n, f.wbits);
     if (kApply && f.detach) finish_detach(hit, base, n, K, f);
 }
 
-hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, const int32_t* block_slot,
-                           const float* val, int64_t val_row, const FinishArgs& f, hipStream_t st) {
-    const int grid = (int)(((int64_t)d + kAggRange - 1) / kAggRange);
+// The RBGS server pass over the ranges of kAggRange components: one
+// workgroup per range, or, for a sparse apply, the visit list the block draw
+// built (meta[0] ranges in visit[], ascending; meta[0] < 0: every range),
+// each workgroup taking every gridDim-th entry.
+template <bool kApply>
+__global__ __launch_bounds__(kGroup) void agg_rbgs_kernel(int32_t K, int32_t d, int32_t B, const int32_t* block_slot,
+                                                          const float* val, int64_t val_row, FinishArgs f,
+                                                          const int32_t* visit, int32_t* meta) {
+    __shared__ RbgsLds L;
+    const int32_t n_ranges = (int32_t)(((int64_t)d + kAggRange - 1) / kAggRange);
+    int32_t count = n_ranges;
+    bool list = false;
+    if (visit) {
+        const int32_t m = meta[0];
+        if (m >= 0) {
+            count = m;
+            list = true;
+        }
+    }
+    for (int32_t vi = blockIdx.x; vi < count; vi += gridDim.x) {
+        const int32_t r = list ? visit[vi] : vi;
+        agg_rbgs_range<kApply>((int64_t)r * kAggRange, K, d, B, block_slot, val, val_row, f, meta + 1, L);
+        __syncthreads();  // the range's LDS is free for the next
+    }
+}
+
+hipError_t launch_agg_rbgs(int32_t K, int32_t d, int32_t B, int32_t n_sel, const int32_t* block_slot,
+                           const float* val, int64_t val_row, const FinishArgs& f, const int32_t* visit,
+                           int32_t* meta, hipStream_t st) {
+    const int64_t n_ranges = ((int64_t)d + kAggRange - 1) / kAggRange;
+    // a sparse apply that writes no dense update visits the drawn list: the
+    // ranges of this step's and the last step's blocks
+    const bool use_list = f.sparse_apply && f.w_out && !f.update;
+    int64_t grid = n_ranges;
+    if (use_list) {
+        const int64_t per_block = ((int64_t)B + kAggRange - 1) / kAggRange + 1;
+        const int64_t want = 2 * (int64_t)n_sel * per_block + 64;
+        grid = want < n_ranges ? want : n_ranges;
+    }
+    const int32_t* vl = use_list ? visit : nullptr;
     if (f.w_out)
-        hipLaunchKernelGGL(agg_rbgs_kernel<true>, dim3(grid), dim3(kGroup), 0, st, K, d, B, block_slot, val,
-                           val_row, f);
+        hipLaunchKernelGGL(agg_rbgs_kernel<true>, dim3((unsigned)grid), dim3(kGroup), 0, st, K, d, B, block_slot,
+                           val, val_row, f, vl, meta);
     else
-        hipLaunchKernelGGL(agg_rbgs_kernel<false>, dim3(grid), dim3(kGroup), 0, st, K, d, B, block_slot, val,
-                           val_row, f);
+        hipLaunchKernelGGL(agg_rbgs_kernel<false>, dim3((unsigned)grid), dim3(kGroup), 0, st, K, d, B, block_slot,
+                           val, val_row, f, vl, meta);
     return hipGetLastError();
 }
 

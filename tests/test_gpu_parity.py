@@ -286,15 +286,30 @@ def test_sparse_momentum_is_bitwise_the_dense_path(name, shrink, K, extra):
         assert st["sparse_applies"] == 4, st          # and its server pass
 
 
-def test_sparse_momentum_with_non_finite_parameters():
+@pytest.mark.parametrize("name,shrink", [("resnet18", 32), ("rbgs", 16)])
+def test_sparse_momentum_with_non_finite_parameters(name, shrink):
+    # non-finite parameters outside the sent components stay marked; the RBGS
+    # server pass then visits every range instead of the drawn blocks' ranges
     def poison(w0):
         w0 = w0.copy()
         w0[[5, 777, 4096, 9000]] = [np.inf, -np.inf, np.nan, np.inf]
         return w0
-    st = run_lockstep(Case(W("resnet18").shrunk(32, K=3), steps=4, fused_apply=True, sparse_w=True,
-                           w0_hook=poison, label="sparse momentum, non-finite w"))
+    st = run_lockstep(Case(W(name).shrunk(shrink, K=3), steps=4, fused_apply=True, sparse_w=True,
+                           w0_hook=poison, label="sparse momentum, non-finite w/" + name))
     assert st["sparse_momentum_steps"] == 3, st
     assert st["sparse_applies"] == 3, st
+
+
+def test_rbgs_sparse_apply_with_partial_and_small_blocks():
+    # the RBGS server pass visits only the ranges of this step's and the last
+    # step's blocks: blocks of 1000 (several per range, a partial last one)
+    # and of 7 components, half and a third of them drawn
+    for wl in (synth.Workload("rb", [10000 + 1234], K=3, ratio=0.5, beta=0.9, eta=0.1, steps=5,
+                              compressor="rbgs", dist="normal", block=1000),
+               synth.Workload("rb7", [999], K=2, ratio=0.3, beta=0.9, eta=0.1, steps=5,
+                              compressor="rbgs", dist="normal", block=7)):
+        st = run_lockstep(Case(wl, steps=5, fused_apply=True, sparse_w=True, label="rbgs sparse/" + wl.name))
+        assert st["sparse_applies"] == 4, st
 
 
 def test_sparse_momentum_falls_back_when_the_buffers_change():
