@@ -575,8 +575,9 @@ namespace {
 
 gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev, const float* const* grads_dev,
                      float* const* err_dev, float* const* y_dev, int32_t* idx_dev, float* val_dev,
-                     int64_t* msg_len_dev) {
+                     int64_t* msg_len_dev, bool defer_zero = false) {
     StepArgs a{};
+    a.defer_zero = defer_zero && ctx->comp != GMC_RBGS ? 1 : 0;
     a.w_t = w_t_dev;
     a.w_prev = w_prev_dev;
     a.c = ctx->c;
@@ -829,8 +830,16 @@ gmc_status gmc_iteration(gmc_ctx* ctx, const float* w_t_dev, float* w_prev_io_de
     if (!w_t_dev || !w_prev_io_dev || !grads_dev || !err_dev || !idx_dev || !val_dev || !msg_len_dev)
         return fail(ctx, GMC_EINVAL, "gmc_iteration: NULL argument");
     if (w_t_dev == w_prev_io_dev) return fail(ctx, GMC_EINVAL, "gmc_iteration: w_prev_io may not alias w_t");
-    GMC_TRY(step_impl(ctx, w_t_dev, w_prev_io_dev, grads_dev, err_dev, nullptr, idx_dev, val_dev, msg_len_dev));
+    // the top-s emit leaves the residual's zeros at the sent components to
+    // the server pass, which stages every message entry anyway: scattered
+    // writes there overlap its chain of dependent loads, while at the emit's
+    // end they hold up the launch
+    const bool defer = ctx->comp != GMC_RBGS;
+    GMC_TRY(step_impl(ctx, w_t_dev, w_prev_io_dev, grads_dev, err_dev, nullptr, idx_dev, val_dev, msg_len_dev,
+                      defer));
     FinishArgs f{};
+    f.zero_e = defer ? 1 : 0;
+    for (int k = 0; defer && k < ctx->K; ++k) f.ez[k] = err_dev[k];
     f.w_in = w_t_dev;
     f.w_out = w_prev_io_dev;
     f.w_prev = ctx->rule == kRuleServerMomentum ? w_prev_io_dev : nullptr;  // read before written, per component

@@ -163,6 +163,9 @@ struct StepArgs {
     // one worker (2: w read everywhere; 1: w read at sparse changes), or 0:
     // each chunk's K workers on one XCD (w read at dense changes)
     int32_t run;
+    // 1: the emit leaves the residual's zeros at the kept components to the
+    // server pass that follows in the same call (FinishArgs::zero_e)
+    int32_t defer_zero;
 };
 
 // The server pass after the sum over workers: update = -(s * sum), the
@@ -188,6 +191,11 @@ struct FinishArgs {
     int32_t sparse_apply;
     const float* e[kMaxWorkers];  // e_{t+1,k}
     float* y[kMaxWorkers];        // w_{t+1,k}
+    // 1: e_{t+1,k}[j] = v - v (+0 for a finite v) for each entry (j, v) of
+    // worker k's message, the residual u - C(u) at the kept components, which
+    // the step before this pass left to it (StepArgs::defer_zero)
+    int32_t zero_e;
+    float* ez[kMaxWorkers];
 };
 
 // Dense detached points: y_k = w - q e_k for every component and worker.

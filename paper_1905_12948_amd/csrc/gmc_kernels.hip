@@ -1270,7 +1270,7 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
                     if (o < kseg) {  // always, when the counts are consistent
                         irow[o] = (int32_t)j;
                         vrow[o] = x[i];
-                        e[j] = x[i] - x[i];  // residual u - C(u) at a kept component
+                        if (!a.defer_zero) e[j] = x[i] - x[i];  // residual u - C(u) at a kept component
                     }
                 }
             }
@@ -1328,7 +1328,7 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
                 const int32_t j = st_idx[stage_slot(q0 + i)];
                 irow[o] = j;
                 vrow[o] = x;
-                e[j] = x - x;  // residual u - C(u) at a kept component
+                if (!a.defer_zero) e[j] = x - x;  // residual u - C(u) at a kept component
             }
         }
         run_above += tot >> 16;
@@ -1932,8 +1932,11 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             int k = 0;
             while (i >= pre[k + 1]) ++k;
             const int64_t q = (int64_t)src[k] + (i - pre[k]);
-            st_idx[i] = idx[(size_t)k * idx_row + q];
-            st_val[i] = val[(size_t)k * val_row + q];
+            const int32_t j = idx[(size_t)k * idx_row + q];
+            const float v = val[(size_t)k * val_row + q];
+            st_idx[i] = j;
+            st_val[i] = v;
+            if (f.zero_e && j - base >= 0 && j - base < n) f.ez[k][j] = v - v;
         }
         __syncthreads();
         for (int k = 0; k < K; ++k) {
@@ -1975,6 +1978,7 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
                     if (i0 + u * kGroup + t < cnt && j >= 0 && j < R) {
                         acc[j] = acc[j] + vv[u];
                         atomicOr(&hb[j >> 5], 1u << (j & 31));
+                        if (f.zero_e && j < n) f.ez[k][jj[u]] = vv[u] - vv[u];
                     }
                 }
             }
