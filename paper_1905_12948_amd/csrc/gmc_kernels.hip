@@ -1335,8 +1335,11 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
         run_ties += tot & 0xffffu;
         // row pointers of the range starts in (prev_last, the round's last
         // index]: the row position of the round's first element at or after
-        // each (binary search over the staged indices, ascending), all
-        // threads sharing the range starts
+        // each, all threads sharing the range starts.  A thread's range
+        // starts ascend, so each answer is at or after its previous one, and
+        // where the indices leave a gap (clustered candidates: thousands of
+        // range starts between two kept components) it is that one: one LDS
+        // read, else a binary search over the staged indices after it.
         __syncthreads();  // the round's values are read; the stage now holds the counts
         int32_t* st_kb = reinterpret_cast<int32_t*>(st_val);
 #pragma unroll
@@ -1344,14 +1347,19 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
             if (q0 + i < ns) st_kb[stage_slot(q0 + i)] = kbv[i];
         __syncthreads();
         const int64_t j_end = st_idx[stage_slot(ns - 1)];
+        int32_t found = 0;  // the answer for this thread's previous range start
         for (int64_t rr = (prev_last + R) / R + threadIdx.x; rr * R <= j_end; rr += kGroup) {
             const int64_t start = rr * R;
-            int32_t lo = 0, hi = ns - 1;  // the first element whose index is >= start (the last one is)
-            while (lo < hi) {
-                const int32_t mid = (lo + hi) >> 1;
-                if ((int64_t)st_idx[stage_slot(mid)] < start) lo = mid + 1; else hi = mid;
+            // the first element whose index is >= start (the last one is)
+            if ((int64_t)st_idx[stage_slot(found)] < start) {
+                int32_t lo = found + 1, hi = ns - 1;
+                while (lo < hi) {
+                    const int32_t mid = (lo + hi) >> 1;
+                    if ((int64_t)st_idx[stage_slot(mid)] < start) lo = mid + 1; else hi = mid;
+                }
+                found = lo;
             }
-            rp[rr] = row0 + st_kb[stage_slot(lo)];
+            rp[rr] = row0 + st_kb[stage_slot(found)];
         }
         prev_last = j_end;
         __syncthreads();  // the stage is read before the next round overwrites it
@@ -1897,7 +1905,6 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             if (f.w_prev) px[i] = ld4(f.w_prev + base + i * (kGroup * 4) + t * 4);
         }
     }
-    for (int q = t; q < R; q += kGroup) acc[q] = 0.0f;
     if (t < NW) {
         hb[t] = 0u;
         wb[t] = 0u;
@@ -1915,6 +1922,11 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
     // fetch); an unmarked range fetches only the words this pass's sent
     // components mark, after the sum, and most such ranges write nothing
     const bool marked = __syncthreads_or(sparse && t < NW && wv[t] != 0u) != 0;
+    // a sparse apply's range with no old marks and no entries changes
+    // nothing: w_out holds w_{t-1}, equal to w_t = w_{t+1} there, and its
+    // marks stay clear
+    if (sparse && !marked && f.update == nullptr && !__syncthreads_or(t < K && pre[t + 1] > 0)) return;
+    for (int q = t; q < R; q += kGroup) acc[q] = 0.0f;
     bool got = false;
     if (sparse && vec && marked) {
 #pragma unroll
