@@ -350,7 +350,7 @@ class GmcOracle:
         if self.compressor != "rbgs":
             return idx_row[:length].astype(np.int32)
         B = self.block
-        parts = [np.arange(b * B, min((b + 1) * B, self.d), dtype=np.int32) for b in idx_row]
+        parts = [np.arange(b * B, min((b + 1) * B, self.d), dtype=np.int32) for b in np.asarray(idx_row).tolist()]
         return np.concatenate(parts)[:length]
 
     def aggregate(self, idx, val, msg_len) -> np.ndarray:
