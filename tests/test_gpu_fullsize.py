@@ -150,25 +150,28 @@ def test_full_size_workload(name, steps, lam, dense):
         assert st["sparse_momentum_steps"] == steps - 1 and st["sparse_applies"] == steps - 1, st
 
 
-def test_largest_dimension():
+@pytest.mark.parametrize("comp", ["topk", "rbgs"])
+def test_largest_dimension(comp):
     """d = 2^31 - 1, the largest the int32 indices allow (its last chunk
-    holds 2047 components), K = 2 workers, global top-k 0.01% (k = 214,749):
-    three gmc_iteration steps with the sparse momentum term (the full-data
-    selection twice: the residual's growth from the first step to the second
-    brings more candidates than the capacity; then the candidate path) and
-    the sparse parameter path from the second step on.
+    holds 2047 components, its last RBGS block 4095), K = 2 workers, three
+    gmc_iteration steps with the sparse momentum term.  Global top-k 0.01%
+    (k = 214,749) takes the full-data selection twice (the residual's growth
+    from the first step to the second brings more candidates than the
+    capacity), then the candidate path; RBGS draws 53 of 524,288 blocks of
+    4096 (more than the block draw's and the server pass's LDS bitmaps hold,
+    so both take their global bitmaps).
 
     The CPU oracle cannot take whole vectors of this size in a test's time,
     so whole vectors are checked on the device against a plain torch
     recomputation of u = (e + g) - c (w_t - w_prev) (one rounding per
     operation, the method's order), and that recomputation is pinned to the
     oracle's per-element function bit for bit on a million sampled
-    components, the ragged tail included.  Per worker and step: the message
-    holds exactly k ascending components whose keys are the k largest (ties
-    towards the lower index), the sent values are u there, the residual is
-    u elsewhere and u - u at the sent components; w_{t+1} equals the
-    oracle's aggregation and apply at every sent component and w_t bit for
-    bit everywhere else."""
+    components, the ragged tail included.  Per worker and step: top-k's
+    message holds exactly k ascending components whose keys are the k
+    largest (ties towards the lower index), RBGS's the oracle's blocks; the
+    sent values are u there, the residual is u elsewhere and u - u at the
+    sent components; w_{t+1} equals the oracle's aggregation and apply at
+    every sent component and w_t bit for bit everywhere else."""
     import torch
     import synth.device as sdev
     from paper_1905_12948_amd import Gmc, GMC_OPT_SPARSE_MOMENTUM
@@ -176,14 +179,16 @@ def test_largest_dimension():
     free, _ = torch.cuda.mem_get_info()
     if free < 150e9:
         pytest.skip("needs about 120 GB of device memory, %.0f GB free" % (free / 1e9))
+    rbgs = comp == "rbgs"
     wl = synth.Workload("largest", [2**31 - 1], K=2, ratio=1e-4, beta=0.9, eta=0.1, steps=3,
-                        compressor="topk", dist="normal", seed=23)
-    d, K = wl.d, wl.K
+                        compressor=comp, dist="normal", seed=23, block=4096)
+    d, K, B = wl.d, wl.K, wl.block
     dev = torch.device("cuda:0")
-    kk = oracle.count(d, wl.ratio)
+    nb = (d + B - 1) // B
+    kk = oracle.count(nb if rbgs else d, wl.ratio)  # blocks (RBGS) or components per worker
     c, s = oracle.constants(wl.beta, wl.eta, K)
-    print("largest dimension: d=%d K=%d k=%d" % (d, K, kk), flush=True)
-    g = Gmc(d, K, "topk", wl.ratio, wl.beta, wl.eta, seed=wl.seed)
+    print("largest dimension, %s: d=%d K=%d %s=%d" % (comp, d, K, "n_sel" if rbgs else "k", kk), flush=True)
+    g = Gmc(d, K, comp, wl.ratio, wl.beta, wl.eta, seed=wl.seed, block=B if rbgs else None)
     g.set_option(GMC_OPT_SPARSE_MOMENTUM, 1)
     bufs = [sdev.w0(wl, dev), None]
     bufs[1] = bufs[0].clone()
@@ -216,23 +221,36 @@ def test_largest_dimension():
         g.iteration(cur, prev, grads, err, idx, val, ln)
         torch.cuda.synchronize()
         gl = ln.cpu().numpy()
-        assert np.all(gl == kk), "step %d: message lengths %s" % (t, gl)
+        if rbgs:
+            blocks = oracle.rbgs_blocks(wl.seed, t, nb, kk)
+            ih = np.concatenate([np.arange(b * B, min((b + 1) * B, d), dtype=np.int64) for b in blocks.tolist()])
+            assert np.all(gl == ih.size), "step %d: message lengths %s" % (t, gl)
+        else:
+            assert np.all(gl == kk), "step %d: message lengths %s" % (t, gl)
         sent_all = []
         for k in range(K):
             tag = "step %d worker %d" % (t, k)
-            ik = idx[k, :kk].long()
-            ih = ik.cpu().numpy()
-            assert ih[0] >= 0 and ih[-1] < d and np.all(np.diff(ih) > 0), tag + ": indices"
-            assert torch.equal(val[k, :kk].view(torch.int32), ref[k][ik].view(torch.int32)), tag + ": sent values"
-            kept = keys(ref[k][ik])
-            T = int(kept.min())
-            assert T > 0, tag + ": the threshold key is zero"
-            last_tie = int(ik[kept == T].max())
+            if rbgs:
+                assert np.array_equal(idx[k, :kk].cpu().numpy(), blocks), tag + ": blocks"
+                ik = torch.from_numpy(ih).to(dev)
+            else:
+                ik = idx[k, :kk].long()
+                ih = ik.cpu().numpy()
+                assert ih[0] >= 0 and ih[-1] < d and np.all(np.diff(ih) > 0), tag + ": indices"
+            n_k = ih.size
+            assert torch.equal(val[k, :n_k].view(torch.int32), ref[k][ik].view(torch.int32)), tag + ": sent values"
+            if not rbgs:
+                kept = keys(ref[k][ik])
+                T = int(kept.min())
+                assert T > 0, tag + ": the threshold key is zero"
+                last_tie = int(ik[kept == T].max())
             ref[k][ik] = ref[k][ik] - ref[k][ik]  # the residual u - C(u)
             for a in range(0, d, step_chunk):
                 b = min(d, a + step_chunk)
                 assert torch.equal(err[k][a:b].view(torch.int32), ref[k][a:b].view(torch.int32)), \
                     tag + ": residual in [%d, %d)" % (a, b)
+                if rbgs:
+                    continue
                 kr = keys(ref[k][a:b])
                 assert int(kr.max()) <= T, tag + ": an unsent component outranks the threshold"
                 ties = torch.nonzero(kr == T).flatten()  # unsent components (T > 0) at the threshold's key
@@ -243,7 +261,7 @@ def test_largest_dimension():
         U = np.unique(np.concatenate(sent_all))
         U_t = torch.from_numpy(U).to(dev)
         il = [np.searchsorted(U, sent_all[k]).astype(np.int32) for k in range(K)]
-        vl = [val[k, :kk].cpu().numpy() for k in range(K)]
+        vl = [val[k, :sent_all[k].size].cpu().numpy() for k in range(K)]
         delta = oracle.aggregate(U.size, s, il, vl)
         w_t_sent = cur[U_t].cpu().numpy()
         oracle.apply(w_t_sent, delta)
@@ -256,4 +274,5 @@ def test_largest_dimension():
     st = g.stats()
     g.close()
     assert st["sparse_momentum_steps"] == wl.steps - 1 and st["sparse_applies"] == wl.steps - 1, st
-    assert st["from_candidates"] == K, st  # the last step's selections
+    if not rbgs:
+        assert st["from_candidates"] == K, st  # the last step's selections

@@ -127,6 +127,15 @@ def test_rbgs_partial_last_block_and_small_blocks():
     run_lockstep(Case(wl, steps=3, label="rbgs-block7"))
 
 
+def test_rbgs_more_blocks_than_the_lds_bitmap():
+    # 275,000 blocks of 4: the block draw keeps its bitmap in global memory
+    # (the workgroup's LDS holds 262,144 blocks)
+    wl = synth.Workload("rb4", [1_100_000], K=2, ratio=0.01, beta=0.9, eta=0.1, steps=3,
+                        compressor="rbgs", dist="normal", block=4)
+    st = run_lockstep(Case(wl, steps=3, fused_apply=True, sparse_w=True, label="rbgs 275k blocks"))
+    assert st["sparse_applies"] == 2, st
+
+
 def test_many_workers_and_a_margin_beyond_the_capacity():
     # K = 64, the most workers a context takes; a margin of 200 k puts the
     # speculative threshold so low that the candidates overflow the 64 k
