@@ -1863,8 +1863,8 @@ hipError_t launch_agg_rowptr(int32_t K, int32_t d, const int32_t* idx, int64_t i
 }
 
 // One workgroup per range of kAggTopkRange components (16 per thread).  The
-// workgroup first issues its loads of w_t (fused apply) and of the
-// previous pass's marks, then fetches the K workers' entries of the range
+// workgroup first issues its loads of w_t (fused apply; a sparse apply loads
+// only the words that change) and of the previous pass's marks, then fetches the K workers' entries of the range
 // into LDS together (one round of loads) and adds them to the range's
 // accumulator one worker after the other; a range with more entries than the
 // staging holds reads them worker by worker instead.  Sent components are
@@ -1916,22 +1916,28 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
         src[t] = lo;
         pre[t + 1] = hi > lo ? hi - lo : 0;
     }
-    // sparse apply: a range the previous pass marked anywhere fetches all
-    // of its w_t while the messages are staged (sent components recur from
-    // step to step, so such a range usually has more to write and no late
-    // fetch); an unmarked range fetches only the words this pass's sent
-    // components mark, after the sum, and most such ranges write nothing
+    // sparse apply: whether the previous pass marked the range anywhere
     const bool marked = __syncthreads_or(sparse && t < NW && wv[t] != 0u) != 0;
     // a sparse apply's range with no old marks and no entries changes
     // nothing: w_out holds w_{t-1}, equal to w_t = w_{t+1} there, and its
     // marks stay clear
     if (sparse && !marked && f.update == nullptr && !__syncthreads_or(t < K && pre[t + 1] > 0)) return;
     for (int q = t; q < R; q += kGroup) acc[q] = 0.0f;
-    bool got = false;
-    if (sparse && vec && marked) {
+    // sparse apply: w_t is fetched only in the 32-component words the
+    // output changes: those of the previous pass's marks now, those of this
+    // pass's entries as soon as the entries are staged (their loads then
+    // overlap the ordered sum); a dense range's are fetched after the sum
+    const bool hb_early = sparse && vec;  // hb is complete before the sum
+    uint32_t got = 0u;                    // bit i: wx[i] holds w_t
+    if (hb_early) {
 #pragma unroll
-        for (int i = 0; i < V; ++i) wx[i] = ld4(f.w_in + base + i * (kGroup * 4) + t * 4);
-        got = true;
+        for (int i = 0; i < V; ++i) {
+            const int q = i * (kGroup * 4) + t * 4;
+            if (wv[q >> 5]) {
+                wx[i] = ld4(f.w_in + base + q);
+                got |= 1u << i;
+            }
+        }
     }
     if (t == 0) {
         pre[0] = 0;
@@ -1951,13 +1957,28 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             if (f.zero_e && j - base >= 0 && j - base < n) f.ez[k][j] = v - v;
         }
         __syncthreads();
+        if (hb_early) {
+            for (int32_t i = t; i < total; i += kGroup) {
+                const int64_t j = (int64_t)st_idx[i] - base;
+                if (j >= 0 && j < R) atomicOr(&hb[j >> 5], 1u << (j & 31));
+            }
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < V; ++i) {
+                const int q = i * (kGroup * 4) + t * 4;
+                if (!((got >> i) & 1u) && hb[q >> 5]) {
+                    wx[i] = ld4(f.w_in + base + q);
+                    got |= 1u << i;
+                }
+            }
+        }
         for (int k = 0; k < K; ++k) {
             if (pre[k + 1] > pre[k]) {
                 for (int32_t i = pre[k] + t; i < pre[k + 1]; i += kGroup) {
                     const int64_t j = (int64_t)st_idx[i] - base;
                     if (j >= 0 && j < R) {
                         acc[j] = acc[j] + st_val[i];
-                        atomicOr(&hb[j >> 5], 1u << (j & 31));
+                        if (!hb_early) atomicOr(&hb[j >> 5], 1u << (j & 31));
                     }
                 }
                 __syncthreads();  // worker k's additions land before worker k+1's
@@ -2009,7 +2030,7 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             const float4 dl = make_float4(-(s * acc[q]), -(s * acc[q + 1]), -(s * acc[q + 2]), -(s * acc[q + 3]));
             if (f.update) st4(f.update + base + q, dl);
             if (kApply && (!sparse || wv[q >> 5])) {
-                const float4 x = (sparse && !got) ? ld4(f.w_in + base + q) : wx[i];
+                const float4 x = (sparse && !((got >> i) & 1u)) ? ld4(f.w_in + base + q) : wx[i];
                 float4 nx = make_float4(x.x + dl.x, x.y + dl.y, x.z + dl.z, x.w + dl.w);
                 if (f.w_prev) {  // momentum on the server
                     const float4 pp = px[i];
