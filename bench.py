@@ -158,38 +158,6 @@ def cpu_baseline(wl, workers: int, steps: int, lam: float = 0.0) -> dict:
                       % (workers, wl.K, wl.d, steps, workers, dt)}
 
 
-def warm_kernels(wl, lam: float, sparse_w: bool, dev) -> None:
-    """Two steps of a small context of the same configuration (the first on
-    the full-data path), so that the code object and every kernel the
-    measured context launches are loaded before its first step is timed."""
-    import torch
-    import synth.device as sdev
-    from paper_1905_12948_amd import Gmc
-
-    small = wl.shrunk(16, K=wl.K)
-    seg = small.topk_segments().tolist() if small.compressor == "topk_seg" else None
-    g = Gmc(small.d, small.K, small.compressor, small.ratio, small.beta, small.eta, seed=small.seed,
-            segments=seg, block=small.block if small.compressor == "rbgs" else None, lam=lam)
-    if sparse_w:
-        from paper_1905_12948_amd import GMC_OPT_SPARSE_MOMENTUM
-        g.set_option(GMC_OPT_SPARSE_MOMENTUM, 1)
-    w = sdev.w0(small, dev)
-    bufs = [w, w.clone()]
-    err = sdev.rows(small.K, small.d, dev, zero=True)
-    wk = sdev.rows(small.K, small.d, dev) if lam > 0.0 else None
-    idx, val, ln = g.alloc_messages(dev)
-    for t in range(2):
-        grads = sdev.grads(small, t, dev)
-        cur, prev = bufs[t % 2], bufs[(t + 1) % 2]
-        if wk is not None:
-            g.step(cur, prev, grads, err, idx, val, ln, w_k=wk)
-            g.finish(idx, val, ln, cur, prev, err=err, w_k=wk)
-        else:
-            g.iteration(cur, prev, grads, err, idx, val, ln)
-    torch.cuda.synchronize()
-    g.close()
-
-
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -268,26 +236,8 @@ def main():
             gm.iteration(cur, prev, G[step_no[0] % len(G)], err, idx, val, ln)
         step_no[0] += 1
 
-    # iteration 0 has no previous threshold (every selection takes the
-    # full-data path) and w_t = w_{t-1}; it is the first warmup step, timed on
-    # its own once the context's scratch is allocated (setting the default
-    # candidate capacity prepares it), so that the one-time allocation stays
-    # out of its time
-    first = None
-    if args.warmup >= 1:
-        from paper_1905_12948_amd import GMC_OPT_CAND_CAP_MULT
-        warm_kernels(wl, lam, sparse_w, dev)
-        gm.set_option(GMC_OPT_CAND_CAP_MULT, 64)
-        torch.cuda.synchronize()
-        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        f0.record()
-        one_step()
-        f1.record()
-        torch.cuda.synchronize()
-        st_first = gm.stats()
-        first = {"ms": round(f0.elapsed_time(f1), 4), "full_data_selections": st_first["full_data"]}
     log("warmup %d steps" % args.warmup)
-    for _ in range(args.warmup - (1 if first else 0)):
+    for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
     stats0 = gm.stats()
@@ -311,6 +261,31 @@ def main():
     prof = gm.profile_read()
     stats1 = gm.stats()
     gm.profile([])
+    # iteration 0 on its own: a fresh context of the same configuration
+    # (every kernel is loaded by now, and its scratch is allocated before the
+    # timed call: setting the default candidate capacity prepares it) takes
+    # one step from e = 0 and w_t = w_{t-1}, with no previous threshold, so
+    # every selection takes the full-data path
+    from paper_1905_12948_amd import GMC_OPT_CAND_CAP_MULT
+    g0 = Gmc(d, K, wl.compressor, wl.ratio, wl.beta, wl.eta, seed=wl.seed, segments=seg,
+             block=wl.block if wl.compressor == "rbgs" else None, lam=lam)
+    g0.set_option(GMC_OPT_CAND_CAP_MULT, 64)
+    if sparse_w:
+        g0.set_option(GMC_OPT_SPARSE_MOMENTUM, 1)
+    err.zero_()
+    bufs[1].copy_(bufs[0])
+    torch.cuda.synchronize()
+    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    f0.record()
+    if detach:
+        g0.step(bufs[0], bufs[1], G[0], err, idx, val, ln, w_k=wk)
+        g0.finish(idx, val, ln, bufs[0], bufs[1], err=err, w_k=wk)
+    else:
+        g0.iteration(bufs[0], bufs[1], G[0], err, idx, val, ln)
+    f1.record()
+    torch.cuda.synchronize()
+    first = {"ms": round(f0.elapsed_time(f1), 4), "full_data_selections": g0.stats()["full_data"]}
+    g0.close()
     if args.calib:
         for _ in range(3):
             calib_copy(cal_dst, cal_src)
