@@ -1172,8 +1172,18 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
     static_assert(kEmitLoads % 4 == 0 && (kEmitLoads + kEmitLoads / 4) % 2 == 1,
                   "one pad word per 4 entries; each thread's row then starts an odd number of words on");
     constexpr int kStageSlots = kEmitStage + kEmitStage / 4;
-    __shared__ int32_t st_idx[kStageSlots];
-    __shared__ float st_val[kStageSlots];
+    __shared__ union {
+        struct {  // candidate path: the staged round
+            int32_t idx[kStageSlots];
+            float val[kStageSlots];
+        } st;
+        struct {  // full-data path: the round's (i, wave) counts and its values
+            uint32_t cnt[2 * kWave + 1];
+            float x[kFullRound];
+        } full;
+    } lds;
+    int32_t* const st_idx = lds.st.idx;
+    float* const st_val = lds.st.val;
     __shared__ uint32_t sh_wsum[kWavesPerGroup];
 
     const SliceId id = slice_id(g, blockIdx.x);
@@ -1225,23 +1235,30 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
         static_assert(kIt * kWavesPerGroup == kWave, "one (i, wave) count per lane of the scanning wave");
         const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
         const uint64_t lt = lanemask_lt();
-        uint32_t* cnt = reinterpret_cast<uint32_t*>(st_idx);  // [kIt][kWavesPerGroup]: above << 16 | ties
-        for (int64_t s0 = v.lo; s0 < v.hi; s0 += kFullRound) {
-            float x[kIt];
-            uint64_t ba[kIt], bt[kIt];
+        uint32_t* cnt = lds.full.cnt;  // [kIt][kWavesPerGroup]: above << 16 | ties
+        float* xs = lds.full.x;        // the round's values, element (i, thread) at i * kGroup + thread
+        // the next round's loads are issued as soon as the current round's
+        // values are counted and parked in LDS, so they are in flight during
+        // the current round's scan and placement
+        float x[kIt];
+        auto load_round = [&](int64_t s0) {
 #pragma unroll
             for (int i = 0; i < kIt; ++i) {
                 const int64_t q = s0 + i * kGroup + threadIdx.x;
                 x[i] = q < v.hi ? v.val[q] : 0.0f;
             }
+        };
+        if (v.lo < v.hi) load_round(v.lo);
+        for (int64_t s0 = v.lo; s0 < v.hi; s0 += kFullRound) {
 #pragma unroll
             for (int i = 0; i < kIt; ++i) {
                 const bool in = s0 + i * kGroup + threadIdx.x < v.hi;
                 const uint32_t key = key_of(x[i]);
-                ba[i] = ballot(in && key > T);
-                bt[i] = ballot(in && key == T);
-                if (lane == 0) cnt[i * kWavesPerGroup + wave] = (popc64(ba[i]) << 16) | popc64(bt[i]);
+                const uint64_t ba = ballot(in && key > T), bt = ballot(in && key == T);
+                if (lane == 0) cnt[i * kWavesPerGroup + wave] = (popc64(ba) << 16) | popc64(bt);
+                xs[i * kGroup + threadIdx.x] = x[i];
             }
+            if (s0 + kFullRound < v.hi) load_round(s0 + kFullRound);
             __syncthreads();
             if (wave == 0) {  // exclusive scan of the 64 counts in index order, and the round's total
                 const uint32_t c = cnt[lane];
@@ -1258,26 +1275,30 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
 #pragma unroll
             for (int i = 0; i < kIt; ++i) {
                 const int64_t q = s0 + i * kGroup + threadIdx.x;
+                const float xi = xs[i * kGroup + threadIdx.x];
+                const uint32_t key = key_of(xi);
+                const bool in = q < v.hi;
+                const uint64_t ba = ballot(in && key > T), bt = ballot(in && key == T);
                 const uint32_t pre = cnt[kWave + i * kWavesPerGroup + wave];
-                const uint32_t a_before = run_above + (pre >> 16) + popc64(ba[i] & lt);
-                const uint32_t t_before = run_ties + (pre & 0xffffu) + popc64(bt[i] & lt);
+                const uint32_t a_before = run_above + (pre >> 16) + popc64(ba & lt);
+                const uint32_t t_before = run_ties + (pre & 0xffffu) + popc64(bt & lt);
                 const int64_t j = seg_lo + q;
                 const int64_t tk = (int64_t)t_before < quota ? (int64_t)t_before : quota;
                 if (q < v.hi && (j & (R - 1)) == 0) rp[j / R] = row0 + (int32_t)(a_before + (uint32_t)tk);
-                const bool above = (ba[i] >> lane) & 1ull, tie = (bt[i] >> lane) & 1ull;
+                const bool above = (ba >> lane) & 1ull, tie = (bt >> lane) & 1ull;
                 if (above || (tie && (int64_t)t_before < quota)) {
                     const uint32_t o = out0 + a_before + (uint32_t)tk;
                     if (o < kseg) {  // always, when the counts are consistent
                         irow[o] = (int32_t)j;
-                        vrow[o] = x[i];
-                        if (!a.defer_zero) e[j] = x[i] - x[i];  // residual u - C(u) at a kept component
+                        vrow[o] = xi;
+                        if (!a.defer_zero) e[j] = xi - xi;  // residual u - C(u) at a kept component
                     }
                 }
             }
             const uint32_t tot = cnt[2 * kWave];
             run_above += tot >> 16;
             run_ties += tot & 0xffffu;
-            __syncthreads();  // the counts are read before the next round writes them
+            __syncthreads();  // the counts and values are read before the next round writes them
         }
         if (v.hi > v.lo) prev_last = seg_lo + v.hi - 1;
     }
