@@ -489,7 +489,7 @@ hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const
 namespace {
 
 constexpr int kSliceLoads = 16;      // independent loads in flight per thread
-constexpr int kEmitLoads = 12;       // staged elements per thread in the emit pass
+constexpr int kEmitLoads = 4;        // staged elements per thread in the emit pass
 constexpr int kEmitStage = kGroup * kEmitLoads;  // elements staged in LDS per round
 constexpr int kFullRound = kGroup * 16;          // full-data elements per round of the emit
 
