@@ -41,6 +41,9 @@ constexpr int kShift1 = 20, kShift2 = 9;
 constexpr int kAggRange = 2048;
 constexpr int kAggTopkRange = 4096;
 constexpr int kAggTopkStage = 512;
+// sparse messages (few entries per range on average) stage fewer, so that
+// eight workgroups fit on a CU instead of seven
+constexpr int kAggTopkStageSmall = 128;
 
 constexpr uint32_t kNoThreshold = 0xffffffffu;  // no speculative candidates
 

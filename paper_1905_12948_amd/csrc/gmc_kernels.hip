@@ -1889,10 +1889,11 @@ hipError_t launch_agg_rowptr(int32_t K, int32_t d, const int32_t* idx, int64_t i
 // into LDS together (one round of loads) and adds them to the range's
 // accumulator one worker after the other; a range with more entries than the
 // staging holds reads them worker by worker instead.  Sent components are
-// kept as a bitmap (hb), so a workgroup needs about 21 KB of LDS and seven
-// fit on a CU: the kernel is bound by its chain of dependent loads, and
-// twice the components per chain halves the chains.
-template <bool kApply>
+// kept as a bitmap (hb), so a workgroup needs about 22 KB of LDS (seven fit
+// on a CU) with a stage of kStage = 512 entries, 19 KB (eight) with 128 for
+// sparse messages: the kernel is bound by its chain of dependent loads, so
+// residency counts, and twice the components per chain halves the chains.
+template <bool kApply, int kStage>
 __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, const int32_t* idx,
                                                           int64_t idx_row, const float* val, int64_t val_row,
                                                           const int32_t* rowptr, int32_t n_ranges, FinishArgs f) {
@@ -1902,8 +1903,8 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
     __shared__ uint32_t hb[NW];  // components some worker sent
     __shared__ uint32_t wb[NW];  // marks for the next worker pass
     __shared__ uint32_t wv[NW];  // sparse apply: the words to write (old marks | sent)
-    __shared__ int32_t st_idx[kAggTopkStage];
-    __shared__ float st_val[kAggTopkStage];
+    __shared__ int32_t st_idx[kStage];
+    __shared__ float st_val[kStage];
     __shared__ int32_t src[kMaxWorkers];
     __shared__ int32_t pre[kMaxWorkers + 1];
     const int r = blockIdx.x;
@@ -1966,7 +1967,7 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
     }
     __syncthreads();
     const int32_t total = pre[K];
-    if (total <= kAggTopkStage) {
+    if (total <= kStage) {
         for (int32_t i = t; i < total; i += kGroup) {
             int k = 0;
             while (i >= pre[k + 1]) ++k;
@@ -2100,12 +2101,23 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
 hipError_t launch_agg_topk(int32_t K, int32_t d, const int32_t* idx, int64_t idx_row,
                            const float* val, int64_t val_row, const int32_t* rowptr,
                            int32_t n_ranges, const FinishArgs& f, hipStream_t st) {
-    if (f.w_out)
-        hipLaunchKernelGGL(agg_topk_kernel<true>, dim3(n_ranges), dim3(kGroup), 0, st, K, d, idx, idx_row, val,
-                           val_row, rowptr, n_ranges, f);
+    // the smaller stage when the messages hold at most 48 entries per range
+    // on average (per-tensor top-s of a decoder-sized model: about 33);
+    // denser messages keep the larger one, since a range with more entries
+    // than the stage reads them worker after worker
+    const bool small = (int64_t)K * idx_row <= 48 * (int64_t)n_ranges;
+    if (f.w_out && small)
+        hipLaunchKernelGGL((agg_topk_kernel<true, kAggTopkStageSmall>), dim3(n_ranges), dim3(kGroup), 0, st, K, d,
+                           idx, idx_row, val, val_row, rowptr, n_ranges, f);
+    else if (f.w_out)
+        hipLaunchKernelGGL((agg_topk_kernel<true, kAggTopkStage>), dim3(n_ranges), dim3(kGroup), 0, st, K, d, idx,
+                           idx_row, val, val_row, rowptr, n_ranges, f);
+    else if (small)
+        hipLaunchKernelGGL((agg_topk_kernel<false, kAggTopkStageSmall>), dim3(n_ranges), dim3(kGroup), 0, st, K, d,
+                           idx, idx_row, val, val_row, rowptr, n_ranges, f);
     else
-        hipLaunchKernelGGL(agg_topk_kernel<false>, dim3(n_ranges), dim3(kGroup), 0, st, K, d, idx, idx_row, val,
-                           val_row, rowptr, n_ranges, f);
+        hipLaunchKernelGGL((agg_topk_kernel<false, kAggTopkStage>), dim3(n_ranges), dim3(kGroup), 0, st, K, d, idx,
+                           idx_row, val, val_row, rowptr, n_ranges, f);
     return hipGetLastError();
 }
 

@@ -136,6 +136,18 @@ def test_rbgs_more_blocks_than_the_lds_bitmap():
     assert st["sparse_applies"] == 2, st
 
 
+def test_sparse_messages_with_one_dense_range():
+    # 200 one-component tensors (k = 1 each) fill the first range, ten large
+    # tensors follow: on average 15 message entries per range, so the server
+    # pass stages few entries per range, while the first range holds more
+    # than 600 and is summed worker after worker from the messages
+    wl = synth.Workload("dense-first", [1] * 200 + [100_000] * 10, K=3, ratio=0.001, beta=0.9, eta=0.1, steps=3,
+                        compressor="topk_seg", dist="normal")
+    run_lockstep(Case(wl, steps=3, label="one dense range"))
+    st = run_lockstep(Case(wl, steps=3, iteration=True, sparse_w=True, label="one dense range, iteration"))
+    assert st["sparse_applies"] == 2, st
+
+
 def test_many_workers_and_a_margin_beyond_the_capacity():
     # K = 64, the most workers a context takes; a margin of 200 k puts the
     # speculative threshold so low that the candidates overflow the 64 k
