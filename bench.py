@@ -262,14 +262,12 @@ def main():
     stats1 = gm.stats()
     gm.profile([])
     # iteration 0 on its own: a fresh context of the same configuration
-    # (every kernel is loaded by now, and its scratch is allocated before the
-    # timed call: setting the default candidate capacity prepares it) takes
-    # one step from e = 0 and w_t = w_{t-1}, with no previous threshold, so
-    # every selection takes the full-data path
-    from paper_1905_12948_amd import GMC_OPT_CAND_CAP_MULT
+    # (every kernel is loaded by now, and the context allocates its scratch
+    # when it is created, before the timed call) takes one step from e = 0
+    # and w_t = w_{t-1}, with no previous threshold, so every selection takes
+    # the full-data path
     g0 = Gmc(d, K, wl.compressor, wl.ratio, wl.beta, wl.eta, seed=wl.seed, segments=seg,
              block=wl.block if wl.compressor == "rbgs" else None, lam=lam)
-    g0.set_option(GMC_OPT_CAND_CAP_MULT, 64)
     if sparse_w:
         g0.set_option(GMC_OPT_SPARSE_MOMENTUM, 1)
     err.zero_()
