@@ -30,6 +30,13 @@
  *     the scale eta/K is applied once afterwards: delta = -(s * acc);
  *   - RBGS draws its blocks with Floyd's sampling algorithm fed by a SplitMix64
  *     stream whose state is seed XOR mix(t+1); the same blocks on every worker.
+ *
+ * PARITY UNPINNED: the exact RBGS block ids (orc_rbgs_draw, orc_rbgs_blocks)
+ * and the exact positions of the sampled-threshold sample
+ * (orc_sample_positions).  The paper prints no draw; these functions follow
+ * their stated definitions, and the tests pin the SplitMix64 mix to its
+ * published outputs and the samplers to properties (distinct, in range,
+ * uniform), not to values the paper fixes.
  */
 #include <math.h>
 #include <stdint.h>
