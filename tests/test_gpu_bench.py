@@ -1,0 +1,58 @@
+"""bench.py end to end on the GPU, in this process: one JSON line with the
+contract's fields for small runs of the tiny, per-tensor, RBGS and
+sampled-threshold workloads (the ResNet-50-sized line is the bench's own
+default run)."""
+import json
+import sys
+
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+@pytest.mark.parametrize("workload", ["tiny", "gpt2", "rbgs", "resnet50_approx"])
+def test_bench_line(workload, capsys, monkeypatch):
+    import bench
+    import synth
+
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--workload", workload, "--steps", "3", "--warmup", "2",
+                                      "--no-cpu-baseline"])
+    print("bench line: %s" % workload, file=sys.stderr, flush=True)
+    bench.main()
+    lines = [ln for ln in capsys.readouterr().out.splitlines() if ln.startswith("{")]
+    assert len(lines) == 1, lines
+    j = json.loads(lines[0])
+    wl = synth.workload(workload)
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+                "scaling", "vs_baseline", "dtype", "data", "config", "roofline", "first_step",
+                "ms_per_step_median", "selection", "hbm_peak_frac"):
+        assert key in j, key
+    assert j["n_gpus"] == 1 and j["steps"] == 3 and j["warmup"] == 2
+    assert j["higher_is_better"] is True and j["dtype"] == "f32" and j["data"] == "synthetic"
+    assert j["config"]["d"] == wl.d and j["config"]["K"] == wl.K and "workload" in j["config"]
+    # the value is K d worker-elements per step over the host clock's time per step
+    assert j["value"] == pytest.approx(wl.K * wl.d / (j["ms_per_step"] * 1e-3) / 1e9, rel=1e-3)
+    r = j["roofline"]
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert 0.0 < r["frac"] <= 1.0 and r["frac"] == pytest.approx(r["achieved"] / r["peak"], abs=1e-3)
+    assert r["kernel"] == ("rbgs_vec_kernel" if wl.compressor == "rbgs" else "topk_fused_vec_kernel")
+    if wl.compressor != "rbgs":
+        assert 0.5 < r["stream_ceiling"]["kernel_time_frac"] <= 1.2
+    # iteration 0: every top-s selection on the full-data path
+    first = j["first_step"]
+    assert first["ms"] > 0.0
+    if wl.compressor == "topk":
+        assert first["full_data_selections"] == wl.K
+    # the timed steps: sparse momentum term on every step, and the selections
+    # resolved from candidates where the workload allows it
+    sel = j["selection"]
+    assert sel["sparse_momentum_steps"] == 3 and sel["sparse_applies"] == 3
+    if wl.compressor == "topk":
+        assert sel["from_candidates"] == 3 * wl.K and sel["full_data"] == 0
