@@ -15,6 +15,8 @@ def _gpu():
     torch = pytest.importorskip("torch")
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
+    yield
+    torch.cuda.empty_cache()  # the later full-size tests need most of the device memory
 
 
 @pytest.mark.parametrize("workload", ["tiny", "gpt2", "rbgs", "resnet50_approx"])
