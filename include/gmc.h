@@ -33,19 +33,30 @@
  *     messages in worker order 0..K-1 starting from +0.0f and writes
  *     update = -(s * sum); components no worker sent get -(s * +0) = -0.0f,
  *     so w + update equals w - s * sum bit for bit everywhere.
- *   - top-s keeps, per segment of n components, k = min(n, max(1,
- *     ceil(ratio * n))) components (the product in binary64), ranked by the
+ *   - Counts: a fraction ratio of n items keeps count(n, ratio) =
+ *     min(n, max(1, ceil(n p / q))) of them, in exact integer arithmetic,
+ *     with the ratio read as the fraction p/q of smallest denominator
+ *     q <= 2^20 whose binary64 quotient equals it (0.07 is 7/100, so 7% of
+ *     100 is 7 although 0.07 * 100 is 7.000000000000001 in binary64); a ratio
+ *     that no such fraction gives is taken at its exact binary value.
+ *     gmc_count evaluates the rule on the host.
+ *   - top-s keeps, per segment of n components, k = count(n, ratio)
+ *     components (the s of top-s, Section 1), ranked by the
  *     magnitude bits bits(u) & 0x7FFFFFFF (NaN above Inf, -0 equal to +0),
  *     ties broken towards the lower index.  A kept component leaves
  *     u - u behind in the residual (+0.0f for finite u).
  *   - RBGS keeps whole blocks: block b covers [b*B, min((b+1)*B, d)); n_sel =
- *     min(nb, max(1, ceil(ratio * nb))) of the nb = ceil(d/B) blocks are
+ *     count(nb, ratio) of the nb = ceil(d/B) blocks are
  *     drawn by Floyd's sampling algorithm from a SplitMix64 stream whose state
  *     starts at seed XOR mix64(t + 1); every worker uses the same blocks
  *     (Section 4: same random seed on all workers), so only values travel.
  *   - Indices are int32: d must be below 2^31.
  *   - Every call returns a gmc_status; on failure gmc_last_error() describes
  *     the cause.  Invalid arguments never reach the device.
+ *   - Call order: the server-side calls (gmc_aggregate, gmc_aggregate_apply,
+ *     gmc_finish, gmc_apply) return GMC_ESTATE until the context's first
+ *     gmc_step (or gmc_step_detach, gmc_iteration) has been enqueued: before
+ *     it the context holds no selection (RBGS: no block table) to aggregate.
  *   - A context is not thread safe; calls on one context must not overlap.
  */
 #ifndef GMC_H
@@ -74,7 +85,7 @@ typedef enum {
  * contributes the component at offset ((x >> 32) * len_i) >> 32, x the
  * i-th output (i = 0, 1, ...) of a SplitMix64 stream started at
  * seed XOR mix64(t + 1) XOR mix64((k + 1) << 32).  theta is the key ranked
- * r = min(|S|, max(1, ceil(ratio |S|))) from the top among the sample's
+ * r = count(|S|, ratio) from the top among the sample's
  * magnitude keys (ratio = 1/1024 in the paper), and the message keeps every
  * component whose key is >= theta, in ascending order: about ratio * d of
  * them, a number that varies (msg_len).  Message capacity: d per worker.
@@ -108,18 +119,26 @@ gmc_status gmc_init(gmc_ctx** out, int64_t d, int32_t K, int32_t compressor, dou
                     double beta, double eta, uint64_t seed);
 
 /*
- * GMC_TOPK_SEGMENTED only: set the segments (tensors) top-s works on.
+ * GMC_TOPK_SEGMENTED only: set the segments (tensors) top-s works on: the
+ * top-s compressor of Section 1 is applied to each segment on its own, with
+ * k = count(segment length, ratio) (per-tensor top-s).
  * seg_off is a host array of n_seg+1 strictly increasing offsets, seg_off[0]
  * = 0, seg_off[n_seg] = d.  Before the first step only (GMC_ESTATE after).
  * Default: one segment [0, d).
  */
 gmc_status gmc_set_segments(gmc_ctx* ctx, int32_t n_seg, const int64_t* seg_off);
 
-/* GMC_RBGS only: block length B (1 <= B <= d, multiple of 4 for the vector
- * path; any B is accepted).  Before the first step only.  Default 4096. */
+/* GMC_RBGS only: block length B of the random blockwise compressor (RBGS,
+ * Sections 4 and 5.2: whole blocks of consecutive components, drawn with a
+ * seed the workers share).  1 <= B <= d; a multiple of 4 takes the vector
+ * path, any B is accepted.  Before the first step only (GMC_ESTATE after).
+ * Default 4096. */
 gmc_status gmc_set_block(gmc_ctx* ctx, int32_t block);
 
-/* Stream all later calls enqueue on (a hipStream_t; NULL = null stream). */
+/* Stream all later calls enqueue on (a hipStream_t; NULL = null stream).
+ * When the stream changes after work has been enqueued, the new stream is
+ * made to wait for everything enqueued so far on the old one (an event), so
+ * consecutive calls on one context stay ordered across the change. */
 gmc_status gmc_set_stream(gmc_ctx* ctx, void* hip_stream);
 
 /* Per-worker message capacity the caller must provide, in elements:
@@ -130,6 +149,12 @@ int64_t gmc_message_len(const gmc_ctx* ctx);
 /* Per-worker index capacity: top-s: k_tot (element indices);
  * RBGS: n_sel (block ids); sampled-threshold top-s: d. */
 int64_t gmc_index_len(const gmc_ctx* ctx);
+
+/* The count rule on the host, no device work and no context: how many of
+ * n items a fraction ratio keeps (the top-s count of a segment of n,
+ * Section 1; RBGS blocks out of nb; the sampled threshold's rank in a sample
+ * of n).  1 <= n < 2^31, 0 < ratio <= 1; returns -1 for other arguments. */
+int64_t gmc_count(int64_t n, double ratio);
 
 /*
  * One worker-side pass of Algorithm 1 for all K workers at step t, then
@@ -294,7 +319,13 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
  *                              L in [1, d] (default 100); before the first step
  *   GMC_OPT_SPARSE_MOMENTUM    1: the caller promises not to change either
  *                              parameter buffer between a server pass and the
- *                              next server pass (default 0).  Then a server
+ *                              next server pass (default 0).  Setting the
+ *                              option (to either value) drops the recorded
+ *                              components: a caller who wrote w in place or
+ *                              swapped in other contents under the same
+ *                              pointers sets it again before the next
+ *                              gmc_step, which then reads w densely once.
+ *                              gmc_set_step and gmc_apply drop them too.  Then a server
  *                              pass out of place (gmc_aggregate_apply,
  *                              gmc_finish, gmc_iteration; not with momentum on
  *                              the server) records which components it

@@ -23,7 +23,9 @@
  *   - u = fl(fl(e + g) - fl(c * fl(w_t - w_prev))), evaluated left to right as
  *     printed in step "e_{t+1/2,k} = e_{t,k} + grad - (beta/eta)(w_t - w_{t-1})";
  *   - the number kept per segment of n components is
- *     k = min(n, max(1, ceil(ratio * n))), the product formed in binary64;
+ *     k = min(n, max(1, ceil(n p / q))) in exact integer arithmetic, with the
+ *     ratio read as the fraction p/q of smallest denominator (q <= 2^20)
+ *     that rounds to it (0.07 is 7/100), else as its exact binary value;
  *   - top-s ranks by the magnitude bits |u| = bits(u) & 0x7FFFFFFF (NaN above
  *     Inf, -0 equal to +0) and breaks ties by the lower index;
  *   - the server sum over workers runs in worker order 0..K-1 from +0.0f and
@@ -47,15 +49,51 @@
 /* Constants and counts                                                       */
 /* ------------------------------------------------------------------------- */
 
-/* Components kept from a segment of n: ceil(ratio * n) with the product
- * formed in binary64, clamped to [1, n].  The paper sets s = d/1024 for its
- * experiments (Section 5.1) and states top-s as keeping the s largest
- * components (Section 1); a ratio that is a power of two gives that s
- * exactly. */
+/*
+ * The ratio read as the fraction the caller means: the smallest denominator
+ * q <= 2^20 for which some integer p in [1, q] gives p/q == ratio after
+ * rounding to binary64.  0.07 is read as 7/100, 0.001 as 1/1000, 1/1024 as
+ * itself.  Returns 0 when no such fraction exists.
+ */
+static int ratio_as_fraction(double ratio, int64_t* p_out, int64_t* q_out)
+{
+    for (int64_t q = 1; q <= ((int64_t)1 << 20); ++q) {
+        double p = floor(ratio * (double)q + 0.5);
+        if (p < 1.0 || p > (double)q) continue;
+        if (p / (double)q == ratio) {
+            *p_out = (int64_t)p;
+            *q_out = q;
+            return 1;
+        }
+    }
+    return 0;
+}
+
+/*
+ * Components kept from a segment of n (top-s keeps s components, Section 1;
+ * the experiments set s = d/1024, Section 5.1): ceil(n p / q) in exact
+ * integer arithmetic for the ratio read as p/q, clamped to [1, n].  A ratio
+ * that no such fraction gives is taken at its exact binary value
+ * m 2^-sh (m an integer below 2^53): ceil(n m / 2^sh), also exact.
+ */
 int64_t orc_count(int64_t n, double ratio)
 {
-    double x = ratio * (double)n;
-    int64_t k = (int64_t)ceil(x);
+    int64_t p, q, k;
+    if (ratio_as_fraction(ratio, &p, &q)) {
+        k = (n * p + q - 1) / q;
+    } else {
+        int e;
+        double f = frexp(ratio, &e);                /* ratio = f 2^e, f in [1/2, 1) */
+        uint64_t m = (uint64_t)ldexp(f, 53);         /* ratio = m 2^(e - 53) exactly */
+        int sh = 53 - e;
+        if (sh >= 120) {
+            k = 1;                                   /* n m < 2^84: the quotient is in (0, 1) */
+        } else {
+            unsigned __int128 num = (unsigned __int128)(uint64_t)n * m;
+            unsigned __int128 one = 1;
+            k = (int64_t)((num + ((one << sh) - 1)) >> sh);
+        }
+    }
     if (k < 1) k = 1;
     if (k > n) k = n;
     return k;

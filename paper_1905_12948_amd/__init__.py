@@ -2,11 +2,11 @@
 Momentum Compression: the K workers' compressed updates (global momentum,
 error feedback, top-s or RBGS, residual), the server's aggregation and the
 apply step, as HIP kernels behind the C ABI in include/gmc.h."""
-from .gmc import (Gmc, GmcError, load, COMPRESSORS, EXPORTS, STAGES, MAX_WORKERS,
+from .gmc import (Gmc, GmcError, load, count, COMPRESSORS, EXPORTS, STAGES, MAX_WORKERS,
                   GMC_OPT_FORCE_FULL_SELECT, GMC_OPT_CAND_MARGIN, GMC_OPT_CAND_CAP_MULT,
                   GMC_OPT_PROFILE, GMC_OPT_SAMPLE_STRATUM,
                   GMC_OPT_SPARSE_MOMENTUM)
 
-__all__ = ["Gmc", "GmcError", "load", "COMPRESSORS", "EXPORTS", "STAGES", "MAX_WORKERS",
+__all__ = ["Gmc", "GmcError", "load", "count", "COMPRESSORS", "EXPORTS", "STAGES", "MAX_WORKERS",
            "GMC_OPT_FORCE_FULL_SELECT", "GMC_OPT_CAND_MARGIN", "GMC_OPT_CAND_CAP_MULT",
            "GMC_OPT_PROFILE", "GMC_OPT_SAMPLE_STRATUM", "GMC_OPT_SPARSE_MOMENTUM"]

@@ -1,6 +1,7 @@
 // C ABI of the GMC device library (declared in include/gmc.h): argument
 // checks, the context and its device scratch, and the launch order of one
 // iteration of Algorithm 1.
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -22,6 +23,16 @@ constexpr int64_t kMaxPendingEvents = 4096;
 
 thread_local std::string g_init_error = "no error";
 
+// The kept fraction as the caller means it: the fraction p/q with the
+// smallest denominator q <= 2^20 whose binary64 quotient is the given ratio
+// (0.07 is 7/100, 1/1024 itself).  q = 0 when there is none: then the ratio
+// is used at its exact binary value mant * 2^-shift.
+struct KeepRatio {
+    int64_t p = 0, q = 0;
+    uint64_t mant = 0;
+    int shift = 0;
+};
+
 }  // namespace
 
 struct gmc_ctx {
@@ -30,12 +41,14 @@ struct gmc_ctx {
     int32_t K = 0;
     int32_t comp = 0;
     double ratio = 0, beta = 0, eta = 0;
+    KeepRatio keep;                // ratio as the fraction it stands for
     double lambda = 0;             // GMC+ detach coefficient
     int32_t rule = kRuleGmc;       // update rule
     uint64_t seed = 0;
     float c = 0, s = 0, h = 1, b = 0, q = 0;  // see derive_constants
     int64_t t = 0;
     hipStream_t stream = nullptr;
+    hipEvent_t stream_ev = nullptr;  // orders a new stream after the old one (gmc_set_stream)
     int device = 0;
     bool started = false;
     std::string err = "no error";
@@ -141,12 +154,39 @@ void derive_constants(gmc_ctx* ctx) {
     ctx->q = (float)(ctx->lambda * eta);
 }
 
-int64_t count_for(int64_t n, double ratio) {
-    const double x = ratio * (double)n;
-    int64_t k = (int64_t)std::ceil(x);
-    if (k < 1) k = 1;
-    if (k > n) k = n;
-    return k;
+KeepRatio read_ratio(double ratio) {
+    KeepRatio r;
+    const int64_t q_max = int64_t(1) << 20;
+    for (int64_t q = 1; q <= q_max; ++q) {
+        const double scaled = ratio * (double)q;
+        const int64_t p = (int64_t)std::floor(scaled + 0.5);
+        if (p >= 1 && p <= q && (double)p / (double)q == ratio) {
+            r.p = p;
+            r.q = q;
+            return r;
+        }
+    }
+    int e = 0;
+    const double f = std::frexp(ratio, &e);  // ratio = f * 2^e, f in [1/2, 1)
+    r.mant = (uint64_t)std::ldexp(f, 53);
+    r.shift = 53 - e;
+    return r;
+}
+
+// top-s keeps ceil(n * ratio) of a segment of n (the paper's s; s = d/1024
+// in Section 5.1), in exact integer arithmetic, clamped to [1, n]
+int64_t count_for(int64_t n, const KeepRatio& r) {
+    int64_t k;
+    if (r.q > 0) {
+        k = (n * r.p + r.q - 1) / r.q;  // n < 2^31, p <= q <= 2^20
+    } else if (r.shift >= 120) {
+        k = 1;  // n * mant < 2^84
+    } else {
+        const unsigned __int128 prod = (unsigned __int128)(uint64_t)n * r.mant;
+        const unsigned __int128 ceil_add = ((unsigned __int128)1 << r.shift) - 1;
+        k = (int64_t)((prod + ceil_add) >> r.shift);
+    }
+    return std::max<int64_t>(1, std::min<int64_t>(k, n));
 }
 
 void release(gmc_ctx* ctx) {
@@ -347,7 +387,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         g.approx = approx ? 1 : 0;
         g.stratum = ctx->stratum;
         g.samp_n = (int32_t)samp_n;
-        g.samp_r = approx ? (int32_t)count_for(samp_n, ctx->ratio) : 0;
+        g.samp_r = approx ? (int32_t)count_for(samp_n, ctx->keep) : 0;
         GMC_TRY(put(T.seg_start, &g.seg_start));
         GMC_TRY(put(T.seg_out, &g.seg_out));
         GMC_TRY(put(T.chunk_start, &g.chunk_start));
@@ -493,12 +533,13 @@ gmc_status gmc_init(gmc_ctx** out, int64_t d, int32_t K, int32_t compressor, dou
     ctx->seed = seed;
     derive_constants(ctx);
     ctx->seg_off = {0, d};
-    ctx->seg_k = {(int32_t)count_for(d, ratio)};
+    ctx->keep = read_ratio(ratio);
+    ctx->seg_k = {(int32_t)count_for(d, ctx->keep)};
     ctx->k_tot = ctx->seg_k[0];
     if (compressor == GMC_RBGS) {
         ctx->block = (int32_t)std::min<int64_t>(4096, d);
         ctx->nb = (int32_t)((d + ctx->block - 1) / ctx->block);
-        ctx->n_sel = (int32_t)count_for(ctx->nb, ratio);
+        ctx->n_sel = (int32_t)count_for(ctx->nb, ctx->keep);
     }
     hipError_t e = hipGetDevice(&ctx->device);
     if (e != hipSuccess) {
@@ -531,7 +572,7 @@ gmc_status gmc_set_segments(gmc_ctx* ctx, int32_t n_seg, const int64_t* seg_off)
     ctx->seg_k.clear();
     ctx->k_tot = 0;
     for (int32_t i = 0; i < n_seg; ++i) {
-        const int64_t k = count_for(seg_off[i + 1] - seg_off[i], ctx->ratio);
+        const int64_t k = count_for(seg_off[i + 1] - seg_off[i], ctx->keep);
         ctx->seg_k.push_back((int32_t)k);
         ctx->k_tot += k;
     }
@@ -546,14 +587,24 @@ gmc_status gmc_set_block(gmc_ctx* ctx, int32_t block) {
     if (block < 1 || block > ctx->d) return fail(ctx, GMC_EINVAL, "gmc_set_block: block must be in [1, d]");
     ctx->block = block;
     ctx->nb = (int32_t)((ctx->d + block - 1) / block);
-    ctx->n_sel = (int32_t)count_for(ctx->nb, ctx->ratio);
+    ctx->n_sel = (int32_t)count_for(ctx->nb, ctx->keep);
     ctx->prepared = false;
     return prepare(ctx);
 }
 
 gmc_status gmc_set_stream(gmc_ctx* ctx, void* hip_stream) {
     if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_set_stream: ctx is NULL");
-    ctx->stream = reinterpret_cast<hipStream_t>(hip_stream);
+    hipStream_t next = reinterpret_cast<hipStream_t>(hip_stream);
+    if (next == ctx->stream) return GMC_OK;
+    if (ctx->started) {
+        // work of earlier calls may still be pending on the old stream and
+        // shares the context's scratch with what comes next
+        GMC_HIP(ctx, hipSetDevice(ctx->device));
+        if (!ctx->stream_ev) GMC_HIP(ctx, hipEventCreateWithFlags(&ctx->stream_ev, hipEventDisableTiming));
+        GMC_HIP(ctx, hipEventRecord(ctx->stream_ev, ctx->stream));
+        GMC_HIP(ctx, hipStreamWaitEvent(next, ctx->stream_ev, 0));
+    }
+    ctx->stream = next;
     return GMC_OK;
 }
 
@@ -567,6 +618,11 @@ int64_t gmc_index_len(const gmc_ctx* ctx) {
     if (!ctx) return -1;
     if (ctx->comp == GMC_TOPK_APPROX) return ctx->d;
     return ctx->comp == GMC_RBGS ? (int64_t)ctx->n_sel : ctx->k_tot;
+}
+
+int64_t gmc_count(int64_t n, double ratio) {
+    if (n < 1 || n > 0x7fffffffLL || !(ratio > 0.0 && ratio <= 1.0)) return -1;
+    return count_for(n, read_ratio(ratio));
 }
 
 }  // extern "C"
@@ -600,7 +656,7 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
     // detached points) in runs of 2 chunks; at the changed components only,
     // runs of 1, or each chunk's workers on one XCD when the components the
     // last server pass changed (at most K times a top-s message) reach 5% of d
-    const int64_t per_worker = ctx->comp == GMC_TOPK_APPROX ? count_for(ctx->d, ctx->ratio) : ctx->k_tot;
+    const int64_t per_worker = ctx->comp == GMC_TOPK_APPROX ? count_for(ctx->d, ctx->keep) : ctx->k_tot;
     const bool dense_marks = ctx->comp != GMC_RBGS && (int64_t)ctx->K * per_worker * 20 >= ctx->d;
     a.run = (!a.wbits || y_dev) ? 2 : (dense_marks ? 0 : 1);
     if (a.wbits) ++ctx->sparse_steps;
@@ -753,6 +809,7 @@ gmc_status gmc_aggregate(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_
                          float* update_dev) {
     if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_aggregate: ctx is NULL");
     if (!idx_dev || !val_dev || !msg_len_dev || !update_dev) return fail(ctx, GMC_EINVAL, "gmc_aggregate: NULL argument");
+    if (!ctx->started) return fail(ctx, GMC_ESTATE, "gmc_aggregate: no gmc_step has been taken yet");
     FinishArgs f{};
     f.update = update_dev;
     return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, f);
@@ -768,6 +825,7 @@ gmc_status gmc_aggregate_apply(gmc_ctx* ctx, const int32_t* idx_dev, const float
         return fail(ctx, GMC_EINVAL, "gmc_aggregate_apply: update may not alias w or w_out");
     if (ctx->rule == kRuleServerMomentum)
         return fail(ctx, GMC_EINVAL, "gmc_aggregate_apply: momentum on the server needs w_{t-1}; use gmc_finish");
+    if (!ctx->started) return fail(ctx, GMC_ESTATE, "gmc_aggregate_apply: no gmc_step has been taken yet");
     FinishArgs f{};
     f.w_in = w_dev;
     f.w_out = w_out_dev;
@@ -786,6 +844,7 @@ gmc_status gmc_finish(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_dev
     if (ctx->rule == kRuleServerMomentum && !w_prev_dev)
         return fail(ctx, GMC_EINVAL, "gmc_finish: momentum on the server needs w_prev");
     if (w_prev_dev && w_prev_dev == w_dev) return fail(ctx, GMC_EINVAL, "gmc_finish: w_prev may not alias w");
+    if (!ctx->started) return fail(ctx, GMC_ESTATE, "gmc_finish: no gmc_step has been taken yet");
     FinishArgs f{};
     f.w_in = w_dev;
     f.w_prev = ctx->rule == kRuleServerMomentum ? w_prev_dev : nullptr;
@@ -852,6 +911,7 @@ gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const fl
     if (w_prev_out_dev == w_dev) return fail(ctx, GMC_EINVAL, "gmc_apply: w_prev_out may not alias w");
     if (ctx->rule == kRuleServerMomentum)
         return fail(ctx, GMC_EINVAL, "gmc_apply: momentum on the server needs w_{t-1}; use gmc_finish");
+    if (!ctx->started) return fail(ctx, GMC_ESTATE, "gmc_apply: no gmc_step has been taken yet");
     ctx->wbits_valid = false;
     ctx->wbits_pair = false;
     GMC_HIP(ctx, hipSetDevice(ctx->device));
@@ -995,6 +1055,7 @@ void gmc_destroy(gmc_ctx* ctx) {
     if (!ctx) return;
     prof_clear(ctx);
     release(ctx);
+    if (ctx->stream_ev) (void)hipEventDestroy(ctx->stream_ev);
     delete ctx;
 }
 

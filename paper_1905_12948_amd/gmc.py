@@ -30,7 +30,8 @@ EXPORTS = ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "g
            "gmc_index_len", "gmc_step", "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step",
            "gmc_set_option", "gmc_stats", "gmc_profile_read", "gmc_last_error", "gmc_destroy",
            "gmc_calib_copy", "gmc_aggregate_apply", "gmc_set_rule", "gmc_set_eta", "gmc_set_lambda",
-           "gmc_step_detach", "gmc_finish", "gmc_detach", "gmc_iteration", "gmc_calib_stream", "gmc_pair_stats")
+           "gmc_step_detach", "gmc_finish", "gmc_detach", "gmc_iteration", "gmc_calib_stream", "gmc_pair_stats",
+           "gmc_count")
 
 RULES = {"gmc": 0, "server_momentum": 1, "lr_in_residual": 2}
 
@@ -86,6 +87,8 @@ def load() -> ctypes.CDLL:
     lib.gmc_iteration.argtypes = [P, P, P, P, P, P, P, P]
     lib.gmc_calib_stream.argtypes = [P, P, P, i64, i32, i64]
     lib.gmc_pair_stats.argtypes = [P, P, P, i32, ctypes.POINTER(i32)]
+    lib.gmc_count.argtypes = [i64, dbl]
+    lib.gmc_count.restype = i64
     for name in ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "gmc_step",
                  "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step", "gmc_set_option",
                  "gmc_stats", "gmc_profile_read", "gmc_calib_copy", "gmc_aggregate_apply",
@@ -129,6 +132,15 @@ def _rows(x, d: int, K: int, name: str) -> List[int]:
     if len(x) != K:
         raise ValueError("%s must hold K=%d tensors" % (name, K))
     return [_check(t, torch.float32, d, "%s[%d]" % (name, k)) for k, t in enumerate(x)]
+
+
+def count(n: int, ratio: float) -> int:
+    """Items a fraction ratio of n keeps (gmc_count: the top-s count of a
+    segment of n, RBGS blocks of nb); host only."""
+    k = int(load().gmc_count(int(n), float(ratio)))
+    if k < 0:
+        raise ValueError("count needs 1 <= n < 2^31 and 0 < ratio <= 1")
+    return k
 
 
 def calib_copy(dst, src):

@@ -23,6 +23,7 @@ from __future__ import annotations
 import itertools
 import math
 import os
+from fractions import Fraction
 
 import numpy as np
 
@@ -99,19 +100,45 @@ def _run_rule(lib, wl: synth.Workload, ratio: float, steps: int, variant: str = 
 # counts and constants
 # ---------------------------------------------------------------------------
 
+def _want_count(n: int, r: Fraction) -> int:
+    return max(1, min(n, -((-n * r.numerator) // r.denominator)))
+
+
 def pin_count_rule(lib):
-    # s = d/1024 (Section 5.1) is exact for a power-of-two ratio
+    """k = ceil(n p / q), clamped to [1, n], with the ratio read as the
+    fraction p/q it stands for: checked with Python's exact rationals parsed
+    from decimal strings (an independent reading of the same numbers), on
+    products that land just above an integer in binary64."""
+    # s = d/1024 (Section 5.1) exactly when 1024 divides d
     for d in (1024, 1 << 20, 25557032):
-        assert oracle.count(d, 1 / 1024, lib) == math.ceil(d / 1024)
+        assert oracle.count(d, 1 / 1024, lib) == -(-d // 1024)
     # the workloads' stated per-worker counts
     assert oracle.count(1 << 20, 0.01, lib) == 10486
     assert oracle.count(25557032, 0.001, lib) == 25558
     assert oracle.count(11173962, 0.01, lib) == 111740
     assert oracle.count(6240, 0.01, lib) == 63
+    # binary64 gives 0.07 * 100 = 7.000000000000001 and 0.07 * 300 = 21.000000000000004:
+    # 7% keeps 7 and 21
+    assert oracle.count(100, 0.07, lib) == 7
+    assert oracle.count(300, 0.07, lib) == 21
     # clamps: at least one, at most all
     assert oracle.count(768, 0.001, lib) == 1
     assert oracle.count(5, 1.0, lib) == 5
     assert oracle.count(1, 1e-9, lib) == 1
+    rng = np.random.default_rng(77)
+    texts = ["0.07", "0.001", "0.01", "0.1", "0.3", "0.123", "0.0005", "0.035", "0.9", "0.99", "0.015",
+             "0.0001", "0.25", "0.2", "0.6", "0.7", "0.17", "0.029"]
+    fracs = [Fraction(t) for t in texts] + [Fraction(1, 1024), Fraction(3, 7), Fraction(1, 3),
+                                            Fraction(999, 1000000), Fraction(1, 1 << 20)]
+    for r in fracs:
+        ns = [1, 2, 3, 7, 100, 300, 768, 1000, 4096] + [int(x) for x in rng.integers(1, 1 << 31, 8)]
+        for n in ns:
+            assert oracle.count(n, float(r), lib) == _want_count(n, r), (n, r)
+    # a ratio that no fraction of denominator <= 2^20 rounds to: its exact binary value
+    for x in (0.1234567891, 1e-7, 0.3333333333, 2.0 ** -30 * 3):
+        assert float(Fraction(x).limit_denominator(1 << 20)) != x
+        for n in (1, 10, 10**6, 2**31 - 1, 987654321):
+            assert oracle.count(n, x, lib) == _want_count(n, Fraction(x)), (n, x)
 
 
 def pin_constants(lib):
@@ -300,6 +327,24 @@ def pin_aggregate_sum(lib):
     want = -(np.float32(0.1 / K) * dense.sum(0))
     bound = (K + 1) * EPS32 * (0.1 / K) * np.abs(dense).sum(0)
     assert np.all(np.abs(delta - want) <= bound + 1e-30)
+
+
+def pin_aggregate_worker_order(lib):
+    """The server adds the messages in worker order 0..K-1 starting from
+    +0.0f (the order is this build's reading; Algorithm 1's server only
+    receives from all workers).  Binary32 makes the order visible:
+    2^24 + 1 rounds back to 2^24 (ties to even), so three workers sending
+    2^24, 1, -2^24 at one index sum to +0, and -2^24, 1, 2^24 sum to 1.
+    All-negative-zero sends sum to +0 from a +0 start (-0 from the first
+    value), so the update there is -(s * +0) = -0."""
+    big = np.float32(2.0 ** 24)
+    one = np.float32(1.0)
+    idx = [np.array([1, 2, 3], np.int32)] * 3
+    val = [np.array([big, -big, -0.0], np.float32), np.array([one, one, -0.0], np.float32),
+           np.array([-big, big, -0.0], np.float32)]
+    delta = oracle.aggregate(5, np.float32(0.5), idx, val, lib)
+    want = np.array([-0.0, -0.0, -0.5, -0.0, -0.0], np.float32)
+    assert np.array_equal(_bits(delta), _bits(want)), delta
 
 
 # ---------------------------------------------------------------------------
@@ -630,7 +675,7 @@ def pin_approx_count_near_target(lib):
 
 ALL_PINS = [pin_count_rule, pin_constants, pin_topk_bruteforce, pin_delta_approximation,
             pin_error_feedback_identity, pin_msgd_reduction, pin_update_rule_eq8, pin_lemma1,
-            pin_aggregate_single_worker, pin_aggregate_sum, pin_splitmix64_vectors,
+            pin_aggregate_single_worker, pin_aggregate_sum, pin_aggregate_worker_order, pin_splitmix64_vectors,
             pin_rbgs_blocks, pin_rbgs_step_and_cost, pin_toy_quadratic_closed_form,
             pin_toy_quadratic_sparse_converges, pin_detach_lambda_zero, pin_gmcplus_average_rule,
             pin_gmcplus_lemma, pin_server_momentum_rule, pin_lr_in_residual_equals_gmc,

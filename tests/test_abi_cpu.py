@@ -86,3 +86,24 @@ def test_binding_rejects_wrong_tensors_before_device_work():
         _check(torch.zeros(4, dtype=torch.float64), torch.float32)
     with pytest.raises(ValueError):
         _check(torch.zeros(4, dtype=torch.float32), torch.float32)   # not on a GPU
+
+
+def test_count_rule_matches_the_oracle(lib):
+    """gmc_count (the library's host count rule) against the oracle's
+    orc_count: the workloads' counts, products that binary64 lands just
+    above an integer (7% of 100 and 300), power-of-two and decimal ratios,
+    a ratio no small fraction gives, and the clamps."""
+    import numpy as np
+    import oracle
+    from paper_1905_12948_amd import count
+    assert count(100, 0.07) == 7 and count(300, 0.07) == 21
+    rng = np.random.default_rng(3)
+    ratios = [0.07, 0.01, 0.001, 1 / 1024, 0.5, 1.0, 0.3, 0.123, 1e-9, 0.1234567891, 3 / 7, 0.0005, 2.0 ** -30]
+    ns = [1, 2, 7, 100, 300, 768, 6240, 1 << 20, 11173962, 25557032, 38597376, 2**31 - 1]
+    ns += [int(x) for x in rng.integers(1, 1 << 31, 20)]
+    for r in ratios:
+        for n in ns:
+            assert lib.gmc_count(n, r) == oracle.count(n, r), (n, r)
+    assert lib.gmc_count(0, 0.5) == -1 and lib.gmc_count(1 << 31, 0.5) == -1
+    assert lib.gmc_count(10, 0.0) == -1 and lib.gmc_count(10, 1.5) == -1
+    assert lib.gmc_count(10, float("nan")) == -1

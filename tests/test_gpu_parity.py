@@ -8,6 +8,7 @@ import math
 import numpy as np
 import pytest
 
+import oracle
 import synth
 from gpu_harness import Case, run_lockstep
 
@@ -66,7 +67,7 @@ def test_long_candidate_lists_stride_the_copy_launch():
     # copy and selection launches are sized for (within the 64 k capacity),
     # so the copy workgroups stride over the extra tiles and the slices run long
     wl = W("resnet18").shrunk(16, K=4)
-    k = math.ceil(wl.ratio * wl.d)
+    k = oracle.count(wl.d, wl.ratio)
     st = run_lockstep(Case(wl, steps=4, options=((OPT_MARGIN, 64),), label="long lists"))
     assert st["from_candidates"] >= 2 * wl.K
     assert st["candidates"] / st["from_candidates"] > 8 * k + 2048

@@ -29,7 +29,14 @@ MUTANTS = {
     "topk_tie_high_index": ("if (x->pos != y->pos) return x->pos < y->pos ? -1 : 1;",
                             "if (x->pos != y->pos) return x->pos > y->pos ? -1 : 1;"),
     "topk_signed_key": ("return b & 0x7fffffffu;", "return b;"),
-    "count_floor": ("int64_t k = (int64_t)ceil(x);", "int64_t k = (int64_t)floor(x);"),
+    "count_floor": ("k = (n * p + q - 1) / q;", "k = (n * p) / q;"),
+    "count_binary64_product": ("k = (n * p + q - 1) / q;", "k = (int64_t)ceil(ratio * (double)n);"),
+    "count_fraction_ignored": ("if (p / (double)q == ratio) {", "if (0) {"),
+    "count_binary_value_floor": ("k = (int64_t)((num + ((one << sh) - 1)) >> sh);", "k = (int64_t)(num >> sh);"),
+    "agg_reverse_worker_order": ("for (int k = 0; k < K; ++k)\n        for (int64_t i = 0; i < len[k]; ++i)",
+                                 "for (int k = K - 1; k >= 0; --k)\n        for (int64_t i = 0; i < len[k]; ++i)"),
+    "agg_start_from_first_value": ("for (int64_t j = 0; j < d; ++j) acc[j] = 0.0f;",
+                                   "for (int64_t j = 0; j < d; ++j) acc[j] = -0.0f;"),
     "apply_sign": ("w[j] = w[j] + delta[j];", "w[j] = w[j] - delta[j];"),
     "floyd_no_dedup": ("blocks[have++] = dup ? (int32_t)J : r;", "blocks[have++] = r;"),
     "rbgs_short_block": ("int64_t lo = (int64_t)blocks[q] * B, hi = lo + B;",
