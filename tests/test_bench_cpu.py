@@ -64,3 +64,18 @@ def test_pmc_summary_matches_the_sources_or_is_ignored(tmp_path, monkeypatch):
     stale.write_text(open(bench.PMC_SUMMARY).read().replace(kv["kernel_source_sha256"], "0" * 64))
     monkeypatch.setattr(bench, "PMC_SUMMARY", str(stale))
     assert bench.read_pmc_summary() is None
+
+
+def test_survey_bytes_of_the_workloads():
+    """The bench's headline fraction takes the dense byte definition: for
+    the ResNet-50-sized step 5,322,405,504 B (12 K d + 16 d + 16 K k)."""
+    import bench
+    import synth
+    wl = synth.workload("resnet50")
+    assert bench.survey_bytes(wl, 25558, detach=False) == 5322405504
+    rb = synth.workload("rbgs")
+    d = 25557032
+    assert bench.survey_bytes(rb, 63 * 4096, detach=False) == 12 * 8 * d + 16 * d + 8 * 8 * 63 * 4096
+    assert bench.survey_bytes(rb, 63 * 4096, detach=True) == 12 * 8 * d + 16 * d + 8 * 8 * 63 * 4096 + 4 * 8 * d
+    h = bench.host_cpu()
+    assert h["nproc"] >= 1

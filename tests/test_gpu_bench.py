@@ -55,6 +55,10 @@ def test_bench_line(workload, capsys, monkeypatch):
     # the timed steps: sparse momentum term on every step, and the selections
     # resolved from candidates where the workload allows it
     sel = j["selection"]
+    assert sel["count_errors"] == 0
     assert sel["sparse_momentum_steps"] == 3 and sel["sparse_applies"] == 3
+    # the headline fraction takes the dense byte definition; the sparse one beside it
+    assert j["alg_bytes_per_step"] == bench.survey_bytes(wl, j["config"]["message_len"], j["config"]["lambda"] > 0)
+    assert "alg_bytes_per_step" in j["sparse_accounting"]
     if wl.compressor == "topk":
         assert sel["from_candidates"] == 3 * wl.K and sel["full_data"] == 0

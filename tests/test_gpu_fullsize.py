@@ -1,25 +1,33 @@
-"""The workloads at their full sizes, in the launch configuration the bench
-times (gmc_iteration with the sparse momentum term: the worker pass, then the
+"""The workloads at their full sizes, over the iteration counts they are
+stated with (tiny 5, ResNet-18-sized 20, ResNet-50-sized 20, RBGS 20,
+decoder-sized 10), in the launch configuration the bench times
+(gmc_iteration with the sparse momentum term: the worker pass, then the
 server pass writing w_{t+1} over w_{t-1}'s buffer, the two parameter buffers
-swapping roles; GMC+ takes gmc_step_detach then gmc_finish), checked against
-the oracle's per-element functions and the defining property of exact top-k
-(a full CPU sort of every worker's vector would take minutes).  One case
-keeps the dense path (gmc_step, then gmc_aggregate_apply writing the update
-vector too).
+swapping roles; GMC+ takes gmc_step_detach then gmc_finish).  One case keeps
+the dense path (gmc_step, then gmc_aggregate_apply writing the update vector
+too).
 
-For each step and two of the K workers (the first and the last):
-  * u (recomputed by the oracle from the step's inputs) equals e_{t+1} off
-    the sent components bit for bit, the sent values bit for bit, and the
-    residual there is u - u;
-  * per segment the message holds exactly k components, ascending, whose
-    keys are the k largest with ties broken towards the lower index (the
-    sampled-threshold top-s: exactly the oracle's selection on the same u);
-w_{t+1} (and the update vector, where written) is compared with the oracle's
-aggregation of all K messages and its apply, for every component.  Step 0
-takes the full-data selection path and the dense parameter path, later steps
-the candidate path and, with the sparse momentum term, read and write the
-parameters only where they change.  With lambda > 0 the two workers'
-detached points are compared with the oracle's too."""
+A CPU sort of every worker's vector at these sizes would take minutes per
+step, so every worker is checked on the device, every step, against a plain
+torch recomputation of u = (e + g) - c (w_t - w_{t-1}) (one rounding per
+operation, the method's order), itself pinned to the oracle's per-element
+function bit for bit on sampled components (the ragged tail included) of
+every worker:
+  * the sent values are u at the message's components, the residual is u
+    elsewhere and u - u there, bit for bit;
+  * top-s: per segment the message holds exactly k ascending components
+    whose keys are the k largest, ties broken towards the lower index;
+  * RBGS: the oracle's blocks, on every worker;
+  * the sampled-threshold top-s: every component whose key reaches the
+    sample's rank-r key, with the sample at the oracle's positions (and the
+    oracle's own selection on the first worker's u);
+  * w_{t+1} equals the oracle's aggregation and apply at every sent
+    component and w_t bit for bit elsewhere; the update vector and GMC+'s
+    detached points (every worker) likewise;
+  * the library's own count check (stats[4]) stays 0.
+Step 0 takes the full-data selection path and the dense parameter path,
+later steps the candidate path and, with the sparse momentum term, read and
+write the parameters only where they change."""
 import numpy as np
 import pytest
 
@@ -29,6 +37,8 @@ from gpu_harness import assert_same_f32
 
 pytestmark = pytest.mark.gpu
 
+MASK = 0x7FFFFFFF
+
 
 @pytest.fixture(scope="module", autouse=True)
 def _gpu():
@@ -37,33 +47,54 @@ def _gpu():
         pytest.skip("no GPU")
 
 
-def keys_of(a: np.ndarray) -> np.ndarray:
-    return a.view(np.uint32) & np.uint32(0x7FFFFFFF)
+def _bits_equal(a, b) -> bool:
+    import torch
+    return torch.equal(a.contiguous().view(torch.int32), b.contiguous().view(torch.int32))
 
 
-def check_topk_segment(u: np.ndarray, sel: np.ndarray, k: int, tag: str):
-    """sel (ascending, global-to-segment offsets) is the top-k of u by key,
-    lowest index first among equal keys."""
-    assert sel.size == k, tag + ": count"
-    assert np.all(np.diff(sel) > 0), tag + ": not ascending"
-    assert sel[0] >= 0 and sel[-1] < u.size, tag + ": out of range"
-    key = keys_of(u)
+def check_topk_segments(u, sel, seg_of, seg_k, n_seg: int, tag: str):
+    """sel (int64, ascending) is, per segment, the top-k of u by magnitude
+    key, the lower index first among equal keys.  seg_of: segment id of every
+    component (None: one segment)."""
+    import torch
+    dev = u.device
+    d = u.numel()
+    assert sel.numel() == 0 or (int(sel[0]) >= 0 and int(sel[-1]) < d), tag + ": out of range"
+    assert bool((sel[1:] > sel[:-1]).all()), tag + ": not ascending"
+    key = u.view(torch.int32) & MASK
     ks = key[sel]
-    T = ks.min()
-    mask = np.zeros(u.size, bool)
-    mask[sel] = True
-    rest = key[~mask]
-    assert rest.size == 0 or rest.max() <= T, tag + ": an unsent component outranks the threshold"
-    tie_sel = sel[ks == T]
-    tie_rest = np.nonzero((~mask) & (key == T))[0]
-    if tie_rest.size and tie_sel.size:
-        assert tie_sel.max() < tie_rest.min(), tag + ": ties not broken towards the lower index"
+    unsent = torch.ones(d, dtype=torch.bool, device=dev)
+    unsent[sel] = False
+    if seg_of is None:
+        assert sel.numel() == int(seg_k[0]), tag + ": count"
+        T = int(ks.min())
+        rest = key[unsent]
+        assert rest.numel() == 0 or int(rest.max()) <= T, tag + ": an unsent component outranks the threshold"
+        last_tie = int(sel[ks == T].max())
+        rest_T = torch.nonzero(unsent & (key == T)).flatten()
+        assert rest_T.numel() == 0 or int(rest_T.min()) > last_tie, tag + ": ties not broken towards the lower index"
+        return
+    sseg = seg_of[sel]
+    cnt = torch.bincount(sseg, minlength=n_seg)
+    assert torch.equal(cnt, seg_k), tag + ": per-segment counts"
+    T = torch.full((n_seg,), 2**31 - 1, dtype=torch.int32, device=dev).scatter_reduce(0, sseg, ks, "amin")
+    top_rest = torch.full((n_seg,), -1, dtype=torch.int32, device=dev).scatter_reduce(
+        0, seg_of[unsent], key[unsent], "amax")
+    assert bool((top_rest <= T).all()), tag + ": an unsent component outranks its segment's threshold"
+    # ties at the threshold: every sent one below every unsent one
+    at_T = ks == T[sseg]
+    last_tie = torch.full((n_seg,), -1, dtype=torch.int64, device=dev).scatter_reduce(0, sseg[at_T], sel[at_T], "amax")
+    rest_T = torch.nonzero(unsent & (key == T[seg_of])).flatten()
+    if rest_T.numel():
+        first = torch.full((n_seg,), 2**62, dtype=torch.int64, device=dev).scatter_reduce(
+            0, seg_of[rest_T], rest_T, "amin")
+        assert bool((first > last_tie).all()), tag + ": ties not broken towards the lower index"
 
 
 @pytest.mark.parametrize("name,steps,lam,dense", [
-    ("tiny", 3, 0.0, False), ("resnet18", 3, 0.0, False), ("resnet50", 3, 0.0, False), ("rbgs", 3, 0.0, False),
-    ("gpt2", 3, 0.0, False), ("rbgs", 3, 0.5, False), ("resnet50", 2, 0.5, False),
-    ("resnet50_approx", 3, 0.0, False), ("resnet50", 2, 0.0, True)])
+    ("tiny", 5, 0.0, False), ("resnet18", 20, 0.0, False), ("resnet50", 20, 0.0, False),
+    ("rbgs", 20, 0.5, False), ("gpt2", 10, 0.0, False), ("resnet50_approx", 20, 0.0, False),
+    ("rbgs", 3, 0.0, False), ("resnet50", 3, 0.5, False), ("resnet50", 3, 0.0, True)])
 def test_full_size_workload(name, steps, lam, dense):
     import torch
     import synth.device as sdev
@@ -75,6 +106,7 @@ def test_full_size_workload(name, steps, lam, dense):
     rbgs = wl.compressor == "rbgs"
     approx = wl.compressor == "approx"
     seg = wl.topk_segments()
+    n_seg = len(seg) - 1
     g = Gmc(d, K, wl.compressor, wl.ratio, wl.beta, wl.eta, seed=wl.seed,
             segments=seg.tolist() if wl.compressor == "topk_seg" else None,
             block=wl.block if rbgs else None, lam=lam)
@@ -82,20 +114,42 @@ def test_full_size_workload(name, steps, lam, dense):
                            seed=wl.seed, seg_off=seg, block=wl.block, lam=lam)
     if not dense:
         g.set_option(GMC_OPT_SPARSE_MOMENTUM, 1)
-    print("full size %s: d=%d K=%d %s lambda=%g %s" % (name, d, K, wl.compressor, lam,
-                                                    "dense" if dense else "sparse momentum"), flush=True)
+    print("full size %s: d=%d K=%d %s lambda=%g %s, %d steps" % (
+        name, d, K, wl.compressor, lam, "dense" if dense else "sparse momentum", steps), flush=True)
+    c = np.float32(orc.c)
+    c_t = torch.tensor(float(c), dtype=torch.float32, device=dev)
+    q_t = torch.tensor(float(orc.q), dtype=torch.float32, device=dev)
+    seg_of = None
+    if n_seg > 1:
+        seg_of = torch.repeat_interleave(torch.arange(n_seg, device=dev),
+                                         torch.from_numpy(np.diff(seg)).to(dev))
+    seg_k = torch.tensor([int(x) for x in getattr(orc, "seg_k", [0])], dtype=torch.int64, device=dev)
+    rng = np.random.default_rng(11)
+    samp = np.unique(np.concatenate([rng.integers(0, d, 20000), np.arange(max(0, d - 3000), d)]))
+    samp_t = torch.from_numpy(samp).to(dev)
     bufs = [sdev.w0(wl, dev), None]
     bufs[1] = bufs[0].clone()
     err = sdev.rows(K, d, dev, zero=True)
     idx, val, ln = g.alloc_messages(dev)
     wk = sdev.rows(K, d, dev) if lam else None
     upd = torch.empty(d, dtype=torch.float32, device=dev)
-    check = [0, K - 1]
     for t in range(steps):
         grads = sdev.grads(wl, t, dev)
         cur, prev = bufs[t % 2], bufs[(t + 1) % 2]
-        w_h, wp_h = cur.cpu().numpy(), prev.cpu().numpy()
-        e_before = {k: err[k].cpu().numpy() for k in check}
+        # reference u of every worker before the step overwrites e (and w_prev)
+        m = (cur - prev).mul_(c_t)
+        ref = torch.empty((K, d), dtype=torch.float32, device=dev)
+        for k in range(K):
+            torch.add(err[k], grads[k], out=ref[k])
+            ref[k].sub_(m)
+        del m
+        wh = {nm: a[samp_t].cpu().numpy() for nm, a in (("w", cur), ("wp", prev))}
+        for k in range(K):
+            u_orc = oracle.precompress(c, wh["w"], wh["wp"], grads[k][samp_t].cpu().numpy(),
+                                       err[k][samp_t].cpu().numpy())
+            assert_same_f32(ref[k][samp_t].cpu().numpy(), u_orc, "%s step %d worker %d: reference u" % (name, t, k))
+        u0_host = ref[0].cpu().numpy() if approx else None
+        w_t = cur.clone()
         if lam:
             g.step(cur, prev, grads, err, idx, val, ln, w_k=wk)
             g.finish(idx, val, ln, cur, prev, err=err, w_k=wk)
@@ -105,45 +159,66 @@ def test_full_size_workload(name, steps, lam, dense):
         else:
             g.iteration(cur, prev, grads, err, idx, val, ln)
         torch.cuda.synchronize()
-        gi, gv, gl = idx.cpu().numpy(), val.cpu().numpy(), ln.cpu().numpy()
+        del grads
+        gl = ln.cpu().numpy()
         if rbgs:
             blocks = oracle.rbgs_blocks(wl.seed, t, orc.nb, orc.n_sel)
-            assert all(np.array_equal(gi[k], blocks) for k in range(K)), "RBGS blocks"
-            m = sum(min((b + 1) * wl.block, d) - b * wl.block for b in blocks)
-            assert np.all(gl == m), "message lengths"
+            bi = np.concatenate([np.arange(b * wl.block, min((b + 1) * wl.block, d), dtype=np.int64)
+                                 for b in blocks.tolist()])
+            assert np.all(gl == bi.size), "%s step %d: message lengths %s" % (name, t, gl)
+            rb_idx = torch.from_numpy(bi).to(dev)
         elif not approx:
-            assert np.all(gl == orc.message_len), "message lengths"
-        for k in check:
+            assert np.all(gl == orc.message_len), "%s step %d: message lengths" % (name, t)
+        sent_all = []
+        for k in range(K):
             tag = "%s step %d worker %d" % (name, t, k)
-            u = orc.precompress(w_h, wp_h, grads[k].cpu().numpy(), e_before[k])
-            e_after = err[k].cpu().numpy()
-            sent = orc.element_indices(gi[k], int(gl[k]))
-            assert_same_f32(gv[k, :int(gl[k])], u[sent], tag + ": sent values")
-            assert_same_f32(e_after[sent], u[sent] - u[sent], tag + ": residual at sent components")
-            rest = np.ones(d, bool)
-            rest[sent] = False
-            assert_same_f32(e_after[rest], u[rest], tag + ": residual elsewhere")
-            if approx:  # the sampled threshold: the oracle's selection on the same u
-                oi_k, ov_k = oracle.compress_approx(u.copy(), wl.seed, t, k, orc.stratum, wl.ratio)
-                assert np.array_equal(sent.astype(np.int64), oi_k.astype(np.int64)), tag + ": kept set"
-                assert_same_f32(gv[k, :int(gl[k])], ov_k, tag + ": kept values")
+            n_k = int(gl[k])
+            if rbgs:
+                assert np.array_equal(idx[k, :orc.n_sel].cpu().numpy(), blocks), tag + ": blocks"
+                ik = rb_idx
+            else:
+                ik = idx[k, :n_k].long()
+            u = ref[k]
+            assert _bits_equal(val[k, :n_k], u[ik]), tag + ": sent values"
+            if approx:
+                pos = oracle.sample_positions(wl.seed, t, k, d, orc.stratum)
+                sk = np.sort(u[torch.from_numpy(pos).to(dev)].view(torch.int32).cpu().numpy() & MASK)[::-1]
+                theta = int(sk[oracle.count(sk.size, wl.ratio) - 1])
+                want = torch.nonzero((u.view(torch.int32) & MASK) >= theta).flatten()
+                assert torch.equal(ik, want), tag + ": kept set against the sample's threshold"
+                if k == 0:
+                    oi0, _ = oracle.compress_approx(u0_host.copy(), wl.seed, t, 0, orc.stratum, wl.ratio)
+                    assert np.array_equal(oi0.astype(np.int64), ik.cpu().numpy()), tag + ": the oracle's selection"
             elif not rbgs:
-                for s_i in range(len(orc.seg_off) - 1):
-                    a, b = int(orc.seg_off[s_i]), int(orc.seg_off[s_i + 1])
-                    sel = sent[(sent >= a) & (sent < b)] - a
-                    check_topk_segment(u[a:b], sel, int(orc.seg_k[s_i]), tag + " segment %d" % s_i)
-        delta = orc.aggregate(gi, gv, gl)
+                check_topk_segments(u, ik, seg_of, seg_k, n_seg, tag)
+            u[ik] = u[ik] - u[ik]   # the residual u - C(u)
+            assert _bits_equal(err[k], u), tag + ": residual"
+            sent_all.append(ik.cpu().numpy())
+        del ref
+        # the server pass: the oracle's sum and apply over the sent components
+        U = np.unique(np.concatenate(sent_all))
+        U_t = torch.from_numpy(U).to(dev)
+        il = [np.searchsorted(U, sent_all[k]).astype(np.int32) for k in range(K)]
+        vl = [val[k, :sent_all[k].size].cpu().numpy() for k in range(K)]
+        delta = oracle.aggregate(U.size, orc.s, il, vl)
+        w_next_U = w_t[U_t].cpu().numpy()
+        oracle.apply(w_next_U, delta)
+        assert_same_f32(prev[U_t].cpu().numpy(), w_next_U, "%s step %d: w_{t+1} at the sent components" % (name, t))
+        exp = w_t
+        exp[U_t] = torch.from_numpy(w_next_U).to(dev)
+        assert _bits_equal(prev, exp), "%s step %d: w_{t+1} elsewhere" % (name, t)
         if dense:
-            assert_same_f32(upd.cpu().numpy(), delta, "%s step %d: update" % (name, t))
-        w_next = w_h.copy()
-        orc.apply(w_next, delta)
-        assert_same_f32(prev.cpu().numpy(), w_next, "%s step %d: w_{t+1}" % (name, t))
+            ue = torch.full((d,), -0.0, dtype=torch.float32, device=dev)
+            ue[U_t] = torch.from_numpy(delta).to(dev)
+            assert _bits_equal(upd, ue), "%s step %d: update vector" % (name, t)
         if lam:
-            for k in check:
-                want = oracle.detach(orc.q, w_next, err[k].cpu().numpy())
-                assert_same_f32(wk[k].cpu().numpy(), want, "%s step %d: detached point of worker %d" % (name, t, k))
-        print("  step %d ok (%s)" % (t, g.stats()), flush=True)
-        del grads
+            for k in range(K):
+                y = prev - err[k] * q_t
+                assert _bits_equal(wk[k], y), "%s step %d: detached point of worker %d" % (name, t, k)
+        del exp
+        st = g.stats()
+        assert st["count_errors"] == 0, st
+        print("  step %d ok (%s)" % (t, st), flush=True)
     st = g.stats()
     g.close()
     if not dense:  # every step after the first moved the parameters only where they change
