@@ -117,7 +117,8 @@ def test_checkpoint_resume_is_bitwise(name, shrink, K):
         assert_same_f32(ec[k].cpu().numpy(), ea[k].cpu().numpy(), tag + ": residual of worker %d" % k)
         n = int(la[k])
         assert int(lc[k]) == n, tag + ": message length"
-        assert torch.equal(ic[k], ia[k]), tag + ": indices of worker %d" % k
+        ni = n if wl.compressor == "approx" else ic.shape[1]   # sampled threshold: rows of varying length
+        assert torch.equal(ic[k, :ni], ia[k, :ni]), tag + ": indices of worker %d" % k
         assert_same_f32(vc[k, :n].cpu().numpy(), va[k, :n].cpu().numpy(), tag + ": values of worker %d" % k)
     for i in range(2):
         assert_same_f32(bc[i].cpu().numpy(), ba[i].cpu().numpy(), tag + ": parameter buffer %d" % i)
