@@ -385,6 +385,29 @@ gmc_status gmc_pair_stats(gmc_ctx* ctx, int32_t* mode, int64_t* cand, int32_t n,
 gmc_status gmc_profile_read(gmc_ctx* ctx, double* ms, int64_t* launches, int32_t n);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * gmc_aggregate for messages of element indices (the top-s compressors:
+ * rows of index_len strictly ascending indices in [0, d), msg_len[k] of them
+ * valid, values in rows of message_len) without a context, with the GMC
+ * rule's scale s = fl32(eta/K): update_dev[j] = -(s * sum_k val_k(j)) in
+ * worker order, -0.0f where no worker sent j, bit for bit what gmc_aggregate
+ * of a top-s context with the same d, K and eta writes.  Enqueued on
+ * hip_stream (NULL: the null stream); asynchronous.
+ *   Allocates nothing: its scratch (the row pointers, 4 K (ceil(d/4096) + 1)
+ *   bytes) is a static device array of GMC_STATIC_SCRATCH_BYTES that each GPU
+ *   holds from the first call on it until the process ends; larger problems
+ *   get GMC_EINVAL.  Every call on a GPU shares that GPU's array (each call
+ *   writes every entry it reads), so calls that overlap on one GPU (other
+ *   streams, other threads) race: order them.  Argument errors are reported
+ *   through gmc_last_error(NULL).
+ */
+#define GMC_STATIC_SCRATCH_BYTES (8u << 20)
+gmc_status gmc_aggregate_static(int64_t d, int32_t K, double eta, const int32_t* idx_dev, int64_t index_len,
+                                const float* val_dev, int64_t message_len, const int64_t* msg_len_dev,
+                                float* update_dev, void* hip_stream);
+
+/*
  * Measurement support, not part of the method: a plain copy of n floats
  * (dst_dev[i] = src_dev[i]) on hip_stream, the reference kernel of known
  * traffic against which memory counters are scaled.  Buffers must not overlap.

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -501,6 +502,45 @@ void prof_clear(gmc_ctx* ctx) {
         if (e_ != hipSuccess) return hip_fail(ctx, e_, #call); \
     } while (0)
 
+
+}  // namespace
+
+// ----------------------------------------------------------------------------
+// Scratch of gmc_aggregate_static, for callers that cannot allocate: the
+// server pass's row pointers, K * (ceil(d / kAggTopkRange) + 1) int32.  One
+// copy per GPU, held until the process ends.  Host code never passes the
+// array's name to a kernel (on the host it is only a stand-in for the
+// symbol): it takes each device's address once with hipGetSymbolAddress and
+// passes that.
+// ----------------------------------------------------------------------------
+
+static __device__ __align__(256) unsigned char scratch[GMC_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kStaticDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kStaticDevices] = {};
+
+// The current device's address of the static scratch (looked up on the
+// device's first call, with that device current).
+gmc_status static_scratch(int device, void** out) {
+    if (device < 0 || device >= kStaticDevices)
+        return fail(nullptr, GMC_EDEVICE, "gmc_aggregate_static: device id beyond the supported 64");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        void* p = nullptr;
+        hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return fail(nullptr, GMC_EDEVICE,
+                        std::string("gmc_aggregate_static: hipGetSymbolAddress: ") + hipGetErrorString(e));
+        }
+        g_scratch_ptr[device] = p;
+    }
+    *out = g_scratch_ptr[device];
+    return GMC_OK;
+}
 
 }  // namespace
 
@@ -1057,6 +1097,40 @@ void gmc_destroy(gmc_ctx* ctx) {
     release(ctx);
     if (ctx->stream_ev) (void)hipEventDestroy(ctx->stream_ev);
     delete ctx;
+}
+
+gmc_status gmc_aggregate_static(int64_t d, int32_t K, double eta, const int32_t* idx_dev, int64_t index_len,
+                                const float* val_dev, int64_t message_len, const int64_t* msg_len_dev,
+                                float* update_dev, void* hip_stream) {
+    if (d < 1 || d > 0x7fffffffLL) return fail(nullptr, GMC_EINVAL, "gmc_aggregate_static: d must be in [1, 2^31)");
+    if (K < 1 || K > GMC_MAX_WORKERS) return fail(nullptr, GMC_EINVAL, "gmc_aggregate_static: K must be in [1, 64]");
+    if (!(eta > 0.0 && std::isfinite(eta)))
+        return fail(nullptr, GMC_EINVAL, "gmc_aggregate_static: eta must be > 0 and finite");
+    if (index_len < 0 || message_len < index_len || index_len > 0x7fffffffLL)
+        return fail(nullptr, GMC_EINVAL, "gmc_aggregate_static: need 0 <= index_len <= message_len, index_len < 2^31");
+    if (!idx_dev || !val_dev || !msg_len_dev || !update_dev)
+        return fail(nullptr, GMC_EINVAL, "gmc_aggregate_static: NULL argument");
+    const int32_t n_ranges = (int32_t)((d + kAggTopkRange - 1) / kAggTopkRange);
+    const size_t need = (size_t)K * (size_t)(n_ranges + 1) * sizeof(int32_t);
+    if (need > (size_t)GMC_STATIC_SCRATCH_BYTES)
+        return fail(nullptr, GMC_EINVAL,
+                    "gmc_aggregate_static: K * (ceil(d/4096) + 1) row pointers need " + std::to_string(need) +
+                        " bytes, more than the static scratch's " + std::to_string((size_t)GMC_STATIC_SCRATCH_BYTES));
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return hip_fail(nullptr, e, "gmc_aggregate_static: hipGetDevice");
+    void* ptr = nullptr;
+    GMC_TRY(static_scratch(device, &ptr));
+    hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+    int32_t* rowptr = reinterpret_cast<int32_t*>(ptr);  // every entry is written before it is read
+    FinishArgs f{};
+    f.update = update_dev;
+    f.s = (float)(eta / (double)K);
+    e = launch_agg_rowptr(K, (int32_t)d, idx_dev, index_len, msg_len_dev, rowptr, n_ranges, st);
+    if (e != hipSuccess) return hip_fail(nullptr, e, "gmc_aggregate_static: row pointers");
+    e = launch_agg_topk(K, (int32_t)d, idx_dev, index_len, val_dev, message_len, rowptr, n_ranges, f, st);
+    if (e != hipSuccess) return hip_fail(nullptr, e, "gmc_aggregate_static: sum");
+    return GMC_OK;
 }
 
 gmc_status gmc_calib_copy(void* hip_stream, float* dst_dev, const float* src_dev, int64_t n) {

@@ -31,7 +31,7 @@ EXPORTS = ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "g
            "gmc_set_option", "gmc_stats", "gmc_profile_read", "gmc_last_error", "gmc_destroy",
            "gmc_calib_copy", "gmc_aggregate_apply", "gmc_set_rule", "gmc_set_eta", "gmc_set_lambda",
            "gmc_step_detach", "gmc_finish", "gmc_detach", "gmc_iteration", "gmc_calib_stream", "gmc_pair_stats",
-           "gmc_count")
+           "gmc_count", "gmc_aggregate_static")
 
 RULES = {"gmc": 0, "server_momentum": 1, "lr_in_residual": 2}
 
@@ -87,6 +87,8 @@ def load() -> ctypes.CDLL:
     lib.gmc_iteration.argtypes = [P, P, P, P, P, P, P, P]
     lib.gmc_calib_stream.argtypes = [P, P, P, i64, i32, i64]
     lib.gmc_pair_stats.argtypes = [P, P, P, i32, ctypes.POINTER(i32)]
+    lib.gmc_aggregate_static.argtypes = [i64, i32, dbl, P, i64, P, i64, P, P, P]
+    lib.gmc_aggregate_static.restype = ctypes.c_int
     lib.gmc_count.argtypes = [i64, dbl]
     lib.gmc_count.restype = i64
     for name in ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "gmc_step",
@@ -141,6 +143,25 @@ def count(n: int, ratio: float) -> int:
     if k < 0:
         raise ValueError("count needs 1 <= n < 2^31 and 0 < ratio <= 1")
     return k
+
+
+def aggregate_static(d: int, K: int, eta: float, idx, val, msg_len, update):
+    """gmc_aggregate_static: the server's update of K top-s messages (idx
+    int32 [K, index_len], val fp32 [K, message_len], msg_len int64 [K]) into
+    update (fp32 [d]) with no context and no device allocation, on torch's
+    current stream."""
+    torch = _torch()
+    lib = load()
+    if idx.dim() != 2 or idx.shape[0] != K or val.dim() != 2 or val.shape[0] != K:
+        raise ValueError("idx and val must be [K, row]")
+    pi = _check(idx, torch.int32, None, "idx")
+    pv = _check(val, torch.float32, None, "val")
+    pl = _check(msg_len, torch.int64, K, "msg_len")
+    pu = _check(update, torch.float32, d, "update")
+    st = lib.gmc_aggregate_static(int(d), int(K), float(eta), pi, int(idx.shape[1]), pv, int(val.shape[1]), pl, pu,
+                                  ctypes.c_void_p(torch.cuda.current_stream(update.device).cuda_stream))
+    if st != GMC_OK:
+        raise GmcError(st, lib.gmc_last_error(None).decode())
 
 
 def calib_copy(dst, src):

@@ -107,3 +107,18 @@ def test_count_rule_matches_the_oracle(lib):
     assert lib.gmc_count(0, 0.5) == -1 and lib.gmc_count(1 << 31, 0.5) == -1
     assert lib.gmc_count(10, 0.0) == -1 and lib.gmc_count(10, 1.5) == -1
     assert lib.gmc_count(10, float("nan")) == -1
+
+
+def test_static_aggregate_refuses_before_device_work(lib):
+    """gmc_aggregate_static checks its arguments and its scratch bound on the
+    host: 64 workers at d = 2^31 - 1 need 128 MiB of row pointers, beyond the
+    8 MiB static array (the pointers are never dereferenced)."""
+    import ctypes
+    p = ctypes.c_void_p(256)
+    assert lib.gmc_aggregate_static(2**31 - 1, 64, 0.1, p, 1, p, 1, p, p, None) == -1
+    assert "static scratch" in lib.gmc_last_error(None).decode()
+    assert lib.gmc_aggregate_static(0, 4, 0.1, p, 1, p, 1, p, p, None) == -1
+    assert lib.gmc_aggregate_static(100, 0, 0.1, p, 1, p, 1, p, p, None) == -1
+    assert lib.gmc_aggregate_static(100, 4, 0.0, p, 1, p, 1, p, p, None) == -1
+    assert lib.gmc_aggregate_static(100, 4, 0.1, p, 5, p, 4, p, p, None) == -1   # message shorter than index row
+    assert lib.gmc_aggregate_static(100, 4, 0.1, None, 1, p, 1, p, p, None) == -1
