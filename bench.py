@@ -318,6 +318,24 @@ def main():
     torch.cuda.synchronize()
     first = {"ms": round(f0.elapsed_time(f1), 4), "full_data_selections": g0.stats()["full_data"]}
     g0.close()
+    # the full-data selection path (the fallback when the candidates cannot
+    # prove they hold the top k): one step from the same state with every
+    # selection forced onto it
+    full = None
+    if wl.compressor in ("topk", "topk_seg"):
+        from paper_1905_12948_amd import GMC_OPT_FORCE_FULL_SELECT
+        g1 = Gmc(d, K, wl.compressor, wl.ratio, wl.beta, wl.eta, seed=wl.seed, segments=seg, lam=lam)
+        g1.set_option(GMC_OPT_FORCE_FULL_SELECT, 1)
+        err.zero_()
+        bufs[1].copy_(bufs[0])
+        torch.cuda.synchronize()
+        f0.record()
+        g1.step(bufs[0], bufs[1], G[0], err, idx, val, ln, w_k=wk if detach else None)
+        f1.record()
+        torch.cuda.synchronize()
+        full = {"ms": round(f0.elapsed_time(f1), 4), "full_data_selections": g1.stats()["full_data"],
+                "what": "gmc_step alone, every selection on the full-data path"}
+        g1.close()
     if args.calib:
         for _ in range(3):
             calib_copy(cal_dst, cal_src)
@@ -366,6 +384,7 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "ms_per_step_median": None if ms_median is None else round(ms_median, 4),
         "first_step": first,
+        "full_data_step": full,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": DESCRIPTIONS[wl.name], "d": d, "K": K, "compressor": wl.compressor,

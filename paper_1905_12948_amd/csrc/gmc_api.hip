@@ -62,6 +62,7 @@ struct gmc_ctx {
     int cap_mult = 64;
     int32_t stratum = 100;         // sampled-threshold top-s: components per sample stratum
     int sparse_w = 0;              // GMC_OPT_SPARSE_MOMENTUM
+    bool seeded = false;           // the first step's thresholds were drawn from a sample
 
     // the last server pass's bitmap of changed components (sparse_w)
     uint32_t* wbits = nullptr;
@@ -223,6 +224,8 @@ struct TopkTables {
     std::vector<int64_t> pair_cand;
     std::vector<int2> tile_map;       // per worker: launched tile -> (segment, first tile in the segment)
     std::vector<int32_t> seg_tile_stride, seg_tile_cap_off;
+    std::vector<int2> seed_map;       // first-step sample: (segment, first run) per workgroup
+    std::vector<int32_t> seg_seed_groups, seg_seed_runs, seg_seed_rank;
     int32_t tiles_cap = 0;            // tile-list entries per worker
     int64_t cand_total = 0;
 };
@@ -285,6 +288,20 @@ TopkTables build_tables(const gmc_ctx* ctx) {
         const int64_t nlaunch = (lc + kTile - 1) / kTile + rank;
         T.seg_tile_stride.push_back((int32_t)nlaunch);
         for (int64_t i = 0; i < nlaunch; ++i) T.tile_map.push_back(make_int2(sg, (int)i));
+        // first-step sample of a large segment: whole runs of kSeedRun every
+        // kSeedStride; the rank aims at kSeedMult k candidates
+        const int64_t runs = n >= kSeedMinLen ? n / kSeedStride : 0;
+        const int64_t groups = (runs + kSeedRunsPerGroup - 1) / kSeedRunsPerGroup;
+        int64_t rank_s = 0;
+        if (runs > 0) {
+            const int64_t m = runs * kSeedRun;
+            const int64_t want = (int64_t)kSeedMult * ctx->seg_k[sg];
+            rank_s = std::max<int64_t>(1, std::min<int64_t>(m, (want * m + n - 1) / n));
+        }
+        T.seg_seed_groups.push_back((int32_t)groups);
+        T.seg_seed_runs.push_back((int32_t)runs);
+        T.seg_seed_rank.push_back((int32_t)rank_s);
+        for (int64_t gi = 0; gi < groups; ++gi) T.seed_map.push_back(make_int2(sg, (int)(gi * kSeedRunsPerGroup)));
     }
     for (int k = 0; k < ctx->K; ++k) {
         for (int sg = 0; sg < n_seg; ++sg) {
@@ -333,6 +350,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         add(nsl, 4); add(nsl, 4); add(ns, 4); add(ns, 4);
         add(np, 4); add(np, 4); add(np, 8);
         add(T.tile_map.size(), sizeof(int2)); add(ns, 4); add(ns, 4);
+        add(T.seed_map.size() + 1, sizeof(int2)); add(ns, 4); add(ns, 4); add(ns, 4);
         add((size_t)K * ng, 4); add((size_t)K * T.tiles_cap, sizeof(int2));
         add(np, sizeof(PairState));
         add(np * kBins, 4);
@@ -416,6 +434,14 @@ gmc_status prepare(gmc_ctx* ctx) {
         GMC_TRY(put(T.seg_tile_stride, &g.seg_tile_stride));
         g.tiles_cap_per_worker = T.tiles_cap;
         GMC_TRY(put(T.seg_tile_cap_off, &g.seg_tile_cap_off));
+        int2* sm = cv.take<int2>(T.seed_map.size() + 1);
+        if (!T.seed_map.empty())
+            GMC_HIP(ctx, hipMemcpy(sm, T.seed_map.data(), T.seed_map.size() * sizeof(int2), hipMemcpyHostToDevice));
+        g.seed_map = sm;
+        g.n_seed_groups = (int32_t)T.seed_map.size();
+        GMC_TRY(put(T.seg_seed_groups, &g.seg_seed_groups));
+        GMC_TRY(put(T.seg_seed_runs, &g.seg_seed_runs));
+        GMC_TRY(put(T.seg_seed_rank, &g.seg_seed_rank));
         ctx->scr.grp_base = cv.take<uint32_t>((size_t)K * ng);
         ctx->scr.tiles = cv.take<int2>((size_t)K * T.tiles_cap);
         TopkScratch& sc = ctx->scr;
@@ -740,6 +766,9 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
         // (partial and unaligned ones element-wise); the element-wise kernel
         // every chunk of the others
         const uint64_t all = ctx->K == 64 ? ~0ull : ((1ull << ctx->K) - 1ull);
+        // the context's first step: speculative thresholds from a sample of u
+        if (!ctx->seeded && !ctx->force_full) GMC_LAUNCH(ctx, launch_topk_seed(a, ctx->geo, ctx->scr, ctx->stream));
+        ctx->seeded = true;
         if (vec_mask) {
             GMC_TRY(prof_begin(ctx, 0, &ev));
             GMC_LAUNCH(ctx, launch_topk_fused_vec(a, ctx->geo, ctx->scr, vec_mask, ctx->stream));

@@ -47,6 +47,16 @@ constexpr int kAggTopkStageSmall = 128;
 
 constexpr uint32_t kNoThreshold = 0xffffffffu;  // no speculative candidates
 
+// First-step threshold from a sample (topk_seed_kernel): runs of kSeedRun
+// consecutive components every kSeedStride of each segment of at least
+// kSeedMinLen components, kSeedRunsPerGroup runs per workgroup; the threshold
+// sits at the sample's key of rank about kSeedMult k |S| / n.
+constexpr int kSeedRun = 32;
+constexpr int kSeedStride = 512;
+constexpr int kSeedRunsPerGroup = 256;
+constexpr int64_t kSeedMinLen = 1 << 16;
+constexpr int kSeedMult = 4;
+
 // Update rules: GMC (Algorithm 1) and the two other ways of combining
 // momentum with error feedback that the appendix compares it with.
 constexpr int kRuleGmc = 0;             // u = (e + g) - (beta/eta)(w_t - w_{t-1})
@@ -119,6 +129,16 @@ struct TopkGeometry {
     const int32_t* seg_tile_stride;   // [n_seg] workgroups launched per (worker, segment)
     int32_t tiles_cap_per_worker;
     const int32_t* seg_tile_cap_off;  // [n_seg]
+    // first-step sample: workgroup g of a worker takes segment seed_map[g].x's
+    // runs seed_map[g].y, +1, ... (kSeedRunsPerGroup of them, fewer at the
+    // segment's end); seg_seed_groups[seg] workgroups per (worker, segment),
+    // seg_seed_runs[seg] runs, seg_seed_rank[seg] the rank in the sample (0:
+    // the segment is not sampled)
+    int32_t n_seed_groups;
+    const int2* seed_map;             // [n_seed_groups]
+    const int32_t* seg_seed_groups;   // [n_seg]
+    const int32_t* seg_seed_runs;     // [n_seg]
+    const int32_t* seg_seed_rank;     // [n_seg]
 };
 
 struct TopkScratch {
@@ -216,6 +236,9 @@ struct DetachArgs {
 // vec_mask: bit k set when worker k's rows (and w_t, w_prev) are 16-byte
 // aligned.  The vector kernel takes every chunk of those workers, the
 // element-wise kernel every chunk of the others.
+// the first step's speculative thresholds from a sample of u (before the
+// fused pass; pairs whose segment is not sampled keep no threshold)
+hipError_t launch_topk_seed(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, hipStream_t st);
 hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                                  uint64_t vec_mask, hipStream_t st);
 hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,

@@ -699,6 +699,88 @@ __device__ __forceinline__ void take_hist2(uint32_t* h, uint32_t* gh, uint32_t* 
     __syncthreads();
 }
 
+// ----------------------------------------------------------------------------
+// first-step threshold from a sample
+//
+// A context's first step has no previous selection to place the speculative
+// threshold with, so without one every pair would take the full-data path
+// (three histogram passes and the emit, each over all of u).  Before that
+// step's worker pass this kernel computes u, as the worker pass will, at a
+// regular sample of each large segment (runs of kSeedRun consecutive
+// components every kSeedStride: a sixteenth of the components, whole cache
+// lines), and sets the pair's threshold at the floor of the 11-bit key bin
+// holding the sample's key of rank about kSeedMult k |S| / n.  The worker
+// pass then collects about that many candidates and the selection resolves
+// from them.  The threshold only decides which components are candidates:
+// the candidates still have to prove that they hold the top k (at least k of
+// them, at most the capacity) or the pair takes the full-data path, so the
+// results never depend on it.
+// ----------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kGroup) void topk_seed_kernel(StepArgs a, TopkGeometry g, TopkScratch s) {
+    static_assert(kSeedRunsPerGroup * kSeedRun == kGroup * 32, "32 sample components per thread");
+    static_assert(kGroup % kSeedRun == 0 && kSeedRun <= kSeedStride, "whole runs per wave step");
+    __shared__ uint32_t h[kBins];
+    __shared__ uint32_t sh_wsum[kWavesPerGroup];
+    __shared__ int sh_res[2];
+    __shared__ int sh_last;
+    const int k = blockIdx.x / g.n_seed_groups;
+    const int2 sm = g.seed_map[blockIdx.x % g.n_seed_groups];
+    const int seg = sm.x;
+    const int p = k * g.n_seg + seg;
+    PairState* ps = &s.pair[p];
+    const int W = g.seg_seed_groups[seg];
+    const int runs = g.seg_seed_runs[seg];
+    const int run_hi = min(sm.y + kSeedRunsPerGroup, runs);
+    const int64_t seg_lo = g.seg_start[seg];
+    for (int b = threadIdx.x; b < kBins; b += kGroup) h[b] = 0u;
+    __syncthreads();
+    const float* e = a.wp.e[k];
+    const float* gr = a.wp.g[k];
+    const float c = a.c, hh = a.h;
+    constexpr int kRunsPerStep = kGroup / kSeedRun;  // runs one pass of the workgroup covers
+    constexpr int kUnroll = 8;
+    for (int i0 = 0; i0 < 32; i0 += kUnroll) {
+        float ev[kUnroll], gv[kUnroll], wt[kUnroll], wp[kUnroll];
+        bool in[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int run = sm.y + (i0 + u) * kRunsPerStep + (int)threadIdx.x / kSeedRun;
+            in[u] = run < run_hi;
+            const int64_t j = seg_lo + (int64_t)run * kSeedStride + (threadIdx.x % kSeedRun);
+            ev[u] = gv[u] = wt[u] = wp[u] = 0.0f;
+            if (in[u]) {
+                ev[u] = e[j];
+                gv[u] = gr[j];
+                wt[u] = a.w_t[j];
+                wp[u] = a.w_prev[j];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            if (in[u]) atomicAdd(&h[key_of(rule_u_rt(a.rule, ev[u], gv[u], wt[u], wp[u], c, hh)) >> kShift1], 1u);
+    }
+    __syncthreads();
+    uint32_t* gh = s.hist + (size_t)p * kBins;
+    const bool solo = W == 1;
+    for (int b = threadIdx.x; !solo && b < kBins; b += kGroup)
+        if (h[b]) atomicAdd(&gh[b], h[b]);
+    if (!finish_slice(&ps->done, W, &sh_last)) return;
+    if (!solo) take_hist<kBins>(h, gh);
+    uint32_t above = 0;
+    const int bin = find_bin(h, kBins, (uint32_t)g.seg_seed_rank[seg], &above, sh_wsum, sh_res);
+    if (threadIdx.x == 0) {
+        ps->tau = bin < 0 ? 0u : (uint32_t)bin << kShift1;  // fewer sampled than the rank: every component
+        store_agent(&ps->done, 0u);
+    }
+}
+
+hipError_t launch_topk_seed(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, hipStream_t st) {
+    if (g.n_seed_groups == 0) return hipSuccess;
+    hipLaunchKernelGGL(topk_seed_kernel, dim3(g.K * g.n_seed_groups), dim3(kGroup), 0, st, a, g, s);
+    return hipGetLastError();
+}
+
 // margin: the speculative threshold's rank, in quarters of k.  h2/gh2: the
 // second pass's histogram of the threshold's bin (PASS 2 only; gh2 holds it
 // unless that bin is the one h covers).

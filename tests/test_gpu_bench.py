@@ -47,11 +47,13 @@ def test_bench_line(workload, capsys, monkeypatch):
     assert r["kernel"] == ("rbgs_vec_kernel" if wl.compressor == "rbgs" else "topk_fused_vec_kernel")
     if wl.compressor != "rbgs":  # the plain stream of the pass's pattern (cache-resident at the tiny size)
         assert 0.0 < r["stream_ceiling"]["kernel_time_frac"] <= 1.2
-    # iteration 0: every top-s selection on the full-data path
+    # iteration 0: thresholds from a sample of u, every global top-s selection
+    # resolved from its candidates; the full-data path measured on its own
     first = j["first_step"]
     assert first["ms"] > 0.0
     if wl.compressor == "topk":
-        assert first["full_data_selections"] == wl.K
+        assert first["full_data_selections"] == 0
+        assert j["full_data_step"]["full_data_selections"] == wl.K and j["full_data_step"]["ms"] > 0.0
     # the timed steps: sparse momentum term on every step, and the selections
     # resolved from candidates where the workload allows it
     sel = j["selection"]

@@ -30,8 +30,19 @@ def W(name):
 
 def test_tiny_full_size():
     st = run_lockstep(Case(W("tiny"), steps=5, label="tiny"))
-    assert st["full_data"] >= 4          # step 0 has no threshold yet
-    assert st["from_candidates"] >= 8    # later steps resolve from candidates
+    # step 0 takes its thresholds from a sample of u, later steps from the
+    # previous selection: every selection resolves from candidates
+    assert st["full_data"] == 0 and st["from_candidates"] == 5 * 4, st
+
+
+def test_sampled_first_threshold_falls_back_on_ties():
+    # every gradient of the first step equal: the sample puts the threshold at
+    # the floor of their key's bin, every component is a candidate, more than
+    # the capacity holds, and the first step takes the full-data path
+    def flat_first(t, g):
+        return np.ones_like(g) if t == 0 else g
+    st = run_lockstep(Case(W("resnet18").shrunk(16, K=4), steps=3, grad_hook=flat_first, label="flat first step"))
+    assert st["full_data"] >= 4, st
 
 
 def test_resnet18_shape_shrunk():
