@@ -208,6 +208,9 @@ def main():
     ap.add_argument("--cpu-workers", type=int, default=2)
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--force-full", action="store_true",
+                    help="every top-s selection of the timed steps on the full-data path (GMC_OPT_FORCE_FULL_SELECT), "
+                         "to profile the fallback path")
     ap.add_argument("--calib", action="store_true",
                     help="also run the plain copy kernel (memory-counter calibration)")
     args = ap.parse_args()
@@ -236,6 +239,9 @@ def main():
     if args.margin is not None:
         from paper_1905_12948_amd import GMC_OPT_CAND_MARGIN
         gm.set_option(GMC_OPT_CAND_MARGIN, args.margin)
+    if args.force_full:
+        from paper_1905_12948_amd import GMC_OPT_FORCE_FULL_SELECT
+        gm.set_option(GMC_OPT_FORCE_FULL_SELECT, 1)
     # the bench keeps w untouched between the server pass and the next worker
     # pass and swaps the two buffers, as the sparse momentum term requires
     sparse_w = not args.dense_momentum
@@ -389,7 +395,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": DESCRIPTIONS[wl.name], "d": d, "K": K, "compressor": wl.compressor,
                    "ratio": wl.ratio, "lambda": lam, "message_len": msg_len, "grad_batches": len(G),
-                   "sparse_momentum": sparse_w},
+                   "sparse_momentum": sparse_w, "forced_full_data": bool(args.force_full)},
         # the step's algorithmic bytes with dense parameter traffic (12 B per
         # worker-element, 16 B per element, 16 B per message entry) over
         # 8 TB/s; the sparse accounting (parameters moved only where they

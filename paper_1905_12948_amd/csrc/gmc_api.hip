@@ -360,6 +360,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         add((size_t)T.cand_total, 4); add((size_t)T.cand_total, 4);
         for (int q = 0; q < 4; ++q) add((size_t)K * nsl, 4);
         add((size_t)K * nsl * kSlHist, 4);
+        add((size_t)K * nsl * kWavesPerGroup, 4);
         add((size_t)K * (ctx->n_ranges + 1), 4);
         if (approx) add((size_t)K * samp_n, 4);
     }
@@ -465,6 +466,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         sc.sl_out = cv.take<uint32_t>((size_t)K * nsl);
         sc.sl_tiebase = cv.take<uint32_t>((size_t)K * nsl);
         sc.sl_hist = cv.take<uint32_t>((size_t)K * nsl * kSlHist);
+        sc.sl_run = cv.take<uint32_t>((size_t)K * nsl * kWavesPerGroup);
         sc.stats = ctx->stats;
         ctx->rowptr = cv.take<int32_t>((size_t)K * (ctx->n_ranges + 1));
         sc.rowptr = ctx->rowptr;  // the emit kernel writes them for gmc_iteration's server pass
@@ -1099,7 +1101,7 @@ gmc_status gmc_pair_stats(gmc_ctx* ctx, int32_t* mode, int64_t* cand, int32_t n,
     std::vector<PairState> host((size_t)np);
     GMC_HIP(ctx, hipMemcpy(host.data(), ctx->scr.pair, sizeof(PairState) * (size_t)np, hipMemcpyDeviceToHost));
     for (int32_t i = 0; i < n && i < np; ++i) {
-        mode[i] = host[(size_t)i].mode;
+        mode[i] = host[(size_t)i].mode == 0 ? 0 : 1;  // collected full data is the full-data path
         cand[i] = (int64_t)host[(size_t)i].cand_used;
     }
     return GMC_OK;

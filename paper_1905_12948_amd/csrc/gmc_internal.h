@@ -47,6 +47,13 @@ constexpr int kAggTopkStageSmall = 128;
 
 constexpr uint32_t kNoThreshold = 0xffffffffu;  // no speculative candidates
 
+// A full-data pair whose first digit leaves few components at or above its
+// bin (at most 1/kCollectDiv of the segment) is "collected": the second pass
+// also gathers those components, in index order, into the pair's staging
+// rows, and the third pass and the emit read only them.
+constexpr int kModeCollected = 3;
+constexpr int64_t kCollectDiv = 8;
+
 // First-step threshold from a sample (topk_seed_kernel): runs of kSeedRun
 // consecutive components every kSeedStride of each segment of at least
 // kSeedMinLen components, kSeedRunsPerGroup runs per workgroup; the threshold
@@ -73,7 +80,8 @@ struct WorkerPtrs {
 struct PairState {
     uint32_t tau;       // candidate threshold key of the next fused pass
     uint32_t cand;      // candidates appended by the fused pass (atomic)
-    int32_t mode;       // 0 = resolve from candidates, 1 = full data
+    int32_t mode;       // 0 = resolve from candidates, 1 = full data, 3 = full data collected
+                        // by the second pass (kModeCollected)
     uint32_t prefix;    // radix digits fixed so far
     int32_t need;       // components still to take below the prefix
     uint32_t T;         // threshold key: k-th largest magnitude key
@@ -159,6 +167,8 @@ struct TopkScratch {
     uint32_t* sl_out;             // [K*n_slices] message offset of the slice's first kept component
     uint32_t* sl_tiebase;         // [K*n_slices] at-threshold components in earlier slices
     uint32_t* sl_hist;            // [K*n_slices][kSlHist] third-pass counts per slice (exact top-s)
+    uint32_t* sl_run;             // [K*n_slices][kWavesPerGroup] components each quarter of a
+                                  // collected slice gathered (kModeCollected)
     float* samp;                  // [K][samp_n] the sample's values (sampled-threshold top-s)
     int32_t* rowptr;              // [K][n_ranges+1] server-pass row pointers, also written by the emit
     int32_t n_ranges;             // ranges of kAggTopkRange components

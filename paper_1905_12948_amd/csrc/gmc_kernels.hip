@@ -489,6 +489,7 @@ hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const
 namespace {
 
 constexpr int kSliceLoads = 16;      // independent loads in flight per thread
+constexpr int kSliceLoads4 = 8;      // 16-byte loads in flight per thread over contiguous u
 constexpr int kEmitLoads = 4;        // staged elements per thread in the emit pass
 constexpr int kEmitStage = kGroup * kEmitLoads;  // elements staged in LDS per round
 constexpr int kFullRound = kGroup * 16;          // full-data elements per round of the emit
@@ -524,6 +525,25 @@ __device__ __forceinline__ Slice open_slice(int mode, uint32_t cand, int k, int 
     return v;
 }
 
+// Run q of a collected slice (kModeCollected): the components wave q of the
+// second pass gathered from its quarter of the full-data slice w of W, in
+// index order, at that quarter's positions in the pair's staging rows (the
+// pair's slot area: indices in its first n words, values in the next n, n the
+// segment's length; the quarter is at most that long, so runs never overlap).
+__device__ __forceinline__ Slice collected_run(const TopkGeometry& g, const TopkScratch& s, int k, int seg, int w,
+                                               int W, int q) {
+    const int64_t n = g.seg_start[seg + 1] - g.seg_start[seg];
+    const int64_t lo = n * w / W, len = n * (w + 1) / W - lo;
+    int32_t* base = reinterpret_cast<int32_t*>(s.slot + ((size_t)k * g.n_chunks + g.cgrp_lo[g.seg_cgrp_lo[seg]]) * kChunk);
+    Slice v;
+    v.seg_lo = g.seg_start[seg];
+    v.idx = base;
+    v.val = reinterpret_cast<const float*>(base + n);
+    v.lo = lo + len * q / kWavesPerGroup;
+    v.hi = v.lo + s.sl_run[((size_t)k * g.n_slices + g.seg_slice_lo[seg] + w) * kWavesPerGroup + q];
+    return v;
+}
+
 // f(key, index) for every element of the slice; loads are issued
 // kSliceLoads at a time per thread.
 template <bool kNeedIdx, class F>
@@ -547,6 +567,43 @@ __device__ __forceinline__ void for_slice(const Slice& v, F f) {
             if (pos < v.hi) f(key_of(x[i]), j[i]);
         }
     }
+}
+
+// f(key) for every element of a contiguous slice (no index array: the full
+// data, or the sample), with 16-byte loads, kSliceLoads4 of them in flight
+// per thread (32 KB per workgroup: the full-data passes are bound by the
+// bytes in flight); the head up to the first 16-byte boundary and the tail
+// element-wise.  The order of the calls is not the index order.
+template <class F>
+__device__ __forceinline__ void for_slice_contig(const Slice& v, F f) {
+    const float* p = v.val;
+    int64_t lo = v.lo;
+    const int64_t hi = v.hi;
+    const int64_t mis = (int64_t)((reinterpret_cast<uintptr_t>(p + lo) >> 2) & 3u);
+    const int64_t head = mis ? (4 - mis < hi - lo ? 4 - mis : hi - lo) : 0;
+    if ((int64_t)threadIdx.x < head) f(key_of(p[lo + threadIdx.x]));
+    lo += head;
+    const int64_t n4 = (hi - lo) / 4;
+    const float4* p4 = reinterpret_cast<const float4*>(p + lo);
+    for (int64_t b = 0; b < n4; b += (int64_t)kGroup * kSliceLoads4) {
+        float4 x[kSliceLoads4];
+#pragma unroll
+        for (int i = 0; i < kSliceLoads4; ++i) {
+            const int64_t q = b + i * kGroup + threadIdx.x;
+            x[i] = q < n4 ? p4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < kSliceLoads4; ++i) {
+            if (b + i * kGroup + threadIdx.x < n4) {
+                f(key_of(x[i].x));
+                f(key_of(x[i].y));
+                f(key_of(x[i].z));
+                f(key_of(x[i].w));
+            }
+        }
+    }
+    const int64_t t0 = lo + n4 * 4;
+    if (t0 + (int64_t)threadIdx.x < hi) f(key_of(p[t0 + threadIdx.x]));
 }
 
 // The bin b (scanning from the top) with above(b) < need <= above(b) + h[b],
@@ -843,6 +900,13 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
         if (PASS == 1) {
             ps->prefix = b;
             ps->need = (int32_t)(need - above);
+            // a full-data pair with few components at or above the digit's
+            // bin: the second pass collects them for the third and the emit
+            if (mode == 1 && !approx) {
+                const int sg = p % g.n_seg;
+                const int64_t n = g.seg_start[sg + 1] - g.seg_start[sg];
+                if ((int64_t)above + (int64_t)h[b] <= n / kCollectDiv) ps->mode = kModeCollected;
+            }
         } else if (PASS == 2) {
             ps->prefix = (prefix << 11) | b;
             ps->need = (int32_t)(need - above);
@@ -924,9 +988,10 @@ __device__ void hist_pass(const StepArgs& a, const TopkGeometry& g, const TopkSc
         if (PASS == 2) h2[b] = 0u;
     }
     __syncthreads();
-    const Slice v = open_slice(mode, cand, id.k, id.seg, id.p, id.w, W, a, g, s);
+    const bool collected = mode == kModeCollected;
+    const Slice v = open_slice(collected ? 1 : mode, cand, id.k, id.seg, id.p, id.w, W, a, g, s);
     uint32_t above = 0;  // third pass: keys above T's 22-bit bin
-    for_slice<false>(v, [&](uint32_t key, int32_t) {
+    auto body = [&](uint32_t key) {
         if (PASS == 1) {
             atomicAdd(&h[key >> kShift1], 1u);
         } else if (PASS == 2) {
@@ -938,7 +1003,90 @@ __device__ void hist_pass(const StepArgs& a, const TopkGeometry& g, const TopkSc
             if (d12 == prefix) atomicAdd(&h[key & 511u], 1u);
             else if (count && d12 > prefix) ++above;
         }
-    });
+    };
+    if (PASS == 2 && collected) {
+        // each wave streams its quarter of the slice, histograms it as above
+        // and gathers, in index order, the components whose first digit is
+        // at or above the prefix (all that the selection can keep) into its
+        // run of the staging rows: ballots only, no workgroup barrier
+        const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+        const uint64_t lt = lanemask_lt();
+        const Slice run = collected_run(g, s, id.k, id.seg, id.w, W, 0);
+        int32_t* ci = const_cast<int32_t*>(run.idx);
+        float* cv = const_cast<float*>(run.val);
+        const int64_t len = v.hi - v.lo;
+        const int64_t ql = v.lo + len * wave / kWavesPerGroup, qh = v.lo + len * (wave + 1) / kWavesPerGroup;
+        uint32_t cnt = 0;
+        // one component per lane (the quarter's unaligned head and its tail)
+        auto one = [&](int64_t pos, bool in) {
+            const float x = in ? v.val[pos] : 0.0f;
+            const uint32_t key = key_of(x);
+            if (in) body(key);
+            const bool take = in && (key >> kShift1) >= prefix;
+            const uint64_t bal = ballot(take);
+            if (take) {
+                const int64_t o = ql + cnt + popc64(bal & lt);
+                ci[o] = v.seg_lo + (int32_t)pos;
+                cv[o] = x;
+            }
+            cnt += popc64(bal);
+        };
+        const int64_t mis = (int64_t)((reinterpret_cast<uintptr_t>(v.val + ql) >> 2) & 3u);
+        const int64_t head = mis ? (4 - mis < qh - ql ? 4 - mis : qh - ql) : 0;
+        one(ql + lane, lane < head);
+        const int64_t lo4 = ql + head;
+        const int64_t n4 = (qh - lo4) / 4;
+        const float4* p4 = reinterpret_cast<const float4*>(v.val + lo4);
+        // the body: float4 (i, lane) holds components lo4 + 4 (i * 64 + lane) + c,
+        // index order i, lane, c
+        for (int64_t b0 = 0; b0 < n4; b0 += (int64_t)kWave * kSliceLoads4) {
+            float4 x[kSliceLoads4];
+#pragma unroll
+            for (int i = 0; i < kSliceLoads4; ++i) {
+                const int64_t q = b0 + i * kWave + lane;
+                x[i] = q < n4 ? p4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int i = 0; i < kSliceLoads4; ++i) {
+                const int64_t q = b0 + i * kWave + lane;
+                const bool in = q < n4;
+                const float xs[4] = {x[i].x, x[i].y, x[i].z, x[i].w};
+                uint32_t take = 0;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const uint32_t key = key_of(xs[c]);
+                    if (in) body(key);
+                    take |= (in && (key >> kShift1) >= prefix ? 1u : 0u) << c;
+                }
+                uint32_t tot;
+                const uint32_t pre = wave_prefix_small((uint32_t)__popc(take), &tot);
+                if (take) {
+                    int64_t o = ql + cnt + pre;
+                    const int64_t pos = lo4 + 4 * q;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        if ((take >> c) & 1u) {
+                            ci[o] = v.seg_lo + (int32_t)(pos + c);
+                            cv[o] = xs[c];
+                            ++o;
+                        }
+                    }
+                }
+                cnt += tot;
+            }
+        }
+        const int64_t t0 = lo4 + 4 * n4;
+        one(t0 + lane, t0 + lane < qh);
+        if (lane == 0)
+            s.sl_run[((size_t)id.k * g.n_slices + g.seg_slice_lo[id.seg] + id.w) * kWavesPerGroup + wave] = cnt;
+    } else if (PASS == 3 && collected) {
+        for (int q = 0; q < kWavesPerGroup; ++q)
+            for_slice<false>(collected_run(g, s, id.k, id.seg, id.w, W, q), [&](uint32_t key, int32_t) { body(key); });
+    } else if (v.idx == nullptr) {
+        for_slice_contig(v, body);
+    } else {
+        for_slice<false>(v, [&](uint32_t key, int32_t) { body(key); });
+    }
     __syncthreads();
     uint32_t* gh = s.hist + (size_t)id.p * kBins;
     uint32_t* gh2 = s.hist2 + (size_t)id.p * kBins;
@@ -1194,10 +1342,12 @@ __global__ __launch_bounds__(kGroup) void topk_count_kernel(StepArgs a, TopkGeom
     const uint32_t T = ps->T;
     const Slice v = open_slice(mode, ps->cand_used, id.k, id.seg, id.p, id.w, id.W, a, g, s);
     uint32_t above = 0, ties = 0;
-    for_slice<false>(v, [&](uint32_t key, int32_t) {
+    auto tally = [&](uint32_t key) {
         above += key > T;
         ties += key == T;
-    });
+    };
+    if (v.idx == nullptr) for_slice_contig(v, tally);
+    else for_slice<false>(v, [&](uint32_t key, int32_t) { tally(key); });
     for (int o = kWave / 2; o > 0; o >>= 1) {
         above += __shfl_down(above, o, kWave);
         ties += __shfl_down(ties, o, kWave);
@@ -1285,7 +1435,10 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
     float* vrow = val + (size_t)id.k * row_len + g.seg_out[id.seg];
     float* e = a.wp.e[id.k];
 
-    const Slice v = open_slice(mode, ps->cand_used, id.k, id.seg, id.p, id.w, id.W, a, g, s);
+    // a collected pair's slice spans the full-data slice; its input is the
+    // four runs the second pass gathered
+    const bool collected = mode == kModeCollected;
+    const Slice v = open_slice(collected ? 1 : mode, ps->cand_used, id.k, id.seg, id.p, id.w, id.W, a, g, s);
     // The server pass's row pointers: the slices' index spans [B(w), B(w+1))
     // tile the segment (B(0) its start, B(W) its end, B(w) the index of the
     // slice's first element), so each range start r*R of the segment lies in
@@ -1384,14 +1537,16 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
         }
         if (v.hi > v.lo) prev_last = seg_lo + v.hi - 1;
     }
-    for (int64_t s0 = v.lo; mode != 1 && s0 < v.hi; s0 += kEmitStage) {
-        const int32_t ns = (int32_t)(v.hi - s0 < kEmitStage ? v.hi - s0 : kEmitStage);
+    // the candidates (or a collected slice's runs), staged in rounds
+    auto emit_list = [&](const Slice& vl) {
+    for (int64_t s0 = vl.lo; s0 < vl.hi; s0 += kEmitStage) {
+        const int32_t ns = (int32_t)(vl.hi - s0 < kEmitStage ? vl.hi - s0 : kEmitStage);
 #pragma unroll
         for (int i = 0; i < kEmitLoads; ++i) {
             const int32_t q = i * kGroup + threadIdx.x;
             if (q < ns) {
-                st_val[stage_slot(q)] = v.val[s0 + q];
-                st_idx[stage_slot(q)] = v.idx ? v.idx[s0 + q] : v.seg_lo + (int32_t)(s0 + q);
+                st_val[stage_slot(q)] = vl.val[s0 + q];
+                st_idx[stage_slot(q)] = vl.idx ? vl.idx[s0 + q] : vl.seg_lo + (int32_t)(s0 + q);
             }
         }
         __syncthreads();
@@ -1466,6 +1621,12 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
         }
         prev_last = j_end;
         __syncthreads();  // the stage is read before the next round overwrites it
+    }
+    };
+    if (collected) {
+        for (int q = 0; q < kWavesPerGroup; ++q) emit_list(collected_run(g, s, id.k, id.seg, id.w, id.W, q));
+    } else if (mode != 1) {
+        emit_list(v);
     }
     // range starts after the slice's last element, up to the span's end
     const int32_t kept = (int32_t)(run_above + (uint32_t)((int64_t)run_ties < quota ? (int64_t)run_ties : quota));
