@@ -379,3 +379,22 @@ def test_iteration_with_non_finite_parameters():
     st = run_lockstep(Case(W("resnet18").shrunk(32, K=3), steps=4, iteration=True, sparse_w=True, w0_hook=poison,
                            label="iteration, non-finite w"))
     assert st["sparse_applies"] == 3, st
+
+
+@pytest.mark.parametrize("iteration", [True, False])
+def test_server_pass_ranges_beyond_the_wave_stage(iteration):
+    """Sparse messages on average, but clustered: the largest gradients all
+    sit in the first 12288 components, so the first three 4096-component
+    ranges hold every worker's whole message (thousands of entries, more
+    than the one-wavefront server pass stages) while the other ranges hold
+    none.  Those ranges take the block kernel after the one-wavefront pass;
+    every output against the oracle."""
+    wl = synth.Workload("clustered", [1 << 22], K=4, ratio=0.002, beta=0.9, eta=0.1, steps=4,
+                        compressor="topk", dist="normal")
+
+    def cluster(t, g):
+        g = g.copy()
+        g[:, :12288] *= np.float32(1000.0)
+        return g
+    run_lockstep(Case(wl, steps=4, grad_hook=cluster, iteration=iteration, fused_apply=not iteration,
+                      sparse_w=True, label="clustered messages"))
