@@ -342,13 +342,26 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
  *                              are bit for bit those of the dense path; other
  *                              calls, or other buffers, fall back to it.
  */
+/*
+ *   GMC_OPT_CHANGE_LIST        with GMC_OPT_SPARSE_MOMENTUM, top-s: the server
+ *                              pass also lists the components it changed and
+ *                              fl(w_{t+1} - w_t) there, and the next worker
+ *                              pass takes w_t - w_prev from that list instead
+ *                              of reading both parameter vectors at the marked
+ *                              cache lines.  0 (default): when the two vectors
+ *                              (8 d bytes) outgrow the 256 MB Infinity Cache;
+ *                              1: always; 2: never.  Results are the same bit
+ *                              for bit.  Setting it drops the recorded
+ *                              components, as GMC_OPT_SPARSE_MOMENTUM does.
+ */
 enum {
     GMC_OPT_FORCE_FULL_SELECT = 1,
     GMC_OPT_CAND_MARGIN = 2,
     GMC_OPT_CAND_CAP_MULT = 3,
     GMC_OPT_PROFILE = 4,
     GMC_OPT_SAMPLE_STRATUM = 5,
-    GMC_OPT_SPARSE_MOMENTUM = 6
+    GMC_OPT_SPARSE_MOMENTUM = 6,
+    GMC_OPT_CHANGE_LIST = 7
 };
 gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value);
 

@@ -63,6 +63,7 @@ struct gmc_ctx {
     int32_t stratum = 100;         // sampled-threshold top-s: components per sample stratum
     int sparse_w = 0;              // GMC_OPT_SPARSE_MOMENTUM
     bool seeded = false;           // the first step's thresholds were drawn from a sample
+    int change_list = 0;           // GMC_OPT_CHANGE_LIST: 0 by size, 1 always, 2 never
 
     // the last server pass's bitmap of changed components (sparse_w)
     uint32_t* wbits = nullptr;
@@ -92,6 +93,7 @@ struct gmc_ctx {
     TopkGeometry geo{};
     TopkScratch scr{};
     int32_t* rowptr = nullptr;
+    int2* dlist = nullptr;         // the last top-s server pass's change list (kDlistStride per range)
     int32_t n_ranges = 0;
     uint32_t* rbgs_bitmap = nullptr;
     int32_t* rbgs_blocks = nullptr;
@@ -189,6 +191,13 @@ int64_t count_for(int64_t n, const KeepRatio& r) {
         k = (int64_t)((prod + ceil_add) >> r.shift);
     }
     return std::max<int64_t>(1, std::min<int64_t>(k, n));
+}
+
+// top-s contexts whose parameter vectors outgrow the Infinity Cache keep the
+// server pass's change list for the next worker pass
+bool use_dlist(const gmc_ctx* ctx) {
+    if (ctx->comp == GMC_RBGS || ctx->dlist == nullptr || ctx->change_list == 2) return false;
+    return ctx->change_list == 1 || 8 * ctx->d > kDlistMinParamBytes;
 }
 
 void release(gmc_ctx* ctx) {
@@ -362,6 +371,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         add((size_t)K * nsl * kSlHist, 4);
         add((size_t)K * nsl * kWavesPerGroup, 4);
         add((size_t)K * (ctx->n_ranges + 1), 4);
+        add((size_t)ctx->n_ranges * kDlistStride, sizeof(int2));
         if (approx) add((size_t)K * samp_n, 4);
     }
     bytes += 256;
@@ -469,6 +479,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         sc.sl_run = cv.take<uint32_t>((size_t)K * nsl * kWavesPerGroup);
         sc.stats = ctx->stats;
         ctx->rowptr = cv.take<int32_t>((size_t)K * (ctx->n_ranges + 1));
+        ctx->dlist = cv.take<int2>((size_t)ctx->n_ranges * kDlistStride);
         sc.rowptr = ctx->rowptr;  // the emit kernel writes them for gmc_iteration's server pass
         sc.n_ranges = ctx->n_ranges;
         sc.samp = approx ? cv.take<float>((size_t)K * samp_n) : nullptr;
@@ -718,6 +729,9 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
                w_prev_dev == ctx->wbits_in)
                   ? ctx->wbits
                   : nullptr;
+    // the top-s worker pass takes w_t - w_prev from that pass's change list
+    // (written beside the bitmap) when it does not need w_t itself
+    a.dlist = (a.wbits && use_dlist(ctx) && !y_dev) ? ctx->dlist : nullptr;
     ctx->wbits_valid = false;
     ctx->wbits_used_t = a.wbits ? ctx->t : -1;
     // workgroup order: w read everywhere (dense momentum term or GMC+'s
@@ -726,7 +740,7 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
     // last server pass changed (at most K times a top-s message) reach 5% of d
     const int64_t per_worker = ctx->comp == GMC_TOPK_APPROX ? count_for(ctx->d, ctx->keep) : ctx->k_tot;
     const bool dense_marks = ctx->comp != GMC_RBGS && (int64_t)ctx->K * per_worker * 20 >= ctx->d;
-    a.run = (!a.wbits || y_dev) ? 2 : (dense_marks ? 0 : 1);
+    a.run = (!a.wbits || y_dev) ? 2 : ((dense_marks && !a.dlist) ? 0 : 1);
     if (a.wbits) ++ctx->sparse_steps;
     for (int k = 0; k < ctx->K; ++k) {
         if (!grads_dev[k] || !err_dev[k] || (y_dev && !y_dev[k]))
@@ -839,6 +853,7 @@ gmc_status aggregate_impl(gmc_ctx* ctx, const int32_t* idx_dev, const float* val
     // on the server (w_{t+1} differs from w_t everywhere there)
     const bool mark = ctx->sparse_w && f.w_in && f.w_out && f.w_in != f.w_out && ctx->rule != kRuleServerMomentum;
     f.wbits = mark ? ctx->wbits : nullptr;
+    f.dlist = (mark && use_dlist(ctx)) ? ctx->dlist : nullptr;
     // w_out is the last pass's input buffer and w_in its output, and the
     // worker pass in between read them through that pass's bitmap: w_out
     // still holds w_{t-1}, which equals w_t off the marks, and w_{t+1}
@@ -1063,6 +1078,13 @@ gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value) {
         case GMC_OPT_SPARSE_MOMENTUM:
             ctx->sparse_w = value ? 1 : 0;
             ctx->wbits_valid = false;
+            ctx->wbits_pair = false;
+            ctx->wbits_used_t = -1;
+            return GMC_OK;
+        case GMC_OPT_CHANGE_LIST:
+            if (value < 0 || value > 2) return fail(ctx, GMC_EINVAL, "gmc_set_option: change list must be 0, 1 or 2");
+            ctx->change_list = (int)value;
+            ctx->wbits_valid = false;  // the list of the last pass may not have been written
             ctx->wbits_pair = false;
             ctx->wbits_used_t = -1;
             return GMC_OK;

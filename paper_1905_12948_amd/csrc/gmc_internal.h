@@ -47,6 +47,18 @@ constexpr int kAggTopkStageSmall = 128;
 
 constexpr uint32_t kNoThreshold = 0xffffffffu;  // no speculative candidates
 
+// The components a top-s server pass changed, per range of kAggTopkRange:
+// a block of kDlistStride int2, [0] = {count, 0} (-1: more than the block
+// holds), then {offset in the range, bits of fl(w_{t+1} - w_t)} per changed
+// component, in no particular order.
+constexpr int kDlistStride = 512;
+constexpr int kDlistCap = kDlistStride - 1;
+// The list is kept when the two parameter vectors (8 d bytes) outgrow the
+// 256 MB Infinity Cache: below that, the worker pass's reads of w_t and w_prev
+// at the marked cache lines are served by that cache (and warm it for the
+// server pass), above it every XCD fetches them from HBM.
+constexpr int64_t kDlistMinParamBytes = int64_t(256) << 20;
+
 // A full-data pair whose first digit leaves few components at or above its
 // bin (at most 1/kCollectDiv of the segment) is "collected": the second pass
 // also gathers those components, in index order, into the pair's staging
@@ -199,6 +211,10 @@ struct StepArgs {
     // 1: the emit leaves the residual's zeros at the kept components to the
     // server pass that follows in the same call (FinishArgs::zero_e)
     int32_t defer_zero;
+    // nullable (with wbits, top-s): the previous server pass's list of the
+    // components it changed and by how much (FinishArgs::dlist); the vector
+    // worker pass then takes w_t - w_prev from it and reads neither buffer
+    const int2* dlist;
 };
 
 // The server pass after the sum over workers: update = -(s * sum), the
@@ -222,6 +238,9 @@ struct FinishArgs {
     // those marks: w_out is written only in the 32-component words where
     // the old marks or this pass's sent components fall
     int32_t sparse_apply;
+    // nullable (with wbits): the list of the components this pass changes
+    // and fl(w_{t+1} - w_t) there, kDlistStride int2 per range
+    int2* dlist;
     const float* e[kMaxWorkers];  // e_{t+1,k}
     float* y[kMaxWorkers];        // w_{t+1,k}
     // 1: e_{t+1,k}[j] = v - v (+0 for a finite v) for each entry (j, v) of

@@ -95,6 +95,20 @@ __device__ __forceinline__ float rule_u(float e, float g, float wt, float wp, fl
     return precompress(e, g, m);
 }
 
+// rule_u with w_t - w_prev given: diff = fl(w_t - w_prev), bit for bit the
+// same result.
+template <int kRule>
+__device__ __forceinline__ float rule_u_diff(float e, float g, float diff, float c, float h) {
+    if (kRule == kRuleServerMomentum) return e + g;
+    const float m = c * diff;
+    if (kRule == kRuleLrInResidual) {
+        const float sg = h * g;
+        const float acc = e + sg;
+        return acc - m;
+    }
+    return precompress(e, g, m);
+}
+
 __device__ __forceinline__ float rule_u_rt(int rule, float e, float g, float wt, float wp, float c, float h) {
     if (rule == kRuleServerMomentum) return rule_u<kRuleServerMomentum>(e, g, wt, wp, c, h);
     if (rule == kRuleLrInResidual) return rule_u<kRuleLrInResidual>(e, g, wt, wp, c, h);
@@ -269,7 +283,12 @@ template <int kRule, bool kDetach, bool kApprox>
 __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                                 uint64_t vec_mask) {
     __shared__ uint32_t wtot[2][kWavesPerGroup];
-    __shared__ int2 stage[kChunk];
+    __shared__ union {
+        int2 stage[kChunk];  // the chunk's candidates, in index order
+        float dl[kChunk];    // w_t - w_prev of the chunk's components (from the change list)
+    } sm;
+    __shared__ int32_t dl_cnt[2];
+    int2* const stage = sm.stage;
     int chunk, k;
     run_order(blockIdx.x, g.K, a.run, &chunk, &k);
     if (chunk >= g.n_chunks || !((vec_mask >> k) & 1ull)) return;  // padding, or the element-wise kernel's
@@ -290,23 +309,70 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
     float* ep = a.wp.e[k] + start + o0;
     const float* gp = a.wp.g[k] + start + o0;
     constexpr bool kNeedW = kRule != kRuleServerMomentum || kDetach;
+    // w_t - w_prev from the last server pass's change list (unless a range
+    // of the chunk overflowed its list): the chunk's changed components are
+    // scattered into LDS, every other one is exactly +0
+    bool use_list = !kDetach && kNeedW && a.dlist != nullptr;
     float4 u[2], gv[2], wt[2], wv[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         u[i] = ld4_stream(ep + i * (kGroup * 4));
         gv[i] = ld4_stream(gp + i * (kGroup * 4));
-        if (kNeedW)
-            load_w4<kDetach>(a, (int64_t)start + o0 + i * (kGroup * 4), &wt[i], &wv[i]);
-        else
-            wt[i] = wv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        wt[i] = wv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (kNeedW && !use_list) load_w4<kDetach>(a, (int64_t)start + o0 + i * (kGroup * 4), &wt[i], &wv[i]);
+    }
+    if (use_list) {
+        const int r0 = start / kAggTopkRange, nr = (start + len - 1) / kAggTopkRange - r0 + 1;  // 1 or 2 ranges
+        int2 head0 = make_int2(0, 0), head1 = make_int2(0, 0);
+        if ((int)threadIdx.x < kWave) {
+            head0 = a.dlist[(size_t)r0 * kDlistStride + threadIdx.x];
+            if (nr > 1) head1 = a.dlist[(size_t)(r0 + 1) * kDlistStride + threadIdx.x];
+        }
+#pragma unroll
+        for (int i = 0; i < kChunk / kGroup; ++i) sm.dl[i * kGroup + threadIdx.x] = 0.0f;
+        if (threadIdx.x == 0) {
+            dl_cnt[0] = head0.x;
+            dl_cnt[1] = nr > 1 ? head1.x : 0;
+        }
+        __syncthreads();
+        const int32_t n0 = dl_cnt[0], n1 = dl_cnt[1];
+        use_list = n0 >= 0 && n1 >= 0;
+        if (use_list) {
+            auto put = [&](int2 en, int rr) {
+                const int j = rr * kAggTopkRange + en.x;
+                if (j >= start && j < start + len) sm.dl[j - start] = __int_as_float(en.y);
+            };
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+                if (h2 >= nr) break;
+                const int32_t cnt = h2 ? n1 : n0;
+                if (threadIdx.x >= 1 && (int32_t)threadIdx.x <= cnt && (int)threadIdx.x < kWave)
+                    put(h2 ? head1 : head0, r0 + h2);
+                for (int32_t e2 = kWave + threadIdx.x; e2 <= cnt; e2 += kGroup)
+                    put(a.dlist[(size_t)(r0 + h2) * kDlistStride + e2], r0 + h2);
+            }
+        }
+        __syncthreads();
+        if (!use_list) {  // a range's list overflowed: the marks and the two parameter vectors
+#pragma unroll
+            for (int i = 0; i < 2; ++i) load_w4<kDetach>(a, (int64_t)start + o0 + i * (kGroup * 4), &wt[i], &wv[i]);
+        }
     }
     uint32_t flags = 0;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-        u[i].x = rule_u<kRule>(u[i].x, gv[i].x, wt[i].x, wv[i].x, c, h);
-        u[i].y = rule_u<kRule>(u[i].y, gv[i].y, wt[i].y, wv[i].y, c, h);
-        u[i].z = rule_u<kRule>(u[i].z, gv[i].z, wt[i].z, wv[i].z, c, h);
-        u[i].w = rule_u<kRule>(u[i].w, gv[i].w, wt[i].w, wv[i].w, c, h);
+        if (use_list) {
+            const float4 df = *reinterpret_cast<const float4*>(&sm.dl[o0 + i * (kGroup * 4)]);
+            u[i].x = rule_u_diff<kRule>(u[i].x, gv[i].x, df.x, c, h);
+            u[i].y = rule_u_diff<kRule>(u[i].y, gv[i].y, df.y, c, h);
+            u[i].z = rule_u_diff<kRule>(u[i].z, gv[i].z, df.z, c, h);
+            u[i].w = rule_u_diff<kRule>(u[i].w, gv[i].w, df.w, c, h);
+        } else {
+            u[i].x = rule_u<kRule>(u[i].x, gv[i].x, wt[i].x, wv[i].x, c, h);
+            u[i].y = rule_u<kRule>(u[i].y, gv[i].y, wt[i].y, wv[i].y, c, h);
+            u[i].z = rule_u<kRule>(u[i].z, gv[i].z, wt[i].z, wv[i].z, c, h);
+            u[i].w = rule_u<kRule>(u[i].w, gv[i].w, wt[i].w, wv[i].w, c, h);
+        }
         st4_stream(ep + i * (kGroup * 4), u[i]);
         if (kDetach) {
             const float q = a.q;
@@ -2150,8 +2216,16 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
     __shared__ float st_val[kStage];
     __shared__ int32_t src[kMaxWorkers];
     __shared__ int32_t pre[kMaxWorkers + 1];
+    __shared__ uint32_t dl_n;    // entries of the change list
     const int r = blockIdx.x;
     const int t = threadIdx.x;
+    // the change list of this range: the components this pass marks, with
+    // fl(w_{t+1} - w_t), for the next worker pass
+    int2* const dlr = (kApply && f.wbits && f.dlist) ? f.dlist + (size_t)r * kDlistStride : nullptr;
+    auto list_change = [&](int q, float wn, float x) {
+        const uint32_t pos = atomicAdd(&dl_n, 1u);
+        if (pos < (uint32_t)kDlistCap) dlr[1 + pos] = make_int2(q, __float_as_int(wn - x));
+    };
     const int64_t base = (int64_t)r * R;
     const int64_t n = (int64_t)d - base < R ? (int64_t)d - base : R;
     const int words = (int)((n + 31) / 32);
@@ -2170,6 +2244,7 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             if (f.w_prev) px[i] = ld4(f.w_prev + base + i * (kGroup * 4) + t * 4);
         }
     }
+    if (t == 0) dl_n = 0u;
     if (t < NW) {
         hb[t] = 0u;
         wb[t] = 0u;
@@ -2186,7 +2261,10 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
     // a sparse apply's range with no old marks and no entries changes
     // nothing: w_out holds w_{t-1}, equal to w_t = w_{t+1} there, and its
     // marks stay clear
-    if (sparse && !marked && f.update == nullptr && !__syncthreads_or(t < K && pre[t + 1] > 0)) return;
+    if (sparse && !marked && f.update == nullptr && !__syncthreads_or(t < K && pre[t + 1] > 0)) {
+        if (dlr && t == 0) dlr[0] = make_int2(0, 0);
+        return;
+    }
     for (int q = t; q < R; q += kGroup) acc[q] = 0.0f;
     // sparse apply: w_t is fetched only in the 32-component words the
     // output changes: those of the previous pass's marks now, those of this
@@ -2289,8 +2367,12 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
         __syncthreads();
     }
     if (vec) {
+        uint32_t lm[V];  // the change list: marked components of each float4 and their changes
+        float4 ld[V];
 #pragma unroll
         for (int i = 0; i < V; ++i) {
+            lm[i] = 0u;
+            ld[i] = make_float4(0.f, 0.f, 0.f, 0.f);
             const int q = i * (kGroup * 4) + t * 4;
             const float4 dl = make_float4(-(s * acc[q]), -(s * acc[q + 1]), -(s * acc[q + 2]), -(s * acc[q + 3]));
             if (f.update) st4(f.update + base + q, dl);
@@ -2308,6 +2390,38 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
                     const uint32_t m = ((hb[q >> 5] >> (q & 31)) & 0xfu) | not_finite(nx.x) | (not_finite(nx.y) << 1) |
                                        (not_finite(nx.z) << 2) | (not_finite(nx.w) << 3);
                     atomicOr(&wb[q >> 5], m << (q & 31));
+                    lm[i] = m;
+                    ld[i] = make_float4(nx.x - x.x, nx.y - x.y, nx.z - x.z, nx.w - x.w);
+                }
+            }
+        }
+        if (dlr) {
+            // one LDS atomic per wavefront for the list positions: the
+            // wavefront's prefix of its threads' marked components
+            uint32_t mine = 0;
+#pragma unroll
+            for (int i = 0; i < V; ++i) mine += (uint32_t)__popc(lm[i]);
+            const int lane = t & (kWave - 1);
+            uint32_t incl = mine;
+#pragma unroll
+            for (int o = 1; o < kWave; o <<= 1) {
+                const uint32_t y = __shfl_up(incl, o, kWave);
+                if (lane >= o) incl += y;
+            }
+            const uint32_t wtotal = __shfl(incl, kWave - 1, kWave);
+            uint32_t wbase = 0;
+            if (lane == kWave - 1 && wtotal) wbase = atomicAdd(&dl_n, wtotal);
+            uint32_t pos = __shfl(wbase, kWave - 1, kWave) + incl - mine;
+#pragma unroll
+            for (int i = 0; i < V; ++i) {
+                const int q = i * (kGroup * 4) + t * 4;
+                const float dv[4] = {ld[i].x, ld[i].y, ld[i].z, ld[i].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if ((lm[i] >> e) & 1u) {
+                        if (pos < (uint32_t)kDlistCap) dlr[1 + pos] = make_int2(q + e, __float_as_int(dv[e]));
+                        ++pos;
+                    }
                 }
             }
         }
@@ -2317,16 +2431,20 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
             const float dl = -(s * acc[q]);
             if (f.update) f.update[j] = dl;
             if (kApply && (!sparse || wv[q >> 5])) {
-                const float wn = next_w(f.w_in[j], dl, f.w_prev, j, f.b);
+                const float x = f.w_in[j];
+                const float wn = next_w(x, dl, f.w_prev, j, f.b);
                 f.w_out[j] = wn;
-                if (f.wbits && (((hb[q >> 5] >> (q & 31)) & 1u) || not_finite(wn)))
+                if (f.wbits && (((hb[q >> 5] >> (q & 31)) & 1u) || not_finite(wn))) {
                     atomicOr(&wb[q >> 5], 1u << (q & 31));
+                    if (dlr) list_change(q, wn, x);
+                }
             }
         }
     }
     if (kApply && f.wbits) {
         __syncthreads();
         if (t < words) f.wbits[(base >> 5) + t] = wb[t];
+        if (dlr && t == 0) dlr[0] = make_int2(dl_n <= (uint32_t)kDlistCap ? (int32_t)dl_n : -1, 0);
     }
     if (kApply && f.detach) {
         // GMC+: the detached points at the sent components, from w_{t+1}

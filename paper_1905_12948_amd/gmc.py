@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libgmc.so")
 GMC_TOPK_GLOBAL, GMC_TOPK_SEGMENTED, GMC_RBGS, GMC_TOPK_APPROX = 0, 1, 2, 3
 GMC_OK, GMC_EINVAL, GMC_ENOMEM, GMC_EDEVICE, GMC_ESTATE = 0, -1, -2, -3, -4
 GMC_OPT_FORCE_FULL_SELECT, GMC_OPT_CAND_MARGIN, GMC_OPT_CAND_CAP_MULT, GMC_OPT_PROFILE = 1, 2, 3, 4
-GMC_OPT_SAMPLE_STRATUM, GMC_OPT_SPARSE_MOMENTUM = 5, 6
+GMC_OPT_SAMPLE_STRATUM, GMC_OPT_SPARSE_MOMENTUM, GMC_OPT_CHANGE_LIST = 5, 6, 7
 MAX_WORKERS = 64
 STAGES = ("fused_vec", "fused_gen", "select", "emit", "aggregate", "apply")
 

@@ -15,6 +15,7 @@ from gpu_harness import Case, run_lockstep
 pytestmark = pytest.mark.gpu
 
 OPT_FULL, OPT_MARGIN, OPT_CAP = 1, 2, 3
+OPT_LIST = 7     # GMC_OPT_CHANGE_LIST
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -398,3 +399,37 @@ def test_server_pass_ranges_beyond_the_wave_stage(iteration):
         return g
     run_lockstep(Case(wl, steps=4, grad_hook=cluster, iteration=iteration, fused_apply=not iteration,
                       sparse_w=True, label="clustered messages"))
+
+
+@pytest.mark.parametrize("name,shrink,K,extra", [
+    ("resnet18", 16, 4, {}), ("resnet50", 32, 16, {}), ("gpt2", 64, 3, {}), ("resnet50_approx", 64, 4, {}),
+    ("resnet18", 16, 4, {"rule": "lr_in_residual"}), ("resnet18", 32, 3, {"row_pad": 1}),
+    ("resnet18", 16, 8, {})])
+def test_change_list_is_bitwise_the_dense_path(name, shrink, K, extra):
+    """The worker pass's momentum term from the server pass's change list
+    (forced on at these sizes), with gmc_iteration and with
+    gmc_aggregate_apply: every output against the oracle."""
+    for iteration in (True, False):
+        st = run_lockstep(Case(W(name).shrunk(shrink, K=K), steps=5, iteration=iteration, fused_apply=not iteration,
+                               sparse_w=True, options=((OPT_LIST, 1),), label="change list/" + name, **extra))
+        assert st["sparse_momentum_steps"] == 4 and st["sparse_applies"] == 4, st
+
+
+def test_change_list_overflow_and_non_finite():
+    """Change lists that overflow (the clustered ranges send every component)
+    and non-finite parameters (listed with w_t - w_t = NaN): the worker pass
+    takes the marks and the parameter vectors for those ranges."""
+    wl = synth.Workload("clustered", [1 << 22], K=4, ratio=0.002, beta=0.9, eta=0.1, steps=4,
+                        compressor="topk", dist="normal")
+
+    def cluster(t, g):
+        g = g.copy()
+        g[:, :12288] *= np.float32(1000.0)
+        return g
+
+    def poison(w0):
+        w0 = w0.copy()
+        w0[[5, 777, 4096, 9000, 3 << 20]] = [np.inf, -np.inf, np.nan, np.inf, np.nan]
+        return w0
+    run_lockstep(Case(wl, steps=4, grad_hook=cluster, iteration=True, sparse_w=True, w0_hook=poison,
+                      options=((OPT_LIST, 1),), label="change list, clustered + non-finite"))
