@@ -226,16 +226,15 @@ struct Carver {
 // Host-side tables of the top-s geometry.
 struct TopkTables {
     std::vector<int32_t> seg_start, seg_out;
-    std::vector<int32_t> chunk_start, chunk_len, chunk_seg;
+    std::vector<int32_t> chunk_start, chunk_len, chunk_seg, chunk_cgrp;
     std::vector<int32_t> cgrp_lo, cgrp_hi, cgrp_seg, cgrp_rank, seg_cgrp_lo, seg_cgrps;
     std::vector<int32_t> slice_seg, slice_rank, seg_slices, seg_slice_lo;
     std::vector<int32_t> pair_k, pair_cap;
     std::vector<int64_t> pair_cand;
     std::vector<int2> tile_map;       // per worker: launched tile -> (segment, first tile in the segment)
-    std::vector<int32_t> seg_tile_stride, seg_tile_cap_off;
+    std::vector<int32_t> seg_tile_stride;
     std::vector<int2> seed_map;       // first-step sample: (segment, first run) per workgroup
     std::vector<int32_t> seg_seed_groups, seg_seed_runs, seg_seed_rank;
-    int32_t tiles_cap = 0;            // tile-list entries per worker
     int64_t cand_total = 0;
 };
 
@@ -271,6 +270,8 @@ TopkTables build_tables(const gmc_ctx* ctx) {
         T.seg_cgrp_lo.push_back((int32_t)T.cgrp_lo.size());
         int32_t rank = 0;
         for (int32_t c = first_chunk; c < last_chunk; c += kCompactChunks) {
+            for (int32_t c2 = c; c2 < std::min(c + kCompactChunks, last_chunk); ++c2)
+                T.chunk_cgrp.push_back((int32_t)T.cgrp_lo.size());
             T.cgrp_lo.push_back(c);
             T.cgrp_hi.push_back(std::min(c + kCompactChunks, last_chunk));
             T.cgrp_seg.push_back(sg);
@@ -292,8 +293,6 @@ TopkTables build_tables(const gmc_ctx* ctx) {
         out += ctx->seg_k[sg];
         // copy tiles: a list of c candidates takes at most c/kTile whole
         // tiles plus a partial one per group
-        T.seg_tile_cap_off.push_back(T.tiles_cap);
-        T.tiles_cap += (int32_t)((cap + kTile - 1) / kTile + rank);
         const int64_t nlaunch = (lc + kTile - 1) / kTile + rank;
         T.seg_tile_stride.push_back((int32_t)nlaunch);
         for (int64_t i = 0; i < nlaunch; ++i) T.tile_map.push_back(make_int2(sg, (int)i));
@@ -354,17 +353,16 @@ gmc_status prepare(gmc_ctx* ctx) {
         const size_t nc = T.chunk_start.size(), ng = T.cgrp_lo.size(), nsl = T.slice_seg.size();
         const size_t ns = T.seg_out.size(), np = (size_t)K * ns;
         add(ns + 1, 4); add(ns, 4);
-        add(nc, 4); add(nc, 4); add(nc, 4);
+        add(nc, 4); add(nc, 4); add(nc, 4); add(nc, 4);
         add(ng, 4); add(ng, 4); add(ng, 4); add(ng, 4); add(ns, 4); add(ns, 4);
         add(nsl, 4); add(nsl, 4); add(ns, 4); add(ns, 4);
         add(np, 4); add(np, 4); add(np, 8);
-        add(T.tile_map.size(), sizeof(int2)); add(ns, 4); add(ns, 4);
+        add(T.tile_map.size(), sizeof(int2)); add(ns, 4);
         add(T.seed_map.size() + 1, sizeof(int2)); add(ns, 4); add(ns, 4); add(ns, 4);
-        add((size_t)K * ng, 4); add((size_t)K * T.tiles_cap, sizeof(int2));
         add(np, sizeof(PairState));
         add(np * kBins, 4);
         add(np * kBins, 4);
-        add((size_t)K * nc, 4); add((size_t)K * nc, 4); add((size_t)K * ng, 4);
+        add((size_t)K * nc, 4); add((size_t)2 * K * ng, 4);
         add((size_t)K * nc * kChunk, sizeof(int2));
         add((size_t)T.cand_total, 4); add((size_t)T.cand_total, 4);
         for (int q = 0; q < 4; ++q) add((size_t)K * nsl, 4);
@@ -423,6 +421,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         GMC_TRY(put(T.chunk_start, &g.chunk_start));
         GMC_TRY(put(T.chunk_len, &g.chunk_len));
         GMC_TRY(put(T.chunk_seg, &g.chunk_seg));
+        GMC_TRY(put(T.chunk_cgrp, &g.chunk_cgrp));
         GMC_TRY(put(T.cgrp_lo, &g.cgrp_lo));
         GMC_TRY(put(T.cgrp_hi, &g.cgrp_hi));
         GMC_TRY(put(T.cgrp_seg, &g.cgrp_seg));
@@ -443,8 +442,6 @@ gmc_status prepare(gmc_ctx* ctx) {
         g.tile_map = tm;
         g.tiles_per_worker = (int32_t)T.tile_map.size();
         GMC_TRY(put(T.seg_tile_stride, &g.seg_tile_stride));
-        g.tiles_cap_per_worker = T.tiles_cap;
-        GMC_TRY(put(T.seg_tile_cap_off, &g.seg_tile_cap_off));
         int2* sm = cv.take<int2>(T.seed_map.size() + 1);
         if (!T.seed_map.empty())
             GMC_HIP(ctx, hipMemcpy(sm, T.seed_map.data(), T.seed_map.size() * sizeof(int2), hipMemcpyHostToDevice));
@@ -453,8 +450,6 @@ gmc_status prepare(gmc_ctx* ctx) {
         GMC_TRY(put(T.seg_seed_groups, &g.seg_seed_groups));
         GMC_TRY(put(T.seg_seed_runs, &g.seg_seed_runs));
         GMC_TRY(put(T.seg_seed_rank, &g.seg_seed_rank));
-        ctx->scr.grp_base = cv.take<uint32_t>((size_t)K * ng);
-        ctx->scr.tiles = cv.take<int2>((size_t)K * T.tiles_cap);
         TopkScratch& sc = ctx->scr;
         sc.pair = cv.take<PairState>(np);
         std::vector<PairState> init(np);
@@ -466,8 +461,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         sc.hist = cv.take<uint32_t>(np * kBins);
         sc.hist2 = cv.take<uint32_t>(np * kBins);
         sc.run_cnt = cv.take<uint32_t>((size_t)K * nc);
-        sc.run_pre = cv.take<uint32_t>((size_t)K * nc);
-        sc.grp_total = cv.take<uint32_t>((size_t)K * ng);
+        sc.grp_acc = cv.take<uint32_t>((size_t)2 * K * ng);
         sc.slot = cv.take<int2>((size_t)K * nc * kChunk);
         sc.cand_idx = cv.take<int32_t>((size_t)T.cand_total);
         sc.cand_val = cv.take<float>((size_t)T.cand_total);

@@ -91,7 +91,7 @@ struct WorkerPtrs {
 // Per (worker, segment) pair state, kept in device memory across kernels.
 struct PairState {
     uint32_t tau;       // candidate threshold key of the next fused pass
-    uint32_t cand;      // candidates appended by the fused pass (atomic)
+    uint32_t unused0;
     int32_t mode;       // 0 = resolve from candidates, 1 = full data, 3 = full data collected
                         // by the second pass (kModeCollected)
     uint32_t prefix;    // radix digits fixed so far
@@ -101,8 +101,7 @@ struct PairState {
     uint32_t done;      // finished workgroups of the current kernel
     uint32_t cand_used; // candidates of this step (cand is reset for the next)
     uint32_t tau_used;  // the candidate threshold this step's fused pass used
-    uint32_t n_tiles;   // copy tiles of this step's candidate list (0: not copied)
-    uint32_t fuse1;     // 1: the copy also does the first histogram pass (else its own workgroups)
+    uint32_t unused1, unused2;
     // exact top-s: the first pass puts the next step's threshold at the floor
     // of the 11-bit bin tau_bin holding the key of rank margin*k/4; with
     // tau_fine the second pass narrows it to the floor of the 22-bit bin
@@ -125,6 +124,7 @@ struct TopkGeometry {
     const int32_t* chunk_start;   // [n_chunks]
     const int32_t* chunk_len;     // [n_chunks]
     const int32_t* chunk_seg;     // [n_chunks]
+    const int32_t* chunk_cgrp;    // [n_chunks] compaction group of the chunk
     const int32_t* cgrp_lo;       // [n_cgroups] first chunk of the group
     const int32_t* cgrp_hi;       // [n_cgroups] one past its last chunk
     const int32_t* cgrp_seg;      // [n_cgroups] its segment
@@ -138,17 +138,14 @@ struct TopkGeometry {
     const int32_t* pair_k;        // [K*n_seg]
     const int32_t* pair_cap;      // [K*n_seg]
     const int64_t* pair_cand;     // [K*n_seg] start of the pair's candidate list
-    // copy tiles.  Layout: a worker's tile list (s.tiles) has room for
-    // tiles_cap_per_worker entries, segment seg's from seg_tile_cap_off[seg]
-    // (enough for a full candidate list).  Launch: tiles_per_worker
-    // workgroups per worker; workgroup tt takes segment tile_map[tt].x's
-    // tiles tile_map[tt].y, + seg_tile_stride[seg], ... (the launch is sized
-    // for the usual candidate count, the stride covers longer lists)
+    // copy tiles (kTile candidates of one compaction group; a group's tiles
+    // follow the groups before it).  Launch: tiles_per_worker workgroups per
+    // worker; workgroup tt takes segment tile_map[tt].x's tiles
+    // tile_map[tt].y, + seg_tile_stride[seg], ... (the launch is sized for
+    // the usual candidate count, the stride covers longer lists)
     int32_t tiles_per_worker;
     const int2* tile_map;             // [tiles_per_worker]
     const int32_t* seg_tile_stride;   // [n_seg] workgroups launched per (worker, segment)
-    int32_t tiles_cap_per_worker;
-    const int32_t* seg_tile_cap_off;  // [n_seg]
     // first-step sample: workgroup g of a worker takes segment seed_map[g].x's
     // runs seed_map[g].y, +1, ... (kSeedRunsPerGroup of them, fewer at the
     // segment's end); seg_seed_groups[seg] workgroups per (worker, segment),
@@ -166,10 +163,10 @@ struct TopkScratch {
     uint32_t* hist;               // [K*n_seg][kBins]
     uint32_t* hist2;              // [K*n_seg][kBins] second-digit histogram of the threshold's bin
     uint32_t* run_cnt;            // [K*n_chunks] candidates of (worker, chunk)
-    uint32_t* run_pre;            // [K*n_chunks] exclusive prefix of run_cnt within the group
-    uint32_t* grp_total;          // [K*n_cgroups]
-    uint32_t* grp_base;           // [K*n_cgroups] the group's first position in the pair's list
-    int2* tiles;                  // [K*tiles_cap_per_worker] (group rank in the segment, tile in the group)
+    // [2][K*n_cgroups] candidates of (worker, compaction group), added up by
+    // the fused pass of the steps of each parity of t; the emit of the step
+    // clears its half for the step after next
+    uint32_t* grp_acc;
     int2* slot;                   // [K*n_chunks][kChunk] candidates of (worker, chunk) in index
                                   // order: (index, bit pattern of u)
     int32_t* cand_idx;            // [sum cap] candidate lists, ascending index

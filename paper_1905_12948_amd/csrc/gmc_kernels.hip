@@ -417,7 +417,11 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
 #pragma unroll
         for (int w = 0; w < kWavesPerGroup; ++w) total += wtot[i][w];
     }
-    if (threadIdx.x == 0) s.run_cnt[run_slot] = total;
+    if (threadIdx.x == 0) {
+        s.run_cnt[run_slot] = total;
+        const int cg = one ? chunk / kCompactChunks : g.chunk_cgrp[chunk];
+        atomicAdd(&s.grp_acc[(size_t)(a.t & 1) * g.K * g.n_cgroups + (size_t)k * g.n_cgroups + cg], total);
+    }
     // gather the candidates in LDS, then write the slot with consecutive
     // threads on consecutive entries (a few whole lines instead of one
     // partial line per candidate)
@@ -483,7 +487,12 @@ __device__ void fused_chunk_wave(const StepArgs& a, const TopkGeometry& g, const
         }
         base += popc64(b);
     }
-    if (lane == 0) s.run_cnt[run_slot] = base;
+    if (lane == 0) {
+        s.run_cnt[run_slot] = base;
+        if (base)
+            atomicAdd(&s.grp_acc[(size_t)(a.t & 1) * g.K * g.n_cgroups + (size_t)k * g.n_cgroups + g.chunk_cgrp[chunk]],
+                      base);
+    }
 }
 
 // The element-wise kernel: one wavefront per (chunk, worker) for the workers
@@ -953,7 +962,6 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
             ps->tau_need = want - ab2;
             ps->mode = mode;
             ps->cand_used = cand;
-            ps->cand = 0u;  // every workgroup of the pair has read it
             if (!approx) {
                 atomicAdd((unsigned long long*)&s.stats[mode == 0 ? 1 : 2], 1ull);
                 if (mode == 0) atomicAdd((unsigned long long*)&s.stats[3], (unsigned long long)cand);
@@ -1007,6 +1015,19 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
     }
 }
 
+// The candidates the fused pass collected for pair (k, seg): the sum of its
+// compaction groups' totals (grp_acc of the step's parity).
+__device__ uint32_t pair_candidates(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int k, int seg,
+                                    uint32_t* sh_wsum) {
+    const uint32_t* ga = s.grp_acc + (size_t)(a.t & 1) * g.K * g.n_cgroups + (size_t)k * g.n_cgroups + g.seg_cgrp_lo[seg];
+    const int ng = g.seg_cgrps[seg];
+    uint32_t mine = 0;
+    for (int r = threadIdx.x; r < ng; r += kGroup) mine += ga[r];
+    uint32_t all;
+    block_scan_excl(mine, &all, sh_wsum);
+    return all;
+}
+
 // The third pass of exact top-s also takes the count of the kept components
 // per slice: each workgroup stores its slice's count above T's 22-bit bin and
 // the suffix sums of its 512-bin histogram of that bin (sl_hist, kSlHist
@@ -1025,11 +1046,13 @@ __device__ void hist_pass(const StepArgs& a, const TopkGeometry& g, const TopkSc
 
     const SliceId id = slice_id(g, blk);
     PairState* ps = &s.pair[id.p];
-    if (PASS == 1 && ps->fuse1) return;  // the compaction copy takes this pass
     // sampled-threshold top-s: the passes select over the sample, rank samp_r
     const bool approx = g.approx != 0;
     const int kp = approx ? g.samp_r : g.pair_k[id.p];
-    const uint32_t cand = PASS == 1 ? ps->cand : ps->cand_used;
+    const uint32_t cand = PASS == 1 ? pair_candidates(a, g, s, id.k, id.seg, sh_wsum) : ps->cand_used;
+    // the compaction copy takes the first pass of the exact top-s pairs that
+    // resolve from their candidates
+    if (PASS == 1 && !approx && !force_full && cand >= (uint32_t)kp && cand <= (uint32_t)g.pair_cap[id.p]) return;
     const int mode = approx      ? 2
                      : PASS == 1 ? ((force_full || cand < (uint32_t)kp || cand > (uint32_t)g.pair_cap[id.p]) ? 1 : 0)
                                  : ps->mode;
@@ -1218,113 +1241,101 @@ hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g, 
 // compaction of the candidates
 // ----------------------------------------------------------------------------
 
-// First half, one workgroup per (worker, compaction group): the exclusive
-// prefix of the group's run counts and the group's total.  The last
-// workgroup of each (worker, segment) then scans the segment's group totals
-// (each group's base in the pair's list, the pair's count), decides whether
-// the list is copied (at most the capacity) and whether the copy also takes
-// the first histogram pass (exact top-s resolving from its candidates), and
-// lays out the copy tiles.
-__global__ __launch_bounds__(kGroup) void topk_compact_count_kernel(TopkGeometry g, TopkScratch s, int force_full) {
-    static_assert(kCompactChunks == kGroup, "one chunk per thread");
-    __shared__ uint32_t wsum[kWavesPerGroup];
-    __shared__ uint32_t carry[2];
-    __shared__ int sh_last;
-    const int k = blockIdx.x / g.n_cgroups;
-    const int cg = blockIdx.x % g.n_cgroups;
-    const int clo = g.cgrp_lo[cg], nch = g.cgrp_hi[cg] - clo;
-    const size_t slot0 = (size_t)k * g.n_chunks + clo;
-    const uint32_t cnt = threadIdx.x < nch ? s.run_cnt[slot0 + threadIdx.x] : 0u;
-    uint32_t total;
-    const uint32_t pre = block_scan_excl(cnt, &total, wsum);
-    if (threadIdx.x < nch) s.run_pre[slot0 + threadIdx.x] = pre;
-    if (threadIdx.x == 0) store_agent(&s.grp_total[(size_t)k * g.n_cgroups + cg], total);
-    const int seg = g.cgrp_seg[cg];
-    const int p = k * g.n_seg + seg;
-    PairState* ps = &s.pair[p];
-    const int ng = g.seg_cgrps[seg];
-    if (!finish_slice(&ps->done, ng, &sh_last)) return;
+// The pair's candidates go, tile by tile (kTile candidates of one compaction
+// group each, the groups in index order), to the pair's list, so the list
+// comes out in ascending index order.  The tiles are laid out from the
+// groups' totals (grp_acc): group r holds ceil(total_r / kTile) tiles, its
+// candidates go to the list at the totals of the groups before it, and within
+// the group each chunk's candidates at the counts of the chunks before it.
+// Workgroup (worker, tile_map entry (seg, i)) takes the pair's tiles i, i +
+// stride, ... (stride = the workgroups launched for the pair, sized for the
+// usual count).  For the pairs of exact top-s that resolve from their
+// candidates the copy also histograms the first digit, and the last of the
+// pair's workgroups picks it (the first histogram pass then skips the pair).
+constexpr int kMaxCopyTiles = 256;  // tiles of one workgroup (at most about cap_mult / 8 + 2)
 
-    // last workgroup of the pair
-    const size_t grp0 = (size_t)k * g.n_cgroups + g.seg_cgrp_lo[seg];
-    if (threadIdx.x == 0) carry[0] = 0u;
-    __syncthreads();
-    for (int r0 = 0; r0 < ng; r0 += kGroup) {
-        const int r = r0 + threadIdx.x;
-        const uint32_t t = r < ng ? load_agent(&s.grp_total[grp0 + r]) : 0u;
-        uint32_t tot;
-        const uint32_t ex = block_scan_excl(t, &tot, wsum);
-        if (r < ng) s.grp_base[grp0 + r] = carry[0] + ex;
-        __syncthreads();
-        if (threadIdx.x == 0) carry[0] += tot;
-        __syncthreads();
-    }
-    const uint32_t all = carry[0];
-    const bool copy = all <= (uint32_t)g.pair_cap[p];
-    const bool fuse = !g.approx && !force_full && copy && all >= (uint32_t)g.pair_k[p];
-    int2* tl = s.tiles + (size_t)k * g.tiles_cap_per_worker + g.seg_tile_cap_off[seg];
-    if (threadIdx.x == 0) carry[1] = 0u;
-    __syncthreads();
-    for (int r0 = 0; r0 < ng; r0 += kGroup) {
-        const int r = r0 + threadIdx.x;
-        const uint32_t t = r < ng && copy ? load_agent(&s.grp_total[grp0 + r]) : 0u;
-        const uint32_t nt = (t + kTile - 1) / kTile;
-        uint32_t tot;
-        const uint32_t ex = carry[1] + block_scan_excl(nt, &tot, wsum);
-        for (uint32_t i = 0; i < nt; ++i) tl[ex + i] = make_int2(r, (int)i);
-        __syncthreads();
-        if (threadIdx.x == 0) carry[1] += tot;
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) {
-        ps->cand = all;
-        ps->n_tiles = carry[1];
-        ps->fuse1 = fuse ? 1u : 0u;
-        store_agent(&ps->done, 0u);
-    }
-}
-
-// Second half: the pair's candidates go, tile by tile (kTile candidates of
-// one group each), to the pair's list at their group's base, so the list
-// comes out in ascending index order.  Workgroup (worker, tile_map entry
-// (seg, i)) takes the pair's tiles i, i + stride, ... (stride = the
-// workgroups launched for the pair, sized for the usual count).  For the
-// pairs of exact top-s that resolve from their candidates the copy also
-// histograms the first digit, and the last of the pair's workgroups picks it
-// (the first histogram kernel then skips the pair).
-__device__ void compact_copy(const TopkGeometry& g, const TopkScratch& s, int margin, int blk) {
+__device__ void compact_copy(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int force_full, int margin,
+                             int blk) {
     __shared__ uint32_t pre[kCompactChunks];
     __shared__ uint32_t h[kBins];
     __shared__ uint32_t sh_wsum[kWavesPerGroup];
     __shared__ int sh_res[2];
     __shared__ int sh_last;
+    __shared__ uint32_t carry[2];
+    __shared__ int32_t my_grp[kMaxCopyTiles];     // this workgroup's m-th tile: its group,
+    __shared__ uint32_t my_base[kMaxCopyTiles];   // the group's first position in the list,
+    __shared__ uint32_t my_tot[kMaxCopyTiles];    // the group's candidates,
+    __shared__ uint32_t my_tile[kMaxCopyTiles];   // the tile within the group
+    static_assert(kCompactChunks == kGroup, "one chunk per thread");
     const int k = blk / g.tiles_per_worker;
     const int2 tm = g.tile_map[blk % g.tiles_per_worker];
     const int seg = tm.x;
     const int p = k * g.n_seg + seg;
     PairState* ps = &s.pair[p];
-    const uint32_t n_tiles = ps->n_tiles;
-    if ((uint32_t)tm.y >= n_tiles) return;
+    const uint32_t i0 = (uint32_t)tm.y;
     const uint32_t stride = (uint32_t)g.seg_tile_stride[seg];
+    // the pair's groups: totals, list bases and tiles, in blocks of kGroup
+    const uint32_t* ga = s.grp_acc + (size_t)(a.t & 1) * g.K * g.n_cgroups + (size_t)k * g.n_cgroups;
+    const int g0 = g.seg_cgrp_lo[seg], ng = g.seg_cgrps[seg];
+    if (threadIdx.x == 0) {
+        carry[0] = 0u;  // candidates before the block
+        carry[1] = 0u;  // tiles before the block
+    }
+    __syncthreads();
+    for (int r0 = 0; r0 < ng; r0 += kGroup) {
+        const int r = r0 + (int)threadIdx.x;
+        const uint32_t tot = r < ng ? ga[g0 + r] : 0u;
+        const uint32_t nt = (tot + kTile - 1) / kTile;
+        uint32_t bt, btt;
+        const uint32_t base = carry[0] + block_scan_excl(tot, &bt, sh_wsum);
+        const uint32_t tp = carry[1] + block_scan_excl(nt, &btt, sh_wsum);
+        // this workgroup's tiles i0 + m stride that fall in [tp, tp + nt)
+        if (nt) {
+            uint32_t tt = i0 >= tp ? i0 : i0 + (tp - i0 + stride - 1) / stride * stride;
+            for (; tt < tp + nt; tt += stride) {
+                const uint32_t m = (tt - i0) / stride;
+                if (m < (uint32_t)kMaxCopyTiles) {
+                    my_grp[m] = g0 + r;
+                    my_base[m] = base;
+                    my_tot[m] = tot;
+                    my_tile[m] = tt - tp;
+                }
+            }
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            carry[0] += bt;
+            carry[1] += btt;
+        }
+        __syncthreads();
+    }
+    const uint32_t all = carry[0];
+    const bool copy = all <= (uint32_t)g.pair_cap[p];
+    const uint32_t n_tiles = copy ? carry[1] : 0u;
+    if (i0 >= n_tiles) return;
     const uint32_t n_wg = n_tiles < stride ? n_tiles : stride;  // workgroups of the pair with tiles
-    const bool fuse = ps->fuse1 != 0u;
+    const uint32_t n_my = (n_tiles - i0 + stride - 1) / stride;
+    const bool fuse = !g.approx && !force_full && all >= (uint32_t)g.pair_k[p];
     if (fuse)
         for (int b = threadIdx.x; b < kBins; b += kGroup) h[b] = 0u;
-    const int2* tl = s.tiles + (size_t)k * g.tiles_cap_per_worker + g.seg_tile_cap_off[seg];
     int32_t* ci0 = s.cand_idx + g.pair_cand[p];
     float* cv0 = s.cand_val + g.pair_cand[p];
-    for (uint32_t tt = (uint32_t)tm.y; tt < n_tiles; tt += stride) {
-        const int2 te = tl[tt];
-        const int cg = g.seg_cgrp_lo[seg] + te.x;
+    for (uint32_t m = 0; m < n_my && m < (uint32_t)kMaxCopyTiles; ++m) {
+        const int cg = my_grp[m];
         const int clo = g.cgrp_lo[cg], nch = g.cgrp_hi[cg] - clo;
-        const size_t gi = (size_t)k * g.n_cgroups + cg;
-        const uint32_t total = s.grp_total[gi], base = s.grp_base[gi];
-        const uint32_t lo = (uint32_t)te.y * kTile;
-        const uint32_t hi = lo + kTile < total ? lo + kTile : total;
+        const uint32_t base = my_base[m];
         const size_t slot0 = (size_t)k * g.n_chunks + clo;
-        __syncthreads();  // the previous tile's searches are done with pre
-        if (threadIdx.x < nch) pre[threadIdx.x] = s.run_pre[slot0 + threadIdx.x];
+        // each chunk's first position within the group
+        const uint32_t cnt = (int)threadIdx.x < nch ? s.run_cnt[slot0 + threadIdx.x] : 0u;
+        uint32_t gt;
+        const uint32_t cpre = block_scan_excl(cnt, &gt, sh_wsum);
+        if ((int)threadIdx.x < nch) pre[threadIdx.x] = cpre;
         __syncthreads();
+        // the group's candidates are its chunks' runs (equal to its total,
+        // which only decided the layout)
+        const uint32_t total = my_tot[m] < gt ? my_tot[m] : gt;
+        const uint32_t lo = my_tile[m] * kTile;
+        const uint32_t hi = lo + kTile < total ? lo + kTile : total;
         int32_t* ci = ci0 + base;
         float* cv = cv0 + base;
         int32_t jv[8];
@@ -1354,6 +1365,7 @@ __device__ void compact_copy(const TopkGeometry& g, const TopkScratch& s, int ma
                 if (fuse) atomicAdd(&h[key_of(xv[i]) >> kShift1], 1u);
             }
         }
+        __syncthreads();  // the searches are done with pre before the next tile's scan
     }
     if (!fuse) return;
     __syncthreads();
@@ -1362,8 +1374,7 @@ __device__ void compact_copy(const TopkGeometry& g, const TopkScratch& s, int ma
     for (int b = threadIdx.x; !solo && b < kBins; b += kGroup)
         if (h[b]) atomicAdd(&gh[b], h[b]);
     if (!finish_slice(&ps->done, (int)n_wg, &sh_last)) return;
-    const uint32_t cand = ps->cand;
-    finish_digit<1>(ps, p, h, gh, g.pair_k[p], 0, cand, 0u, margin, 0, false, g, s, sh_wsum, sh_res, nullptr,
+    finish_digit<1>(ps, p, h, gh, g.pair_k[p], 0, all, 0u, margin, 0, false, g, s, sh_wsum, sh_res, nullptr,
                     nullptr, nullptr, nullptr, solo);
 }
 
@@ -1371,21 +1382,18 @@ __device__ void compact_copy(const TopkGeometry& g, const TopkScratch& s, int ma
 // K * tiles_per_worker workgroups copy (with the first pass of the pairs that
 // resolve from their candidates), the K * n_slices after them take the first
 // pass of the others (full data, or the sample of the sampled-threshold
-// top-s); which pairs those are the count kernel decided (PairState::fuse1).
+// top-s); both decide which pairs those are from the groups' totals.
 __global__ __launch_bounds__(kGroup) void topk_copy_pass1_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
                                                                  int force_full, int margin) {
     const int n_copy = g.K * g.tiles_per_worker;
     if ((int)blockIdx.x < n_copy)
-        compact_copy(g, s, margin, blockIdx.x);
+        compact_copy(a, g, s, force_full, margin, blockIdx.x);
     else
         hist_pass<1>(a, g, s, force_full, margin, nullptr, 0, (int)blockIdx.x - n_copy);
 }
 
 hipError_t launch_topk_compact(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int force_full,
                                int margin, hipStream_t st) {
-    hipLaunchKernelGGL(topk_compact_count_kernel, dim3(g.K * g.n_cgroups), dim3(kGroup), 0, st, g, s, force_full);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
     const int64_t grid = (int64_t)g.K * g.tiles_per_worker + (int64_t)g.K * g.n_slices;
     hipLaunchKernelGGL(topk_copy_pass1_kernel, dim3((unsigned)grid), dim3(kGroup), 0, st, a, g, s, force_full, margin);
     return hipGetLastError();
@@ -1484,6 +1492,13 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
     float* const st_val = lds.st.val;
     __shared__ uint32_t sh_wsum[kWavesPerGroup];
 
+    // this step's group totals have been read (the copy and the first pass):
+    // clear them for the step after next, which adds into the same half
+    {
+        const size_t nz = (size_t)g.K * g.n_cgroups;
+        uint32_t* z = s.grp_acc + (size_t)(a.t & 1) * nz;
+        for (size_t i = (size_t)blockIdx.x * kGroup + threadIdx.x; i < nz; i += (size_t)gridDim.x * kGroup) z[i] = 0u;
+    }
     const SliceId id = slice_id(g, blockIdx.x);
     const PairState* ps = &s.pair[id.p];
     const int mode = ps->mode;
