@@ -200,7 +200,7 @@ def main():
     ap.add_argument("--workload", default="resnet50", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--grad-batches", type=int, default=4)
     ap.add_argument("--margin", type=int, default=None,
-                    help="rank of the speculative threshold in quarters of k (default 6)")
+                    help="rank of the speculative threshold in quarters of k (default 4)")
     ap.add_argument("--lam", type=float, default=None,
                     help="GMC+ detach coefficient (default 0.5 for the rbgs workload, else 0: plain GMC)")
     ap.add_argument("--dense-momentum", action="store_true",
@@ -208,6 +208,8 @@ def main():
     ap.add_argument("--cpu-workers", type=int, default=2)
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--change-list", type=int, default=None, choices=(0, 1, 2),
+                    help="GMC_OPT_CHANGE_LIST: 0 by size (default), 1 always, 2 never")
     ap.add_argument("--force-full", action="store_true",
                     help="every top-s selection of the timed steps on the full-data path (GMC_OPT_FORCE_FULL_SELECT), "
                          "to profile the fallback path")
@@ -242,6 +244,9 @@ def main():
     if args.force_full:
         from paper_1905_12948_amd import GMC_OPT_FORCE_FULL_SELECT
         gm.set_option(GMC_OPT_FORCE_FULL_SELECT, 1)
+    if args.change_list is not None:
+        from paper_1905_12948_amd import GMC_OPT_CHANGE_LIST
+        gm.set_option(GMC_OPT_CHANGE_LIST, args.change_list)
     # the bench keeps w untouched between the server pass and the next worker
     # pass and swaps the two buffers, as the sparse momentum term requires
     sparse_w = not args.dense_momentum

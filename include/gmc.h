@@ -305,10 +305,10 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
  *   GMC_OPT_FORCE_FULL_SELECT  1: every top-s selection takes the full-data
  *                              path (no speculative candidates)
  *   GMC_OPT_CAND_MARGIN        rank of the next step's speculative threshold,
- *                              in quarters of k (4..4096; default 6: the
+ *                              in quarters of k (4..4096; default 4: the
  *                              threshold sits at the floor of the 22-bit key
- *                              bin holding this step's key of rank 1.5 k, and
- *                              the residual's growth brings about 2.5-3.5 k
+ *                              bin holding this step's key of rank k, and
+ *                              the residual's growth brings about 1.3-2 k
  *                              candidates the next step)
  *   GMC_OPT_CAND_CAP_MULT      candidate capacity as a multiple of k (>= 1);
  *                              reallocates scratch; before the first step

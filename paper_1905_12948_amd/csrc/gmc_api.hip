@@ -58,7 +58,7 @@ struct gmc_ctx {
     std::vector<int64_t> seg_off;  // top-s segments (host)
     int32_t block = 4096;          // RBGS block length
     int force_full = 0;
-    int margin = 6;                // speculative threshold rank, quarters of k (1.5 k)
+    int margin = 4;                // speculative threshold rank, quarters of k (k)
     int cap_mult = 64;
     int32_t stratum = 100;         // sampled-threshold top-s: components per sample stratum
     int sparse_w = 0;              // GMC_OPT_SPARSE_MOMENTUM
