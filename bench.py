@@ -309,8 +309,9 @@ def main():
     # iteration 0 on its own: a fresh context of the same configuration
     # (every kernel is loaded by now, and the context allocates its scratch
     # when it is created, before the timed call) takes one step from e = 0
-    # and w_t = w_{t-1}, with no previous threshold, so every selection takes
-    # the full-data path
+    # and w_t = w_{t-1}, with no previous threshold: the seed kernel's
+    # threshold from a strided sample of u stands in for it, and only a
+    # selection whose candidates miss the count takes the full-data path
     g0 = Gmc(d, K, wl.compressor, wl.ratio, wl.beta, wl.eta, seed=wl.seed, segments=seg,
              block=wl.block if wl.compressor == "rbgs" else None, lam=lam)
     if sparse_w:

@@ -279,7 +279,6 @@ TopkTables build_tables(const gmc_ctx* ctx) {
         }
         T.seg_cgrps.push_back(rank);
         // slices of the selection passes
-        const int64_t cap = pair_capacity(ctx, n, ctx->seg_k[sg]);
         const int64_t lc = pair_launch(ctx, n, ctx->seg_k[sg]);
         int64_t w = std::max((n + kSliceElems - 1) / kSliceElems, (lc + kSliceCands - 1) / kSliceCands);
         w = std::max<int64_t>(1, std::min<int64_t>(w, kMaxSlices));
@@ -362,7 +361,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         add(np, sizeof(PairState));
         add(np * kBins, 4);
         add(np * kBins, 4);
-        add((size_t)K * nc, 4); add((size_t)2 * K * ng, 4);
+        add((size_t)K * nc, 4); add((size_t)2 * kGrpSub * K * ng, 4);
         add((size_t)K * nc * kChunk, sizeof(int2));
         add((size_t)T.cand_total, 4); add((size_t)T.cand_total, 4);
         for (int q = 0; q < 4; ++q) add((size_t)K * nsl, 4);
@@ -461,7 +460,7 @@ gmc_status prepare(gmc_ctx* ctx) {
         sc.hist = cv.take<uint32_t>(np * kBins);
         sc.hist2 = cv.take<uint32_t>(np * kBins);
         sc.run_cnt = cv.take<uint32_t>((size_t)K * nc);
-        sc.grp_acc = cv.take<uint32_t>((size_t)2 * K * ng);
+        sc.grp_acc = cv.take<uint32_t>((size_t)2 * kGrpSub * K * ng);
         sc.slot = cv.take<int2>((size_t)K * nc * kChunk);
         sc.cand_idx = cv.take<int32_t>((size_t)T.cand_total);
         sc.cand_val = cv.take<float>((size_t)T.cand_total);

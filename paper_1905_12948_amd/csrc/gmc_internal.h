@@ -25,6 +25,11 @@ constexpr int kChunk = kWave * 4 * kVecIters;   // 2048 elements
 // read the list (or, on the full-data path, the segment's u) as "slices":
 // seg_slices even shares, one workgroup each.
 constexpr int kCompactChunks = 256;        // chunks per compaction group (one per thread)
+// Each group's total is kept as kGrpSub sub-totals, chunk c adding into
+// c % kGrpSub: the device-scope adds of a group's chunks then spread over
+// that many addresses (with only a few groups, a small workload's adds all
+// met on a handful of words and stretched its worker pass).
+constexpr int kGrpSub = 16;
 constexpr int kTile = kGroup * 8;          // candidates one copy workgroup moves
 constexpr int64_t kSliceElems = 1 << 19;   // full-data elements per slice (at most)
 constexpr int64_t kSliceCands = 8192;      // usual candidates per slice (more when a list runs long)
@@ -163,9 +168,10 @@ struct TopkScratch {
     uint32_t* hist;               // [K*n_seg][kBins]
     uint32_t* hist2;              // [K*n_seg][kBins] second-digit histogram of the threshold's bin
     uint32_t* run_cnt;            // [K*n_chunks] candidates of (worker, chunk)
-    // [2][K*n_cgroups] candidates of (worker, compaction group), added up by
-    // the fused pass of the steps of each parity of t; the emit of the step
-    // clears its half for the step after next
+    // [2][kGrpSub][K*n_cgroups] candidates of (worker, compaction group),
+    // added up by the fused pass of the steps of each parity of t, chunk c
+    // into sub-total c % kGrpSub (grp_slot); the emit of the step clears its
+    // half for the step after next
     uint32_t* grp_acc;
     int2* slot;                   // [K*n_chunks][kChunk] candidates of (worker, chunk) in index
                                   // order: (index, bit pattern of u)

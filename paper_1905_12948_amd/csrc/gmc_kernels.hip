@@ -73,6 +73,25 @@ __device__ __forceinline__ bool aligned16(const void* p) {
     return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
 }
 
+// The sub-total of (worker k, compaction group cg) that chunk adds into, in
+// the half of grp_acc of the parity of t.
+__device__ __forceinline__ uint32_t* grp_slot(const TopkScratch& s, const TopkGeometry& g, uint64_t t, int k, int cg,
+                                              int chunk) {
+    const size_t nz = (size_t)g.K * g.n_cgroups;
+    return s.grp_acc + ((size_t)(t & 1) * kGrpSub + (size_t)(chunk % kGrpSub)) * nz + (size_t)k * g.n_cgroups + cg;
+}
+
+// The candidates of (worker k, compaction group cg) of the step of t: the sum
+// of the group's sub-totals.
+__device__ __forceinline__ uint32_t grp_total(const TopkScratch& s, const TopkGeometry& g, uint64_t t, int k, int cg) {
+    const size_t nz = (size_t)g.K * g.n_cgroups;
+    const uint32_t* p = s.grp_acc + (size_t)(t & 1) * kGrpSub * nz + (size_t)k * g.n_cgroups + cg;
+    uint32_t v = 0;
+#pragma unroll
+    for (int i = 0; i < kGrpSub; ++i) v += p[(size_t)i * nz];
+    return v;
+}
+
 // u = (e + g) - m, two roundings, in this order.
 __device__ __forceinline__ float precompress(float e, float g, float m) {
     const float acc = e + g;
@@ -420,7 +439,7 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
     if (threadIdx.x == 0) {
         s.run_cnt[run_slot] = total;
         const int cg = one ? chunk / kCompactChunks : g.chunk_cgrp[chunk];
-        atomicAdd(&s.grp_acc[(size_t)(a.t & 1) * g.K * g.n_cgroups + (size_t)k * g.n_cgroups + cg], total);
+        atomicAdd(grp_slot(s, g, a.t, k, cg, chunk), total);
     }
     // gather the candidates in LDS, then write the slot with consecutive
     // threads on consecutive entries (a few whole lines instead of one
@@ -490,8 +509,7 @@ __device__ void fused_chunk_wave(const StepArgs& a, const TopkGeometry& g, const
     if (lane == 0) {
         s.run_cnt[run_slot] = base;
         if (base)
-            atomicAdd(&s.grp_acc[(size_t)(a.t & 1) * g.K * g.n_cgroups + (size_t)k * g.n_cgroups + g.chunk_cgrp[chunk]],
-                      base);
+            atomicAdd(grp_slot(s, g, a.t, k, g.chunk_cgrp[chunk], chunk), base);
     }
 }
 
@@ -1019,10 +1037,9 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
 // compaction groups' totals (grp_acc of the step's parity).
 __device__ uint32_t pair_candidates(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int k, int seg,
                                     uint32_t* sh_wsum) {
-    const uint32_t* ga = s.grp_acc + (size_t)(a.t & 1) * g.K * g.n_cgroups + (size_t)k * g.n_cgroups + g.seg_cgrp_lo[seg];
-    const int ng = g.seg_cgrps[seg];
+    const int g0 = g.seg_cgrp_lo[seg], ng = g.seg_cgrps[seg];
     uint32_t mine = 0;
-    for (int r = threadIdx.x; r < ng; r += kGroup) mine += ga[r];
+    for (int r = threadIdx.x; r < ng; r += kGroup) mine += grp_total(s, g, a.t, k, g0 + r);
     uint32_t all;
     block_scan_excl(mine, &all, sh_wsum);
     return all;
@@ -1275,7 +1292,6 @@ __device__ void compact_copy(const StepArgs& a, const TopkGeometry& g, const Top
     const uint32_t i0 = (uint32_t)tm.y;
     const uint32_t stride = (uint32_t)g.seg_tile_stride[seg];
     // the pair's groups: totals, list bases and tiles, in blocks of kGroup
-    const uint32_t* ga = s.grp_acc + (size_t)(a.t & 1) * g.K * g.n_cgroups + (size_t)k * g.n_cgroups;
     const int g0 = g.seg_cgrp_lo[seg], ng = g.seg_cgrps[seg];
     if (threadIdx.x == 0) {
         carry[0] = 0u;  // candidates before the block
@@ -1284,7 +1300,7 @@ __device__ void compact_copy(const StepArgs& a, const TopkGeometry& g, const Top
     __syncthreads();
     for (int r0 = 0; r0 < ng; r0 += kGroup) {
         const int r = r0 + (int)threadIdx.x;
-        const uint32_t tot = r < ng ? ga[g0 + r] : 0u;
+        const uint32_t tot = r < ng ? grp_total(s, g, a.t, k, g0 + r) : 0u;
         const uint32_t nt = (tot + kTile - 1) / kTile;
         uint32_t bt, btt;
         const uint32_t base = carry[0] + block_scan_excl(tot, &bt, sh_wsum);
@@ -1495,7 +1511,7 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
     // this step's group totals have been read (the copy and the first pass):
     // clear them for the step after next, which adds into the same half
     {
-        const size_t nz = (size_t)g.K * g.n_cgroups;
+        const size_t nz = (size_t)kGrpSub * g.K * g.n_cgroups;
         uint32_t* z = s.grp_acc + (size_t)(a.t & 1) * nz;
         for (size_t i = (size_t)blockIdx.x * kGroup + threadIdx.x; i < nz; i += (size_t)gridDim.x * kGroup) z[i] = 0u;
     }
