@@ -210,6 +210,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--change-list", type=int, default=None, choices=(0, 1, 2),
                     help="GMC_OPT_CHANGE_LIST: 0 by size (default), 1 always, 2 never")
+    ap.add_argument("--in-place", action="store_true",
+                    help="one parameter buffer updated in place (gmc_iteration_inplace; GMC_OPT_CHANGE_LIST 3): "
+                         "top-s only")
     ap.add_argument("--force-full", action="store_true",
                     help="every top-s selection of the timed steps on the full-data path (GMC_OPT_FORCE_FULL_SELECT), "
                          "to profile the fallback path")
@@ -244,9 +247,12 @@ def main():
     if args.force_full:
         from paper_1905_12948_amd import GMC_OPT_FORCE_FULL_SELECT
         gm.set_option(GMC_OPT_FORCE_FULL_SELECT, 1)
-    if args.change_list is not None:
+    if args.in_place and (wl.compressor == "rbgs" or args.dense_momentum or lam):
+        print("--in-place is for top-s with the sparse momentum term and no detached points", file=sys.stderr)
+        sys.exit(2)
+    if args.change_list is not None or args.in_place:
         from paper_1905_12948_amd import GMC_OPT_CHANGE_LIST
-        gm.set_option(GMC_OPT_CHANGE_LIST, args.change_list)
+        gm.set_option(GMC_OPT_CHANGE_LIST, 3 if args.in_place else args.change_list)
     # the bench keeps w untouched between the server pass and the next worker
     # pass and swaps the two buffers, as the sparse momentum term requires
     sparse_w = not args.dense_momentum
@@ -274,7 +280,9 @@ def main():
 
     def one_step():
         cur, prev = bufs[step_no[0] % 2], bufs[(step_no[0] + 1) % 2]
-        if detach:
+        if args.in_place:  # one buffer: w_{t+1} over w_t, w_{t-1} kept as the change list
+            gm.iteration_inplace(w, w if step_no[0] == 0 else None, G[step_no[0] % len(G)], err, idx, val, ln)
+        elif detach:
             gm.step(cur, prev, G[step_no[0] % len(G)], err, idx, val, ln, w_k=wk)
             gm.finish(idx, val, ln, cur, prev, err=err, w_k=wk)
         else:  # worker and server pass in one call: w_{t+1} over w_{t-1}'s buffer
@@ -401,7 +409,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": DESCRIPTIONS[wl.name], "d": d, "K": K, "compressor": wl.compressor,
                    "ratio": wl.ratio, "lambda": lam, "message_len": msg_len, "grad_batches": len(G),
-                   "sparse_momentum": sparse_w, "forced_full_data": bool(args.force_full)},
+                   "sparse_momentum": sparse_w, "forced_full_data": bool(args.force_full),
+                   "in_place": bool(args.in_place)},
         # the step's algorithmic bytes with dense parameter traffic (12 B per
         # worker-element, 16 B per element, 16 B per message entry) over
         # 8 TB/s; the sparse accounting (parameters moved only where they

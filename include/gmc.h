@@ -159,7 +159,15 @@ int64_t gmc_count(int64_t n, double ratio);
 /*
  * One worker-side pass of Algorithm 1 for all K workers at step t, then
  * t <- t + 1.
- *   w_t_dev, w_prev_dev   [d] fp32: w_t and w_{t-1}; read only
+ *   w_t_dev, w_prev_dev   [d] fp32: w_t and w_{t-1}; read only.  w_prev_dev
+ *                         may be NULL right after a top-s server pass that
+ *                         updated w_t_dev in place and kept its changes
+ *                         (GMC_OPT_SPARSE_MOMENTUM with GMC_OPT_CHANGE_LIST
+ *                         3): w_t - w_{t-1} is then that pass's exact
+ *                         fl(w_{t+1} - w_t), bit for bit what the two
+ *                         vectors give; GMC_ESTATE otherwise (no such pass,
+ *                         or its record was dropped), and not with
+ *                         gmc_step_detach
  *   grads_dev             host array of K device pointers, each [d] fp32:
  *                         g_{t,k}; read only
  *   err_dev               host array of K device pointers, each [d] fp32:
@@ -172,8 +180,9 @@ int64_t gmc_count(int64_t n, double ratio);
  *   msg_len_dev           [K] int64 out: values written per worker (k_tot,
  *                         RBGS: n_sel blocks' worth, sampled-threshold
  *                         top-s: the number kept)
- * Device buffers must not overlap each other.  Pointers that are not 16-byte
- * aligned are accepted (slower path).  w is never written.
+ * Device buffers must not overlap each other, except that w_t_dev and
+ * w_prev_dev may be one buffer (w_{-1} = w_0 at t = 0).  Pointers that are not
+ * 16-byte aligned are accepted (slower path).  w is never written.
  */
 gmc_status gmc_step(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev,
                     const float* const* grads_dev, float* const* err_dev,
@@ -196,7 +205,9 @@ gmc_status gmc_aggregate(gmc_ctx* ctx, const int32_t* idx_dev, const float* val_
  * gmc_aggregate computes it,
  *   w_out_dev[j] = w_dev[j] + update[j]   for every j in [0, d),
  * and update_dev[j] = update[j] when update_dev is not NULL.  w_out_dev may
- * equal w_dev (in place); otherwise the two must not overlap.  Out of place
+ * equal w_dev (in place: for top-s under GMC_OPT_SPARSE_MOMENTUM with
+ * GMC_OPT_CHANGE_LIST 3 the pass keeps its changes, and the next gmc_step
+ * passes w_prev = NULL); otherwise the two must not overlap.  Out of place
  * the caller keeps w_{t+1} in w_out_dev and w_t in w_dev, i.e. swaps the
  * roles of its two parameter buffers for the next gmc_step instead of
  * copying w into w_prev.  update_dev may not alias either.  Not with
@@ -290,6 +301,31 @@ gmc_status gmc_iteration(gmc_ctx* ctx, const float* w_t_dev, float* w_prev_io_de
                          float* const* err_dev, int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev);
 
 /*
+ * One whole iteration of Algorithm 1 with the parameters updated in place
+ * (one buffer instead of two): gmc_step(w, w_prev, ...) and then the server
+ * pass w <- w + update.  The workers' momentum term needs w_t - w_{t-1},
+ * which the in-place pass keeps as its change list (every component it
+ * changed, with fl(w_{t+1} - w_t)), so the next iteration passes
+ * w_prev_dev = NULL.  Top-s (global, segmented or sampled threshold) under
+ * GMC_RULE_GMC or GMC_RULE_LR_IN_RESIDUAL, with GMC_OPT_SPARSE_MOMENTUM and
+ * GMC_OPT_CHANGE_LIST 3 (GMC_EINVAL otherwise).  Results equal gmc_iteration's
+ * bit for bit.  The server pass then writes w only in the 32-component words
+ * of the components sent now, where an out-of-place pass also rewrites those
+ * the previous pass changed.
+ *   w_dev       [d] fp32: w_t in, w_{t+1} out
+ *   w_prev_dev  [d] fp32 w_{t-1}, read only; NULL after an in-place
+ *               iteration whose record stands (GMC_ESTATE if it was dropped:
+ *               gmc_set_step, the options that drop the recorded
+ *               components, gmc_apply).  At t = 0 pass w_dev (w_{-1} = w_0).
+ * A caller that saves a run to resume it exactly keeps w_{t-1} as well (for
+ * example by running the last iteration before the save out of place, with
+ * gmc_iteration); a resumed context starts with w_prev_dev = w_{t-1}.
+ * The remaining arguments are gmc_step's.
+ */
+gmc_status gmc_iteration_inplace(gmc_ctx* ctx, float* w_dev, const float* w_prev_dev, const float* const* grads_dev,
+                                 float* const* err_dev, int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev);
+
+/*
  * GMC+'s detached points as one dense pass (Algorithm 2, detach):
  * w_k_dev[k][j] = w_dev[j] - q err_dev[k][j] for every worker and component,
  * with w_dev = w_{t+1} and err = e_{t+1,k}; any rule.
@@ -340,7 +376,10 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
  *                              where it differs from w_{t-1} (the recorded
  *                              components and the ones sent now).  Results
  *                              are bit for bit those of the dense path; other
- *                              calls, or other buffers, fall back to it.
+ *                              calls, or other buffers, fall back to it.  A
+ *                              server pass in place records its changes only
+ *                              with GMC_OPT_CHANGE_LIST 3 (gmc_step with
+ *                              w_prev = NULL, gmc_iteration_inplace).
  */
 /*
  *   GMC_OPT_CHANGE_LIST        with GMC_OPT_SPARSE_MOMENTUM, top-s: the server
@@ -350,9 +389,18 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
  *                              of reading both parameter vectors at the marked
  *                              cache lines.  0 (default): when the two vectors
  *                              (8 d bytes) outgrow the 256 MB Infinity Cache;
- *                              1: always; 2: never.  Results are the same bit
- *                              for bit.  Setting it drops the recorded
- *                              components, as GMC_OPT_SPARSE_MOMENTUM does.
+ *                              1: always; 2: never; 3: always, with room for
+ *                              every component of each 4096-component range
+ *                              (8 d bytes of scratch instead of d bytes), so
+ *                              that a server pass in place (gmc_aggregate_apply
+ *                              or gmc_finish with w_out = w,
+ *                              gmc_iteration_inplace) keeps its changes too
+ *                              and the next gmc_step may pass w_prev = NULL.
+ *                              Results are the same bit for bit.  Setting it
+ *                              drops the recorded components, as
+ *                              GMC_OPT_SPARSE_MOMENTUM does; setting or
+ *                              clearing 3 reallocates scratch and is allowed
+ *                              before the first step only (GMC_ESTATE).
  */
 enum {
     GMC_OPT_FORCE_FULL_SELECT = 1,

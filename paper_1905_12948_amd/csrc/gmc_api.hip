@@ -63,7 +63,12 @@ struct gmc_ctx {
     int32_t stratum = 100;         // sampled-threshold top-s: components per sample stratum
     int sparse_w = 0;              // GMC_OPT_SPARSE_MOMENTUM
     bool seeded = false;           // the first step's thresholds were drawn from a sample
-    int change_list = 0;           // GMC_OPT_CHANGE_LIST: 0 by size, 1 always, 2 never
+    int change_list = 0;           // GMC_OPT_CHANGE_LIST: 0 by size, 1 always, 2 never, 3 whole ranges
+    int32_t dl_stride = kDlistStride;  // int2 per range of the change list (kDlistStrideFull with 3)
+    // device word: the epoch of the last pass that wrote a non-finite w; the
+    // record of a pass counts while it equals nf_epoch (bumped to drop it)
+    int32_t* nf = nullptr;
+    int32_t nf_epoch = 1;
 
     // the last server pass's bitmap of changed components (sparse_w)
     uint32_t* wbits = nullptr;
@@ -93,7 +98,7 @@ struct gmc_ctx {
     TopkGeometry geo{};
     TopkScratch scr{};
     int32_t* rowptr = nullptr;
-    int2* dlist = nullptr;         // the last top-s server pass's change list (kDlistStride per range)
+    int2* dlist = nullptr;         // the last top-s server pass's change list (dl_stride per range)
     int32_t n_ranges = 0;
     uint32_t* rbgs_bitmap = nullptr;
     int32_t* rbgs_blocks = nullptr;
@@ -197,7 +202,17 @@ int64_t count_for(int64_t n, const KeepRatio& r) {
 // server pass's change list for the next worker pass
 bool use_dlist(const gmc_ctx* ctx) {
     if (ctx->comp == GMC_RBGS || ctx->dlist == nullptr || ctx->change_list == 2) return false;
-    return ctx->change_list == 1 || 8 * ctx->d > kDlistMinParamBytes;
+    return ctx->change_list == 1 || ctx->change_list == 3 || 8 * ctx->d > kDlistMinParamBytes;
+}
+
+// Drops the record of the last server pass's changes (bitmap, change list
+// and the non-finite flag): the next worker pass reads w densely and the
+// next server pass writes w everywhere.
+void drop_record(gmc_ctx* ctx) {
+    ctx->wbits_valid = false;
+    ctx->wbits_pair = false;
+    ctx->wbits_used_t = -1;
+    ctx->nf_epoch += 1;
 }
 
 void release(gmc_ctx* ctx) {
@@ -368,7 +383,8 @@ gmc_status prepare(gmc_ctx* ctx) {
         add((size_t)K * nsl * kSlHist, 4);
         add((size_t)K * nsl * kWavesPerGroup, 4);
         add((size_t)K * (ctx->n_ranges + 1), 4);
-        add((size_t)ctx->n_ranges * kDlistStride, sizeof(int2));
+        add((size_t)ctx->n_ranges * ctx->dl_stride, sizeof(int2));
+        add(1, 4);
         if (approx) add((size_t)K * samp_n, 4);
     }
     bytes += 256;
@@ -472,7 +488,8 @@ gmc_status prepare(gmc_ctx* ctx) {
         sc.sl_run = cv.take<uint32_t>((size_t)K * nsl * kWavesPerGroup);
         sc.stats = ctx->stats;
         ctx->rowptr = cv.take<int32_t>((size_t)K * (ctx->n_ranges + 1));
-        ctx->dlist = cv.take<int2>((size_t)ctx->n_ranges * kDlistStride);
+        ctx->dlist = cv.take<int2>((size_t)ctx->n_ranges * ctx->dl_stride);
+        ctx->nf = cv.take<int32_t>(1);
         sc.rowptr = ctx->rowptr;  // the emit kernel writes them for gmc_iteration's server pass
         sc.n_ranges = ctx->n_ranges;
         sc.samp = approx ? cv.take<float>((size_t)K * samp_n) : nullptr;
@@ -717,14 +734,19 @@ gmc_status step_impl(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev
     a.seed = ctx->seed;
     a.t = (uint64_t)ctx->t;
     // w_t - w_prev is +0 outside the bitmap when w_t, w_prev are the last
-    // server pass's output and input and no step ran since
-    a.wbits = (ctx->sparse_w && ctx->wbits_valid && ctx->wbits_t == ctx->t && w_t_dev == ctx->wbits_out &&
-               w_prev_dev == ctx->wbits_in)
-                  ? ctx->wbits
-                  : nullptr;
+    // server pass's output and input and no step ran since; after a pass in
+    // place (output = input) the caller passes w_prev = NULL instead
+    const bool rec = ctx->sparse_w && ctx->wbits_valid && ctx->wbits_t == ctx->t && w_t_dev == ctx->wbits_out;
+    const bool rec_inplace = rec && ctx->wbits_in == ctx->wbits_out;
+    a.wbits = (rec && (rec_inplace ? w_prev_dev == nullptr : w_prev_dev == ctx->wbits_in)) ? ctx->wbits : nullptr;
     // the top-s worker pass takes w_t - w_prev from that pass's change list
     // (written beside the bitmap) when it does not need w_t itself
     a.dlist = (a.wbits && use_dlist(ctx) && !y_dev) ? ctx->dlist : nullptr;
+    a.dl_stride = ctx->dl_stride;
+    if (!w_prev_dev && !(a.dlist && ctx->dl_stride == kDlistStrideFull && ctx->comp != GMC_RBGS && !y_dev))
+        return fail(ctx, GMC_ESTATE,
+                    "gmc_step: w_prev may be NULL only right after a server pass that updated w_t in place and "
+                    "listed its changes (GMC_OPT_SPARSE_MOMENTUM with GMC_OPT_CHANGE_LIST 3)");
     ctx->wbits_valid = false;
     ctx->wbits_used_t = a.wbits ? ctx->t : -1;
     // workgroup order: w read everywhere (dense momentum term or GMC+'s
@@ -811,7 +833,7 @@ extern "C" {
 gmc_status gmc_step(gmc_ctx* ctx, const float* w_t_dev, const float* w_prev_dev, const float* const* grads_dev,
                     float* const* err_dev, int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev) {
     if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_step: ctx is NULL");
-    if (!w_t_dev || !w_prev_dev || !grads_dev || !err_dev || !idx_dev || !val_dev || !msg_len_dev)
+    if (!w_t_dev || !grads_dev || !err_dev || !idx_dev || !val_dev || !msg_len_dev)
         return fail(ctx, GMC_EINVAL, "gmc_step: NULL argument");
     return step_impl(ctx, w_t_dev, w_prev_dev, grads_dev, err_dev, nullptr, idx_dev, val_dev, msg_len_dev);
 }
@@ -842,19 +864,27 @@ gmc_status aggregate_impl(gmc_ctx* ctx, const int32_t* idx_dev, const float* val
     f.s = ctx->s;
     f.b = ctx->b;
     f.q = ctx->q;
-    // the bitmap for the next worker pass: out of place, and not with momentum
-    // on the server (w_{t+1} differs from w_t everywhere there)
-    const bool mark = ctx->sparse_w && f.w_in && f.w_out && f.w_in != f.w_out && ctx->rule != kRuleServerMomentum;
+    // the bitmap for the next worker pass: not with momentum on the server
+    // (w_{t+1} differs from w_t everywhere there); in place only for top-s
+    // with a change list that holds whole ranges (the next worker pass then
+    // has no w_{t-1} and takes w_{t+1} - w_t from it) and without GMC+'s
+    // detached points
+    const bool inplace = f.w_in && f.w_in == f.w_out;
+    const bool mark = ctx->sparse_w && f.w_in && f.w_out && ctx->rule != kRuleServerMomentum &&
+                      (!inplace || (ctx->comp != GMC_RBGS && ctx->dl_stride == kDlistStrideFull && !f.detach));
     f.wbits = mark ? ctx->wbits : nullptr;
     f.dlist = (mark && use_dlist(ctx)) ? ctx->dlist : nullptr;
-    // w_out is the last pass's input buffer and w_in its output, and the
-    // worker pass in between read them through that pass's bitmap: w_out
-    // still holds w_{t-1}, which equals w_t off the marks, and w_{t+1}
-    // equals w_t off the marks and this pass's sent components
-    f.sparse_apply = (mark && ctx->wbits_pair && ctx->wbits_used_t == ctx->t - 1 && ctx->wbits_in == f.w_out &&
-                      ctx->wbits_out == f.w_in)
-                         ? 1
-                         : 0;
+    f.dl_stride = ctx->dl_stride;
+    f.nf = ctx->nf;
+    f.nf_epoch = ctx->nf_epoch;
+    // out of place: w_out is the last pass's input buffer and w_in its
+    // output, and the worker pass in between read them through that pass's
+    // bitmap: w_out still holds w_{t-1}, which equals w_t off the marks, and
+    // w_{t+1} equals w_t off the marks and this pass's sent components.  In
+    // place: w_in is the last pass's output, so it holds w_t everywhere.
+    const bool chain = mark && ctx->wbits_pair && ctx->wbits_used_t == ctx->t - 1 && ctx->wbits_out == f.w_in;
+    f.sparse_apply = (chain && (inplace || ctx->wbits_in == f.w_out)) ? 1 : 0;
+    f.inplace = (f.sparse_apply && inplace) ? 1 : 0;
     if (f.sparse_apply) ++ctx->sparse_applies;
     ctx->wbits_used_t = -1;
     ctx->wbits_pair = mark;
@@ -984,6 +1014,26 @@ gmc_status gmc_iteration(gmc_ctx* ctx, const float* w_t_dev, float* w_prev_io_de
     return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, f, true);
 }
 
+gmc_status gmc_iteration_inplace(gmc_ctx* ctx, float* w_dev, const float* w_prev_dev, const float* const* grads_dev,
+                                 float* const* err_dev, int32_t* idx_dev, float* val_dev, int64_t* msg_len_dev) {
+    if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_iteration_inplace: ctx is NULL");
+    if (!w_dev || !grads_dev || !err_dev || !idx_dev || !val_dev || !msg_len_dev)
+        return fail(ctx, GMC_EINVAL, "gmc_iteration_inplace: NULL argument");
+    if (ctx->comp == GMC_RBGS || ctx->rule == kRuleServerMomentum)
+        return fail(ctx, GMC_EINVAL, "gmc_iteration_inplace: top-s under GMC_RULE_GMC or GMC_RULE_LR_IN_RESIDUAL only");
+    if (!ctx->sparse_w || ctx->dl_stride != kDlistStrideFull)
+        return fail(ctx, GMC_EINVAL,
+                    "gmc_iteration_inplace: needs GMC_OPT_SPARSE_MOMENTUM and GMC_OPT_CHANGE_LIST 3, which keep "
+                    "w_{t+1} - w_t for the next iteration");
+    GMC_TRY(step_impl(ctx, w_dev, w_prev_dev, grads_dev, err_dev, nullptr, idx_dev, val_dev, msg_len_dev, true));
+    FinishArgs f{};
+    f.zero_e = 1;
+    for (int k = 0; k < ctx->K; ++k) f.ez[k] = err_dev[k];
+    f.w_in = w_dev;
+    f.w_out = w_dev;
+    return aggregate_impl(ctx, idx_dev, val_dev, msg_len_dev, f, true);
+}
+
 gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const float* update_dev) {
     if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_apply: ctx is NULL");
     if (!w_dev || !update_dev) return fail(ctx, GMC_EINVAL, "gmc_apply: NULL argument");
@@ -991,8 +1041,7 @@ gmc_status gmc_apply(gmc_ctx* ctx, float* w_dev, float* w_prev_out_dev, const fl
     if (ctx->rule == kRuleServerMomentum)
         return fail(ctx, GMC_EINVAL, "gmc_apply: momentum on the server needs w_{t-1}; use gmc_finish");
     if (!ctx->started) return fail(ctx, GMC_ESTATE, "gmc_apply: no gmc_step has been taken yet");
-    ctx->wbits_valid = false;
-    ctx->wbits_pair = false;
+    drop_record(ctx);
     GMC_HIP(ctx, hipSetDevice(ctx->device));
     hipEvent_t ev;
     GMC_TRY(prof_begin(ctx, 5, &ev));
@@ -1037,9 +1086,7 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t) {
     if (!ctx) return fail(nullptr, GMC_EINVAL, "gmc_set_step: ctx is NULL");
     if (t < 0) return fail(ctx, GMC_EINVAL, "gmc_set_step: t must be >= 0");
     ctx->t = t;
-    ctx->wbits_valid = false;  // a resume may bring other parameters
-    ctx->wbits_pair = false;
-    ctx->wbits_used_t = -1;
+    drop_record(ctx);  // a resume may bring other parameters
     return GMC_OK;
 }
 
@@ -1070,17 +1117,23 @@ gmc_status gmc_set_option(gmc_ctx* ctx, int32_t option, int64_t value) {
             return prepare(ctx);
         case GMC_OPT_SPARSE_MOMENTUM:
             ctx->sparse_w = value ? 1 : 0;
-            ctx->wbits_valid = false;
-            ctx->wbits_pair = false;
-            ctx->wbits_used_t = -1;
+            drop_record(ctx);
             return GMC_OK;
-        case GMC_OPT_CHANGE_LIST:
-            if (value < 0 || value > 2) return fail(ctx, GMC_EINVAL, "gmc_set_option: change list must be 0, 1 or 2");
+        case GMC_OPT_CHANGE_LIST: {
+            if (value < 0 || value > 3)
+                return fail(ctx, GMC_EINVAL, "gmc_set_option: change list must be 0, 1, 2 or 3");
+            const int32_t stride = value == 3 ? kDlistStrideFull : kDlistStride;
+            if (stride != ctx->dl_stride && ctx->started)
+                return fail(ctx, GMC_ESTATE, "gmc_set_option: change list 3 is set or cleared before the first step only");
             ctx->change_list = (int)value;
-            ctx->wbits_valid = false;  // the list of the last pass may not have been written
-            ctx->wbits_pair = false;
-            ctx->wbits_used_t = -1;
+            drop_record(ctx);  // the list of the last pass may not have been written
+            if (stride != ctx->dl_stride) {
+                ctx->dl_stride = stride;
+                ctx->prepared = false;
+                return prepare(ctx);
+            }
             return GMC_OK;
+        }
         case GMC_OPT_PROFILE:
             if (ctx->profile) GMC_HIP(ctx, hipStreamSynchronize(ctx->stream));
             prof_clear(ctx);

@@ -53,11 +53,13 @@ constexpr int kAggTopkStageSmall = 128;
 constexpr uint32_t kNoThreshold = 0xffffffffu;  // no speculative candidates
 
 // The components a top-s server pass changed, per range of kAggTopkRange:
-// a block of kDlistStride int2, [0] = {count, 0} (-1: more than the block
-// holds), then {offset in the range, bits of fl(w_{t+1} - w_t)} per changed
-// component, in no particular order.
+// a block of dl_stride int2 (kDlistStride, or kDlistStrideFull for a list
+// that holds every component of a range, which in-place server passes
+// need), [0] = {count, 0} (-1: more than the block holds), then {offset in
+// the range, bits of fl(w_{t+1} - w_t)} per changed component, in no
+// particular order.
 constexpr int kDlistStride = 512;
-constexpr int kDlistCap = kDlistStride - 1;
+constexpr int kDlistStrideFull = kAggTopkRange + 1;
 // The list is kept when the two parameter vectors (8 d bytes) outgrow the
 // 256 MB Infinity Cache: below that, the worker pass's reads of w_t and w_prev
 // at the marked cache lines are served by that cache (and warm it for the
@@ -216,8 +218,11 @@ struct StepArgs {
     int32_t defer_zero;
     // nullable (with wbits, top-s): the previous server pass's list of the
     // components it changed and by how much (FinishArgs::dlist); the vector
-    // worker pass then takes w_t - w_prev from it and reads neither buffer
+    // worker pass then takes w_t - w_prev from it and reads neither buffer.
+    // With w_prev NULL (the last server pass updated w_t in place, and its
+    // list holds every change) every worker path takes it from the list.
     const int2* dlist;
+    int32_t dl_stride;  // int2 per range of dlist
 };
 
 // The server pass after the sum over workers: update = -(s * sum), the
@@ -242,8 +247,19 @@ struct FinishArgs {
     // the old marks or this pass's sent components fall
     int32_t sparse_apply;
     // nullable (with wbits): the list of the components this pass changes
-    // and fl(w_{t+1} - w_t) there, kDlistStride int2 per range
+    // and fl(w_{t+1} - w_t) there, dl_stride int2 per range
     int2* dlist;
+    int32_t dl_stride;
+    // 1 (with sparse_apply, w_out == w_in): the previous pass also updated
+    // this buffer in place, so it already holds w_t everywhere and only the
+    // words of this pass's sent components are written; the previous marks
+    // are visited as well once some pass has written a non-finite w (nf)
+    int32_t inplace;
+    // nf[0] == nf_epoch: some pass since the recorded components were last
+    // dropped wrote a non-finite w_{t+1} (the passes with wbits store the
+    // epoch there when they do; the host bumps it to drop the record)
+    int32_t* nf;
+    int32_t nf_epoch;
     const float* e[kMaxWorkers];  // e_{t+1,k}
     float* y[kMaxWorkers];        // w_{t+1,k}
     // 1: e_{t+1,k}[j] = v - v (+0 for a finite v) for each entry (j, v) of

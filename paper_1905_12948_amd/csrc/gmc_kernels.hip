@@ -134,6 +134,12 @@ __device__ __forceinline__ float rule_u_rt(int rule, float e, float g, float wt,
     return rule_u<kRuleGmc>(e, g, wt, wp, c, h);
 }
 
+__device__ __forceinline__ float rule_u_diff_rt(int rule, float e, float g, float diff, float c, float h) {
+    if (rule == kRuleServerMomentum) return rule_u_diff<kRuleServerMomentum>(e, g, diff, c, h);
+    if (rule == kRuleLrInResidual) return rule_u_diff<kRuleLrInResidual>(e, g, diff, c, h);
+    return rule_u_diff<kRuleGmc>(e, g, diff, c, h);
+}
+
 // The output mix of SplitMix64 (Steele, Lea and Flood, OOPSLA 2014).
 __device__ __forceinline__ uint64_t splitmix64_mix(uint64_t z) {
     z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
@@ -296,7 +302,36 @@ __device__ __forceinline__ void store_agent(uint32_t* p, uint32_t v) {
 // ---------------------------------------------------------------------------
 
 __device__ void fused_chunk_wave(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int chunk,
-                                 int k);
+                                 int k, const float* dl);
+
+// w_t - w_prev of the components [start, start + len) (len <= kChunk) from
+// the last server pass's change list into dl (LDS): fl(w_{t+1} - w_t) of
+// every component that pass changed, +0 for the others.  False when a range
+// of the chunk overflowed its list (never for a list that holds whole
+// ranges).  The whole workgroup calls it; cnt: 2 words of LDS.
+__device__ bool scatter_changes(const StepArgs& a, int start, int len, float* dl, int32_t* cnt) {
+    const int nt = (int)blockDim.x;
+    const int r0 = start / kAggTopkRange, nr = (start + len - 1) / kAggTopkRange - r0 + 1;  // 1 or 2 ranges
+    for (int i = threadIdx.x; i < kChunk; i += nt) dl[i] = 0.0f;
+    if (threadIdx.x == 0) {
+        cnt[0] = a.dlist[(size_t)r0 * a.dl_stride].x;
+        cnt[1] = nr > 1 ? a.dlist[(size_t)(r0 + 1) * a.dl_stride].x : 0;
+    }
+    __syncthreads();
+    const int32_t n0 = cnt[0], n1 = cnt[1];
+    const bool ok = n0 >= 0 && n1 >= 0;
+    for (int h2 = 0; ok && h2 < nr; ++h2) {
+        const int32_t c = h2 ? n1 : n0;
+        const int2* L = a.dlist + (size_t)(r0 + h2) * a.dl_stride;
+        for (int32_t e = 1 + (int32_t)threadIdx.x; e <= c; e += nt) {
+            const int2 en = L[e];
+            const int j = (r0 + h2) * kAggTopkRange + en.x;
+            if (j >= start && j < start + len) dl[j - start] = __int_as_float(en.y);
+        }
+    }
+    __syncthreads();
+    return ok;
+}
 
 template <int kRule, bool kDetach, bool kApprox>
 __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
@@ -316,7 +351,15 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
     const int start = one ? chunk * kChunk : g.chunk_start[chunk];
     const int len = one ? min(kChunk, a.d - start) : g.chunk_len[chunk];
     if ((start & 3) != 0 || len != kChunk) {  // partial or unaligned chunk: element-wise, one wavefront
-        if (threadIdx.x < kWave) fused_chunk_wave(a, g, s, chunk, k);
+        // with w_prev NULL (the last server pass updated w in place) w_t -
+        // w_prev exists only in that pass's change list, which holds whole
+        // ranges
+        const float* dl = nullptr;
+        if (a.w_prev == nullptr) {
+            scatter_changes(a, start, len, sm.dl, dl_cnt);
+            dl = sm.dl;
+        }
+        if (threadIdx.x < kWave) fused_chunk_wave(a, g, s, chunk, k, dl);
         return;
     }
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
@@ -344,8 +387,8 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
         const int r0 = start / kAggTopkRange, nr = (start + len - 1) / kAggTopkRange - r0 + 1;  // 1 or 2 ranges
         int2 head0 = make_int2(0, 0), head1 = make_int2(0, 0);
         if ((int)threadIdx.x < kWave) {
-            head0 = a.dlist[(size_t)r0 * kDlistStride + threadIdx.x];
-            if (nr > 1) head1 = a.dlist[(size_t)(r0 + 1) * kDlistStride + threadIdx.x];
+            head0 = a.dlist[(size_t)r0 * a.dl_stride + threadIdx.x];
+            if (nr > 1) head1 = a.dlist[(size_t)(r0 + 1) * a.dl_stride + threadIdx.x];
         }
 #pragma unroll
         for (int i = 0; i < kChunk / kGroup; ++i) sm.dl[i * kGroup + threadIdx.x] = 0.0f;
@@ -368,11 +411,11 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
                 if (threadIdx.x >= 1 && (int32_t)threadIdx.x <= cnt && (int)threadIdx.x < kWave)
                     put(h2 ? head1 : head0, r0 + h2);
                 for (int32_t e2 = kWave + threadIdx.x; e2 <= cnt; e2 += kGroup)
-                    put(a.dlist[(size_t)(r0 + h2) * kDlistStride + e2], r0 + h2);
+                    put(a.dlist[(size_t)(r0 + h2) * a.dl_stride + e2], r0 + h2);
             }
         }
         __syncthreads();
-        if (!use_list) {  // a range's list overflowed: the marks and the two parameter vectors
+        if (!use_list) {  // a range's list overflowed (w_prev is then set): the marks and the two parameter vectors
 #pragma unroll
             for (int i = 0; i < 2; ++i) load_w4<kDetach>(a, (int64_t)start + o0 + i * (kGroup * 4), &wt[i], &wv[i]);
         }
@@ -462,9 +505,11 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
 
 // Element-wise pass of one wavefront over one (chunk, worker): the chunks the
 // vector path cannot take (a segment's partial last chunk, chunks with an
-// unaligned start) and the workers whose rows are not 16-byte aligned.
+// unaligned start) and the workers whose rows are not 16-byte aligned.  dl
+// (nullable, LDS): w_t - w_prev of the chunk's components (scatter_changes),
+// used instead of the two parameter vectors.
 __device__ void fused_chunk_wave(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s, int chunk,
-                                 int k) {
+                                 int k, const float* dl) {
     const int lane = threadIdx.x & (kWave - 1);
     const int start = g.chunk_start[chunk];
     const int len = g.chunk_len[chunk];
@@ -482,7 +527,8 @@ __device__ void fused_chunk_wave(const StepArgs& a, const TopkGeometry& g, const
         const int o = i * kWave + lane;
         if (o < len) {
             const int j = start + o;
-            const float u = rule_u_rt(a.rule, e[j], gr[j], a.w_t[j], a.w_prev[j], c, a.h);
+            const float u = dl ? rule_u_diff_rt(a.rule, e[j], gr[j], dl[o], c, a.h)
+                               : rule_u_rt(a.rule, e[j], gr[j], a.w_t[j], a.w_prev[j], c, a.h);
             e[j] = u;
             if (a.detach) a.wp.y[k][j] = detached(a.w_t[j], u, a.q);
             flags |= (key_of(u) >= tau ? 1u : 0u) << i;
@@ -513,17 +559,23 @@ __device__ void fused_chunk_wave(const StepArgs& a, const TopkGeometry& g, const
     }
 }
 
-// The element-wise kernel: one wavefront per (chunk, worker) for the workers
-// outside vec_mask (the vector kernel takes every chunk of the others,
-// partial ones included).
-__global__ __launch_bounds__(kGroup) void topk_fused_gen_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
-                                                                uint64_t vec_mask) {
-    const int wave = threadIdx.x >> 6;
-    const int64_t wid = (int64_t)blockIdx.x * kWavesPerGroup + wave;
-    if (wid >= (int64_t)g.n_chunks * g.K) return;  // wave-uniform; no workgroup barrier below
+// The element-wise kernel: one workgroup of one wavefront per (chunk,
+// worker) for the workers outside vec_mask (the vector kernel takes every
+// chunk of the others, partial ones included).
+__global__ __launch_bounds__(kWave) void topk_fused_gen_kernel(StepArgs a, TopkGeometry g, TopkScratch s,
+                                                               uint64_t vec_mask) {
+    __shared__ float dl[kChunk];
+    __shared__ int32_t dl_cnt[2];
+    const int64_t wid = blockIdx.x;
+    if (wid >= (int64_t)g.n_chunks * g.K) return;
     const int chunk = (int)(wid / g.K), k = (int)(wid % g.K);
     if ((vec_mask >> k) & 1ull) return;  // the vector kernel's
-    fused_chunk_wave(a, g, s, chunk, k);
+    const float* d = nullptr;
+    if (a.w_prev == nullptr) {  // w_t - w_prev from the last in-place server pass's list
+        scatter_changes(a, g.chunk_start[chunk], g.chunk_len[chunk], dl, dl_cnt);
+        d = dl;
+    }
+    fused_chunk_wave(a, g, s, chunk, k, d);
 }
 
 template <bool kApprox>
@@ -560,9 +612,8 @@ hipError_t launch_topk_fused_vec(const StepArgs& a, const TopkGeometry& g, const
 
 hipError_t launch_topk_fused_gen(const StepArgs& a, const TopkGeometry& g, const TopkScratch& s,
                                  uint64_t vec_mask, hipStream_t st) {
-    const int64_t waves = (int64_t)g.n_chunks * g.K;
-    const int grid = (int)((waves + kWavesPerGroup - 1) / kWavesPerGroup);
-    hipLaunchKernelGGL(topk_fused_gen_kernel, dim3(grid), dim3(kGroup), 0, st, a, g, s, vec_mask);
+    const int64_t grid = (int64_t)g.n_chunks * g.K;
+    hipLaunchKernelGGL(topk_fused_gen_kernel, dim3((unsigned)grid), dim3(kWave), 0, st, a, g, s, vec_mask);
     return hipGetLastError();
 }
 
@@ -2252,10 +2303,11 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
     const int t = threadIdx.x;
     // the change list of this range: the components this pass marks, with
     // fl(w_{t+1} - w_t), for the next worker pass
-    int2* const dlr = (kApply && f.wbits && f.dlist) ? f.dlist + (size_t)r * kDlistStride : nullptr;
+    int2* const dlr = (kApply && f.wbits && f.dlist) ? f.dlist + (size_t)r * f.dl_stride : nullptr;
+    const uint32_t dl_cap = (uint32_t)f.dl_stride - 1u;
     auto list_change = [&](int q, float wn, float x) {
         const uint32_t pos = atomicAdd(&dl_n, 1u);
-        if (pos < (uint32_t)kDlistCap) dlr[1 + pos] = make_int2(q, __float_as_int(wn - x));
+        if (pos < dl_cap) dlr[1 + pos] = make_int2(q, __float_as_int(wn - x));
     };
     const int64_t base = (int64_t)r * R;
     const int64_t n = (int64_t)d - base < R ? (int64_t)d - base : R;
@@ -2276,10 +2328,16 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
         }
     }
     if (t == 0) dl_n = 0u;
+    // in place, w already holds w_t everywhere: only this pass's sent
+    // components are written, and the previous marks are visited only once
+    // a non-finite w has been written (they then keep their marks, and the
+    // next worker pass its NaN momentum term)
+    const bool old_marks = sparse && (!f.inplace || (f.nf && *f.nf == f.nf_epoch));
+    bool nonfinite = false;  // this thread wrote a non-finite w_{t+1}
     if (t < NW) {
         hb[t] = 0u;
         wb[t] = 0u;
-        wv[t] = (sparse && t < words) ? f.wbits[(base >> 5) + t] : 0u;
+        wv[t] = (old_marks && t < words) ? f.wbits[(base >> 5) + t] : 0u;
     }
     if (t < K) {
         const int32_t* rp = rowptr + (size_t)t * (n_ranges + 1);
@@ -2418,8 +2476,10 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
                 }
                 st4(f.w_out + base + q, nx);
                 if (f.wbits) {
-                    const uint32_t m = ((hb[q >> 5] >> (q & 31)) & 0xfu) | not_finite(nx.x) | (not_finite(nx.y) << 1) |
-                                       (not_finite(nx.z) << 2) | (not_finite(nx.w) << 3);
+                    const uint32_t nfm = not_finite(nx.x) | (not_finite(nx.y) << 1) | (not_finite(nx.z) << 2) |
+                                         (not_finite(nx.w) << 3);
+                    nonfinite |= nfm != 0u;
+                    const uint32_t m = ((hb[q >> 5] >> (q & 31)) & 0xfu) | nfm;
                     atomicOr(&wb[q >> 5], m << (q & 31));
                     lm[i] = m;
                     ld[i] = make_float4(nx.x - x.x, nx.y - x.y, nx.z - x.z, nx.w - x.w);
@@ -2450,7 +2510,7 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     if ((lm[i] >> e) & 1u) {
-                        if (pos < (uint32_t)kDlistCap) dlr[1 + pos] = make_int2(q + e, __float_as_int(dv[e]));
+                        if (pos < dl_cap) dlr[1 + pos] = make_int2(q + e, __float_as_int(dv[e]));
                         ++pos;
                     }
                 }
@@ -2469,13 +2529,15 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
                     atomicOr(&wb[q >> 5], 1u << (q & 31));
                     if (dlr) list_change(q, wn, x);
                 }
+                if (f.wbits && not_finite(wn)) nonfinite = true;
             }
         }
     }
     if (kApply && f.wbits) {
+        if (nonfinite && f.nf) *f.nf = f.nf_epoch;  // the same value from every writer
         __syncthreads();
         if (t < words) f.wbits[(base >> 5) + t] = wb[t];
-        if (dlr && t == 0) dlr[0] = make_int2(dl_n <= (uint32_t)kDlistCap ? (int32_t)dl_n : -1, 0);
+        if (dlr && t == 0) dlr[0] = make_int2(dl_n <= dl_cap ? (int32_t)dl_n : -1, 0);
     }
     if (kApply && f.detach) {
         // GMC+: the detached points at the sent components, from w_{t+1}

@@ -31,7 +31,7 @@ EXPORTS = ("gmc_init", "gmc_set_segments", "gmc_set_block", "gmc_set_stream", "g
            "gmc_set_option", "gmc_stats", "gmc_profile_read", "gmc_last_error", "gmc_destroy",
            "gmc_calib_copy", "gmc_aggregate_apply", "gmc_set_rule", "gmc_set_eta", "gmc_set_lambda",
            "gmc_step_detach", "gmc_finish", "gmc_detach", "gmc_iteration", "gmc_calib_stream", "gmc_pair_stats",
-           "gmc_count", "gmc_aggregate_static")
+           "gmc_count", "gmc_aggregate_static", "gmc_iteration_inplace")
 
 RULES = {"gmc": 0, "server_momentum": 1, "lr_in_residual": 2}
 
@@ -85,6 +85,7 @@ def load() -> ctypes.CDLL:
     lib.gmc_finish.argtypes = [P, P, P, P, P, P, P, P, P, P]
     lib.gmc_detach.argtypes = [P, P, P, P]
     lib.gmc_iteration.argtypes = [P, P, P, P, P, P, P, P]
+    lib.gmc_iteration_inplace.argtypes = [P, P, P, P, P, P, P, P]
     lib.gmc_calib_stream.argtypes = [P, P, P, i64, i32, i64]
     lib.gmc_pair_stats.argtypes = [P, P, P, i32, ctypes.POINTER(i32)]
     lib.gmc_aggregate_static.argtypes = [i64, i32, dbl, P, i64, P, i64, P, P, P]
@@ -95,7 +96,7 @@ def load() -> ctypes.CDLL:
                  "gmc_aggregate", "gmc_apply", "gmc_get_step", "gmc_set_step", "gmc_set_option",
                  "gmc_stats", "gmc_profile_read", "gmc_calib_copy", "gmc_aggregate_apply",
                  "gmc_set_rule", "gmc_set_eta", "gmc_set_lambda", "gmc_step_detach", "gmc_finish",
-                 "gmc_detach", "gmc_iteration", "gmc_calib_stream", "gmc_pair_stats"):
+                 "gmc_detach", "gmc_iteration", "gmc_calib_stream", "gmc_pair_stats", "gmc_iteration_inplace"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -284,11 +285,12 @@ class Gmc:
     def step(self, w_t, w_prev, grads, err, idx, val, msg_len, w_k=None):
         """Worker pass; with ``w_k`` ([K, >=d] or K tensors) also GMC+'s
         detached points where they are already final (gmc_step_detach;
-        ``finish`` with the same ``w_k`` completes them)."""
+        ``finish`` with the same ``w_k`` completes them).  ``w_prev`` may be
+        None right after a server pass in place that kept its changes."""
         torch = _torch()
         d, K = self.d, self.K
         pw = _check(w_t, torch.float32, d, "w_t")
-        pp = _check(w_prev, torch.float32, d, "w_prev")
+        pp = None if w_prev is None else _check(w_prev, torch.float32, d, "w_prev")
         gp = (ctypes.c_void_p * K)(*_rows(grads, d, K, "grads"))
         ep = (ctypes.c_void_p * K)(*_rows(err, d, K, "err"))
         pi = _check(idx, torch.int32, K * self.index_len, "idx")
@@ -335,6 +337,23 @@ class Gmc:
         pl = _check(msg_len, torch.int64, K, "msg_len")
         self._stream(w_t.device)
         self._call(self._lib.gmc_iteration(self._ctx, pw, pp, gp, ep, pi, pv, pl))
+
+    def iteration_inplace(self, w, w_prev, grads, err, idx, val, msg_len):
+        """One whole iteration with w updated in place; ``w_prev`` is w_{t-1}
+        (``w`` itself at t = 0) or None after an in-place iteration (the
+        context keeps w_{t+1} - w_t; GMC_OPT_SPARSE_MOMENTUM and
+        GMC_OPT_CHANGE_LIST 3)."""
+        torch = _torch()
+        d, K = self.d, self.K
+        pw = _check(w, torch.float32, d, "w")
+        pp = None if w_prev is None else _check(w_prev, torch.float32, d, "w_prev")
+        gp = (ctypes.c_void_p * K)(*_rows(grads, d, K, "grads"))
+        ep = (ctypes.c_void_p * K)(*_rows(err, d, K, "err"))
+        pi = _check(idx, torch.int32, K * self.index_len, "idx")
+        pv = _check(val, torch.float32, K * self.message_len, "val")
+        pl = _check(msg_len, torch.int64, K, "msg_len")
+        self._stream(w.device)
+        self._call(self._lib.gmc_iteration_inplace(self._ctx, pw, pp, gp, ep, pi, pv, pl))
 
     def detach(self, w, err, w_k):
         """GMC+'s detached points in one dense pass: w_k = w - (lambda eta) err."""

@@ -55,6 +55,10 @@ class Case:
     sparse_w: bool = False        # GMC_OPT_SPARSE_MOMENTUM
     w0_hook: Optional[Callable] = None     # w0 -> w0, host side
     iteration: bool = False       # gmc_iteration (worker and server pass in one call, buffers swapped)
+    # one parameter buffer updated in place: "iteration" (gmc_iteration_inplace)
+    # or "apply" (gmc_step, then gmc_aggregate_apply with w_out = w); w_prev is
+    # w itself at t = 0 and NULL after
+    inplace: str = ""
 
 
 def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
@@ -115,12 +119,19 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
             g.set_eta(eta_t)
             orc.set_eta(eta_t)
         fused_detach = case.detach == "fused"
-        if case.iteration:
+        if case.inplace:
+            w_prev_arg = w if t == 0 else None   # w_{-1} = w_0, then the context's record
+            if case.inplace == "iteration":
+                g.iteration_inplace(w, w_prev_arg, g_rows, e_rows, idx, val, ln)
+            else:
+                g.step(w, w_prev_arg, g_rows, e_rows, idx, val, ln)
+                g.aggregate_apply(idx, val, ln, w, w, update=upd if case.write_update else None)
+        elif case.iteration:
             g.iteration(w, wp, g_rows, e_rows, idx, val, ln)
             w, wp = wp, w
         else:
             g.step(w, wp, g_rows, e_rows, idx, val, ln, w_k=wk_rows if fused_detach else None)
-        if case.iteration:
+        if case.iteration or case.inplace:
             pass
         elif use_finish:
             g.finish(idx, val, ln, w, wp, w_prev=wp, update=upd if case.write_update else None,
@@ -158,10 +169,12 @@ def run_lockstep(case: Case, device="cuda:0", check_every=1, verbose=True):
             m = int(ol[k])
             assert_same_f32(gv[k, :m], ov[k, :m], tag + ": values of worker %d" % k)
             assert_same_f32(e_rows[k].cpu().numpy(), e_h[k], tag + ": residual of worker %d" % k)
-        if not case.iteration and (case.write_update or not (case.fused_apply or use_finish)):
+        if not case.iteration and case.inplace != "iteration" and \
+                (case.write_update or not (case.fused_apply or use_finish or case.inplace)):
             assert_same_f32(upd.cpu().numpy(), od, tag + ": update")
         assert_same_f32(w.cpu().numpy(), w_h, tag + ": w")
-        assert_same_f32(wp.cpu().numpy(), wp_h, tag + ": w_prev")
+        if not case.inplace:  # in place there is no second buffer
+            assert_same_f32(wp.cpu().numpy(), wp_h, tag + ": w_prev")
         if case.detach:
             for k in range(K):
                 assert_same_f32(wk_rows[k].cpu().numpy(), wk_h[k], tag + ": detached point of worker %d" % k)
