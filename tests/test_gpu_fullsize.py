@@ -25,9 +25,11 @@ every worker:
     component and w_t bit for bit elsewhere; the update vector and GMC+'s
     detached points (every worker) likewise;
   * the library's own count check (stats[4]) stays 0.
-Step 0 takes the full-data selection path and the dense parameter path,
-later steps the candidate path and, with the sparse momentum term, read and
-write the parameters only where they change."""
+Step 0 takes its speculative thresholds from a sample of u (the seed pass)
+and the dense parameter path, later steps the previous selection's
+thresholds and, with the sparse momentum term, read and write the parameters
+only where they change; a selection whose candidates cannot prove they hold
+the top k takes the full-data path."""
 import numpy as np
 import pytest
 
