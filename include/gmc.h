@@ -317,9 +317,11 @@ gmc_status gmc_iteration(gmc_ctx* ctx, const float* w_t_dev, float* w_prev_io_de
  *               iteration whose record stands (GMC_ESTATE if it was dropped:
  *               gmc_set_step, the options that drop the recorded
  *               components, gmc_apply).  At t = 0 pass w_dev (w_{-1} = w_0).
- * A caller that saves a run to resume it exactly keeps w_{t-1} as well (for
- * example by running the last iteration before the save out of place, with
- * gmc_iteration); a resumed context starts with w_prev_dev = w_{t-1}.
+ * A caller that saves a run to resume it exactly needs w_{t-1} as well: it
+ * runs the last iteration before the save as gmc_step(w, NULL, ...) and
+ * gmc_aggregate_apply(w, w_next) into a second buffer, saves w (now w_{t-1})
+ * and w_next (w_t), and a resumed context (gmc_set_step) starts with
+ * gmc_iteration_inplace(w_next, w, ...), then NULL.
  * The remaining arguments are gmc_step's.
  */
 gmc_status gmc_iteration_inplace(gmc_ctx* ctx, float* w_dev, const float* w_prev_dev, const float* const* grads_dev,

@@ -137,3 +137,76 @@ def test_inplace_call_order():
         torch.zeros(10000, device=dev), None, torch.zeros((2, 10000), device=dev), torch.zeros((2, 10000), device=dev),
         *gr.alloc_messages(dev)))
     gr.close()
+
+
+def test_inplace_checkpoint_resume():
+    """The save/resume procedure of the in-place mode: the last iteration
+    before the save runs its server pass out of place (gmc_step with w_prev =
+    NULL, gmc_aggregate_apply into a second buffer), so the caller holds
+    w_{t-1} and w_t; a fresh context restored with gmc_set_step continues in
+    place from them.  Eight iterations so equal eight uninterrupted in-place
+    iterations bit for bit, and the oracle's."""
+    import torch
+    from paper_1905_12948_amd import Gmc
+    from gpu_harness import assert_same_f32
+    import oracle
+    wl = W("gpt2").shrunk(64, K=3)
+    d, K = wl.d, wl.K
+    seg = wl.topk_segments()
+    dev = torch.device("cuda:0")
+    grads = [torch.from_numpy(wl.grads(t)).to(dev) for t in range(8)]
+
+    def ctx():
+        g = Gmc(d, K, "topk_seg", wl.ratio, wl.beta, wl.eta, seed=wl.seed, segments=seg.tolist())
+        g.set_option(OPT_SPARSE, 1)
+        g.set_option(OPT_LIST, 3)
+        return g
+
+    # uninterrupted
+    ga = ctx()
+    wa = torch.from_numpy(wl.w0()).to(dev)
+    ea = torch.zeros((K, d), device=dev)
+    ia, va, la = ga.alloc_messages(dev)
+    for t in range(8):
+        ga.iteration_inplace(wa, wa if t == 0 else None, grads[t], ea, ia, va, la)
+    torch.cuda.synchronize()
+    # four in place, the fifth with its server pass out of place, save
+    gb = ctx()
+    wb = torch.from_numpy(wl.w0()).to(dev)
+    eb = torch.zeros((K, d), device=dev)
+    ib, vb, lb = gb.alloc_messages(dev)
+    for t in range(4):
+        gb.iteration_inplace(wb, wb if t == 0 else None, grads[t], eb, ib, vb, lb)
+    w_next = torch.empty_like(wb)
+    gb.step(wb, None, grads[4], eb, ib, vb, lb)
+    gb.aggregate_apply(ib, vb, lb, wb, w_next)
+    torch.cuda.synchronize()
+    saved = dict(t=gb.t, w_prev=wb.cpu().clone(), w=w_next.cpu().clone(), e=eb.cpu().clone())
+    gb.close()
+    assert saved["t"] == 5
+    # resume in a fresh context, in place
+    gc = ctx()
+    gc.t = saved["t"]
+    wc = saved["w"].to(dev)
+    wpc = saved["w_prev"].to(dev)
+    ec = saved["e"].to(dev)
+    ic, vc, lc = gc.alloc_messages(dev)
+    for t in range(5, 8):
+        gc.iteration_inplace(wc, wpc if t == 5 else None, grads[t], ec, ic, vc, lc)
+    torch.cuda.synchronize()
+    assert_same_f32(wc.cpu().numpy(), wa.cpu().numpy(), "resumed in place: w")
+    assert_same_f32(ec.cpu().numpy(), ea.cpu().numpy(), "resumed in place: residuals")
+    assert torch.equal(ic, ia) and torch.equal(lc, la)
+    # and the oracle's
+    orc = oracle.GmcOracle(d, K, "topk", wl.ratio, wl.beta, wl.eta, seed=wl.seed, seg_off=seg)
+    w_h, wp_h = wl.w0(), wl.w0()
+    e_h = np.zeros((K, d), np.float32)
+    for t in range(8):
+        oi, ov, ol = orc.step(w_h, wp_h, wl.grads(t), e_h)
+        wn = orc.next_params(w_h, wp_h, orc.aggregate(oi, ov, ol))
+        wp_h, w_h = w_h, wn
+    assert_same_f32(wa.cpu().numpy(), w_h, "in place: w_8 against the oracle")
+    assert_same_f32(ea.cpu().numpy(), e_h, "in place: e_8 against the oracle")
+    for g in (ga, gc):
+        assert g.stats()["count_errors"] == 0
+        g.close()
