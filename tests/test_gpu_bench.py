@@ -19,13 +19,14 @@ def _gpu():
     torch.cuda.empty_cache()  # the later full-size tests need most of the device memory
 
 
-@pytest.mark.parametrize("workload", ["tiny", "gpt2", "rbgs", "resnet50_approx"])
-def test_bench_line(workload, capsys, monkeypatch):
+@pytest.mark.parametrize("workload,extra", [("tiny", []), ("gpt2", []), ("rbgs", []), ("resnet50_approx", []),
+                                            ("gpt2", ["--in-place"])])
+def test_bench_line(workload, extra, capsys, monkeypatch):
     import bench
     import synth
 
     monkeypatch.setattr(sys, "argv", ["bench.py", "--workload", workload, "--steps", "3", "--warmup", "2",
-                                      "--no-cpu-baseline"])
+                                      "--no-cpu-baseline"] + extra)
     print("bench line: %s" % workload, file=sys.stderr, flush=True)
     bench.main()
     lines = [ln for ln in capsys.readouterr().out.splitlines() if ln.startswith("{")]
@@ -45,8 +46,12 @@ def test_bench_line(workload, capsys, monkeypatch):
     assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
     assert 0.0 < r["frac"] <= 1.0 and r["frac"] == pytest.approx(r["achieved"] / r["peak"], abs=1e-3)
     assert r["kernel"] == ("rbgs_vec_kernel" if wl.compressor == "rbgs" else "topk_fused_vec_kernel")
-    if wl.compressor != "rbgs":  # the plain stream of the pass's pattern (cache-resident at the tiny size)
-        assert 0.0 < r["stream_ceiling"]["kernel_time_frac"] <= 1.2
+    if wl.compressor != "rbgs":
+        # the plain stream of the pass's pattern: the pass runs at about its
+        # speed (cache-resident and launch-bound at the tiny size, where the
+        # candidate staging weighs more)
+        low = 0.25 if workload == "tiny" else 0.85
+        assert low < r["stream_ceiling"]["kernel_time_frac"] <= 1.2, r["stream_ceiling"]
     # iteration 0: thresholds from a sample of u, every global top-s selection
     # resolved from its candidates; the full-data path measured on its own
     first = j["first_step"]
@@ -58,6 +63,7 @@ def test_bench_line(workload, capsys, monkeypatch):
     # resolved from candidates where the workload allows it
     sel = j["selection"]
     assert sel["count_errors"] == 0
+    assert j["config"]["in_place"] == ("--in-place" in extra)
     assert sel["sparse_momentum_steps"] == 3 and sel["sparse_applies"] == 3
     # the headline fraction takes the dense byte definition; the sparse one beside it
     assert j["alg_bytes_per_step"] == bench.survey_bytes(wl, j["config"]["message_len"], j["config"]["lambda"] > 0)
