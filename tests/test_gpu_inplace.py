@@ -210,3 +210,15 @@ def test_inplace_checkpoint_resume():
     for g in (ga, gc):
         assert g.stats()["count_errors"] == 0
         g.close()
+
+
+@pytest.mark.parametrize("sizes,K,ratio", [([1], 3, 0.5), ([3], 2, 0.5), ([2, 1, 5], 2, 0.3), ([2048], 1, 1e-6),
+                                           ([2049], 2, 0.999), ([4096 * 3 + 5, 1, 4093], 3, 0.05)])
+def test_inplace_degenerate_sizes(sizes, K, ratio):
+    # one-component segments, d = 1, a chunk's last partial range, ranges
+    # that a segment boundary splits; every worker sends nearly every
+    # component in the 0.999 case, so whole ranges change
+    wl = synth.Workload("small", sizes, K=K, ratio=ratio, beta=0.9, eta=0.1, steps=4,
+                        compressor="topk_seg", dist="normal")
+    run_lockstep(Case(wl, steps=4, inplace="iteration", sparse_w=True, options=FULL_LIST,
+                      label="in place small%s" % sizes))
