@@ -479,11 +479,9 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
 #pragma unroll
         for (int w = 0; w < kWavesPerGroup; ++w) total += wtot[i][w];
     }
-    if (threadIdx.x == 0) {
-        s.run_cnt[run_slot] = total;
-        const int cg = one ? chunk / kCompactChunks : g.chunk_cgrp[chunk];
-        atomicAdd(grp_slot(s, g, a.t, k, cg, chunk), total);
-    }
+    // the chunk's compaction group (a table lookup with several segments),
+    // loaded now so that its latency overlaps the staging
+    const int cg = one ? chunk / kCompactChunks : g.chunk_cgrp[chunk];
     // gather the candidates in LDS, then write the slot with consecutive
     // threads on consecutive entries (a few whole lines instead of one
     // partial line per candidate)
@@ -500,6 +498,14 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
     __syncthreads();
     int2* sp = s.slot + run_slot * kChunk;
     for (uint32_t q = threadIdx.x; q < total; q += kGroup) sp[q] = stage[q];
+    // the count and the device-scope add into the group's total come last:
+    // nothing after them waits for their completion (a wait on the add,
+    // which travels to the memory-side atomic unit, held up every wave of
+    // the workgroup through the staging barriers: 20-30 us per pass)
+    if (threadIdx.x == 0) {
+        s.run_cnt[run_slot] = total;
+        atomicAdd(grp_slot(s, g, a.t, k, cg, chunk), total);
+    }
 }
 
 
