@@ -380,6 +380,16 @@ def main():
 
     ms_step = elapsed * 1e3 / args.steps
     msg_len = int(round(float(ln.double().mean().item())))  # varies per worker for the sampled threshold
+    # relative communication cost of the last timed step (Section 5.2):
+    # values the K workers send plus K times the components of the server's
+    # update, over the 2 K d values dense exchanges would move (top-s also
+    # sends an index with each value)
+    ln_h = [int(x) for x in ln.cpu().tolist()]
+    if wl.compressor == "rbgs":
+        support = ln_h[0]  # every worker sends the same blocks
+    else:
+        support = int(torch.unique(torch.cat([idx[k, :ln_h[k]] for k in range(K)])).numel())
+    rcc = (sum(ln_h) + K * support) / (2.0 * K * d)
     ab = algorithmic_bytes(wl, msg_len, detach, sparse_w)
     fused_ms_total, fused_n = prof["fused_vec"]
     fused_ms = fused_ms_total / max(fused_n, 1)
@@ -410,7 +420,8 @@ def main():
         "config": {"workload": DESCRIPTIONS[wl.name], "d": d, "K": K, "compressor": wl.compressor,
                    "ratio": wl.ratio, "lambda": lam, "message_len": msg_len, "grad_batches": len(G),
                    "sparse_momentum": sparse_w, "forced_full_data": bool(args.force_full),
-                   "in_place": bool(args.in_place)},
+                   "in_place": bool(args.in_place),
+                   "rcc": round(rcc, 7), "update_support": support},
         # the step's algorithmic bytes with dense parameter traffic (12 B per
         # worker-element, 16 B per element, 16 B per message entry) over
         # 8 TB/s; the sparse accounting (parameters moved only where they

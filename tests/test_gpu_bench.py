@@ -64,6 +64,12 @@ def test_bench_line(workload, extra, capsys, monkeypatch):
     sel = j["selection"]
     assert sel["count_errors"] == 0
     assert j["config"]["in_place"] == ("--in-place" in extra)
+    # relative communication cost: messages plus the update's support, over
+    # 2 K d; the support is at most the union of the K messages
+    c = j["config"]
+    assert 0 < c["update_support"] <= wl.K * c["message_len"] + wl.K
+    assert c["rcc"] == pytest.approx((wl.K * c["message_len"] + wl.K * c["update_support"]) / (2 * wl.K * wl.d),
+                                     rel=0.05)
     assert sel["sparse_momentum_steps"] == 3 and sel["sparse_applies"] == 3
     # the headline fraction takes the dense byte definition; the sparse one beside it
     assert j["alg_bytes_per_step"] == bench.survey_bytes(wl, j["config"]["message_len"], j["config"]["lambda"] > 0)
