@@ -58,6 +58,46 @@ def log(msg: str):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
+class TimingEvents:
+    """HIP events on torch's current stream that only time: created with
+    hipEventDisableSystemFence, so that recording one adds no system-scope
+    cache write-back and invalidate to the work it brackets (a
+    torch.cuda.Event record does, a few microseconds per record)."""
+
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self, n: int):
+        import ctypes
+        self._ct = ctypes
+        # the HIP runtime torch has loaded (the soname matches the loaded copy)
+        self._hip = ctypes.CDLL("libamdhip64.so.7")
+        self._ev = [ctypes.c_void_p() for _ in range(n)]
+        for e in self._ev:
+            self._ok(self._hip.hipEventCreateWithFlags(ctypes.byref(e), ctypes.c_uint(self.DISABLE_SYSTEM_FENCE)),
+                     "hipEventCreateWithFlags")
+
+    @staticmethod
+    def _ok(rc: int, what: str):
+        if rc != 0:
+            raise RuntimeError("%s failed with HIP error %d" % (what, rc))
+
+    def record(self, i: int):
+        import torch
+        self._ok(self._hip.hipEventRecord(self._ev[i], self._ct.c_void_p(torch.cuda.current_stream().cuda_stream)),
+                 "hipEventRecord")
+
+    def elapsed_ms(self, i: int, j: int) -> float:
+        self._ok(self._hip.hipEventSynchronize(self._ev[j]), "hipEventSynchronize")
+        ms = self._ct.c_float()
+        self._ok(self._hip.hipEventElapsedTime(self._ct.byref(ms), self._ev[i], self._ev[j]), "hipEventElapsedTime")
+        return ms.value
+
+    def close(self):
+        for e in self._ev:
+            self._hip.hipEventDestroy(e)
+        self._ev = []
+
+
 def kernel_source_hash():
     """sha256 over the kernel sources, or None where they are not present."""
     h = hashlib.sha256()
@@ -297,20 +337,16 @@ def main():
     gm.profile(["fused_vec"])
 
     log("timing %d steps" % args.steps)
-    # an event after each step on the context's stream (torch's current one)
-    # gives the per-step times for the median; the value comes from the
-    # host clock around the whole timed region
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    # the value comes from the host clock around the whole timed region; the
+    # only events in it are the library's pair around each worker pass (the
+    # roofline's kernel time): every event record is a barrier packet in the
+    # queue, 1-3 us of the step
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    evs[0].record()
-    for i in range(args.steps):
+    for _ in range(args.steps):
         one_step()
-        evs[i + 1].record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    per_step = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
-    ms_median = per_step[len(per_step) // 2] if per_step else None
     prof = gm.profile_read()
     stats1 = gm.stats()
     gm.profile([])
@@ -327,16 +363,16 @@ def main():
     err.zero_()
     bufs[1].copy_(bufs[0])
     torch.cuda.synchronize()
-    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    f0.record()
+    fev = TimingEvents(2)
+    fev.record(0)
     if detach:
         g0.step(bufs[0], bufs[1], G[0], err, idx, val, ln, w_k=wk)
         g0.finish(idx, val, ln, bufs[0], bufs[1], err=err, w_k=wk)
     else:
         g0.iteration(bufs[0], bufs[1], G[0], err, idx, val, ln)
-    f1.record()
+    fev.record(1)
     torch.cuda.synchronize()
-    first = {"ms": round(f0.elapsed_time(f1), 4), "full_data_selections": g0.stats()["full_data"]}
+    first = {"ms": round(fev.elapsed_ms(0, 1), 4), "full_data_selections": g0.stats()["full_data"]}
     g0.close()
     # the full-data selection path (the fallback when the candidates cannot
     # prove they hold the top k): one step from the same state with every
@@ -349,11 +385,11 @@ def main():
         err.zero_()
         bufs[1].copy_(bufs[0])
         torch.cuda.synchronize()
-        f0.record()
+        fev.record(0)
         g1.step(bufs[0], bufs[1], G[0], err, idx, val, ln, w_k=wk if detach else None)
-        f1.record()
+        fev.record(1)
         torch.cuda.synchronize()
-        full = {"ms": round(f0.elapsed_time(f1), 4), "full_data_selections": g1.stats()["full_data"],
+        full = {"ms": round(fev.elapsed_ms(0, 1), 4), "full_data_selections": g1.stats()["full_data"],
                 "what": "gmc_step alone, every selection on the full-data path"}
         g1.close()
     if args.calib:
@@ -367,17 +403,17 @@ def main():
     if wl.compressor != "rbgs" and not detach:
         for _ in range(2):
             calib_stream(err, G[0])
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         reps = 5
-        ev0.record()
+        fev.record(0)
         for _ in range(reps):
             calib_stream(err, G[0])
-        ev1.record()
+        fev.record(1)
         torch.cuda.synchronize()
-        stream_ms = ev0.elapsed_time(ev1) / reps
+        stream_ms = fev.elapsed_ms(0, 1) / reps
         stream = {"kernel": "calib_stream_kernel", "bytes": 12 * K * d, "avg_ms": round(stream_ms, 4),
                   "achieved": round(12 * K * d / (stream_ms * 1e-3) / 1e9, 1)}
 
+    fev.close()
     ms_step = elapsed * 1e3 / args.steps
     msg_len = int(round(float(ln.double().mean().item())))  # varies per worker for the sampled threshold
     # relative communication cost of the last timed step (Section 5.2):
@@ -412,7 +448,6 @@ def main():
         "metric": METRIC if wl.name == "resnet50" else METRIC.split(",")[0] + ", " + wl.name,
         "value": round(value, 2), "unit": UNIT, "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
-        "ms_per_step_median": None if ms_median is None else round(ms_median, 4),
         "first_step": first,
         "full_data_step": full,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",

@@ -352,7 +352,9 @@ gmc_status gmc_set_step(gmc_ctx* ctx, int64_t t);
  *                              reallocates scratch; before the first step
  *   GMC_OPT_PROFILE            bit mask of the stages to time with HIP events
  *                              on the context's stream (0: off); see
- *                              gmc_profile_read for the stage numbers
+ *                              gmc_profile_read for the stage numbers.  The
+ *                              events are recorded without a system-scope
+ *                              fence: they time, they do not order host reads
  *   GMC_OPT_SAMPLE_STRATUM     GMC_TOPK_APPROX: components per sample stratum
  *                              L in [1, d] (default 100); before the first step
  *   GMC_OPT_SPARSE_MOMENTUM    1: the caller promises not to change either

@@ -500,11 +500,13 @@ gmc_status prepare(gmc_ctx* ctx) {
 }
 
 // -- profiling ---------------------------------------------------------------
+// The stage events only time: recorded without the system-scope fence (a
+// cache write-back and invalidate that would lengthen the step they time).
 
 gmc_status prof_begin(gmc_ctx* ctx, int stage, hipEvent_t* ev) {
     *ev = nullptr;
     if (!((ctx->profile >> stage) & 1u)) return GMC_OK;
-    GMC_HIP(ctx, hipEventCreate(ev));
+    GMC_HIP(ctx, hipEventCreateWithFlags(ev, hipEventDisableSystemFence));
     GMC_HIP(ctx, hipEventRecord(*ev, ctx->stream));
     return GMC_OK;
 }
@@ -526,7 +528,7 @@ gmc_status prof_fold(gmc_ctx* ctx, int stage) {
 gmc_status prof_end(gmc_ctx* ctx, int stage, hipEvent_t start) {
     if (!start) return GMC_OK;
     hipEvent_t stop;
-    GMC_HIP(ctx, hipEventCreate(&stop));
+    GMC_HIP(ctx, hipEventCreateWithFlags(&stop, hipEventDisableSystemFence));
     GMC_HIP(ctx, hipEventRecord(stop, ctx->stream));
     ctx->pending[stage].emplace_back(start, stop);
     if ((int64_t)ctx->pending[stage].size() >= kMaxPendingEvents) return prof_fold(ctx, stage);

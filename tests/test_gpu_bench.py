@@ -35,7 +35,7 @@ def test_bench_line(workload, extra, capsys, monkeypatch):
     wl = synth.workload(workload)
     for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
                 "scaling", "vs_baseline", "dtype", "data", "config", "roofline", "first_step",
-                "ms_per_step_median", "selection", "hbm_peak_frac"):
+                "selection", "hbm_peak_frac"):
         assert key in j, key
     assert j["n_gpus"] == 1 and j["steps"] == 3 and j["warmup"] == 2
     assert j["higher_is_better"] is True and j["dtype"] == "f32" and j["data"] == "synthetic"
