@@ -737,10 +737,12 @@ __device__ __forceinline__ void for_slice_contig(const Slice& v, F f) {
     const float4* p4 = reinterpret_cast<const float4*>(p + lo);
     for (int64_t b = 0; b < n4; b += (int64_t)kGroup * kSliceLoads4) {
         float4 x[kSliceLoads4];
+        // every load unconditional (a position past the end reads the last
+        // float4, dropped below), so all kSliceLoads4 are in flight at once
 #pragma unroll
         for (int i = 0; i < kSliceLoads4; ++i) {
             const int64_t q = b + i * kGroup + threadIdx.x;
-            x[i] = q < n4 ? p4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+            x[i] = p4[q < n4 ? q : n4 - 1];
         }
 #pragma unroll
         for (int i = 0; i < kSliceLoads4; ++i) {
@@ -1341,8 +1343,11 @@ __device__ void compact_copy(const StepArgs& a, const TopkGeometry& g, const Top
     __shared__ uint32_t my_tot[kMaxCopyTiles];    // the group's candidates,
     __shared__ uint32_t my_tile[kMaxCopyTiles];   // the tile within the group
     static_assert(kCompactChunks == kGroup, "one chunk per thread");
-    const int k = blk / g.tiles_per_worker;
-    const int2 tm = g.tile_map[blk % g.tiles_per_worker];
+    // tile-major: the K workers' i-th tiles are consecutive workgroups, so
+    // the tiles that hold candidates (the first ones of every pair) are
+    // dispatched first and the spare ones after them
+    const int k = blk % g.K;
+    const int2 tm = g.tile_map[blk / g.K];
     const int seg = tm.x;
     const int p = k * g.n_seg + seg;
     PairState* ps = &s.pair[p];
@@ -1411,20 +1416,32 @@ __device__ void compact_copy(const StepArgs& a, const TopkGeometry& g, const Top
         const uint32_t hi = lo + kTile < total ? lo + kTile : total;
         int32_t* ci = ci0 + base;
         float* cv = cv0 + base;
+        // the eight loads of a thread go out together: no load sits under a
+        // per-element branch (a position past the tile's end reads the
+        // tile's first candidate, and its value is dropped)
         int32_t jv[8];
         float xv[8];
+        if (lo < hi) {
+            uint32_t q[8];
+            int a0[8];  // the chunk c with pre[c] <= q < pre[c+1]: the last c with pre[c] <= q
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const uint32_t q = lo + i * kGroup + threadIdx.x;
-            jv[i] = 0;
-            xv[i] = 0.0f;
-            if (q < hi) {
-                int a0 = 0, a1 = nch - 1;  // chunk c with pre[c] <= q < pre[c+1]
-                while (a0 < a1) {
-                    const int mid = (a0 + a1 + 1) >> 1;
-                    if (pre[mid] <= q) a0 = mid; else a1 = mid - 1;
+            for (int i = 0; i < 8; ++i) {
+                const uint32_t q0 = lo + i * kGroup + threadIdx.x;
+                q[i] = q0 < hi ? q0 : lo;
+                a0[i] = 0;
+            }
+            // the eight searches step by step: eight LDS reads per step
+#pragma unroll
+            for (int st = kCompactChunks / 2; st > 0; st >>= 1) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const int c = a0[i] + st < nch ? a0[i] + st : nch - 1;
+                    a0[i] = (a0[i] + st < nch && pre[c] <= q[i]) ? a0[i] + st : a0[i];
                 }
-                const int2 c = s.slot[(slot0 + a0) * kChunk + (q - pre[a0])];
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int2 c = s.slot[(slot0 + a0[i]) * kChunk + (q[i] - pre[a0[i]])];
                 jv[i] = c.x;
                 xv[i] = __int_as_float(c.y);
             }
@@ -1695,12 +1712,34 @@ __global__ __launch_bounds__(kGroup) void topk_emit_kernel(StepArgs a, TopkGeome
     auto emit_list = [&](const Slice& vl) {
     for (int64_t s0 = vl.lo; s0 < vl.hi; s0 += kEmitStage) {
         const int32_t ns = (int32_t)(vl.hi - s0 < kEmitStage ? vl.hi - s0 : kEmitStage);
+        // all of a thread's loads go out before the first is stored: a
+        // position past the round's end reads the round's first element
+        // (dropped), so no load sits under a per-element branch
+        float xl[kEmitLoads];
+        int32_t jl[kEmitLoads];
+        if (vl.idx) {
+#pragma unroll
+            for (int i = 0; i < kEmitLoads; ++i) {
+                const int32_t q = i * kGroup + threadIdx.x;
+                const int64_t pos = s0 + (q < ns ? q : 0);
+                xl[i] = vl.val[pos];
+                jl[i] = vl.idx[pos];
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < kEmitLoads; ++i) {
+                const int32_t q = i * kGroup + threadIdx.x;
+                const int64_t pos = s0 + (q < ns ? q : 0);
+                xl[i] = vl.val[pos];
+                jl[i] = vl.seg_lo + (int32_t)pos;
+            }
+        }
 #pragma unroll
         for (int i = 0; i < kEmitLoads; ++i) {
             const int32_t q = i * kGroup + threadIdx.x;
             if (q < ns) {
-                st_val[stage_slot(q)] = vl.val[s0 + q];
-                st_idx[stage_slot(q)] = vl.idx ? vl.idx[s0 + q] : vl.seg_lo + (int32_t)(s0 + q);
+                st_val[stage_slot(q)] = xl[i];
+                st_idx[stage_slot(q)] = jl[i];
             }
         }
         __syncthreads();
