@@ -33,7 +33,7 @@ constexpr int kGrpSub = 16;
 constexpr int kTile = kGroup * 8;          // candidates one copy workgroup moves
 constexpr int64_t kSliceElems = 1 << 19;   // full-data elements per slice (at most)
 constexpr int64_t kSliceCands = 8192;      // usual candidates per slice (more when a list runs long)
-constexpr int64_t kHistSliceCands = 8192;  // candidates per histogram-pass workgroup (fewer workgroups)
+constexpr int64_t kHistSliceCands = 4096;  // candidates per second-pass workgroup (one round of loads each)
 constexpr int kMaxSlices = 256;
 constexpr int kSlHist = 513;               // per slice: suffix sums of a 512-bin histogram + a count above
 

@@ -1133,10 +1133,10 @@ __device__ void hist_pass(const StepArgs& a, const TopkGeometry& g, const TopkSc
                      : PASS == 1 ? ((force_full || cand < (uint32_t)kp || cand > (uint32_t)g.pair_cap[id.p]) ? 1 : 0)
                                  : ps->mode;
     const uint32_t prefix = PASS == 1 ? 0u : ps->prefix;
-    // a candidate list is histogrammed in slices of about kHistSliceCands
-    // (each workgroup merges its slice's histogram into the pair's with one
-    // global atomic per nonzero bin, so fewer, fuller slices cost less); the
-    // other workgroups of the pair leave at once
+    // a candidate list is histogrammed in slices of about kHistSliceCands,
+    // one round of loads per workgroup (each merges its slice's histogram
+    // into the pair's with one global atomic per nonzero bin); the other
+    // workgroups of the pair leave at once
     // the third pass of exact top-s counts per slice for the emit kernel, so
     // it keeps the emit's slices
     const bool count = PASS == 3 && !approx;
