@@ -204,15 +204,23 @@ __host__ __device__ inline int64_t run_order_grid(int64_t n_chunks, int K, int r
     return (n_chunks + run - 1) / run * run * K;
 }
 
-// w_t and w_prev of the four components at j for the worker passes.  With the
-// previous server pass's bitmap (a.wbits), unmarked components have
-// w_t == w_prev, finite: w_t - w_prev is exactly +0 there, so the loads are
-// skipped (w_t is still read when the detached points need it) and the
-// momentum term comes out +0, bit for bit what the dense loads give.
+// The previous server pass's mark word of the components at j (a.wbits set).
+// The top-s vector pass loads it before its stream of e and g: a wait for the
+// word then leaves those loads in flight (vmcnt counts in issue order).
+__device__ __forceinline__ uint32_t mark_word(const StepArgs& a, int64_t j) {
+    return a.wbits ? a.wbits[j >> 5] : 0u;
+}
+
+// w_t and w_prev of the four components at j for the worker passes (word:
+// mark_word(a, j)).  With the previous server pass's bitmap (a.wbits),
+// unmarked components have w_t == w_prev, finite: w_t - w_prev is exactly +0
+// there, so the loads are skipped (w_t is still read when the detached points
+// need it) and the momentum term comes out +0, bit for bit what the dense
+// loads give.
 template <bool kDetach>
-__device__ __forceinline__ void load_w4(const StepArgs& a, int64_t j, float4* wt, float4* wv) {
+__device__ __forceinline__ void load_w4(const StepArgs& a, int64_t j, uint32_t word, float4* wt, float4* wv) {
     if (a.wbits) {
-        const uint32_t marked = (a.wbits[j >> 5] >> (j & 31)) & 0xfu;
+        const uint32_t marked = (word >> (j & 31)) & 0xfu;
         if (marked) {
             *wt = ld4(a.w_t + j);
             *wv = ld4(a.w_prev + j);
@@ -376,12 +384,20 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
     // scattered into LDS, every other one is exactly +0
     bool use_list = !kDetach && kNeedW && a.dlist != nullptr;
     float4 u[2], gv[2], wt[2], wv[2];
+    uint32_t mw[2] = {0u, 0u};  // the mark words first, then the stream (see mark_word)
+    if (kNeedW && !use_list) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) mw[i] = mark_word(a, (int64_t)start + o0 + i * (kGroup * 4));
+    }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         u[i] = ld4_stream(ep + i * (kGroup * 4));
         gv[i] = ld4_stream(gp + i * (kGroup * 4));
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
         wt[i] = wv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (kNeedW && !use_list) load_w4<kDetach>(a, (int64_t)start + o0 + i * (kGroup * 4), &wt[i], &wv[i]);
+        if (kNeedW && !use_list) load_w4<kDetach>(a, (int64_t)start + o0 + i * (kGroup * 4), mw[i], &wt[i], &wv[i]);
     }
     if (use_list) {
         const int r0 = start / kAggTopkRange, nr = (start + len - 1) / kAggTopkRange - r0 + 1;  // 1 or 2 ranges
@@ -417,7 +433,10 @@ __global__ __launch_bounds__(kGroup) void topk_fused_vec_kernel(StepArgs a, Topk
         __syncthreads();
         if (!use_list) {  // a range's list overflowed (w_prev is then set): the marks and the two parameter vectors
 #pragma unroll
-            for (int i = 0; i < 2; ++i) load_w4<kDetach>(a, (int64_t)start + o0 + i * (kGroup * 4), &wt[i], &wv[i]);
+            for (int i = 0; i < 2; ++i) {
+                const int64_t j = (int64_t)start + o0 + i * (kGroup * 4);
+                load_w4<kDetach>(a, j, mark_word(a, j), &wt[i], &wv[i]);
+            }
         }
     }
     uint32_t flags = 0;
@@ -2099,7 +2118,7 @@ __global__ __launch_bounds__(kGroup) void rbgs_vec_kernel(StepArgs a, int32_t K,
         u[i] = ld4_stream(ep + i * (kGroup * 4));
         gv[i] = ld4_stream(gp + i * (kGroup * 4));
         if (kNeedW)
-            load_w4<kDetach>(a, start + i * (kGroup * 4), &wt[i], &wv[i]);
+            load_w4<kDetach>(a, start + i * (kGroup * 4), mark_word(a, start + i * (kGroup * 4)), &wt[i], &wv[i]);
         else
             wt[i] = wv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
