@@ -2482,8 +2482,11 @@ __global__ __launch_bounds__(kGroup) void agg_topk_kernel(int32_t K, int32_t d, 
         }
     } else {
         // a dense range (up to K entries per component): worker after
-        // worker straight from the messages, kDirect loads in flight per thread
-        constexpr int kDirect = 4;
+        // worker straight from the messages, kDirect loads in flight per
+        // thread (eight with the larger stage, for dense messages: a worker
+        // sending 2048 entries of the range then takes one round trip; the
+        // sparse-message kernel keeps four and its registers)
+        constexpr int kDirect = kStage >= 512 ? 8 : 4;
         for (int k = 0; k < K; ++k) {
             const int32_t cnt = pre[k + 1] - pre[k];
             const int32_t* ip = idx + (size_t)k * idx_row + src[k];
