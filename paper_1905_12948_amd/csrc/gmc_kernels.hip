@@ -1039,14 +1039,22 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
         // speculative threshold of the next step: the floor of the bin that
         // holds the key of rank margin*k/4 this step (the second pass of
         // exact top-s narrows it to 22 bits)
-        uint32_t mine = 0;
-        for (int b = threadIdx.x; b < nbins; b += kGroup) mine += h[b];
-        uint32_t total;
-        block_scan_excl(mine, &total, sh_wsum);
         const uint64_t want64 = ((uint64_t)margin * (uint64_t)kp + 3) / 4;
-        const uint32_t want = (uint32_t)(want64 < total ? want64 : total);
-        uint32_t ab2 = 0;
-        int tb = find_bin(h, nbins, want, &ab2, sh_wsum, sh_res);
+        uint32_t total, want, ab2 = 0;
+        int tb;
+        if (want64 == (uint64_t)need && bin >= 0) {
+            // rank k itself (the default margin): T's bin, found above, in a
+            // histogram of at least k keys
+            total = want = need;
+            ab2 = above;
+            tb = bin;
+        } else {
+            uint32_t mine = 0;
+            for (int b = threadIdx.x; b < nbins; b += kGroup) mine += h[b];
+            block_scan_excl(mine, &total, sh_wsum);
+            want = (uint32_t)(want64 < total ? want64 : total);
+            tb = find_bin(h, nbins, want, &ab2, sh_wsum, sh_res);
+        }
         if (threadIdx.x == 0) {
             const bool widen = want64 > total;
             if (widen && tb > 0) --tb;  // too few counted: widen by one bin
@@ -1102,9 +1110,12 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
         // the speculative threshold at the floor of the 22-bit bin holding
         // the key of rank margin*k/4: the tau_need-th key of bin tau_bin
         if (ps->tau_fine) {
-            const uint32_t tb = ps->tau_bin;
-            uint32_t ab = 0;
-            const int sb = find_bin(fine2 ? h2 : h, kBins, ps->tau_need, &ab, sh_wsum, sh_res);
+            const uint32_t tb = ps->tau_bin, tn = ps->tau_need;
+            int sb = bin;  // the threshold at T's own rank in T's bin: the bin found above
+            if (fine2 || tn != need) {
+                uint32_t ab = 0;
+                sb = find_bin(fine2 ? h2 : h, kBins, tn, &ab, sh_wsum, sh_res);
+            }
             if (threadIdx.x == 0 && sb >= 0) ps->tau = (tb << kShift1) | ((uint32_t)sb << kShift2);
         }
         if (threadIdx.x == 0) store_agent(&ps->done, 0u);
