@@ -1022,12 +1022,21 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
     // second pass: the threshold's bin histogram comes in with T's.  A pair
     // that one workgroup covered (solo) has its whole histogram in LDS
     // already and never wrote the global one.
-    const bool fine2 = PASS == 2 && ps->tau_fine != 0u && ps->tau_bin != prefix;
+    // the pair's fields this pick reads, loaded before the histogram is taken
+    // (a load after take_hist would also wait for its clearing stores: vmcnt
+    // counts in issue order)
+    const uint32_t need = PASS == 1 ? (uint32_t)kp : (uint32_t)ps->need;
+    const uint32_t tau_prev = PASS == 1 ? ps->tau : 0u;
+    const uint32_t tau_fine = PASS == 2 ? ps->tau_fine : 0u;
+    const uint32_t tau_bin = PASS == 2 ? ps->tau_bin : 0u;
+    const uint32_t tau_need = PASS == 2 ? ps->tau_need : 0u;
+    const uint32_t cand_used = PASS == 3 ? ps->cand_used : 0u;
+    const uint32_t tau_used = PASS == 3 ? ps->tau_used : 0u;
+    const bool fine2 = PASS == 2 && tau_fine != 0u && tau_bin != prefix;
     if (!solo) {
         if (fine2) take_hist2<kBins>(h, gh, h2, gh2);
         else take_hist<nbins>(h, gh);
     }
-    const uint32_t need = PASS == 1 ? (uint32_t)kp : (uint32_t)ps->need;
     uint32_t above = 0;
     const int bin = find_bin(h, nbins, need, &above, sh_wsum, sh_res);
     if (PASS == 3 && T_out) {  // every thread: the threshold and the ties to take
@@ -1059,7 +1068,7 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
             const bool widen = want64 > total;
             if (widen && tb > 0) --tb;  // too few counted: widen by one bin
             if (tb < 0) tb = 0;
-            ps->tau_used = ps->tau;
+            ps->tau_used = tau_prev;
             ps->tau = (uint32_t)tb << kShift1;
             ps->tau_fine = (!approx && !widen) ? 1u : 0u;
             ps->tau_bin = (uint32_t)tb;
@@ -1097,8 +1106,8 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
                 // the candidates hold them all when T reaches the threshold
                 // the fused pass collected with and none were dropped
                 ps->r = 0x7fffffff;
-                const uint32_t cu = ps->cand_used;
-                const int m = (!force_full && T >= ps->tau_used && cu <= (uint32_t)g.pair_cap[p]) ? 0 : 1;
+                const uint32_t cu = cand_used;
+                const int m = (!force_full && T >= tau_used && cu <= (uint32_t)g.pair_cap[p]) ? 0 : 1;
                 ps->mode = m;
                 atomicAdd((unsigned long long*)&s.stats[m == 0 ? 1 : 2], 1ull);
                 if (m == 0) atomicAdd((unsigned long long*)&s.stats[3], (unsigned long long)cu);
@@ -1109,8 +1118,8 @@ __device__ void finish_digit(PairState* ps, int p, uint32_t* h, uint32_t* gh, in
     if (PASS == 2) {
         // the speculative threshold at the floor of the 22-bit bin holding
         // the key of rank margin*k/4: the tau_need-th key of bin tau_bin
-        if (ps->tau_fine) {
-            const uint32_t tb = ps->tau_bin, tn = ps->tau_need;
+        if (tau_fine) {
+            const uint32_t tb = tau_bin, tn = tau_need;
             int sb = bin;  // the threshold at T's own rank in T's bin: the bin found above
             if (fine2 || tn != need) {
                 uint32_t ab = 0;
