@@ -147,9 +147,10 @@ struct TopkGeometry {
     const int64_t* pair_cand;     // [K*n_seg] start of the pair's candidate list
     // copy tiles (kTile candidates of one compaction group; a group's tiles
     // follow the groups before it).  Launch: tiles_per_worker workgroups per
-    // worker; workgroup tt takes segment tile_map[tt].x's tiles
-    // tile_map[tt].y, + seg_tile_stride[seg], ... (the launch is sized for
-    // the usual candidate count, the stride covers longer lists)
+    // worker, tile-major (workgroup b is worker b % K's entry tt = b / K);
+    // it takes segment tile_map[tt].x's tiles tile_map[tt].y,
+    // + seg_tile_stride[seg], ... (the launch is sized for the usual
+    // candidate count, the stride covers longer lists)
     int32_t tiles_per_worker;
     const int2* tile_map;             // [tiles_per_worker]
     const int32_t* seg_tile_stride;   // [n_seg] workgroups launched per (worker, segment)

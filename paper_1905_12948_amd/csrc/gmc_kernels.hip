@@ -1364,7 +1364,7 @@ hipError_t launch_topk_hist(int pass, const StepArgs& a, const TopkGeometry& g, 
 // the group each chunk's candidates at the counts of the chunks before it.
 // Workgroup (worker, tile_map entry (seg, i)) takes the pair's tiles i, i +
 // stride, ... (stride = the workgroups launched for the pair, sized for the
-// usual count).  For the pairs of exact top-s that resolve from their
+// usual count); the grid is tile-major, the K workers' entries consecutive.  For the pairs of exact top-s that resolve from their
 // candidates the copy also histograms the first digit, and the last of the
 // pair's workgroups picks it (the first histogram pass then skips the pair).
 constexpr int kMaxCopyTiles = 256;  // tiles of one workgroup (at most about cap_mult / 8 + 2)
